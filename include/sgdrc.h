@@ -1,0 +1,204 @@
+/*
+ * sgdrc.h -- C ABI of the MI355X colour-restricted tensor path.
+ *
+ * Software-defined resource control in the manner of SGDRC (PPoPP '25):
+ * device memory is split into "colours" by an XOR hash of page addresses;
+ * tensors are stored on pages of chosen colours through a page-indirection
+ * table and read through it by every kernel; each launch runs only on the
+ * compute units (CUs) named by a per-stream mask.
+ *
+ * Conventions for every call below
+ * --------------------------------
+ *  - Return value: SGDRC_OK (0) or a negative SGDRC_E* code.  On error
+ *    nothing is enqueued and no caller memory is touched; the text of the
+ *    last error of the calling thread is given by sgdrc_last_error().
+ *    Arguments are checked before the context, so argument errors are
+ *    reported (SGDRC_EINVAL) even when ctx is NULL.
+ *  - Pointers prefixed d_ (and the pool/pt pointers of sgdrc_paged) are
+ *    device pointers on the context's device; all others are host pointers.
+ *    The caller owns every buffer it passes and keeps it alive until the
+ *    enqueued work is done.  The library owns only its context workspace.
+ *  - ``stream`` is a hipStream_t handle (NULL = the legacy default stream).
+ *    Every operation is asynchronous on that stream except
+ *    colour_alloc_pagetable, which returns after its work has finished.
+ *  - Page tables are arrays of uint32 pool-page indices.  Logical byte b of
+ *    a paged tensor lives at pool + pt[b >> page_shift] * 2^page_shift +
+ *    (b & (2^page_shift - 1)).  Kernels check every page-table entry
+ *    against the pool size they are given; an entry out of range is skipped
+ *    (its bytes are neither read nor written) and raises the device error
+ *    flag SGDRC_DEVERR_PT_RANGE, reported by sgdrc_device_error().
+ *  - A context serves one device.  It may be used from several host
+ *    threads; operations on one stream are ordered, operations on different
+ *    streams may run concurrently (each stream gets its own work queue).
+ */
+#ifndef SGDRC_H
+#define SGDRC_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SGDRC_OK 0
+#define SGDRC_EINVAL (-22) /* bad argument */
+#define SGDRC_ENOMEM (-12) /* pool holds fewer qualifying pages than requested */
+#define SGDRC_ENODEV (-19) /* no usable gfx950 device, or ctx is NULL/not initialised */
+#define SGDRC_EHIP (-5)    /* HIP runtime error */
+
+#define SGDRC_MAX_MASKS 8
+#define SGDRC_MAX_CUS 256
+#define SGDRC_MIN_PAGE_SHIFT 12 /* 4 KiB */
+#define SGDRC_MAX_PAGE_SHIFT 30 /* 1 GiB */
+#define SGDRC_MAX_BATCH 8
+
+/* device error flags (bitwise OR, sticky until read) */
+#define SGDRC_DEVERR_PT_RANGE 1u
+
+/* element encodings */
+enum { SGDRC_F32 = 0, SGDRC_BF16 = 1, SGDRC_F16 = 2 };
+
+typedef struct sgdrc_ctx sgdrc_ctx;
+
+/* K XOR masks, 1 <= n_masks <= 8.  Colour bit k of an address a is the
+ * parity of (a & masks[k]); bit 0 is the least significant colour bit, so
+ * there are 2^K colours.  Masks may only select address bits 0..47. */
+typedef struct {
+    uint32_t n_masks;
+    uint32_t reserved; /* must be 0 */
+    uint64_t masks[SGDRC_MAX_MASKS];
+} sgdrc_hash;
+
+/* A set of colours: bit c of the 256-bit field (word c/64, bit c%64). */
+typedef struct {
+    uint64_t bits[4];
+} sgdrc_colour_set;
+
+/* A set of logical CUs: bit i = logical CU i, 0 <= i < sgdrc_num_cus().
+ * Logical CUs are numbered in (XCC, shader engine, shader array, CU) order,
+ * so CUs 32x..32x+31 are the CUs of XCC x on a 256-CU MI355X. */
+typedef struct {
+    uint64_t bits[4];
+} sgdrc_cu_mask;
+
+/* A paged tensor: device pool base (256-byte aligned), device page table,
+ * and the pool's capacity in pages (every pt entry must be below it). */
+typedef struct {
+    void *pool;
+    const uint32_t *pt;
+    uint64_t pool_pages;
+} sgdrc_paged;
+
+/* ---------------------------------------------------------------- context */
+
+/* Create a context on HIP device ``device`` (must be gfx950).  Probes the
+ * CU topology by running a kernel that records the XCC_ID and HW_ID
+ * registers of every CU, and allocates the context workspace (CU lookup
+ * table, per-stream work-queue counters, device error word).  Synchronous. */
+int sgdrc_init(int device, sgdrc_ctx **out);
+
+/* Wait for the device, then free the context and its workspace. */
+int sgdrc_destroy(sgdrc_ctx *ctx);
+
+/* Number of CUs found by the probe (a negative code if ctx is invalid). */
+int sgdrc_num_cus(const sgdrc_ctx *ctx);
+
+/* Hardware identity of logical CU ``cu``: (XCC_ID << 8) | HW_ID[15:8]
+ * (the CU, shader-array and shader-engine fields). */
+int sgdrc_cu_key(const sgdrc_ctx *ctx, uint32_t cu, uint32_t *key);
+
+/* Text of the calling thread's last error ("" if none). */
+const char *sgdrc_last_error(void);
+
+/* Wait for the device, then return and clear the device error flags. */
+int sgdrc_device_error(sgdrc_ctx *ctx, uint32_t *flags);
+
+/* Optional per-launch work log, for tests of the CU gate and tile queue.
+ * When set, every tile that a kernel processes adds 1 to
+ * d_cu_tiles[logical CU] (num_cus entries) and to d_tile_visits[tile index]
+ * (tiles beyond tile_cap are not logged).  NULL pointers switch it off.
+ * Applies to launches enqueued after the call. */
+int sgdrc_set_worklog(sgdrc_ctx *ctx, uint32_t *d_cu_tiles, uint32_t *d_tile_visits,
+                      uint64_t tile_cap);
+
+/* Tile count of the last launch enqueued on ``stream`` through this
+ * context (0 if none); lets a caller size and read the work log. */
+int sgdrc_last_tiles(sgdrc_ctx *ctx, void *stream, uint64_t *tiles);
+
+/* ------------------------------------------------------------- operations */
+
+/* Tidal compute-unit masking (paper section 7.1, Elastic SM Scaling; the
+ * per-launch TPC mask there is replaced by an in-kernel gate).  Sets the CU
+ * set used by every later launch on ``stream``: each workgroup reads its
+ * CU identity from the hardware registers and exits unless that CU is in
+ * the set; the remaining workgroups take tiles from an atomic queue until it
+ * is empty.  mask == NULL restores all CUs.  Host-only, takes effect at the
+ * next launch, never recreates the stream.  EINVAL: empty mask or a bit at
+ * or above sgdrc_num_cus(). */
+int set_cu_mask(sgdrc_ctx *ctx, void *stream, const sgdrc_cu_mask *mask);
+
+/* Batched colouring (paper section 6, SPT step 1, marking each page's
+ * colour; the hash is the linear XOR form discussed in section 3.2).
+ * d_colours[i] = colour(d_addrs[i]) for i < n.  If d_hist != NULL it
+ * receives the number of addresses of each colour (2^K uint64 entries,
+ * overwritten).  d_addrs must be 8-byte aligned.  n == 0 is valid (hist is
+ * zeroed).  EINVAL: bad hash, NULL pointers with n > 0. */
+int colour_classify(sgdrc_ctx *ctx, const sgdrc_hash *hash, const uint64_t *d_addrs,
+                    uint64_t n, uint8_t *d_colours, uint64_t *d_hist, void *stream);
+
+/* Page-table build (paper section 6, SPT steps 2-3, per-colour page lists
+ * of a reserved pool).  Pool page i (0 <= i < pool_pages) has the address
+ * addr_origin + i * 2^page_shift and qualifies when its colour is in
+ * ``set``.  Writes to d_pt the first min(found, n_needed) qualifying page
+ * indices in ascending order, and sets *n_found = found, the number of
+ * qualifying pages in the whole pool.  Returns SGDRC_ENOMEM when
+ * found < n_needed (d_pt then holds all ``found`` pages).  Synchronous:
+ * returns after the result is in d_pt.  EINVAL: bad hash, page_shift
+ * outside [12, 30], addr_origin not page aligned, pool beyond 2^48 bytes of
+ * address space, pool_pages > 2^32, n_needed > pool_pages, empty set or
+ * a colour >= 2^K in it. */
+int colour_alloc_pagetable(sgdrc_ctx *ctx, const sgdrc_hash *hash, uint64_t addr_origin,
+                           uint32_t page_shift, uint64_t pool_pages,
+                           const sgdrc_colour_set *set, uint64_t n_needed, uint32_t *d_pt,
+                           uint64_t *n_found, void *stream);
+
+/* Bimodal relayout (paper section 7.2, moving a tensor between its
+ * all-channel and its restricted page set): copies n_bytes logical bytes,
+ * logical byte b going from src's page pt[b >> s] to dst's page
+ * pt[b >> s] at the same in-page offset.  Both tables hold
+ * ceil(n_bytes / 2^page_shift) entries.  Bytes of dst pages beyond n_bytes
+ * are not written.  src and dst must not overlap.  EINVAL: NULL pointers,
+ * pools not 256-byte aligned, page_shift outside [12, 30]. */
+int bimodal_relayout(sgdrc_ctx *ctx, const sgdrc_paged *dst, const sgdrc_paged *src,
+                     uint64_t n_bytes, uint32_t page_shift, void *stream);
+
+/* Colour-restricted streaming triad (paper section 6, SPT step 4, the
+ * re-indexed vector kernel): a[i] = fmaf(s, c[i], b[i]) for i < n_elems,
+ * one rounding, every fp32 element reached through its array's page table
+ * (ceil(4 n_elems / 2^page_shift) entries each).  a may alias b or c
+ * element-for-element (same pool and table) but must not otherwise overlap
+ * them.  EINVAL: as for bimodal_relayout. */
+int colored_stream(sgdrc_ctx *ctx, const sgdrc_paged *a, const sgdrc_paged *b,
+                   const sgdrc_paged *c, float s, uint64_t n_elems, uint32_t page_shift,
+                   void *stream);
+
+/* Colour-restricted GEMV / small-batch GEMM of a memory-bound layer (paper
+ * section 7.2): d_y[b*M + m] = sum_k W[m][k] * x[b][k], fp32 result,
+ * products summed in fp32.  W is row-major [M x K] of w_dtype, stored
+ * through w's page table (ceil(M K esize / 2^page_shift) entries); d_x is
+ * contiguous [batch x K] of x_dtype (16-byte aligned); d_y is contiguous
+ * [batch x M] fp32.  Batches 5..8 with bf16 x bf16 or f16 x f16 operands
+ * run on MFMA; all other cases on the vector ALUs.  The sum order depends
+ * only on (M, K, batch, dtypes), never on the CU mask, so results are
+ * bitwise reproducible.  EINVAL: batch outside 1..8, M or K zero, K *
+ * esize(w_dtype) not a multiple of 16, unknown dtype, NULL pointers,
+ * unaligned pointers. */
+int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, uint32_t K,
+                 const void *d_x, int x_dtype, uint32_t batch, float *d_y,
+                 uint32_t page_shift, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SGDRC_H */

@@ -1,0 +1,230 @@
+"""Python binding of libsgdrc, the MI355X colour-restricted tensor path.
+
+Argument marshalling only: every operation runs in the HIP kernels of
+``libsgdrc.so``; there is no fallback.  If the library has not been built
+(``python -m paper_2407_13996_amd.build``) every entry point raises.
+
+Device buffers are passed as torch tensors (or raw integer device
+addresses); streams as ``torch.cuda.Stream`` objects, raw ``hipStream_t``
+integers, or None for torch's current stream.  The function names match the
+C ABI in ``include/sgdrc.h``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libsgdrc.so")
+
+OK, EINVAL, ENOMEM, ENODEV, EHIP = 0, -22, -12, -19, -5
+F32, BF16, F16 = 0, 1, 2
+DEVERR_PT_RANGE = 1
+DEVFLAG_GATE_FALLBACK = 2
+MAX_MASKS = 8
+
+
+class SgdrcError(RuntimeError):
+    def __init__(self, code: int, message: str, n_found: int | None = None):
+        super().__init__(f"sgdrc error {code}: {message}")
+        self.code = code
+        self.n_found = n_found
+
+
+class Hash(ctypes.Structure):
+    _fields_ = [("n_masks", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+                ("masks", ctypes.c_uint64 * MAX_MASKS)]
+
+
+class ColourSet(ctypes.Structure):
+    _fields_ = [("bits", ctypes.c_uint64 * 4)]
+
+
+class CuMask(ctypes.Structure):
+    _fields_ = [("bits", ctypes.c_uint64 * 4)]
+
+
+class Paged(ctypes.Structure):
+    _fields_ = [("pool", ctypes.c_void_p), ("pt", ctypes.c_void_p),
+                ("pool_pages", ctypes.c_uint64)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libsgdrc.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2407_13996_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, u32, u64, i32 = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int
+        P = ctypes.POINTER
+        sigs = {
+            "sgdrc_init": ([i32, P(vp)], i32),
+            "sgdrc_destroy": ([vp], i32),
+            "sgdrc_num_cus": ([vp], i32),
+            "sgdrc_cu_key": ([vp, u32, P(u32)], i32),
+            "sgdrc_last_error": ([], ctypes.c_char_p),
+            "sgdrc_device_error": ([vp, P(u32)], i32),
+            "sgdrc_set_worklog": ([vp, vp, vp, u64], i32),
+            "sgdrc_last_tiles": ([vp, vp, P(u64)], i32),
+            "set_cu_mask": ([vp, vp, P(CuMask)], i32),
+            "colour_classify": ([vp, P(Hash), vp, u64, vp, vp, vp], i32),
+            "colour_alloc_pagetable": ([vp, P(Hash), u64, u32, u64, P(ColourSet), u64, vp,
+                                        P(u64), vp], i32),
+            "bimodal_relayout": ([vp, P(Paged), P(Paged), u64, u32, vp], i32),
+            "colored_stream": ([vp, P(Paged), P(Paged), P(Paged), ctypes.c_float, u64, u32, vp],
+                               i32),
+            "colored_gemv": ([vp, P(Paged), i32, u32, u32, vp, i32, u32, vp, u32, vp], i32),
+        }
+        for name, (args, res) in sigs.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
+
+
+def last_error() -> str:
+    return lib().sgdrc_last_error().decode()
+
+
+def _check(rc: int, n_found: int | None = None) -> None:
+    if rc != OK:
+        raise SgdrcError(rc, last_error(), n_found)
+
+
+def _addr(x) -> int | None:
+    if x is None:
+        return None
+    if hasattr(x, "data_ptr"):
+        return int(x.data_ptr())
+    return int(x)
+
+
+def _stream(s):
+    if s is None:
+        import torch
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if hasattr(s, "cuda_stream"):
+        return ctypes.c_void_p(s.cuda_stream)
+    return ctypes.c_void_p(int(s))
+
+
+def make_hash(masks) -> Hash:
+    masks = [int(m) for m in masks]
+    h = Hash()
+    h.n_masks = len(masks)
+    h.reserved = 0
+    for i, m in enumerate(masks[:MAX_MASKS]):
+        h.masks[i] = m
+    return h
+
+
+def make_set(words, cls=ColourSet):
+    s = cls()
+    for i, w in enumerate(words):
+        s.bits[i] = int(w)
+    return s
+
+
+def words_of(indices) -> list:
+    words = [0, 0, 0, 0]
+    for c in indices:
+        words[int(c) >> 6] |= 1 << (int(c) & 63)
+    return words
+
+
+def paged(pool, pt, pool_pages: int) -> Paged:
+    return Paged(_addr(pool), _addr(pt), int(pool_pages))
+
+
+class Context:
+    """One libsgdrc context on a HIP device."""
+
+    def __init__(self, device: int = 0):
+        h = ctypes.c_void_p()
+        _check(lib().sgdrc_init(int(device), ctypes.byref(h)))
+        self.handle = h
+        self.device = device
+
+    @property
+    def num_cus(self) -> int:
+        n = lib().sgdrc_num_cus(self.handle)
+        if n < 0:
+            _check(n)
+        return n
+
+    def cu_key(self, cu: int) -> int:
+        k = ctypes.c_uint32()
+        _check(lib().sgdrc_cu_key(self.handle, int(cu), ctypes.byref(k)))
+        return k.value
+
+    def device_error(self) -> int:
+        f = ctypes.c_uint32()
+        _check(lib().sgdrc_device_error(self.handle, ctypes.byref(f)))
+        return f.value
+
+    def set_worklog(self, cu_tiles=None, tile_visits=None) -> None:
+        cap = 0 if tile_visits is None else int(tile_visits.numel())
+        _check(lib().sgdrc_set_worklog(self.handle, _addr(cu_tiles), _addr(tile_visits), cap))
+
+    def last_tiles(self, stream=None) -> int:
+        t = ctypes.c_uint64()
+        _check(lib().sgdrc_last_tiles(self.handle, _stream(stream), ctypes.byref(t)))
+        return t.value
+
+    def close(self) -> None:
+        if self.handle is not None and self.handle.value:
+            _check(lib().sgdrc_destroy(self.handle))
+        self.handle = None
+
+
+def _h(ctx):
+    return ctx.handle if isinstance(ctx, Context) else ctx
+
+
+def set_cu_mask(ctx, stream, cus) -> None:
+    """cus: iterable of logical CU indices, or None for all CUs."""
+    m = None if cus is None else ctypes.byref(make_set(words_of(cus), CuMask))
+    _check(lib().set_cu_mask(_h(ctx), _stream(stream), m))
+
+
+def colour_classify(ctx, masks, addrs, colours, hist=None, stream=None) -> None:
+    _check(lib().colour_classify(_h(ctx), ctypes.byref(make_hash(masks)), _addr(addrs),
+                                 int(addrs.numel()), _addr(colours), _addr(hist),
+                                 _stream(stream)))
+
+
+def colour_alloc_pagetable(ctx, masks, addr_origin: int, page_shift: int, pool_pages: int,
+                           colours, n_needed: int, pt, stream=None) -> int:
+    """Returns n_found; raises SgdrcError (code ENOMEM, .n_found) on shortfall."""
+    found = ctypes.c_uint64()
+    rc = lib().colour_alloc_pagetable(_h(ctx), ctypes.byref(make_hash(masks)), int(addr_origin),
+                                      int(page_shift), int(pool_pages),
+                                      ctypes.byref(make_set(words_of(colours))), int(n_needed),
+                                      _addr(pt), ctypes.byref(found), _stream(stream))
+    _check(rc, found.value)
+    return found.value
+
+
+def bimodal_relayout(ctx, dst: Paged, src: Paged, n_bytes: int, page_shift: int,
+                     stream=None) -> None:
+    _check(lib().bimodal_relayout(_h(ctx), ctypes.byref(dst), ctypes.byref(src), int(n_bytes),
+                                  int(page_shift), _stream(stream)))
+
+
+def colored_stream(ctx, a: Paged, b: Paged, c: Paged, s: float, n_elems: int, page_shift: int,
+                   stream=None) -> None:
+    _check(lib().colored_stream(_h(ctx), ctypes.byref(a), ctypes.byref(b), ctypes.byref(c),
+                                float(s), int(n_elems), int(page_shift), _stream(stream)))
+
+
+def colored_gemv(ctx, w: Paged, w_dtype: int, M: int, K: int, x, x_dtype: int, batch: int, y,
+                 page_shift: int, stream=None) -> None:
+    _check(lib().colored_gemv(_h(ctx), ctypes.byref(w), int(w_dtype), int(M), int(K), _addr(x),
+                              int(x_dtype), int(batch), _addr(y), int(page_shift),
+                              _stream(stream)))

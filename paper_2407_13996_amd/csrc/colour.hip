@@ -1,0 +1,384 @@
+// Batched XOR-hash colouring and the ordered page-table build.
+//
+// Colour bit k of an address is the parity of (address & M_k).  The
+// classify kernel streams 8-byte addresses with 16-byte non-temporal loads
+// (16 addresses per lane per step) and writes one colour byte each, packed
+// 16 to a lane store.  The page-table build is an ordered stream compaction
+// over the pool's page addresses: a counting pass, a scan of per-workgroup
+// counts, and an emitting pass that places each qualifying page with a
+// wavefront ballot and a masked bit count, so the table comes out in
+// ascending page order regardless of scheduling.
+#include <cstring>
+#include <mutex>
+
+#include "host_common.hpp"
+
+namespace sgdrc {
+
+struct HashArgs {
+    uint32_t lo[SGDRC_MAX_MASKS];  // mask bits 0..31
+    uint32_t hi[SGDRC_MAX_MASKS];  // mask bits 32..47
+};
+
+struct SetArgs {
+    uint32_t w[8];  // 256-bit colour set
+};
+
+template <int K>
+__device__ __forceinline__ uint32_t colour_of(uint32_t lo, uint32_t hi, const HashArgs &h)
+{
+    uint32_t c = 0;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        uint32_t ones = __builtin_popcount(lo & h.lo[k]) + __builtin_popcount(hi & h.hi[k]);
+        c |= (ones & 1u) << k;
+    }
+    return c;
+}
+
+constexpr int kClsThreads = 256;
+constexpr int kClsPerLane = 16;  // addresses per lane per step (128 bytes)
+constexpr int kClsSteps = 4;
+constexpr uint64_t kClsTile = (uint64_t)kClsThreads * kClsPerLane * kClsSteps;
+
+template <int K, bool HIST>
+__global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__restrict__ addrs,
+                                                          uint64_t n, uint8_t *__restrict__ colours,
+                                                          HashArgs h, uint64_t *hist_acc,
+                                                          uint64_t *hist_out, uint32_t n_tiles,
+                                                          Gate g)
+{
+    __shared__ uint32_t s_hist[HIST ? 256 : 1];
+    if (HIST) {
+        s_hist[threadIdx.x] = 0;
+        __syncthreads();
+    }
+    auto body = [&](uint32_t t, uint32_t) {
+        const uint64_t tile0 = (uint64_t)t * kClsTile;
+#pragma unroll 1
+        for (int s = 0; s < kClsSteps; ++s) {
+            const uint64_t i0 = tile0 + ((uint64_t)s * kClsThreads + threadIdx.x) * kClsPerLane;
+            if (i0 + kClsPerLane <= n) {
+                u32x4 v[kClsPerLane / 2];
+#pragma unroll
+                for (int j = 0; j < kClsPerLane / 2; ++j)
+                    v[j] = load_nt(addrs + i0 + 2 * j);
+                uint32_t packed[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+                for (int j = 0; j < kClsPerLane / 2; ++j) {
+                    uint32_t c0 = colour_of<K>(v[j].x, v[j].y, h);
+                    uint32_t c1 = colour_of<K>(v[j].z, v[j].w, h);
+                    packed[j >> 1] |= (c0 | (c1 << 8)) << ((j & 1) * 16);
+                    if (HIST) {
+                        atomicAdd(&s_hist[c0], 1u);
+                        atomicAdd(&s_hist[c1], 1u);
+                    }
+                }
+                u32x4 out = {packed[0], packed[1], packed[2], packed[3]};
+                store_nt(colours + i0, out);
+            } else if (i0 < n) {
+                for (uint64_t i = i0; i < n; ++i) {
+                    uint64_t a = addrs[i];
+                    uint32_t c = colour_of<K>((uint32_t)a, (uint32_t)(a >> 32), h);
+                    colours[i] = (uint8_t)c;
+                    if (HIST)
+                        atomicAdd(&s_hist[c], 1u);
+                }
+            }
+        }
+    };
+    auto flush = [&]() {
+        if (HIST) {
+            __syncthreads();
+            const uint32_t bins = 1u << K;
+            if (threadIdx.x < bins) {
+                uint32_t v = s_hist[threadIdx.x];
+                if (v)
+                    __hip_atomic_fetch_add(&hist_acc[threadIdx.x], (uint64_t)v, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+                s_hist[threadIdx.x] = 0;
+            }
+            __threadfence();
+        }
+    };
+    auto epilogue = [&]() {
+        if (HIST) {
+            const uint32_t bins = 1u << K;
+            if (threadIdx.x < bins) {
+                uint64_t v = __hip_atomic_load(&hist_acc[threadIdx.x], __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+                hist_out[threadIdx.x] = v;
+                __hip_atomic_store(&hist_acc[threadIdx.x], (uint64_t)0, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+    };
+    gated_tile_loop(g, n_tiles, body, flush, epilogue);
+}
+
+constexpr int kPtThreads = 256;
+constexpr int kPtIters = 16;
+constexpr uint64_t kPtBlockPages = (uint64_t)kPtThreads * kPtIters;
+
+// One pass of the ordered compaction.  Workgroup b covers pages
+// [b*4096, (b+1)*4096) in 16 rounds of 256 consecutive pages.  The counting
+// pass writes the number of qualifying pages per workgroup; the emitting
+// pass writes each qualifying page at its rank among all qualifying pages.
+template <int K, bool EMIT>
+__global__ __launch_bounds__(kPtThreads) void k_pt_pass(HashArgs h, uint64_t origin, uint32_t shift,
+                                                        uint64_t pool_pages, SetArgs set,
+                                                        uint32_t *block_counts,
+                                                        const uint64_t *block_offsets,
+                                                        uint32_t *pt, uint64_t n_needed)
+{
+    __shared__ uint32_t s_set[8];
+    __shared__ uint32_t s_wave[kPtThreads / 64];
+    if (threadIdx.x < 8)
+        s_set[threadIdx.x] = set.w[threadIdx.x];
+    __syncthreads();
+    const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63u;
+    const uint64_t base = (uint64_t)blockIdx.x * kPtBlockPages;
+    uint64_t running = EMIT ? block_offsets[blockIdx.x] : 0;
+    uint32_t total = 0;
+    for (int it = 0; it < kPtIters; ++it) {
+        const uint64_t page = base + (uint64_t)it * kPtThreads + threadIdx.x;
+        bool q = false;
+        if (page < pool_pages) {
+            const uint64_t a = origin + (page << shift);
+            const uint32_t c = colour_of<K>((uint32_t)a, (uint32_t)(a >> 32), h);
+            q = ((s_set[c >> 5] >> (c & 31u)) & 1u) != 0u;
+        }
+        const uint64_t bal = __ballot(q);
+        const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+            (uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+        if (lane == 0)
+            s_wave[wave] = (uint32_t)__popcll(bal);
+        __syncthreads();
+        uint32_t before = 0, sum = 0;
+#pragma unroll
+        for (uint32_t w = 0; w < kPtThreads / 64; ++w) {
+            const uint32_t cw = s_wave[w];
+            before += w < wave ? cw : 0u;
+            sum += cw;
+        }
+        if (EMIT && q) {
+            const uint64_t pos = running + before + below;
+            if (pos < n_needed)
+                pt[pos] = (uint32_t)page;
+        }
+        running += sum;
+        total += sum;
+        __syncthreads();
+    }
+    if (!EMIT && threadIdx.x == 0)
+        block_counts[blockIdx.x] = total;
+}
+
+// Exclusive scan of the per-workgroup counts (one workgroup, chunks of 1024).
+__global__ __launch_bounds__(1024) void k_pt_scan(const uint32_t *counts, uint64_t *offsets,
+                                                  uint64_t nblocks, uint64_t *total)
+{
+    __shared__ uint64_t s[1024];
+    uint64_t carry = 0;
+    for (uint64_t base = 0; base < nblocks; base += 1024) {
+        const uint64_t i = base + threadIdx.x;
+        const uint64_t v = i < nblocks ? counts[i] : 0;
+        s[threadIdx.x] = v;
+        __syncthreads();
+        for (uint32_t off = 1; off < 1024; off <<= 1) {
+            uint64_t t = threadIdx.x >= off ? s[threadIdx.x - off] : 0;
+            __syncthreads();
+            s[threadIdx.x] += t;
+            __syncthreads();
+        }
+        if (i < nblocks)
+            offsets[i] = carry + s[threadIdx.x] - v;
+        carry += s[1023];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0)
+        *total = carry;
+}
+
+static HashArgs hash_args(const sgdrc_hash *h)
+{
+    HashArgs a;
+    std::memset(&a, 0, sizeof a);
+    for (uint32_t k = 0; k < h->n_masks; ++k) {
+        a.lo[k] = (uint32_t)h->masks[k];
+        a.hi[k] = (uint32_t)(h->masks[k] >> 32);
+    }
+    return a;
+}
+
+template <int K>
+static int launch_classify(Ctx *c, const HashArgs &h, const uint64_t *d_addrs, uint64_t n,
+                           uint8_t *d_colours, uint64_t *d_hist, void *stream)
+{
+    const uint64_t n_tiles = (n + kClsTile - 1) / kClsTile;
+    if (n_tiles >= (1ull << 31))
+        return set_error(SGDRC_EINVAL, "n too large");
+    Gate g;
+    int allowed = 0;
+    int rc = make_gate(c, stream, n_tiles, &g, &allowed);
+    if (rc)
+        return rc;
+    uint64_t *acc = c->d_hist_acc + (size_t)(g.q - c->d_queues) * kHistBins;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (d_hist) {
+        static const int occ = occupancy(k_classify<K, true>, kClsThreads);
+        uint32_t grid = gated_grid(c, occ, n_tiles, allowed);
+        hipLaunchKernelGGL((k_classify<K, true>), dim3(grid), dim3(kClsThreads), 0, s, d_addrs, n,
+                           d_colours, h, acc, d_hist, (uint32_t)n_tiles, g);
+    } else {
+        static const int occ = occupancy(k_classify<K, false>, kClsThreads);
+        uint32_t grid = gated_grid(c, occ, n_tiles, allowed);
+        hipLaunchKernelGGL((k_classify<K, false>), dim3(grid), dim3(kClsThreads), 0, s, d_addrs,
+                           n, d_colours, h, acc, d_hist, (uint32_t)n_tiles, g);
+    }
+    SGDRC_HIP(hipGetLastError());
+    return SGDRC_OK;
+}
+
+template <int K>
+static int launch_pagetable(Ctx *c, const HashArgs &h, uint64_t origin, uint32_t shift,
+                            uint64_t pool_pages, const SetArgs &set, uint64_t n_needed,
+                            uint32_t *d_pt, uint64_t nblocks, uint32_t *d_counts,
+                            uint64_t *d_offsets, uint64_t *d_total, hipStream_t s)
+{
+    hipLaunchKernelGGL((k_pt_pass<K, false>), dim3((uint32_t)nblocks), dim3(kPtThreads), 0, s, h,
+                       origin, shift, pool_pages, set, d_counts, (const uint64_t *)nullptr,
+                       (uint32_t *)nullptr, (uint64_t)0);
+    SGDRC_HIP(hipGetLastError());
+    hipLaunchKernelGGL(k_pt_scan, dim3(1), dim3(1024), 0, s, (const uint32_t *)d_counts, d_offsets,
+                       nblocks, d_total);
+    SGDRC_HIP(hipGetLastError());
+    if (n_needed > 0) {
+        hipLaunchKernelGGL((k_pt_pass<K, true>), dim3((uint32_t)nblocks), dim3(kPtThreads), 0, s,
+                           h, origin, shift, pool_pages, set, d_counts,
+                           (const uint64_t *)d_offsets, d_pt, n_needed);
+        SGDRC_HIP(hipGetLastError());
+    }
+    return SGDRC_OK;
+}
+
+static std::mutex g_pt_mu;  // page-table scratch is per context; builds are serialised
+
+}  // namespace sgdrc
+
+using namespace sgdrc;
+
+#define SGDRC_DISPATCH_K(nm, fn, ...)                         \
+    switch (nm) {                                             \
+    case 1: rc = fn<1>(__VA_ARGS__); break;                   \
+    case 2: rc = fn<2>(__VA_ARGS__); break;                   \
+    case 3: rc = fn<3>(__VA_ARGS__); break;                   \
+    case 4: rc = fn<4>(__VA_ARGS__); break;                   \
+    case 5: rc = fn<5>(__VA_ARGS__); break;                   \
+    case 6: rc = fn<6>(__VA_ARGS__); break;                   \
+    case 7: rc = fn<7>(__VA_ARGS__); break;                   \
+    default: rc = fn<8>(__VA_ARGS__); break;                  \
+    }
+
+extern "C" {
+
+int colour_classify(sgdrc_ctx *ctx, const sgdrc_hash *hash, const uint64_t *d_addrs, uint64_t n,
+                    uint8_t *d_colours, uint64_t *d_hist, void *stream)
+{
+    clear_error();
+    int rc = check_hash(hash);
+    if (rc)
+        return rc;
+    if (n > 0 && (!d_addrs || !d_colours))
+        return set_error(SGDRC_EINVAL, "NULL address or colour buffer");
+    if ((reinterpret_cast<uintptr_t>(d_addrs) & 15u) || (reinterpret_cast<uintptr_t>(d_colours) & 15u))
+        return set_error(SGDRC_EINVAL, "address and colour buffers must be 16-byte aligned");
+    if (reinterpret_cast<uintptr_t>(d_hist) & 7u)
+        return set_error(SGDRC_EINVAL, "histogram not 8-byte aligned");
+    Ctx *c = nullptr;
+    rc = check_ctx(ctx, &c);
+    if (rc)
+        return rc;
+    HashArgs h = hash_args(hash);
+    SGDRC_DISPATCH_K(hash->n_masks, launch_classify, c, h, d_addrs, n, d_colours, d_hist, stream);
+    return rc;
+}
+
+int colour_alloc_pagetable(sgdrc_ctx *ctx, const sgdrc_hash *hash, uint64_t addr_origin,
+                           uint32_t page_shift, uint64_t pool_pages, const sgdrc_colour_set *set,
+                           uint64_t n_needed, uint32_t *d_pt, uint64_t *n_found, void *stream)
+{
+    clear_error();
+    int rc = check_hash(hash);
+    if (rc)
+        return rc;
+    rc = check_shift(page_shift);
+    if (rc)
+        return rc;
+    if (!set || !n_found)
+        return set_error(SGDRC_EINVAL, "NULL colour set or n_found");
+    if (addr_origin & ((1ull << page_shift) - 1ull))
+        return set_error(SGDRC_EINVAL, "addr_origin not aligned to the page size");
+    if (pool_pages == 0 || pool_pages > (1ull << 32))
+        return set_error(SGDRC_EINVAL, "pool_pages must be in 1..2^32");
+    if (addr_origin >= (1ull << 48) || pool_pages > (((1ull << 48) - addr_origin) >> page_shift))
+        return set_error(SGDRC_EINVAL, "pool extends beyond the 48-bit address space");
+    if (n_needed > pool_pages)
+        return set_error(SGDRC_EINVAL, "n_needed exceeds pool_pages");
+    if (n_needed > 0 && (!d_pt || (reinterpret_cast<uintptr_t>(d_pt) & 3u)))
+        return set_error(SGDRC_EINVAL, "page table pointer NULL or not 4-byte aligned");
+    const uint32_t colours = 1u << hash->n_masks;
+    bool any = false;
+    for (uint32_t cc = 0; cc < 256; ++cc) {
+        if ((set->bits[cc >> 6] >> (cc & 63)) & 1ull) {
+            if (cc >= colours)
+                return set_error(SGDRC_EINVAL, "colour %u in set, hash has %u colours", cc, colours);
+            any = true;
+        }
+    }
+    if (!any)
+        return set_error(SGDRC_EINVAL, "empty colour set");
+    Ctx *c = nullptr;
+    rc = check_ctx(ctx, &c);
+    if (rc)
+        return rc;
+
+    std::lock_guard<std::mutex> lock(g_pt_mu);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const uint64_t nblocks = (pool_pages + kPtBlockPages - 1) / kPtBlockPages;
+    const size_t need = 256 + nblocks * sizeof(uint64_t) + nblocks * sizeof(uint32_t);
+    if (c->scratch_bytes < need) {
+        SGDRC_HIP(hipDeviceSynchronize());
+        if (c->d_scratch)
+            SGDRC_HIP(hipFree(c->d_scratch));
+        c->d_scratch = nullptr;
+        c->scratch_bytes = 0;
+        size_t bytes = need < (1u << 20) ? (1u << 20) : need;
+        SGDRC_HIP(hipMalloc(&c->d_scratch, bytes));
+        c->scratch_bytes = bytes;
+    }
+    uint8_t *base = static_cast<uint8_t *>(c->d_scratch);
+    uint64_t *d_total = reinterpret_cast<uint64_t *>(base);
+    uint64_t *d_offsets = reinterpret_cast<uint64_t *>(base + 256);
+    uint32_t *d_counts = reinterpret_cast<uint32_t *>(base + 256 + nblocks * sizeof(uint64_t));
+
+    SetArgs sa;
+    for (int i = 0; i < 4; ++i) {
+        sa.w[2 * i] = (uint32_t)set->bits[i];
+        sa.w[2 * i + 1] = (uint32_t)(set->bits[i] >> 32);
+    }
+    HashArgs h = hash_args(hash);
+    SGDRC_DISPATCH_K(hash->n_masks, launch_pagetable, c, h, addr_origin, page_shift, pool_pages,
+                     sa, n_needed, d_pt, nblocks, d_counts, d_offsets, d_total, s);
+    if (rc)
+        return rc;
+    SGDRC_HIP(hipMemcpyAsync(c->h_pinned, d_total, sizeof(uint64_t), hipMemcpyDeviceToHost, s));
+    SGDRC_HIP(hipStreamSynchronize(s));
+    *n_found = c->h_pinned[0];
+    if (*n_found < n_needed)
+        return set_error(SGDRC_ENOMEM, "pool holds %llu pages of the set, %llu needed",
+                         (unsigned long long)*n_found, (unsigned long long)n_needed);
+    return SGDRC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,369 @@
+// Context management, CU-topology probe, per-stream CU masks and errors.
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "host_common.hpp"
+
+namespace sgdrc {
+
+static thread_local std::string t_error;
+
+int set_error(int code, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    t_error = buf;
+    return code;
+}
+
+void clear_error() { t_error.clear(); }
+
+int hip_fail(hipError_t e, const char *what)
+{
+    return set_error(SGDRC_EHIP, "%s failed: %s", what, hipGetErrorString(e));
+}
+
+int check_ctx(const sgdrc_ctx *ctx, Ctx **out)
+{
+    if (!ctx)
+        return set_error(SGDRC_ENODEV, "context is NULL");
+    Ctx *c = reinterpret_cast<Ctx *>(const_cast<sgdrc_ctx *>(ctx));
+    if (c->magic != kCtxMagic)
+        return set_error(SGDRC_ENODEV, "not an initialised sgdrc context");
+    int dev = -1;
+    SGDRC_HIP(hipGetDevice(&dev));
+    if (dev != c->device)
+        return set_error(SGDRC_EINVAL, "current device %d is not the context's device %d", dev,
+                         c->device);
+    *out = c;
+    return SGDRC_OK;
+}
+
+int popcount_mask(const sgdrc_cu_mask &m)
+{
+    int n = 0;
+    for (int i = 0; i < 4; ++i)
+        n += __builtin_popcountll(m.bits[i]);
+    return n;
+}
+
+int stream_state(Ctx *c, void *stream, StreamState **out)
+{
+    std::lock_guard<std::mutex> lock(c->mu);
+    auto it = c->streams.find(stream);
+    if (it == c->streams.end()) {
+        if (c->next_slot >= kMaxStreams)
+            return set_error(SGDRC_EINVAL, "more than %d streams used with one context",
+                             kMaxStreams);
+        StreamState st;
+        st.slot = c->next_slot++;
+        st.mask = c->all_cus;
+        it = c->streams.emplace(stream, st).first;
+    }
+    *out = &it->second;
+    return SGDRC_OK;
+}
+
+int make_gate(Ctx *c, void *stream, uint64_t n_tiles, Gate *g, int *allowed_cus)
+{
+    StreamState *st = nullptr;
+    int rc = stream_state(c, stream, &st);
+    if (rc)
+        return rc;
+    std::lock_guard<std::mutex> lock(c->mu);
+    std::memcpy(g->mask, st->mask.bits, sizeof g->mask);
+    g->lut = c->d_lut;
+    g->q = c->d_queues + st->slot;
+    g->err = c->d_err;
+    g->log_cu = c->log_cu;
+    g->log_tile = c->log_tile;
+    g->log_cap = c->log_cap;
+    st->last_tiles = n_tiles;
+    *allowed_cus = popcount_mask(st->mask);
+    return SGDRC_OK;
+}
+
+uint32_t gated_grid(const Ctx *c, int blocks_per_cu, uint64_t n_tiles, int allowed_cus)
+{
+    uint64_t cap = (uint64_t)blocks_per_cu * (uint64_t)c->num_cus;
+    uint64_t want = (n_tiles * (uint64_t)c->num_cus + (uint64_t)allowed_cus - 1) /
+                    (uint64_t)std::max(allowed_cus, 1);
+    want = std::max<uint64_t>(want, (uint64_t)c->num_cus);
+    return (uint32_t)std::min(want, cap);
+}
+
+int check_hash(const sgdrc_hash *h)
+{
+    if (!h)
+        return set_error(SGDRC_EINVAL, "hash is NULL");
+    if (h->n_masks < 1 || h->n_masks > SGDRC_MAX_MASKS)
+        return set_error(SGDRC_EINVAL, "n_masks %u outside 1..%d", h->n_masks, SGDRC_MAX_MASKS);
+    if (h->reserved != 0)
+        return set_error(SGDRC_EINVAL, "hash.reserved must be 0");
+    for (uint32_t k = 0; k < h->n_masks; ++k)
+        if (h->masks[k] >> 48)
+            return set_error(SGDRC_EINVAL, "mask %u selects address bits above 47", k);
+    return SGDRC_OK;
+}
+
+int check_shift(uint32_t page_shift)
+{
+    if (page_shift < SGDRC_MIN_PAGE_SHIFT || page_shift > SGDRC_MAX_PAGE_SHIFT)
+        return set_error(SGDRC_EINVAL, "page_shift %u outside [%d, %d]", page_shift,
+                         SGDRC_MIN_PAGE_SHIFT, SGDRC_MAX_PAGE_SHIFT);
+    return SGDRC_OK;
+}
+
+int check_paged(const sgdrc_paged *p, const char *name)
+{
+    if (!p)
+        return set_error(SGDRC_EINVAL, "%s is NULL", name);
+    if (!p->pool || !p->pt)
+        return set_error(SGDRC_EINVAL, "%s: NULL pool or page table", name);
+    if (reinterpret_cast<uintptr_t>(p->pool) & 255u)
+        return set_error(SGDRC_EINVAL, "%s: pool not 256-byte aligned", name);
+    if (reinterpret_cast<uintptr_t>(p->pt) & 3u)
+        return set_error(SGDRC_EINVAL, "%s: page table not 4-byte aligned", name);
+    if (p->pool_pages == 0)
+        return set_error(SGDRC_EINVAL, "%s: pool_pages is 0", name);
+    return SGDRC_OK;
+}
+
+// Each workgroup records the hardware key of the CU it runs on; the sleep
+// keeps workgroups resident long enough for the dispatcher to spread the
+// grid over every CU.
+__global__ void k_cu_probe(uint32_t *keys, uint32_t n, uint32_t spins)
+{
+    uint32_t key = hw_key();
+    for (uint32_t i = 0; i < spins; ++i)
+        __builtin_amdgcn_s_sleep(8);
+    if (threadIdx.x == 0 && blockIdx.x < n)
+        keys[blockIdx.x] = key;
+}
+
+static int probe_topology(Ctx *c, int expected)
+{
+    std::vector<uint32_t> uniq;
+    for (int attempt = 0; attempt < 3; ++attempt) {
+        const uint32_t n = (uint32_t)expected * (48u << attempt);
+        uint32_t *d_keys = nullptr;
+        SGDRC_HIP(hipMalloc(&d_keys, n * sizeof(uint32_t)));
+        hipLaunchKernelGGL(k_cu_probe, dim3(n), dim3(64), 0, 0, d_keys, n, 32u << attempt);
+        hipError_t e = hipGetLastError();
+        if (e == hipSuccess)
+            e = hipDeviceSynchronize();
+        std::vector<uint32_t> keys(n);
+        if (e == hipSuccess)
+            e = hipMemcpy(keys.data(), d_keys, n * sizeof(uint32_t), hipMemcpyDeviceToHost);
+        (void)hipFree(d_keys);
+        if (e != hipSuccess)
+            return hip_fail(e, "CU probe");
+        std::sort(keys.begin(), keys.end());
+        keys.erase(std::unique(keys.begin(), keys.end()), keys.end());
+        uniq = keys;
+        if ((int)uniq.size() >= expected)
+            break;
+    }
+    if ((int)uniq.size() != expected)
+        return set_error(SGDRC_ENODEV, "CU probe found %zu distinct CUs, device reports %d",
+                         uniq.size(), expected);
+    if (expected > SGDRC_MAX_CUS)
+        return set_error(SGDRC_ENODEV, "device has %d CUs, more than %d", expected,
+                         SGDRC_MAX_CUS);
+    std::vector<uint16_t> lut(kLutSize, kLutNone);
+    for (int i = 0; i < expected; ++i) {
+        if (uniq[i] >= (uint32_t)kLutSize)
+            return set_error(SGDRC_ENODEV, "CU key 0x%x out of range", uniq[i]);
+        c->keys[i] = uniq[i];
+        lut[uniq[i]] = (uint16_t)i;
+    }
+    c->num_cus = expected;
+    std::memset(&c->all_cus, 0, sizeof c->all_cus);
+    for (int i = 0; i < expected; ++i)
+        c->all_cus.bits[i >> 6] |= 1ull << (i & 63);
+    SGDRC_HIP(hipMemcpy(c->d_lut, lut.data(), kLutSize * sizeof(uint16_t), hipMemcpyHostToDevice));
+    return SGDRC_OK;
+}
+
+static void free_ctx(Ctx *c)
+{
+    if (c->d_lut) (void)hipFree(c->d_lut);
+    if (c->d_queues) (void)hipFree(c->d_queues);
+    if (c->d_hist_acc) (void)hipFree(c->d_hist_acc);
+    if (c->d_err) (void)hipFree(c->d_err);
+    if (c->d_scratch) (void)hipFree(c->d_scratch);
+    if (c->h_pinned) (void)hipHostFree(c->h_pinned);
+    c->magic = 0;
+    delete c;
+}
+
+}  // namespace sgdrc
+
+using namespace sgdrc;
+
+extern "C" {
+
+int sgdrc_init(int device, sgdrc_ctx **out)
+{
+    clear_error();
+    if (!out)
+        return set_error(SGDRC_EINVAL, "out is NULL");
+    *out = nullptr;
+    int count = 0;
+    if (hipGetDeviceCount(&count) != hipSuccess || count <= 0)
+        return set_error(SGDRC_ENODEV, "no HIP device");
+    if (device < 0 || device >= count)
+        return set_error(SGDRC_ENODEV, "device %d outside 0..%d", device, count - 1);
+    hipDeviceProp_t prop;
+    SGDRC_HIP(hipGetDeviceProperties(&prop, device));
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return set_error(SGDRC_ENODEV, "device %d is %s, not gfx950", device, prop.gcnArchName);
+    SGDRC_HIP(hipSetDevice(device));
+
+    Ctx *c = new (std::nothrow) Ctx();
+    if (!c)
+        return set_error(SGDRC_EHIP, "out of host memory");
+    c->device = device;
+    int rc = SGDRC_OK;
+    hipError_t e = hipSuccess;
+#define TRY(call)                                   \
+    do {                                            \
+        e = (call);                                 \
+        if (e != hipSuccess) {                      \
+            rc = hip_fail(e, #call);                \
+            free_ctx(c);                            \
+            return rc;                              \
+        }                                           \
+    } while (0)
+    TRY(hipMalloc(&c->d_lut, kLutSize * sizeof(uint16_t)));
+    TRY(hipMalloc(&c->d_queues, kMaxStreams * sizeof(TileQueue)));
+    TRY(hipMemset(c->d_queues, 0, kMaxStreams * sizeof(TileQueue)));
+    TRY(hipMalloc(&c->d_hist_acc, (size_t)kMaxStreams * kHistBins * sizeof(uint64_t)));
+    TRY(hipMemset(c->d_hist_acc, 0, (size_t)kMaxStreams * kHistBins * sizeof(uint64_t)));
+    TRY(hipMalloc(&c->d_err, sizeof(uint32_t)));
+    TRY(hipMemset(c->d_err, 0, sizeof(uint32_t)));
+    TRY(hipHostMalloc(&c->h_pinned, 8 * sizeof(uint64_t), hipHostMallocDefault));
+#undef TRY
+    rc = probe_topology(c, prop.multiProcessorCount);
+    if (rc) {
+        free_ctx(c);
+        return rc;
+    }
+    *out = reinterpret_cast<sgdrc_ctx *>(c);
+    return SGDRC_OK;
+}
+
+int sgdrc_destroy(sgdrc_ctx *ctx)
+{
+    clear_error();
+    Ctx *c = nullptr;
+    int rc = check_ctx(ctx, &c);
+    if (rc)
+        return rc;
+    SGDRC_HIP(hipDeviceSynchronize());
+    free_ctx(c);
+    return SGDRC_OK;
+}
+
+int sgdrc_num_cus(const sgdrc_ctx *ctx)
+{
+    if (!ctx)
+        return set_error(SGDRC_ENODEV, "context is NULL");
+    const Ctx *c = reinterpret_cast<const Ctx *>(ctx);
+    if (c->magic != kCtxMagic)
+        return set_error(SGDRC_ENODEV, "not an initialised sgdrc context");
+    return c->num_cus;
+}
+
+int sgdrc_cu_key(const sgdrc_ctx *ctx, uint32_t cu, uint32_t *key)
+{
+    if (!key)
+        return set_error(SGDRC_EINVAL, "key is NULL");
+    int n = sgdrc_num_cus(ctx);
+    if (n < 0)
+        return n;
+    if (cu >= (uint32_t)n)
+        return set_error(SGDRC_EINVAL, "cu %u >= %d", cu, n);
+    *key = reinterpret_cast<const Ctx *>(ctx)->keys[cu];
+    return SGDRC_OK;
+}
+
+const char *sgdrc_last_error(void) { return t_error.c_str(); }
+
+int sgdrc_device_error(sgdrc_ctx *ctx, uint32_t *flags)
+{
+    clear_error();
+    if (!flags)
+        return set_error(SGDRC_EINVAL, "flags is NULL");
+    Ctx *c = nullptr;
+    int rc = check_ctx(ctx, &c);
+    if (rc)
+        return rc;
+    SGDRC_HIP(hipDeviceSynchronize());
+    SGDRC_HIP(hipMemcpy(flags, c->d_err, sizeof(uint32_t), hipMemcpyDeviceToHost));
+    SGDRC_HIP(hipMemset(c->d_err, 0, sizeof(uint32_t)));
+    SGDRC_HIP(hipDeviceSynchronize());
+    return SGDRC_OK;
+}
+
+int sgdrc_set_worklog(sgdrc_ctx *ctx, uint32_t *d_cu_tiles, uint32_t *d_tile_visits,
+                      uint64_t tile_cap)
+{
+    clear_error();
+    Ctx *c = nullptr;
+    int rc = check_ctx(ctx, &c);
+    if (rc)
+        return rc;
+    std::lock_guard<std::mutex> lock(c->mu);
+    c->log_cu = d_cu_tiles;
+    c->log_tile = d_tile_visits;
+    c->log_cap = d_tile_visits ? tile_cap : 0;
+    return SGDRC_OK;
+}
+
+int sgdrc_last_tiles(sgdrc_ctx *ctx, void *stream, uint64_t *tiles)
+{
+    clear_error();
+    if (!tiles)
+        return set_error(SGDRC_EINVAL, "tiles is NULL");
+    Ctx *c = nullptr;
+    int rc = check_ctx(ctx, &c);
+    if (rc)
+        return rc;
+    std::lock_guard<std::mutex> lock(c->mu);
+    auto it = c->streams.find(stream);
+    *tiles = it == c->streams.end() ? 0 : it->second.last_tiles;
+    return SGDRC_OK;
+}
+
+int set_cu_mask(sgdrc_ctx *ctx, void *stream, const sgdrc_cu_mask *mask)
+{
+    clear_error();
+    if (mask && popcount_mask(*mask) == 0)
+        return set_error(SGDRC_EINVAL, "empty CU mask");
+    Ctx *c = nullptr;
+    int rc = check_ctx(ctx, &c);
+    if (rc)
+        return rc;
+    if (mask) {
+        for (int i = c->num_cus; i < SGDRC_MAX_CUS; ++i)
+            if ((mask->bits[i >> 6] >> (i & 63)) & 1ull)
+                return set_error(SGDRC_EINVAL, "CU mask names CU %d, device has %d", i,
+                                 c->num_cus);
+    }
+    StreamState *st = nullptr;
+    rc = stream_state(c, stream, &st);
+    if (rc)
+        return rc;
+    std::lock_guard<std::mutex> lock(c->mu);
+    st->mask = mask ? *mask : c->all_cus;
+    return SGDRC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,412 @@
+// Colour-restricted GEMV / small-batch GEMM: y[b][m] = sum_k W[m][k] x[b][k].
+//
+// W is row-major [M x K] in a paged pool and is streamed once from HBM with
+// 16-byte non-temporal loads; x and y are small and contiguous.  A tile is a
+// block of whole rows, so each output is produced by exactly one workgroup
+// in a fixed summation order: per-lane fp32 FMA chains over that lane's
+// 16-byte slices of the row, a butterfly over the 64 lanes, then the four
+// waves' partials added in wave order.  The result therefore depends only on
+// (M, K, batch, dtypes) and not on which CUs ran the tiles.
+//
+// Page translation: the page-table entries covering a tile's rows are staged
+// in LDS at the start of the tile (at most kPtCap; beyond that each lane
+// reads the table directly), and every 16-byte slice is mapped with one LDS
+// read plus a shift and an add.
+//
+// Batches 5..8 with bf16 x bf16 or f16 x f16 operands use the gfx950
+// 16x16x32 MFMA: a 16-row block of W is the A operand, x (batch padded to 16
+// columns with zeros) the B operand.
+#include "host_common.hpp"
+
+namespace sgdrc {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kGemvThreads = 256;
+constexpr int kGemvWaves = kGemvThreads / 64;
+constexpr int kGemvRows = 4;     // rows per tile, vector-ALU path
+constexpr int kGemvU = 2;        // 16-byte slices per lane and row in flight
+constexpr int kMfmaRows = 16;    // rows per tile, MFMA path
+constexpr int kMfmaNI = 4;       // MFMAs per wave step
+constexpr int kPtCap = 64;       // page-table entries staged per tile
+
+template <int DT> struct Dt;
+template <> struct Dt<SGDRC_F32> { static constexpr int size = 4; };
+template <> struct Dt<SGDRC_BF16> { static constexpr int size = 2; };
+template <> struct Dt<SGDRC_F16> { static constexpr int size = 2; };
+
+__device__ __forceinline__ float bf16_lo(uint32_t v) { return __uint_as_float(v << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t v) { return __uint_as_float(v & 0xFFFF0000u); }
+__device__ __forceinline__ float f16_lo(uint32_t v)
+{
+    return (float)__builtin_bit_cast(f16x2, v).x;
+}
+__device__ __forceinline__ float f16_hi(uint32_t v)
+{
+    return (float)__builtin_bit_cast(f16x2, v).y;
+}
+
+// Decode N elements of type DT held in the words w[0..] into f[0..N).
+template <int DT, int N>
+__device__ __forceinline__ void decode(const uint32_t *w, float *f)
+{
+    if (DT == SGDRC_F32) {
+#pragma unroll
+        for (int i = 0; i < N; ++i)
+            f[i] = __uint_as_float(w[i]);
+    } else if (DT == SGDRC_BF16) {
+#pragma unroll
+        for (int i = 0; i < N / 2; ++i) {
+            f[2 * i] = bf16_lo(w[i]);
+            f[2 * i + 1] = bf16_hi(w[i]);
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < N / 2; ++i) {
+            f[2 * i] = f16_lo(w[i]);
+            f[2 * i + 1] = f16_hi(w[i]);
+        }
+    }
+}
+
+// Page table entries of one tile: either staged in LDS or read directly.
+struct TilePages {
+    uint64_t p_lo;
+    uint32_t np;
+};
+
+__device__ __forceinline__ TilePages stage_pages(const uint32_t *pt, uint64_t pool_pages,
+                                                 uint64_t byte_lo, uint64_t byte_hi,
+                                                 uint32_t shift, uint32_t *s_pt, uint32_t *err)
+{
+    TilePages tp;
+    tp.p_lo = byte_lo >> shift;
+    tp.np = (uint32_t)(((byte_hi - 1) >> shift) - tp.p_lo + 1);
+    if (tp.np <= (uint32_t)kPtCap && threadIdx.x < tp.np)
+        s_pt[threadIdx.x] = checked_page(pt, tp.p_lo + threadIdx.x, pool_pages, err);
+    __syncthreads();
+    return tp;
+}
+
+__device__ __forceinline__ uint32_t page_of(const TilePages &tp, const uint32_t *s_pt,
+                                            const uint32_t *pt, uint64_t pool_pages, uint64_t j,
+                                            uint32_t *err)
+{
+    if (tp.np <= (uint32_t)kPtCap)
+        return s_pt[j - tp.p_lo];
+    return checked_page(pt, j, pool_pages, err);
+}
+
+template <int WT, int XT, int NB>
+__global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
+    const uint8_t *__restrict__ w_pool, const uint32_t *__restrict__ pt, uint64_t pool_pages,
+    uint32_t M, uint32_t K, const uint8_t *__restrict__ x, uint32_t nb, float *__restrict__ y,
+    uint32_t shift, uint32_t n_tiles, Gate g)
+{
+    constexpr int WSZ = Dt<WT>::size, XSZ = Dt<XT>::size;
+    constexpr int EPV = 16 / WSZ;                 // elements per 16-byte slice of W
+    constexpr int XW = EPV * XSZ / 4;             // 32-bit words of x per slice and batch
+    __shared__ uint32_t s_pt[kPtCap];
+    __shared__ float s_red[kGemvWaves][kGemvRows * NB];
+    const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63u;
+    const uint64_t row_bytes = (uint64_t)K * WSZ;
+    const uint32_t KV = (uint32_t)(row_bytes / 16u);
+    const uint64_t pmask = (1ull << shift) - 1ull;
+
+    auto body = [&](uint32_t t, uint32_t) {
+        const uint32_t m0 = t * kGemvRows;
+        const uint32_t m_end = min(m0 + (uint32_t)kGemvRows, M);
+        const TilePages tp = stage_pages(pt, pool_pages, (uint64_t)m0 * row_bytes,
+                                         (uint64_t)m_end * row_bytes, shift, s_pt, g.err);
+        float acc[kGemvRows][NB];
+#pragma unroll
+        for (int r = 0; r < kGemvRows; ++r)
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+                acc[r][b] = 0.0f;
+
+        for (uint32_t j = 0; (j * kGemvWaves + wave) * 64u < KV; j += kGemvU) {
+            u32x4 wv[kGemvU][kGemvRows];
+            uint32_t xv[kGemvU][NB][XW];
+#pragma unroll
+            for (int u = 0; u < kGemvU; ++u) {
+                const uint32_t kv = ((j + u) * kGemvWaves + wave) * 64u + lane;
+                const bool ok = kv < KV;
+#pragma unroll
+                for (int r = 0; r < kGemvRows; ++r) {
+                    wv[u][r] = u32x4{0u, 0u, 0u, 0u};
+                    if (ok && m0 + r < M) {
+                        const uint64_t off = (uint64_t)(m0 + r) * row_bytes + (uint64_t)kv * 16u;
+                        const uint32_t p = page_of(tp, s_pt, pt, pool_pages, off >> shift, g.err);
+                        if (p != kBadPage)
+                            wv[u][r] = load_nt(w_pool + ((uint64_t)p << shift) + (off & pmask));
+                    }
+                }
+#pragma unroll
+                for (int b = 0; b < NB; ++b) {
+#pragma unroll
+                    for (int i = 0; i < XW; ++i)
+                        xv[u][b][i] = 0u;
+                    if (ok && (uint32_t)b < nb) {
+                        const uint8_t *xp = x + ((uint64_t)b * K + (uint64_t)kv * EPV) * XSZ;
+                        if (XW == 2) {
+                            u32x2 v = *reinterpret_cast<const u32x2 *>(xp);
+                            xv[u][b][0] = v.x;
+                            xv[u][b][1] = v.y;
+                        } else {
+#pragma unroll
+                            for (int q = 0; q < XW / 4; ++q) {
+                                u32x4 v = *reinterpret_cast<const u32x4 *>(xp + 16 * q);
+                                xv[u][b][4 * q + 0] = v.x;
+                                xv[u][b][4 * q + 1] = v.y;
+                                xv[u][b][4 * q + 2] = v.z;
+                                xv[u][b][4 * q + 3] = v.w;
+                            }
+                        }
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kGemvU; ++u) {
+                float xf[NB][EPV];
+#pragma unroll
+                for (int b = 0; b < NB; ++b)
+                    decode<XT, EPV>(xv[u][b], xf[b]);
+#pragma unroll
+                for (int r = 0; r < kGemvRows; ++r) {
+                    const uint32_t ww[4] = {wv[u][r].x, wv[u][r].y, wv[u][r].z, wv[u][r].w};
+                    float wf[EPV];
+                    decode<WT, EPV>(ww, wf);
+#pragma unroll
+                    for (int e = 0; e < EPV; ++e)
+#pragma unroll
+                        for (int b = 0; b < NB; ++b)
+                            acc[r][b] = __builtin_fmaf(wf[e], xf[b][e], acc[r][b]);
+                }
+            }
+        }
+        // butterfly over the 64 lanes: every lane ends with the same sum
+#pragma unroll
+        for (int r = 0; r < kGemvRows; ++r)
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                float v = acc[r][b];
+#pragma unroll
+                for (int off = 32; off >= 1; off >>= 1)
+                    v += __shfl_xor(v, off, 64);
+                acc[r][b] = v;
+            }
+        if (lane == 0) {
+#pragma unroll
+            for (int r = 0; r < kGemvRows; ++r)
+#pragma unroll
+                for (int b = 0; b < NB; ++b)
+                    s_red[wave][r * NB + b] = acc[r][b];
+        }
+        __syncthreads();
+        if (threadIdx.x < (uint32_t)(kGemvRows * NB)) {
+            const uint32_t r = threadIdx.x / NB, b = threadIdx.x % NB;
+            float v = s_red[0][threadIdx.x];
+#pragma unroll
+            for (int w = 1; w < kGemvWaves; ++w)
+                v += s_red[w][threadIdx.x];
+            if (b < nb && m0 + r < M)
+                y[(uint64_t)b * M + m0 + r] = v;
+        }
+        __syncthreads();
+    };
+    gated_tile_loop(g, n_tiles, body, NoOp(), NoOp());
+}
+
+template <int DT>
+__device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c)
+{
+    if (DT == SGDRC_BF16)
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                       __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                      __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+}
+
+// Batch 5..8 on MFMA.  Lane l supplies row (l % 16) of the 16-row W block
+// and batch column (l % 16) of x, both for the k-slice of its lane group
+// g = l / 16; lanes of one group read the same k-slice of W and x, so the
+// k order inside the instruction matches between the operands.  The
+// accumulator holds rows 4g..4g+3 of batch column l % 16.
+template <int DT>
+__global__ __launch_bounds__(kGemvThreads) void k_gemm_mfma(
+    const uint8_t *__restrict__ w_pool, const uint32_t *__restrict__ pt, uint64_t pool_pages,
+    uint32_t M, uint32_t K, const uint8_t *__restrict__ x, uint32_t nb, float *__restrict__ y,
+    uint32_t shift, uint32_t n_tiles, Gate g)
+{
+    __shared__ uint32_t s_pt[kPtCap];
+    __shared__ f32x4 s_red[kGemvWaves][64];
+    const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63u;
+    const uint32_t rl = lane & 15u, grp = lane >> 4;
+    const uint64_t row_bytes = (uint64_t)K * 2u;
+    const uint32_t KV = (uint32_t)(row_bytes / 16u);
+    const uint64_t pmask = (1ull << shift) - 1ull;
+
+    auto body = [&](uint32_t t, uint32_t) {
+        const uint32_t m0 = t * kMfmaRows;
+        const uint32_t m_end = min(m0 + (uint32_t)kMfmaRows, M);
+        const TilePages tp = stage_pages(pt, pool_pages, (uint64_t)m0 * row_bytes,
+                                         (uint64_t)m_end * row_bytes, shift, s_pt, g.err);
+        const uint32_t row = m0 + rl;
+        const bool row_ok = row < M;
+        const bool col_ok = rl < nb;
+        f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        for (uint32_t j = 0; (j * kGemvWaves + wave) * kMfmaNI * 4u < KV; ++j) {
+            u32x4 av[kMfmaNI], bv[kMfmaNI];
+#pragma unroll
+            for (int i = 0; i < kMfmaNI; ++i) {
+                const uint32_t kv = ((j * kGemvWaves + wave) * kMfmaNI + i) * 4u + grp;
+                av[i] = u32x4{0u, 0u, 0u, 0u};
+                bv[i] = u32x4{0u, 0u, 0u, 0u};
+                if (kv < KV) {
+                    if (row_ok) {
+                        const uint64_t off = (uint64_t)row * row_bytes + (uint64_t)kv * 16u;
+                        const uint32_t p = page_of(tp, s_pt, pt, pool_pages, off >> shift, g.err);
+                        if (p != kBadPage)
+                            av[i] = load_nt(w_pool + ((uint64_t)p << shift) + (off & pmask));
+                    }
+                    if (col_ok)
+                        bv[i] = *reinterpret_cast<const u32x4 *>(
+                            x + ((uint64_t)rl * K + (uint64_t)kv * 8u) * 2u);
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < kMfmaNI; ++i)
+                acc = mfma16x16x32<DT>(av[i], bv[i], acc);
+        }
+        s_red[wave][lane] = acc;
+        __syncthreads();
+        if (wave == 0) {
+            f32x4 v = s_red[0][lane];
+#pragma unroll
+            for (int w = 1; w < kGemvWaves; ++w) {
+                f32x4 o = s_red[w][lane];
+                v.x += o.x;
+                v.y += o.y;
+                v.z += o.z;
+                v.w += o.w;
+            }
+            if (col_ok) {
+                const float vals[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const uint32_t m = m0 + grp * 4u + (uint32_t)i;
+                    if (m < M)
+                        y[(uint64_t)rl * M + m] = vals[i];
+                }
+            }
+        }
+        __syncthreads();
+    };
+    gated_tile_loop(g, n_tiles, body, NoOp(), NoOp());
+}
+
+typedef void (*GemvKernel)(const uint8_t *, const uint32_t *, uint64_t, uint32_t, uint32_t,
+                           const uint8_t *, uint32_t, float *, uint32_t, uint32_t, Gate);
+
+template <int WT, int XT>
+static GemvKernel pick_valu(uint32_t batch)
+{
+    if (batch <= 1) return k_gemv_valu<WT, XT, 1>;
+    if (batch <= 2) return k_gemv_valu<WT, XT, 2>;
+    if (batch <= 4) return k_gemv_valu<WT, XT, 4>;
+    return k_gemv_valu<WT, XT, 8>;
+}
+
+template <int WT>
+static GemvKernel pick_valu_x(int x_dtype, uint32_t batch)
+{
+    switch (x_dtype) {
+    case SGDRC_F32: return pick_valu<WT, SGDRC_F32>(batch);
+    case SGDRC_BF16: return pick_valu<WT, SGDRC_BF16>(batch);
+    default: return pick_valu<WT, SGDRC_F16>(batch);
+    }
+}
+
+static int kernel_occupancy(GemvKernel k)
+{
+    static std::mutex mu;
+    static std::unordered_map<const void *, int> cache;
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = cache.find((const void *)k);
+    if (it != cache.end())
+        return it->second;
+    int n = occupancy(k, kGemvThreads);
+    cache[(const void *)k] = n;
+    return n;
+}
+
+static int dtype_size(int dt) { return dt == SGDRC_F32 ? 4 : 2; }
+
+}  // namespace sgdrc
+
+using namespace sgdrc;
+
+extern "C" {
+
+int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, uint32_t K,
+                 const void *d_x, int x_dtype, uint32_t batch, float *d_y, uint32_t page_shift,
+                 void *stream)
+{
+    clear_error();
+    int rc = check_shift(page_shift);
+    if (rc)
+        return rc;
+    if ((rc = check_paged(w, "w")))
+        return rc;
+    if (w_dtype < SGDRC_F32 || w_dtype > SGDRC_F16 || x_dtype < SGDRC_F32 || x_dtype > SGDRC_F16)
+        return set_error(SGDRC_EINVAL, "unknown dtype (w %d, x %d)", w_dtype, x_dtype);
+    if (batch < 1 || batch > SGDRC_MAX_BATCH)
+        return set_error(SGDRC_EINVAL, "batch %u outside 1..%d", batch, SGDRC_MAX_BATCH);
+    if (M == 0 || K == 0)
+        return set_error(SGDRC_EINVAL, "M and K must be positive");
+    if (((uint64_t)K * dtype_size(w_dtype)) % 16u)
+        return set_error(SGDRC_EINVAL, "K * element size must be a multiple of 16 bytes");
+    if ((uint64_t)K * dtype_size(w_dtype) / 16u >= (1ull << 31))
+        return set_error(SGDRC_EINVAL, "K too large");
+    if (!d_x || !d_y)
+        return set_error(SGDRC_EINVAL, "NULL x or y");
+    if ((reinterpret_cast<uintptr_t>(d_x) & 15u) || (reinterpret_cast<uintptr_t>(d_y) & 3u))
+        return set_error(SGDRC_EINVAL, "x must be 16-byte and y 4-byte aligned");
+    Ctx *c = nullptr;
+    rc = check_ctx(ctx, &c);
+    if (rc)
+        return rc;
+
+    const bool mfma = batch >= 5 && w_dtype == x_dtype && w_dtype != SGDRC_F32;
+    GemvKernel k;
+    uint64_t n_tiles;
+    if (mfma) {
+        k = w_dtype == SGDRC_BF16 ? k_gemm_mfma<SGDRC_BF16> : k_gemm_mfma<SGDRC_F16>;
+        n_tiles = (M + kMfmaRows - 1) / kMfmaRows;
+    } else {
+        switch (w_dtype) {
+        case SGDRC_F32: k = pick_valu_x<SGDRC_F32>(x_dtype, batch); break;
+        case SGDRC_BF16: k = pick_valu_x<SGDRC_BF16>(x_dtype, batch); break;
+        default: k = pick_valu_x<SGDRC_F16>(x_dtype, batch); break;
+        }
+        n_tiles = (M + kGemvRows - 1) / kGemvRows;
+    }
+    Gate g;
+    int allowed = 0;
+    rc = make_gate(c, stream, n_tiles, &g, &allowed);
+    if (rc)
+        return rc;
+    const uint32_t grid = gated_grid(c, kernel_occupancy(k), n_tiles, allowed);
+    hipLaunchKernelGGL(k, dim3(grid), dim3(kGemvThreads), 0, reinterpret_cast<hipStream_t>(stream),
+                       static_cast<const uint8_t *>(w->pool), w->pt, w->pool_pages, M, K,
+                       static_cast<const uint8_t *>(d_x), batch, d_y, page_shift,
+                       (uint32_t)n_tiles, g);
+    SGDRC_HIP(hipGetLastError());
+    return SGDRC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,98 @@
+// Host-side internals of libsgdrc: the context, error reporting, per-stream
+// state and launch sizing.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdint>
+#include <mutex>
+#include <string>
+#include <unordered_map>
+
+#include "device_common.hpp"
+#include "sgdrc.h"
+
+namespace sgdrc {
+
+constexpr uint32_t kCtxMagic = 0x53474452u;  // "SGDR"
+constexpr int kMaxStreams = 256;
+constexpr int kHistBins = 256;
+
+struct StreamState {
+    int slot = -1;
+    sgdrc_cu_mask mask{};
+    uint64_t last_tiles = 0;
+};
+
+struct Ctx {
+    uint32_t magic = kCtxMagic;
+    int device = -1;
+    int num_cus = 0;
+    uint32_t keys[SGDRC_MAX_CUS] = {};   // logical CU -> hardware key
+    sgdrc_cu_mask all_cus{};
+
+    uint16_t *d_lut = nullptr;           // kLutSize entries
+    TileQueue *d_queues = nullptr;       // kMaxStreams
+    uint64_t *d_hist_acc = nullptr;      // kMaxStreams x kHistBins
+    uint32_t *d_err = nullptr;           // one word
+
+    void *d_scratch = nullptr;           // page-table build scratch
+    size_t scratch_bytes = 0;
+    uint64_t *h_pinned = nullptr;        // 8 words of pinned host memory
+
+    uint32_t *log_cu = nullptr;
+    uint32_t *log_tile = nullptr;
+    uint64_t log_cap = 0;
+
+    std::mutex mu;
+    std::unordered_map<void *, StreamState> streams;
+    int next_slot = 0;
+};
+
+// ------------------------------------------------------------ error text
+
+int set_error(int code, const char *fmt, ...);
+void clear_error();
+int hip_fail(hipError_t e, const char *what);
+
+#define SGDRC_HIP(call)                                   \
+    do {                                                  \
+        hipError_t e_ = (call);                           \
+        if (e_ != hipSuccess)                             \
+            return ::sgdrc::hip_fail(e_, #call);          \
+    } while (0)
+
+// Validates ctx and makes sure the caller's current device is ctx's.
+int check_ctx(const sgdrc_ctx *ctx, Ctx **out);
+
+// Per-stream state (creates it, with all CUs allowed, on first use).
+int stream_state(Ctx *c, void *stream, StreamState **out);
+
+// Gate arguments for a launch of ``n_tiles`` tiles on ``stream``.
+int make_gate(Ctx *c, void *stream, uint64_t n_tiles, Gate *g, int *allowed_cus);
+
+// Grid size for a gated persistent kernel: enough workgroups that the
+// allowed CUs see about one per tile, at least one per CU, at most what
+// fits on the device at once.
+uint32_t gated_grid(const Ctx *c, int blocks_per_cu, uint64_t n_tiles, int allowed_cus);
+
+int popcount_mask(const sgdrc_cu_mask &m);
+
+int check_hash(const sgdrc_hash *h);
+int check_shift(uint32_t page_shift);
+int check_paged(const sgdrc_paged *p, const char *name);
+
+inline Ctx *as_ctx(sgdrc_ctx *c) { return reinterpret_cast<Ctx *>(c); }
+
+// Blocks per CU of a kernel at the given block size (cached by caller).
+template <typename K>
+int occupancy(K kernel, int block)
+{
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, block, 0) != hipSuccess || n < 1)
+        n = 1;
+    return n;
+}
+
+}  // namespace sgdrc

@@ -1,0 +1,142 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+declared in include/sgdrc.h, and rejects bad arguments on the host before
+touching the device (arguments are checked before the context, so a NULL
+context still reports EINVAL for a bad argument and ENODEV otherwise)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2407_13996_amd as sg
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sgdrc.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)
+    return sorted(set(n for n in names if n not in ("if", "while")))
+
+
+@pytest.fixture(scope="module")
+def L():
+    return sg.lib()
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ["colour_classify", "colour_alloc_pagetable", "bimodal_relayout", "colored_stream",
+              "colored_gemv", "set_cu_mask", "sgdrc_init", "sgdrc_destroy"]:
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    missing = [n for n in declared_functions() if not hasattr(L, n)]
+    assert not missing, missing
+
+
+NULL = None
+
+
+def good_hash(k=4):
+    return sg.make_hash([1 << (16 + i) for i in range(k)])
+
+
+def test_classify_argument_errors(L):
+    h = good_hash()
+    assert L.colour_classify(NULL, None, 16, 1, 32, None, None) == sg.EINVAL   # NULL hash
+    bad = good_hash(); bad.n_masks = 0
+    assert L.colour_classify(NULL, ctypes.byref(bad), 16, 1, 32, None, None) == sg.EINVAL
+    bad = good_hash(); bad.n_masks = 9
+    assert L.colour_classify(NULL, ctypes.byref(bad), 16, 1, 32, None, None) == sg.EINVAL
+    bad = good_hash(); bad.masks[0] = 1 << 48
+    assert L.colour_classify(NULL, ctypes.byref(bad), 16, 1, 32, None, None) == sg.EINVAL
+    assert "47" in sg.last_error()
+    assert L.colour_classify(NULL, ctypes.byref(h), 8, 1, 32, None, None) == sg.EINVAL  # misaligned
+    assert L.colour_classify(NULL, ctypes.byref(h), 0, 5, 32, None, None) == sg.EINVAL  # NULL addrs
+    assert L.colour_classify(NULL, ctypes.byref(h), 16, 1, 32, None, None) == sg.ENODEV
+    assert L.colour_classify(NULL, ctypes.byref(h), 0, 0, 0, None, None) == sg.ENODEV   # n = 0 ok
+
+
+def call_pt(L, h, origin=0, shift=16, pool=1024, colours=(0,), n=8, pt=256, found=True):
+    f = ctypes.c_uint64()
+    s = sg.make_set(sg.words_of(colours))
+    return L.colour_alloc_pagetable(NULL, ctypes.byref(h) if h is not None else None, origin, shift,
+                                    pool, ctypes.byref(s), n, pt,
+                                    ctypes.byref(f) if found else None, None)
+
+
+def test_pagetable_argument_errors(L):
+    h = good_hash(4)
+    assert call_pt(L, h) == sg.ENODEV
+    assert call_pt(L, None) == sg.EINVAL
+    assert call_pt(L, h, shift=11) == sg.EINVAL
+    assert call_pt(L, h, shift=31) == sg.EINVAL
+    assert call_pt(L, h, origin=4096, shift=16) == sg.EINVAL          # origin not page aligned
+    assert call_pt(L, h, colours=(16,)) == sg.EINVAL                  # colour >= 2^K
+    assert call_pt(L, h, colours=()) == sg.EINVAL                     # empty set
+    assert call_pt(L, h, n=2000) == sg.EINVAL                         # n_needed > pool_pages
+    assert call_pt(L, h, pool=0) == sg.EINVAL
+    assert call_pt(L, h, pool=(1 << 32) + 1) == sg.EINVAL
+    assert call_pt(L, h, origin=(1 << 48) - (1 << 16), pool=2) == sg.EINVAL  # past 2^48
+    assert call_pt(L, h, pt=None) == sg.EINVAL
+    assert call_pt(L, h, found=False) == sg.EINVAL
+
+
+def pg(pool=256, pt=256, pages=4):
+    return sg.Paged(pool, pt, pages)
+
+
+def test_relayout_and_stream_argument_errors(L):
+    r = ctypes.byref
+    assert L.bimodal_relayout(NULL, r(pg()), r(pg()), 100, 16, None) == sg.ENODEV
+    assert L.bimodal_relayout(NULL, r(pg()), r(pg()), 100, 11, None) == sg.EINVAL
+    assert L.bimodal_relayout(NULL, r(pg(pool=128)), r(pg()), 100, 16, None) == sg.EINVAL
+    assert L.bimodal_relayout(NULL, r(pg(pt=0)), r(pg()), 100, 16, None) == sg.EINVAL
+    assert L.bimodal_relayout(NULL, r(pg(pages=0)), r(pg()), 100, 16, None) == sg.EINVAL
+    assert L.bimodal_relayout(NULL, None, r(pg()), 100, 16, None) == sg.EINVAL
+    assert L.colored_stream(NULL, r(pg()), r(pg()), r(pg()), 3.0, 100, 16, None) == sg.ENODEV
+    assert L.colored_stream(NULL, r(pg()), r(pg(pt=2)), r(pg()), 3.0, 100, 16, None) == sg.EINVAL
+
+
+def test_gemv_argument_errors(L):
+    r = ctypes.byref
+    w = pg()
+    ok = dict(wd=sg.BF16, M=64, K=64, xd=sg.BF16, b=1, x=256, y=256, shift=21)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return L.colored_gemv(NULL, r(w), a["wd"], a["M"], a["K"], a["x"], a["xd"], a["b"], a["y"],
+                              a["shift"], None)
+    assert call() == sg.ENODEV
+    assert call(b=0) == sg.EINVAL
+    assert call(b=9) == sg.EINVAL
+    assert call(wd=3) == sg.EINVAL
+    assert call(xd=-1) == sg.EINVAL
+    assert call(M=0) == sg.EINVAL
+    assert call(K=12) == sg.EINVAL          # 24 bytes per row: not a multiple of 16
+    assert call(wd=sg.F32, K=12) == sg.ENODEV
+    assert call(x=0) == sg.EINVAL
+    assert call(x=264) == sg.EINVAL         # x not 16-byte aligned
+    assert call(shift=40) == sg.EINVAL
+
+
+def test_context_calls_reject_null(L):
+    assert L.sgdrc_num_cus(NULL) == sg.ENODEV
+    m = sg.make_set([0, 0, 0, 0], sg.CuMask)
+    assert L.set_cu_mask(NULL, None, ctypes.byref(m)) == sg.EINVAL     # empty mask
+    m = sg.make_set([1, 0, 0, 0], sg.CuMask)
+    assert L.set_cu_mask(NULL, None, ctypes.byref(m)) == sg.ENODEV
+    f = ctypes.c_uint32()
+    assert L.sgdrc_device_error(NULL, ctypes.byref(f)) == sg.ENODEV
+    assert L.sgdrc_init(0, None) == sg.EINVAL
+
+
+def test_binding_raises_with_message():
+    with pytest.raises(sg.SgdrcError) as e:
+        sg.set_cu_mask(None, 0, [])
+    assert e.value.code == sg.EINVAL and "empty" in str(e.value)

@@ -1,0 +1,376 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Bit-exact for colours, histograms, page tables, relayout and the triad;
+GEMV within the fp32-accumulation bound
+    |y - y_ref| <= 1e-3 * sum_k |W[m][k] x[b][k]|   and
+    max|y - y_ref| / max|y_ref| <= 1e-3
+against the oracle's double-precision sum.  Sizes span several tiles with
+ragged tails; every seed and shape is printed before its GPU step.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import synth
+import paper_2407_13996_amd as sg
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def ctx(orc):
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    c = sg.Context(0)
+    yield c
+    assert c.device_error() == 0
+    c.close()
+
+
+DEV = "cuda:0"
+
+
+_SIGNED = {np.dtype(np.uint16): np.int16, np.dtype(np.uint32): np.int32,
+           np.dtype(np.uint64): np.int64}
+
+
+def to_dev(a: np.ndarray):
+    """Upload; unsigned arrays travel as same-width signed views (raw bytes)."""
+    a = np.ascontiguousarray(a)
+    if a.dtype in _SIGNED:
+        a = a.view(_SIGNED[a.dtype])
+    return torch.from_numpy(a).to(DEV)
+
+
+def to_host(t) -> np.ndarray:
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def gemv_ok(y, ref, absdot):
+    err = np.abs(y.astype(np.float64) - ref)
+    assert np.all(err <= 1e-3 * absdot + 1e-30), float((err / (absdot + 1e-30)).max())
+    assert err.max() <= 1e-3 * max(np.abs(ref).max(), 1e-30)
+
+
+# ---------------------------------------------------------------- topology
+
+def test_topology(ctx):
+    n = ctx.num_cus
+    props = torch.cuda.get_device_properties(0)
+    say(f"num_cus={n} device reports {props.multi_processor_count}")
+    assert n == props.multi_processor_count
+    keys = [ctx.cu_key(i) for i in range(n)]
+    assert len(set(keys)) == n and keys == sorted(keys)
+    per_xcc = {}
+    for k in keys:
+        per_xcc[k >> 8] = per_xcc.get(k >> 8, 0) + 1
+    say("CUs per XCC:", per_xcc)
+
+
+# ---------------------------------------------------------------- classify
+
+@pytest.mark.parametrize("n,K,hist", [(65536, 4, True), (65536 + 13, 6, True), (5, 8, True),
+                                      (100003, 3, False), (0, 4, True)])
+def test_classify_matches_oracle(ctx, orc, n, K, hist):
+    say(f"classify n={n} K={K} hist={hist}")
+    masks = synth.xor_masks(K, seed=1, min_bit=12)
+    addrs = synth.page_addresses(max(n, 1), seed=0)[:n]
+    d_addrs = to_dev(addrs) if n else torch.empty(0, dtype=torch.int64, device=DEV)
+    d_col = torch.full((max(n, 16) + 16,), 0xEE, dtype=torch.uint8, device=DEV)
+    d_hist = torch.full((1 << K,), 12345, dtype=torch.int64, device=DEV) if hist else None
+    sg.colour_classify(ctx, masks, d_addrs, d_col, d_hist)
+    got = to_host(d_col)
+    ref, ref_hist = orc.classify(addrs, masks)
+    assert (got[:n] == ref).all()
+    assert (got[n:] == 0xEE).all()
+    if hist:
+        assert (to_host(d_hist).astype(np.uint64) == ref_hist).all()
+
+
+def test_classify_repeated_launches_reset_histogram(ctx, orc):
+    masks = synth.xor_masks(6, seed=2, min_bit=12)
+    addrs = synth.page_addresses(300000, seed=3)
+    d_addrs = to_dev(addrs)
+    d_col = torch.empty(300016, dtype=torch.uint8, device=DEV)
+    d_hist = torch.empty(64, dtype=torch.int64, device=DEV)
+    _, ref_hist = orc.classify(addrs, masks)
+    for i in range(3):
+        sg.colour_classify(ctx, masks, d_addrs, d_col, d_hist)
+        assert (to_host(d_hist).astype(np.uint64) == ref_hist).all(), i
+
+
+# --------------------------------------------------------------- page table
+
+@pytest.mark.parametrize("shift,pool,K,S,n,origin", [
+    (16, 1024, 4, range(4), 64, 1 << 40),          # config 1: 4 MiB in 64 KiB pages, colours 0..3 of 16
+    (12, 200003, 6, range(16), 40000, 0),
+    (21, 5000, 6, range(48), 3000, 1 << 33),
+    (16, 393216, 6, range(8), 3 * 16384, 1 << 36),  # three 1 GiB arrays at 8 of 64 colours
+])
+def test_pagetable_matches_oracle(ctx, orc, shift, pool, K, S, n, origin):
+    say(f"pagetable shift={shift} pool={pool} K={K} |S|={len(S)} n={n}")
+    masks = synth.xor_masks(K, seed=1, min_bit=shift)
+    words = synth.colour_set_bits(S)
+    d_pt = torch.full((n + 8,), -1, dtype=torch.int32, device=DEV)
+    found = sg.colour_alloc_pagetable(ctx, masks, origin, shift, pool, S, n, d_pt)
+    ref, ref_found = orc.pagetable(masks, origin, shift, pool, words, n)
+    assert found == ref_found
+    got = to_host(d_pt).view(np.uint32)
+    assert (got[:n] == ref).all()
+    assert (got[n:] == 0xFFFFFFFF).all()
+
+
+def test_pagetable_shortfall_reports_enomem(ctx, orc):
+    masks = synth.xor_masks(4, seed=1, min_bit=16)
+    d_pt = torch.zeros(1000, dtype=torch.int32, device=DEV)
+    ref, ref_found = orc.pagetable(masks, 0, 16, 1000, synth.colour_set_bits([5]), 1000)
+    with pytest.raises(sg.SgdrcError) as e:
+        sg.colour_alloc_pagetable(ctx, masks, 0, 16, 1000, [5], 1000, d_pt)
+    assert e.value.code == sg.ENOMEM and e.value.n_found == ref_found
+    assert (to_host(d_pt).view(np.uint32)[:ref_found] == ref).all()
+
+
+def test_pagetable_singletons_partition_the_pool(ctx):
+    masks = synth.xor_masks(3, seed=9, min_bit=12)
+    pool = 50000
+    seen = torch.zeros(pool, dtype=torch.int32, device=DEV)
+    for c in range(8):
+        d_pt = torch.empty(pool, dtype=torch.int32, device=DEV)
+        try:
+            sg.colour_alloc_pagetable(ctx, masks, 0, 12, pool, [c], pool, d_pt)
+        except sg.SgdrcError as e:
+            assert e.code == sg.ENOMEM
+            seen[d_pt[:e.n_found].long()] += 1
+    assert bool((seen == 1).all())
+
+
+# ---------------------------------------------------------------- relayout
+
+def make_tables(orc, shift, n_pages, S, seed, K=6):
+    """Oracle page table of n_pages pages of colours S, and a pool size with room."""
+    S = list(S)
+    pool_pages = int(n_pages * (1 << K) / len(S) * 1.5) + 64
+    masks = synth.xor_masks(K, seed=seed, min_bit=shift)
+    pt, found = orc.pagetable(masks, 0, shift, pool_pages, synth.colour_set_bits(S), n_pages)
+    assert found >= n_pages
+    return pt, pool_pages
+
+
+@pytest.mark.parametrize("shift,n_bytes", [(12, 37 * 4096 + 1234), (16, 9 * 65536 + 17),
+                                           (21, 2 * 2097152 + 4096 * 3 + 5), (15, 1),
+                                           (16, 64 * 65536)])
+def test_relayout_matches_oracle(ctx, orc, shift, n_bytes):
+    say(f"relayout shift={shift} n_bytes={n_bytes}")
+    P = 1 << shift
+    n_pages = -(-n_bytes // P)
+    pt_s, src_pages = make_tables(orc, shift, n_pages, range(16), 1)
+    pt_d, dst_pages = make_tables(orc, shift, n_pages, range(16, 48), 2)
+    src = synth.random_bytes(src_pages * P, seed=3)
+    dst0 = synth.random_bytes(dst_pages * P, seed=4)
+    d_src, d_dst = to_dev(src), to_dev(dst0)
+    sg.bimodal_relayout(ctx, sg.paged(d_dst, to_dev(pt_d), dst_pages),
+                        sg.paged(d_src, to_dev(pt_s), src_pages), n_bytes, shift)
+    ref = dst0.copy()
+    orc.relayout(ref, pt_d, src, pt_s, n_bytes, shift)
+    assert (to_host(d_dst) == ref).all()
+
+
+def test_relayout_round_trip_fp16_is_identity(ctx, orc):
+    shift = 16
+    n_pages = 300
+    n_bytes = n_pages * 65536 - 6
+    data = synth.random_u16(n_pages * 32768, seed=5)
+    d_all = to_dev(data)
+    pt_all = torch.arange(n_pages, dtype=torch.int32, device=DEV)
+    pt_s, pool_s = make_tables(orc, shift, n_pages, range(16), 3)
+    pt_s = to_dev(pt_s)
+    d_s = torch.zeros(pool_s * 32768, dtype=torch.int16, device=DEV)
+    d_back = torch.zeros_like(d_all)
+    sg.bimodal_relayout(ctx, sg.paged(d_s, pt_s, pool_s), sg.paged(d_all, pt_all, n_pages),
+                        n_bytes, shift)
+    sg.bimodal_relayout(ctx, sg.paged(d_back, pt_all, n_pages), sg.paged(d_s, pt_s, pool_s),
+                        n_bytes, shift)
+    back = to_host(d_back).view(np.uint16)
+    assert (back[:n_bytes // 2] == data[:n_bytes // 2]).all()
+    assert (back[n_bytes // 2:] == 0).all()
+
+
+# ------------------------------------------------------------------- triad
+
+@pytest.mark.parametrize("shift,n", [(12, 5 * 1024 + 77), (16, 3 * 16384 + 5), (16, 40 * 16384),
+                                     (21, 524288 + 3), (13, 7)])
+def test_triad_matches_oracle(ctx, orc, shift, n):
+    say(f"triad shift={shift} n={n}")
+    P = 1 << shift
+    n_pages = -(-n * 4 // P)
+    tabs = [make_tables(orc, shift, n_pages, range(8 * i, 8 * i + 16), 10 + i) for i in range(3)]
+    pools = max(t[1] for t in tabs)
+    pts = [t[0] for t in tabs]
+    epp = P // 4
+    a0 = synth.uniform_f32(pools * epp, seed=1)
+    b = synth.uniform_f32(pools * epp, seed=2)
+    c = synth.uniform_f32(pools * epp, seed=3)
+    d_a, d_b, d_c = to_dev(a0), to_dev(b), to_dev(c)
+    sg.colored_stream(ctx, sg.paged(d_a, to_dev(pts[0]), pools), sg.paged(d_b, to_dev(pts[1]), pools),
+                      sg.paged(d_c, to_dev(pts[2]), pools), 3.0, n, shift)
+    ref = a0.copy()
+    orc.triad(ref, pts[0], b, pts[1], c, pts[2], 3.0, n, shift)
+    assert (to_host(d_a).view(np.uint32) == ref.view(np.uint32)).all()
+
+
+def test_triad_in_place_alias(ctx, orc):
+    shift, n = 16, 10 * 16384 + 3
+    pages = 11
+    pt = torch.arange(pages, dtype=torch.int32, device=DEV)
+    b = synth.uniform_f32(pages * 16384, seed=7)
+    c = synth.uniform_f32(pages * 16384, seed=8)
+    d_b, d_c = to_dev(b), to_dev(c)
+    sg.colored_stream(ctx, sg.paged(d_b, pt, pages), sg.paged(d_b, pt, pages),
+                      sg.paged(d_c, pt, pages), -0.5, n, shift)
+    ref = b.copy()
+    ident = np.arange(pages, dtype=np.uint32)
+    orc.triad(ref, ident, b, ident, c, ident, -0.5, n, shift)
+    assert (to_host(d_b).view(np.uint32) == ref.view(np.uint32)).all()
+
+
+# -------------------------------------------------------------------- GEMV
+
+def w_bits(dt, n, seed):
+    if dt == sg.F32:
+        return synth.normal_f32(n, seed=seed).view(np.uint32)
+    if dt == sg.BF16:
+        return synth.normal_bf16(n, seed=seed, sigma=0.02)
+    return synth.normal_f32(n, seed=seed, sigma=0.5).astype(np.float16).view(np.uint16)
+
+
+def x_bits(dt, n, seed):
+    if dt == sg.F32:
+        return synth.normal_f32(n, seed=seed).view(np.uint32)
+    if dt == sg.BF16:
+        return synth.normal_bf16(n, seed=seed)
+    return synth.normal_f32(n, seed=seed).astype(np.float16).view(np.uint16)
+
+
+def run_gemv(ctx, orc, M, K, B, wd, xd, shift, S=range(48), seed=0, masks_seed=1, cus=None,
+             check=True, n_masks=6):
+    P = 1 << shift
+    wb = w_bits(wd, M * K, seed + 1)
+    xb = x_bits(xd, B * K, seed + 2)
+    wbytes = wb.view(np.uint8)
+    n_pages = -(-wbytes.size // P)
+    pt, pool_pages = make_tables(orc, shift, n_pages, S, masks_seed, K=n_masks)
+    pool = np.zeros(pool_pages * P, dtype=np.uint8)
+    padded = np.zeros(n_pages * P, dtype=np.uint8)
+    padded[:wbytes.size] = wbytes
+    pool.reshape(pool_pages, P)[pt.astype(np.int64)] = padded.reshape(n_pages, P)
+    d_pool, d_pt, d_x = to_dev(pool), to_dev(pt), to_dev(xb)
+    d_y = torch.full((B * M,), float("nan"), dtype=torch.float32, device=DEV)
+    if cus is not None:
+        sg.set_cu_mask(ctx, None, cus)
+    sg.colored_gemv(ctx, sg.paged(d_pool, d_pt, pool_pages), wd, M, K, d_x, xd, B, d_y, shift)
+    if cus is not None:
+        sg.set_cu_mask(ctx, None, None)
+    y = to_host(d_y).reshape(B, M)
+    if check:
+        ref, absdot = orc.gemv(pool, pt, wd, M, K, xb, xd, B, shift)
+        gemv_ok(y, ref, absdot)
+    return y
+
+
+def test_gemv_config1_fp32_1024(ctx, orc):
+    say("gemv 1024x1024 fp32 B=1, 64 KiB pages, colours 0..3 of 16")
+    run_gemv(ctx, orc, 1024, 1024, 1, sg.F32, sg.F32, 16, S=range(4), n_masks=4)
+
+
+@pytest.mark.parametrize("B", [1, 2, 3, 4, 5, 8])
+def test_gemv_bf16_ragged(ctx, orc, B):
+    say(f"gemv bf16 1003x1000 B={B}")
+    run_gemv(ctx, orc, 1003, 1000, B, sg.BF16, sg.BF16, 12, seed=B)
+
+
+@pytest.mark.parametrize("wd,xd,B", [(sg.F32, sg.BF16, 2), (sg.BF16, sg.F32, 8), (sg.F16, sg.F16, 6),
+                                     (sg.F16, sg.F32, 1), (sg.F32, sg.F16, 7), (sg.BF16, sg.F16, 4)])
+def test_gemv_dtype_mix(ctx, orc, wd, xd, B):
+    say(f"gemv dtypes w={wd} x={xd} B={B}")
+    run_gemv(ctx, orc, 517, 264, B, wd, xd, 12, seed=10 + B)
+
+
+@pytest.mark.parametrize("M,K,B", [(4096, 11008, 1), (11008, 4096, 8)])
+def test_gemv_config3_full_size(ctx, orc, M, K, B):
+    say(f"gemv bf16 {M}x{K} B={B}, 2 MiB pages, colours 0..47 of 64")
+    run_gemv(ctx, orc, M, K, B, sg.BF16, sg.BF16, 21, seed=M + B)
+
+
+def test_gemv_bitwise_identical_across_cu_masks(ctx, orc):
+    n = ctx.num_cus
+    ys = []
+    for cus in [None, range(64), range(n // 2, n), synth.random_cu_subset(n, 37, seed=4)]:
+        say(f"gemv mask {None if cus is None else len(list(cus))} CUs")
+        for B in (1, 8):
+            ys.append((B, run_gemv(ctx, orc, 777, 2048, B, sg.BF16, sg.BF16, 16, seed=B,
+                                   cus=cus, check=(cus is None))))
+    for B in (1, 8):
+        same = [y for b, y in ys if b == B]
+        for y in same[1:]:
+            assert (y.view(np.uint32) == same[0].view(np.uint32)).all()
+
+
+# ------------------------------------------------------- CU gate and queue
+
+def test_cu_mask_confines_work_and_visits_each_tile_once(ctx, orc):
+    n = ctx.num_cus
+    shift, elems = 16, 600 * 16384
+    pages = elems * 4 >> shift
+    pt = torch.arange(pages, dtype=torch.int32, device=DEV)
+    b = to_dev(synth.uniform_f32(elems, seed=1))
+    c = to_dev(synth.uniform_f32(elems, seed=2))
+    ref = None
+    stream = torch.cuda.current_stream()
+    for cus in [list(range(64)), list(range(128, n)), synth.random_cu_subset(n, 20, seed=3),
+                list(range(n)), [5]]:
+        say(f"gate mask of {len(cus)} CUs")
+        a = torch.zeros_like(b)
+        cu_log = torch.zeros(n, dtype=torch.int32, device=DEV)
+        tile_log = torch.zeros(4096, dtype=torch.int32, device=DEV)
+        ctx.set_worklog(cu_log, tile_log)
+        sg.set_cu_mask(ctx, stream, cus)
+        sg.colored_stream(ctx, sg.paged(a, pt, pages), sg.paged(b, pt, pages),
+                          sg.paged(c, pt, pages), 3.0, elems, shift, stream)
+        tiles = ctx.last_tiles(stream)
+        ctx.set_worklog(None, None)
+        sg.set_cu_mask(ctx, stream, None)
+        assert ctx.device_error() == 0
+        cl, tl = to_host(cu_log), to_host(tile_log)
+        assert tiles == elems * 4 // 32768
+        assert (tl[:tiles] == 1).all() and (tl[tiles:] == 0).all()
+        worked = set(np.nonzero(cl)[0].tolist())
+        assert worked <= set(cus)
+        assert cl.sum() == tiles
+        say(f"  {len(worked)} of {len(cus)} allowed CUs took tiles")
+        out = to_host(a)
+        if ref is None:
+            ref = out
+        assert (out.view(np.uint32) == ref.view(np.uint32)).all()
+
+
+def test_out_of_range_page_entry_is_flagged_not_accessed(ctx):
+    shift = 16
+    pages = 8
+    pt = torch.arange(pages, dtype=torch.int32, device=DEV)
+    bad = pt.clone()
+    bad[3] = pages + 100
+    src = torch.ones(pages * 65536, dtype=torch.uint8, device=DEV)
+    dst = torch.zeros_like(src)
+    sg.bimodal_relayout(ctx, sg.paged(dst, pt, pages), sg.paged(src, bad, pages),
+                        pages * 65536, shift)
+    assert ctx.device_error() & sg.DEVERR_PT_RANGE
+    d = to_host(dst).reshape(pages, 65536)
+    assert (d[3] == 0).all() and (d[[0, 1, 2, 4, 5, 6, 7]] == 1).all()
+    assert ctx.device_error() == 0
