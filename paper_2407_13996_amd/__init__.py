@@ -139,7 +139,11 @@ def words_of(indices) -> list:
 
 
 def paged(pool, pt, pool_pages: int) -> Paged:
-    return Paged(_addr(pool), _addr(pt), int(pool_pages))
+    """A Paged descriptor; it keeps references to tensors passed for pool and
+    pt so that their memory stays allocated while the descriptor lives."""
+    p = Paged(_addr(pool), _addr(pt), int(pool_pages))
+    p._keep = (pool, pt)
+    return p
 
 
 class Context:

@@ -53,7 +53,7 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
         s_hist[threadIdx.x] = 0;
         __syncthreads();
     }
-    auto body = [&](uint32_t t, uint32_t) {
+    auto body = [&](uint32_t t, uint32_t, uint32_t &) {
         const uint64_t tile0 = (uint64_t)t * kClsTile;
 #pragma unroll 1
         for (int s = 0; s < kClsSteps; ++s) {

@@ -118,65 +118,72 @@ __device__ __forceinline__ void reset_queue(TileQueue *q)
     }
 }
 
-// Runs ``body(tile, cu)`` for every tile this workgroup obtains, under the
-// gate.  Workgroups on CUs outside the mask take no tiles.  ``flush()``
+// Runs ``body(tile, cu, err)`` for every tile this workgroup obtains, under
+// the gate.  Workgroups on CUs outside the mask take no tiles.  ``flush()``
 // runs after a workgroup's tile loop (to publish per-workgroup partials).
 // The last workgroup to arrive finishes any tiles left over (possible only
 // when no workgroup landed on an allowed CU; flagged), flushes again, calls
 // ``epilogue()`` with every other workgroup's work complete, and resets the
 // queue for the next launch on the stream.
+//
+// Bodies must not return early or branch around the rest of the tile on a
+// per-lane condition: the loop contains barriers, and a lane-dependent exit
+// from it lets the compiler send some lanes of a wave back to the barrier
+// while others still owe the next ticket.  Bodies record problems in the
+// per-thread ``err`` bits instead; they are raised once, after the loop.
 template <typename Body, typename Flush, typename Epilogue>
 __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles, Body body,
                                                 Flush flush, Epilogue epilogue)
 {
     __shared__ uint32_t s_ticket;
     __shared__ uint32_t s_flag;
+    uint32_t err = 0u;
     const uint32_t cu = my_cu(g);
     if (cu_allowed(g, cu)) {
         for (;;) {
-            uint32_t t = claim_tile(g.q, &s_ticket);
+            const uint32_t t = claim_tile(g.q, &s_ticket);
             if (t >= n_tiles)
                 break;
             log_tile(g, cu, t);
-            body(t, cu);
+            body(t, cu, err);
         }
         flush();
     }
     if (arrive_last(g.q, &s_flag)) {
-        bool fell_back = false;
+        uint32_t leftover = 0u;
         for (;;) {
-            uint32_t t = claim_tile(g.q, &s_ticket);
+            const uint32_t t = claim_tile(g.q, &s_ticket);
             if (t >= n_tiles)
                 break;
-            fell_back = true;
+            leftover += 1u;
             log_tile(g, cu, t);
-            body(t, cu);
+            body(t, cu, err);
         }
-        if (fell_back) {
+        if (leftover != 0u) {
             flush();
-            if (threadIdx.x == 0)
-                raise_flag(g.err, kDevFlagGateFallback);
+            err |= threadIdx.x == 0 ? kDevFlagGateFallback : 0u;
         }
         __syncthreads();
         epilogue();
         reset_queue(g.q);
     }
+    if (err != 0u)
+        raise_flag(g.err, err);
 }
 
 struct NoOp {
     __device__ void operator()() const {}
 };
 
-// Page-table lookup with the range check every kernel applies.
+// Page-table lookup with the range check every kernel applies: an entry
+// outside the pool yields kBadPage and sets kDevErrPtRange in ``err``.
 __device__ __forceinline__ uint32_t checked_page(const uint32_t *pt, uint64_t j,
-                                                 uint64_t pool_pages, uint32_t *err)
+                                                 uint64_t pool_pages, uint32_t &err)
 {
-    uint32_t p = pt[j];
-    if ((uint64_t)p >= pool_pages) {
-        raise_flag(err, kDevErrPtRange);
-        return kBadPage;
-    }
-    return p;
+    const uint32_t p = pt[j];
+    const bool bad = (uint64_t)p >= pool_pages;
+    err |= bad ? kDevErrPtRange : 0u;
+    return bad ? kBadPage : p;
 }
 
 __device__ __forceinline__ u32x4 load_nt(const void *p)

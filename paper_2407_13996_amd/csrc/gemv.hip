@@ -79,7 +79,7 @@ struct TilePages {
 
 __device__ __forceinline__ TilePages stage_pages(const uint32_t *pt, uint64_t pool_pages,
                                                  uint64_t byte_lo, uint64_t byte_hi,
-                                                 uint32_t shift, uint32_t *s_pt, uint32_t *err)
+                                                 uint32_t shift, uint32_t *s_pt, uint32_t &err)
 {
     TilePages tp;
     tp.p_lo = byte_lo >> shift;
@@ -92,7 +92,7 @@ __device__ __forceinline__ TilePages stage_pages(const uint32_t *pt, uint64_t po
 
 __device__ __forceinline__ uint32_t page_of(const TilePages &tp, const uint32_t *s_pt,
                                             const uint32_t *pt, uint64_t pool_pages, uint64_t j,
-                                            uint32_t *err)
+                                            uint32_t &err)
 {
     if (tp.np <= (uint32_t)kPtCap)
         return s_pt[j - tp.p_lo];
@@ -115,11 +115,11 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
     const uint32_t KV = (uint32_t)(row_bytes / 16u);
     const uint64_t pmask = (1ull << shift) - 1ull;
 
-    auto body = [&](uint32_t t, uint32_t) {
+    auto body = [&](uint32_t t, uint32_t, uint32_t &err) {
         const uint32_t m0 = t * kGemvRows;
         const uint32_t m_end = min(m0 + (uint32_t)kGemvRows, M);
         const TilePages tp = stage_pages(pt, pool_pages, (uint64_t)m0 * row_bytes,
-                                         (uint64_t)m_end * row_bytes, shift, s_pt, g.err);
+                                         (uint64_t)m_end * row_bytes, shift, s_pt, err);
         float acc[kGemvRows][NB];
 #pragma unroll
         for (int r = 0; r < kGemvRows; ++r)
@@ -139,7 +139,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
                     wv[u][r] = u32x4{0u, 0u, 0u, 0u};
                     if (ok && m0 + r < M) {
                         const uint64_t off = (uint64_t)(m0 + r) * row_bytes + (uint64_t)kv * 16u;
-                        const uint32_t p = page_of(tp, s_pt, pt, pool_pages, off >> shift, g.err);
+                        const uint32_t p = page_of(tp, s_pt, pt, pool_pages, off >> shift, err);
                         if (p != kBadPage)
                             wv[u][r] = load_nt(w_pool + ((uint64_t)p << shift) + (off & pmask));
                     }
@@ -250,11 +250,11 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemm_mfma(
     const uint32_t KV = (uint32_t)(row_bytes / 16u);
     const uint64_t pmask = (1ull << shift) - 1ull;
 
-    auto body = [&](uint32_t t, uint32_t) {
+    auto body = [&](uint32_t t, uint32_t, uint32_t &err) {
         const uint32_t m0 = t * kMfmaRows;
         const uint32_t m_end = min(m0 + (uint32_t)kMfmaRows, M);
         const TilePages tp = stage_pages(pt, pool_pages, (uint64_t)m0 * row_bytes,
-                                         (uint64_t)m_end * row_bytes, shift, s_pt, g.err);
+                                         (uint64_t)m_end * row_bytes, shift, s_pt, err);
         const uint32_t row = m0 + rl;
         const bool row_ok = row < M;
         const bool col_ok = rl < nb;
@@ -269,7 +269,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemm_mfma(
                 if (kv < KV) {
                     if (row_ok) {
                         const uint64_t off = (uint64_t)row * row_bytes + (uint64_t)kv * 16u;
-                        const uint32_t p = page_of(tp, s_pt, pt, pool_pages, off >> shift, g.err);
+                        const uint32_t p = page_of(tp, s_pt, pt, pool_pages, off >> shift, err);
                         if (p != kBadPage)
                             av[i] = load_nt(w_pool + ((uint64_t)p << shift) + (off & pmask));
                     }

@@ -17,13 +17,6 @@ constexpr uint64_t kStreamTile = (uint64_t)kStreamThreads * 16u * kStreamUnroll;
 constexpr int kStreamTileShift = 15;
 constexpr int kTilePagesMax = (int)(kStreamTile >> SGDRC_MIN_PAGE_SHIFT);  // 8
 
-// Logical -> physical translation for one array of a tile.
-struct TileMap {
-    uint8_t *base;       // pool
-    uint64_t pmask;      // page size - 1
-    uint32_t shift;
-};
-
 // Byte-wise copy of the ragged end of a 16-byte chunk.
 __device__ __forceinline__ void copy_tail(uint8_t *d, const uint8_t *s, uint32_t n)
 {
@@ -40,20 +33,19 @@ __global__ __launch_bounds__(kStreamThreads) void k_relayout(
     __shared__ uint32_t s_pd[kTilePagesMax], s_ps[kTilePagesMax];
     const uint64_t pmask = (1ull << shift) - 1ull;
     const uint64_t n_pages = (n_bytes + pmask) >> shift;
-    auto body = [&](uint32_t t, uint32_t) {
+    auto body = [&](uint32_t t, uint32_t, uint32_t &err) {
         const uint64_t t0 = (uint64_t)t * kStreamTile;
         const uint64_t tile_bytes = n_bytes - t0 < kStreamTile ? n_bytes - t0 : kStreamTile;
         if (BIG) {
             const uint64_t j = t0 >> shift;
             const uint32_t pd = pt_d[j], ps = pt_s[j];
-            if (pd >= dst_pages || ps >= src_pages) {
-                if (threadIdx.x == 0)
-                    raise_flag(g.err, kDevErrPtRange);
-                return;
-            }
+            const bool bad = pd >= dst_pages || ps >= src_pages;
+            err |= bad ? kDevErrPtRange : 0u;
             uint8_t *d = dst + ((uint64_t)pd << shift) + (t0 & pmask);
             const uint8_t *s = src + ((uint64_t)ps << shift) + (t0 & pmask);
-            if (tile_bytes == kStreamTile) {
+            if (bad) {
+                // skip the tile: nothing outside the pools is touched
+            } else if (tile_bytes == kStreamTile) {
                 u32x4 v[kStreamUnroll];
 #pragma unroll
                 for (int u = 0; u < kStreamUnroll; ++u)
@@ -77,8 +69,8 @@ __global__ __launch_bounds__(kStreamThreads) void k_relayout(
                 const uint64_t j = j0 + threadIdx.x;
                 uint32_t pd = kBadPage, ps = kBadPage;
                 if (j < n_pages) {
-                    pd = checked_page(pt_d, j, dst_pages, g.err);
-                    ps = checked_page(pt_s, j, src_pages, g.err);
+                    pd = checked_page(pt_d, j, dst_pages, err);
+                    ps = checked_page(pt_s, j, src_pages, err);
                 }
                 s_pd[threadIdx.x] = pd;
                 s_ps[threadIdx.x] = ps;
@@ -136,22 +128,21 @@ __global__ __launch_bounds__(kStreamThreads) void k_triad(
     __shared__ uint32_t s_pa[kTilePagesMax], s_pb[kTilePagesMax], s_pc[kTilePagesMax];
     const uint64_t pmask = (1ull << shift) - 1ull;
     const uint64_t n_pages = (n_bytes + pmask) >> shift;
-    auto body = [&](uint32_t t, uint32_t) {
+    auto body = [&](uint32_t t, uint32_t, uint32_t &err) {
         const uint64_t t0 = (uint64_t)t * kStreamTile;
         const uint64_t tile_bytes = n_bytes - t0 < kStreamTile ? n_bytes - t0 : kStreamTile;
         if (BIG) {
             const uint64_t j = t0 >> shift;
             const uint32_t pa = pt_a[j], pb = pt_b[j], pc = pt_c[j];
-            if (pa >= a_pages || pb >= b_pages || pc >= c_pages) {
-                if (threadIdx.x == 0)
-                    raise_flag(g.err, kDevErrPtRange);
-                return;
-            }
+            const bool bad = pa >= a_pages || pb >= b_pages || pc >= c_pages;
+            err |= bad ? kDevErrPtRange : 0u;
             const uint64_t in = t0 & pmask;
             uint8_t *ap = a + ((uint64_t)pa << shift) + in;
             const uint8_t *bp = b + ((uint64_t)pb << shift) + in;
             const uint8_t *cp = c + ((uint64_t)pc << shift) + in;
-            if (tile_bytes == kStreamTile) {
+            if (bad) {
+                // skip the tile: nothing outside the pools is touched
+            } else if (tile_bytes == kStreamTile) {
                 u32x4 vb[kStreamUnroll], vc[kStreamUnroll];
 #pragma unroll
                 for (int u = 0; u < kStreamUnroll; ++u) {
@@ -185,9 +176,9 @@ __global__ __launch_bounds__(kStreamThreads) void k_triad(
                 const uint64_t j = j0 + threadIdx.x;
                 uint32_t pa = kBadPage, pb = kBadPage, pc = kBadPage;
                 if (j < n_pages) {
-                    pa = checked_page(pt_a, j, a_pages, g.err);
-                    pb = checked_page(pt_b, j, b_pages, g.err);
-                    pc = checked_page(pt_c, j, c_pages, g.err);
+                    pa = checked_page(pt_a, j, a_pages, err);
+                    pb = checked_page(pt_b, j, b_pages, err);
+                    pc = checked_page(pt_c, j, c_pages, err);
                 }
                 s_pa[threadIdx.x] = pa;
                 s_pb[threadIdx.x] = pb;
