@@ -1,0 +1,426 @@
+#!/usr/bin/env python3
+"""Benchmark of the colour-restricted tensor path on one MI355X.
+
+Headline workload (the colour-restricted streaming configuration): triad
+a = b + 3c on three 1 GiB fp32 arrays (2^28 elements, U[-1,1)) stored in
+64 KiB pages of one pool, with 6 XOR masks (64 colours) and colour sets of
+8, 16, 32 and 64 of the 64 colours, all CUs enabled.  One step = the four
+triad passes (one per colour set); ``value`` is the algorithmic HBM traffic
+of the timed steps (12 bytes per element per pass) divided by their wall
+time.  Inputs are resident in HBM before timing starts.
+
+The other steps of the path are measured in the same run and reported under
+"rows": batched classify (2^26 addresses), the page-table build, the bimodal
+relayout of a 4 GiB fp16 tensor in both directions, and the memory-bound
+GEMV sweep (bf16 4096x11008 and 11008x4096, batch 1/2/4/8, CU masks of
+64/128/192/256 CUs) with p50/p99 kernel latency.  The CPU oracle is timed on
+a bounded sample of the headline workload ("cpu_baseline").
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "colour-restricted HBM GB/s (% of colour-scaled peak); colored GEMV p99 latency"
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--rows", default="classify,pagetable,relayout,gemv",
+                    help="comma list of extra rows to measure ('' for none)")
+    ap.add_argument("--gemv-launches", type=int, default=300)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-passes", type=int, default=3)
+    return ap.parse_args()
+
+
+def pctl(xs, q):
+    import numpy as np
+    return float(np.percentile(np.asarray(xs, dtype=np.float64), q))
+
+
+class Timer:
+    """Per-launch HIP event pairs on one stream."""
+
+    def __init__(self, torch, stream):
+        self.torch, self.stream, self.pairs = torch, stream, []
+
+    def start(self):
+        e = self.torch.cuda.Event(enable_timing=True)
+        e.record(self.stream)
+        return e
+
+    def stop(self, e0, tag=None):
+        e1 = self.torch.cuda.Event(enable_timing=True)
+        e1.record(self.stream)
+        self.pairs.append((tag, e0, e1))
+
+    def durations_ms(self, tag=None):
+        return [a.elapsed_time(b) for t, a, b in self.pairs if tag is None or t == tag]
+
+
+def aligned_pool(torch, n_pages, shift):
+    """A device byte pool of n_pages pages whose base is page aligned."""
+    P = 1 << shift
+    raw = torch.empty(n_pages * P + P, dtype=torch.uint8, device="cuda:0")
+    base = raw.data_ptr()
+    off = (-base) % P
+    return raw, base + off
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the colour-restricted path is per device and "
+              "this build runs no collectives; use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2407_13996_amd as sg
+    import synth
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    ctx = sg.Context(0)
+    stream = torch.cuda.Stream(device=0)
+    timer = Timer(torch, stream)
+    props = torch.cuda.get_device_properties(0)
+    log(f"device {props.name} {props.gcnArchName} CUs={ctx.num_cus}")
+
+    # ------------------------------------------------------------ headline
+    shift = 16
+    P = 1 << shift
+    n = 1 << 28
+    pages = (n * 4) >> shift
+    fractions = [8, 16, 32, 64]
+    masks = synth.xor_masks(6, seed=1, min_bit=shift)
+    pool_pages = int(3 * pages * 64 / min(fractions) * 1.04) + 64
+    log(f"pool {pool_pages} pages of 64 KiB ({pool_pages * P / 2**30:.1f} GiB), masks "
+        + " ".join(hex(m) for m in masks))
+    raw_pool, base = aligned_pool(torch, pool_pages, shift)
+    with torch.cuda.stream(stream):
+        b_host = synth.uniform_f32(n, seed=2)
+        c_host = synth.uniform_f32(n, seed=3)
+        b_lin = torch.from_numpy(b_host).to(dev)
+        c_lin = torch.from_numpy(c_host).to(dev)
+        ident = torch.arange(pages, dtype=torch.int32, device=dev)
+        tables = {}
+        for nc in fractions:
+            pt = torch.empty(3 * pages, dtype=torch.int32, device=dev)
+            t0 = time.perf_counter()
+            found = sg.colour_alloc_pagetable(ctx, masks, base, shift, pool_pages, range(nc),
+                                              3 * pages, pt, stream)
+            t_pt = time.perf_counter() - t0
+            tables[nc] = (pt, found, t_pt)
+        log("page tables built")
+
+    def paged_arrays(nc):
+        pt = tables[nc][0]
+        return [sg.paged(base, pt[i * pages:(i + 1) * pages], pool_pages) for i in range(3)]
+
+    def place_inputs(nc):
+        a, b, c = paged_arrays(nc)
+        sg.bimodal_relayout(ctx, b, sg.paged(b_lin, ident, pages), n * 4, shift, stream)
+        sg.bimodal_relayout(ctx, c, sg.paged(c_lin, ident, pages), n * 4, shift, stream)
+        return a, b, c
+
+    bytes_per_pass = 12 * n
+    per_frac = {}
+    with torch.cuda.stream(stream):
+        arrays = {}
+        for nc in fractions:
+            arrays[nc] = place_inputs(nc)
+        torch.cuda.synchronize()
+        # warmup
+        for _ in range(args.warmup):
+            for nc in fractions:
+                a, b, c = arrays[nc]
+                sg.colored_stream(ctx, a, b, c, 3.0, n, shift, stream)
+        torch.cuda.synchronize()
+        log(f"timing {args.steps} steps x {len(fractions)} triad passes")
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            for nc in fractions:
+                a, b, c = arrays[nc]
+                e0 = timer.start()
+                sg.colored_stream(ctx, a, b, c, 3.0, n, shift, stream)
+                timer.stop(e0, ("triad", nc))
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+    all_ms = []
+    for nc in fractions:
+        d = timer.durations_ms(("triad", nc))
+        all_ms += d
+        f = nc / 64
+        med = pctl(d, 50)
+        gbs = bytes_per_pass / (med * 1e-3) / 1e9
+        per_frac[nc] = {
+            "colours": f"{nc}/64", "median_ms": round(med, 4), "p99_ms": round(pctl(d, 99), 4),
+            "GBps": round(gbs, 1), "colour_scaled_peak_GBps": f * HBM_PEAK_GBS,
+            "pct_of_colour_scaled_peak": round(100 * gbs / (f * HBM_PEAK_GBS), 1),
+            "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1),
+            "pagetable_ms": round(tables[nc][2] * 1e3, 3),
+        }
+        log(f"triad {nc}/64 colours: {med:.4f} ms  {gbs:.0f} GB/s")
+    value = args.steps * len(fractions) * bytes_per_pass / wall / 1e9
+    avg_ms = float(np.mean(all_ms))
+    achieved = bytes_per_pass / (avg_ms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": "k_triad (64 KiB pages)", "avg_launch_ms": round(avg_ms, 4),
+                "bytes_per_launch": bytes_per_pass}
+
+    result = {
+        "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "colour-restricted triad a=b+3c, three 1 GiB fp32 arrays "
+                               "(2^28 elements) in 64 KiB pages, 6 XOR masks (64 colours), "
+                               "colour sets 8/16/32/64 of 64, all CUs; one step = 4 passes",
+                   "page_bytes": P, "elements": n, "num_cus": ctx.num_cus,
+                   "masks": [hex(m) for m in masks]},
+        "roofline": roofline,
+        "per_fraction": [per_frac[nc] for nc in fractions],
+    }
+
+    # ------------------------------------------------------------ sampled check
+    # GPU result of the 8/64 pass on a few logical pages (compared against the
+    # oracle in the CPU-baseline leg).
+    a8 = arrays[8][0]
+    sample_pages = [0, 1, 777, pages - 1]
+    pt8 = tables[8][0][:pages].cpu().numpy().astype(np.int64)
+    pool_view = torch.empty(0)  # placeholder for readability
+    del pool_view
+    gpu_pages = {}
+    for j in sample_pages:
+        addr = base + int(pt8[j]) * P
+        off = addr - raw_pool.data_ptr()
+        gpu_pages[j] = raw_pool[off:off + P].cpu().numpy().view(np.float32).copy()
+
+    rows = {}
+    want = [r for r in args.rows.split(",") if r]
+    if "classify" in want:
+        rows["classify"] = bench_classify(torch, sg, synth, ctx, stream, timer)
+    if "pagetable" in want:
+        rows["pagetable"] = {
+            "what": "colour_alloc_pagetable over the headline pool (synchronous call)",
+            "pool_pages": pool_pages, "n_needed": 3 * pages,
+            "ms": {f"{nc}/64": round(tables[nc][2] * 1e3, 3) for nc in fractions},
+            "pool_pages_per_s": {f"{nc}/64": round(pool_pages / tables[nc][2], 0)
+                                 for nc in fractions}}
+    # free the headline pool before the larger rows
+    del arrays, raw_pool, b_lin, c_lin
+    torch.cuda.empty_cache()
+    if "relayout" in want:
+        rows["relayout"] = bench_relayout(torch, sg, synth, ctx, stream, timer)
+    if "gemv" in want:
+        rows["gemv"] = bench_gemv(torch, sg, synth, ctx, stream, timer, args.gemv_launches)
+    if rows:
+        result["rows"] = rows
+
+    if not args.no_cpu:
+        result["cpu_baseline"] = cpu_baseline(np, synth, masks, shift, pages, pool_pages, base,
+                                              b_host, c_host, fractions, args.cpu_passes,
+                                              gpu_pages)
+    err = ctx.device_error()
+    result["device_error_flags"] = err
+    ctx.close()
+    print(json.dumps(result), flush=True)
+
+
+def bench_classify(torch, sg, synth, ctx, stream, timer, n=1 << 26, reps=50):
+    log(f"classify {n} addresses")
+    masks = synth.xor_masks(6, seed=1, min_bit=12)
+    addrs = synth.page_addresses(n, seed=0)
+    d_addrs = torch.from_numpy(addrs.view("int64")).to("cuda:0")
+    d_col = torch.empty(n, dtype=torch.uint8, device="cuda:0")
+    d_hist = torch.empty(64, dtype=torch.int64, device="cuda:0")
+    with torch.cuda.stream(stream):
+        for _ in range(5):
+            sg.colour_classify(ctx, masks, d_addrs, d_col, d_hist, stream)
+        for _ in range(reps):
+            e0 = timer.start()
+            sg.colour_classify(ctx, masks, d_addrs, d_col, d_hist, stream)
+            timer.stop(e0, "classify")
+        torch.cuda.synchronize()
+    d = timer.durations_ms("classify")
+    med = pctl(d, 50)
+    gbs = 9 * n / (med * 1e-3) / 1e9
+    log(f"classify: {med * 1e3:.1f} us  {gbs:.0f} GB/s")
+    return {"what": "2^26 random 4 KiB-aligned addresses, 6 masks, colours + histogram",
+            "median_us": round(med * 1e3, 2), "p99_us": round(pctl(d, 99) * 1e3, 2),
+            "addrs_per_s": round(n / (med * 1e-3), 0), "GBps": round(gbs, 1),
+            "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1), "bytes_per_addr": 9}
+
+
+def bench_relayout(torch, sg, synth, ctx, stream, timer, reps=10):
+    shift = 16
+    P = 1 << shift
+    n_bytes = 4 << 30
+    pages = n_bytes >> shift
+    masks = synth.xor_masks(6, seed=1, min_bit=shift)
+    pool_pages = int(pages * 64 / 16 * 1.04) + 64
+    log(f"relayout 4 GiB fp16, restricted pool {pool_pages} pages")
+    g = torch.Generator(device="cuda:0")
+    g.manual_seed(5)
+    all_form = torch.randint(-32768, 32767, (n_bytes // 2,), dtype=torch.int16, device="cuda:0",
+                             generator=g)
+    ident = torch.arange(pages, dtype=torch.int32, device="cuda:0")
+    raw, base = aligned_pool(torch, pool_pages, shift)
+    pt = torch.empty(pages, dtype=torch.int32, device="cuda:0")
+    sg.colour_alloc_pagetable(ctx, masks, base, shift, pool_pages, range(16), pages, pt, stream)
+    back = torch.empty_like(all_form)
+    A = sg.paged(all_form, ident, pages)
+    S = sg.paged(base, pt, pool_pages)
+    B = sg.paged(back, ident, pages)
+    with torch.cuda.stream(stream):
+        for _ in range(2):
+            sg.bimodal_relayout(ctx, S, A, n_bytes, shift, stream)
+            sg.bimodal_relayout(ctx, B, S, n_bytes, shift, stream)
+        for _ in range(reps):
+            e0 = timer.start()
+            sg.bimodal_relayout(ctx, S, A, n_bytes, shift, stream)
+            timer.stop(e0, "to_restricted")
+            e0 = timer.start()
+            sg.bimodal_relayout(ctx, B, S, n_bytes, shift, stream)
+            timer.stop(e0, "to_all")
+        torch.cuda.synchronize()
+    same = bool(torch.equal(back, all_form))
+    out = {"what": "4 GiB fp16 (65,536 pages of 64 KiB), all colours <-> 16 of 64 colours",
+           "round_trip_identity": same}
+    for tag in ("to_restricted", "to_all"):
+        d = timer.durations_ms(tag)
+        med = pctl(d, 50)
+        gbs = 2 * n_bytes / (med * 1e-3) / 1e9
+        out[tag] = {"median_ms": round(med, 4), "GBps": round(gbs, 1),
+                    "pages_per_s": round(pages / (med * 1e-3), 0),
+                    "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1)}
+        log(f"relayout {tag}: {med:.3f} ms  {gbs:.0f} GB/s")
+    del raw
+    return out
+
+
+def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
+    shift = 21
+    P = 1 << shift
+    copies = 4
+    masks = synth.xor_masks(6, seed=1, min_bit=shift)
+    n_cus = ctx.num_cus
+    out = []
+    g = torch.Generator(device="cuda:0")
+    g.manual_seed(7)
+    x = (torch.randn(8 * 11008, generator=g, device="cuda:0")).to(torch.bfloat16)
+    for (M, K) in [(4096, 11008), (11008, 4096)]:
+        w_bytes = M * K * 2
+        pages = -(-w_bytes // P)
+        pool_pages = int(copies * pages * 64 / 48 * 1.1) + 16
+        raw, base = aligned_pool(torch, pool_pages, shift)
+        pt = torch.empty(copies * pages, dtype=torch.int32, device="cuda:0")
+        sg.colour_alloc_pagetable(ctx, masks, base, shift, pool_pages, range(48), copies * pages,
+                                  pt, stream)
+        w = (torch.randn(M * K, generator=g, device="cuda:0") * 0.02).to(torch.bfloat16)
+        ident = torch.arange(pages, dtype=torch.int32, device="cuda:0")
+        W = []
+        for i in range(copies):
+            Wi = sg.paged(base, pt[i * pages:(i + 1) * pages], pool_pages)
+            sg.bimodal_relayout(ctx, Wi, sg.paged(w, ident, pages), w_bytes, shift, stream)
+            W.append(Wi)
+        y = torch.empty(8 * M, dtype=torch.float32, device="cuda:0")
+        log(f"gemv {M}x{K}: {copies} weight copies rotated")
+        for B in (1, 2, 4, 8):
+            for ncu in (64, 128, 192, 256):
+                if ncu > n_cus:
+                    continue
+                tag = ("gemv", M, B, ncu)
+                with torch.cuda.stream(stream):
+                    sg.set_cu_mask(ctx, stream, range(ncu))
+                    for i in range(20):
+                        sg.colored_gemv(ctx, W[i % copies], sg.BF16, M, K, x, sg.BF16, B, y,
+                                        shift, stream)
+                    for i in range(launches):
+                        e0 = timer.start()
+                        sg.colored_gemv(ctx, W[i % copies], sg.BF16, M, K, x, sg.BF16, B, y,
+                                        shift, stream)
+                        timer.stop(e0, tag)
+                    sg.set_cu_mask(ctx, stream, None)
+                    torch.cuda.synchronize()
+                d = timer.durations_ms(tag)
+                nbytes = M * K * 2 + B * K * 2 + B * M * 4
+                med, p99 = pctl(d, 50), pctl(d, 99)
+                gbs = nbytes / (med * 1e-3) / 1e9
+                out.append({"M": M, "K": K, "batch": B, "cus": ncu,
+                            "path": "mfma" if B >= 5 else "valu",
+                            "p50_us": round(med * 1e3, 2), "p99_us": round(p99 * 1e3, 2),
+                            "GBps": round(gbs, 1),
+                            "pct_of_colour_scaled_peak": round(100 * gbs / (0.75 * HBM_PEAK_GBS), 1),
+                            "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1)})
+                log(f"gemv {M}x{K} B={B} cus={ncu}: p50 {med * 1e3:.1f} us p99 {p99 * 1e3:.1f} us "
+                    f"{gbs:.0f} GB/s")
+        del raw, W
+        torch.cuda.empty_cache()
+    return {"what": "bf16 W on 48/64 colours in 2 MiB pages, bf16 x, fp32 y; "
+                    f"{copies} rotated weight copies; {launches} launches per point",
+            "bytes": "M*K*2 + B*K*2 + B*M*4", "points": out}
+
+
+def cpu_baseline(np, synth, masks, shift, pages, pool_pages, base, b_host, c_host, fractions,
+                 passes, gpu_pages):
+    """The CPU oracle (single-threaded C) on the headline workload: the full
+    arrays, every colour set, ``passes`` passes; page tables from the oracle."""
+    import oracle
+    P = 1 << shift
+    epp = P // 4
+    n = b_host.size
+    log(f"cpu baseline: oracle triad, {passes} passes x {len(fractions)} colour sets")
+    total_s = 0.0
+    elems = 0
+    check = None
+    for nc in fractions:
+        pt, found = oracle.pagetable(masks, base, shift, pool_pages, synth.colour_set_bits(range(nc)),
+                                     3 * pages)
+        assert found >= 3 * pages
+        pa, pb, pc = pt[:pages], pt[pages:2 * pages], pt[2 * pages:]
+        pool = np.zeros(pool_pages * epp, dtype=np.float32)
+        view = pool.reshape(pool_pages, epp)
+        view[pb.astype(np.int64)] = b_host.reshape(pages, epp)
+        view[pc.astype(np.int64)] = c_host.reshape(pages, epp)
+        for _ in range(passes):
+            t0 = time.perf_counter()
+            oracle.triad(pool, pa, pool, pb, pool, pc, 3.0, n, shift)
+            total_s += time.perf_counter() - t0
+            elems += n
+        if nc == 8:
+            check = all(np.array_equal(view[int(pa[j])].view(np.uint32), gpu_pages[j].view(np.uint32))
+                        for j in gpu_pages)
+        del pool, view
+    gbs = 12 * elems / total_s / 1e9
+    log(f"cpu baseline: {total_s:.1f} s, {gbs:.2f} GB/s, sampled GPU pages bit-exact: {check}")
+    return {"value": round(gbs, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"full headline arrays (2^28 elements each), colour sets 8/16/32/64 of 64, "
+                      f"{passes} passes each; {total_s:.1f} s of single-threaded C",
+            "seconds": round(total_s, 2), "gpu_pages_match_oracle": check}
+
+
+if __name__ == "__main__":
+    main()
