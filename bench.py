@@ -3,7 +3,7 @@
 
 Headline workload (the colour-restricted streaming configuration): triad
 a = b + 3c on three 1 GiB fp32 arrays (2^28 elements, U[-1,1)) stored in
-64 KiB pages of one pool, with 6 XOR masks (64 colours) and colour sets of
+64 KiB pages (one pool per colour set), with 6 XOR masks (64 colours) and colour sets of
 8, 16, 32 and 64 of the 64 colours, all CUs enabled.  One step = the four
 triad passes (one per colour set); ``value`` is the algorithmic HBM traffic
 of the timed steps (12 bytes per element per pass) divided by their wall
@@ -114,29 +114,32 @@ def main():
     pages = (n * 4) >> shift
     fractions = [8, 16, 32, 64]
     masks = synth.xor_masks(6, seed=1, min_bit=shift)
-    pool_pages = int(3 * pages * 64 / min(fractions) * 1.04) + 64
-    log(f"pool {pool_pages} pages of 64 KiB ({pool_pages * P / 2**30:.1f} GiB), masks "
-        + " ".join(hex(m) for m in masks))
-    raw_pool, base = aligned_pool(torch, pool_pages, shift)
+    log("masks " + " ".join(hex(m) for m in masks))
     with torch.cuda.stream(stream):
         b_host = synth.uniform_f32(n, seed=2)
         c_host = synth.uniform_f32(n, seed=3)
         b_lin = torch.from_numpy(b_host).to(dev)
         c_lin = torch.from_numpy(c_host).to(dev)
         ident = torch.arange(pages, dtype=torch.int32, device=dev)
+        # one pool per colour set, so that the four page sets never share pages
         tables = {}
         for nc in fractions:
+            pool_pages = int(3 * pages * 64 / nc * 1.04) + 64
+            raw, base = aligned_pool(torch, pool_pages, shift)
             pt = torch.empty(3 * pages, dtype=torch.int32, device=dev)
             t0 = time.perf_counter()
             found = sg.colour_alloc_pagetable(ctx, masks, base, shift, pool_pages, range(nc),
                                               3 * pages, pt, stream)
             t_pt = time.perf_counter() - t0
-            tables[nc] = (pt, found, t_pt)
-        log("page tables built")
+            tables[nc] = {"pt": pt, "found": found, "seconds": t_pt, "raw": raw, "base": base,
+                          "pool_pages": pool_pages}
+            log(f"pool {nc}/64: {pool_pages} pages of 64 KiB ({pool_pages * P / 2**30:.1f} GiB), "
+                f"page table {t_pt * 1e3:.2f} ms")
 
     def paged_arrays(nc):
-        pt = tables[nc][0]
-        return [sg.paged(base, pt[i * pages:(i + 1) * pages], pool_pages) for i in range(3)]
+        t = tables[nc]
+        return [sg.paged(t["base"], t["pt"][i * pages:(i + 1) * pages], t["pool_pages"])
+                for i in range(3)]
 
     def place_inputs(nc):
         a, b, c = paged_arrays(nc)
@@ -179,7 +182,7 @@ def main():
             "GBps": round(gbs, 1), "colour_scaled_peak_GBps": f * HBM_PEAK_GBS,
             "pct_of_colour_scaled_peak": round(100 * gbs / (f * HBM_PEAK_GBS), 1),
             "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1),
-            "pagetable_ms": round(tables[nc][2] * 1e3, 3),
+            "pagetable_ms": round(tables[nc]["seconds"] * 1e3, 3),
         }
         log(f"triad {nc}/64 colours: {med:.4f} ms  {gbs:.0f} GB/s")
     value = args.steps * len(fractions) * bytes_per_pass / wall / 1e9
@@ -207,16 +210,14 @@ def main():
     # ------------------------------------------------------------ sampled check
     # GPU result of the 8/64 pass on a few logical pages (compared against the
     # oracle in the CPU-baseline leg).
-    a8 = arrays[8][0]
+    t8 = tables[8]
     sample_pages = [0, 1, 777, pages - 1]
-    pt8 = tables[8][0][:pages].cpu().numpy().astype(np.int64)
-    pool_view = torch.empty(0)  # placeholder for readability
-    del pool_view
+    pt8 = t8["pt"][:pages].cpu().numpy().astype(np.int64)
     gpu_pages = {}
     for j in sample_pages:
-        addr = base + int(pt8[j]) * P
-        off = addr - raw_pool.data_ptr()
-        gpu_pages[j] = raw_pool[off:off + P].cpu().numpy().view(np.float32).copy()
+        off = t8["base"] + int(pt8[j]) * P - t8["raw"].data_ptr()
+        gpu_pages[j] = t8["raw"][off:off + P].cpu().numpy().view(np.float32).copy()
+    pools_desc = {nc: (tables[nc]["base"], tables[nc]["pool_pages"]) for nc in fractions}
 
     rows = {}
     want = [r for r in args.rows.split(",") if r]
@@ -225,12 +226,13 @@ def main():
     if "pagetable" in want:
         rows["pagetable"] = {
             "what": "colour_alloc_pagetable over the headline pool (synchronous call)",
-            "pool_pages": pool_pages, "n_needed": 3 * pages,
-            "ms": {f"{nc}/64": round(tables[nc][2] * 1e3, 3) for nc in fractions},
-            "pool_pages_per_s": {f"{nc}/64": round(pool_pages / tables[nc][2], 0)
+            "n_needed": 3 * pages,
+            "pool_pages": {f"{nc}/64": tables[nc]["pool_pages"] for nc in fractions},
+            "ms": {f"{nc}/64": round(tables[nc]["seconds"] * 1e3, 3) for nc in fractions},
+            "pool_pages_per_s": {f"{nc}/64": round(tables[nc]["pool_pages"] / tables[nc]["seconds"], 0)
                                  for nc in fractions}}
-    # free the headline pool before the larger rows
-    del arrays, raw_pool, b_lin, c_lin
+    # free the headline pools before the larger rows
+    del arrays, tables, t8, b_lin, c_lin
     torch.cuda.empty_cache()
     if "relayout" in want:
         rows["relayout"] = bench_relayout(torch, sg, synth, ctx, stream, timer)
@@ -240,7 +242,7 @@ def main():
         result["rows"] = rows
 
     if not args.no_cpu:
-        result["cpu_baseline"] = cpu_baseline(np, synth, masks, shift, pages, pool_pages, base,
+        result["cpu_baseline"] = cpu_baseline(np, synth, masks, shift, pages, pools_desc,
                                               b_host, c_host, fractions, args.cpu_passes,
                                               gpu_pages)
     err = ctx.device_error()
@@ -250,25 +252,35 @@ def main():
 
 
 def bench_classify(torch, sg, synth, ctx, stream, timer, n=1 << 26, reps=50):
+    out = {}
+    for hist in (False, True):
+        out["with_histogram" if hist else "colours_only"] = bench_classify_one(
+            torch, sg, synth, ctx, stream, timer, n, reps, hist)
+    return out
+
+
+def bench_classify_one(torch, sg, synth, ctx, stream, timer, n, reps, hist):
     log(f"classify {n} addresses")
     masks = synth.xor_masks(6, seed=1, min_bit=12)
     addrs = synth.page_addresses(n, seed=0)
     d_addrs = torch.from_numpy(addrs.view("int64")).to("cuda:0")
     d_col = torch.empty(n, dtype=torch.uint8, device="cuda:0")
-    d_hist = torch.empty(64, dtype=torch.int64, device="cuda:0")
+    d_hist = torch.empty(64, dtype=torch.int64, device="cuda:0") if hist else None
+    tag = ("classify", hist)
     with torch.cuda.stream(stream):
         for _ in range(5):
             sg.colour_classify(ctx, masks, d_addrs, d_col, d_hist, stream)
         for _ in range(reps):
             e0 = timer.start()
             sg.colour_classify(ctx, masks, d_addrs, d_col, d_hist, stream)
-            timer.stop(e0, "classify")
+            timer.stop(e0, tag)
         torch.cuda.synchronize()
-    d = timer.durations_ms("classify")
+    d = timer.durations_ms(tag)
     med = pctl(d, 50)
     gbs = 9 * n / (med * 1e-3) / 1e9
-    log(f"classify: {med * 1e3:.1f} us  {gbs:.0f} GB/s")
-    return {"what": "2^26 random 4 KiB-aligned addresses, 6 masks, colours + histogram",
+    log(f"classify (histogram {hist}): {med * 1e3:.1f} us  {gbs:.0f} GB/s")
+    return {"what": "2^26 random 4 KiB-aligned addresses, 6 masks"
+                    + (", colours + histogram" if hist else ", colours"),
             "median_us": round(med * 1e3, 2), "p99_us": round(pctl(d, 99) * 1e3, 2),
             "addrs_per_s": round(n / (med * 1e-3), 0), "GBps": round(gbs, 1),
             "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1), "bytes_per_addr": 9}
@@ -384,7 +396,7 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
             "bytes": "M*K*2 + B*K*2 + B*M*4", "points": out}
 
 
-def cpu_baseline(np, synth, masks, shift, pages, pool_pages, base, b_host, c_host, fractions,
+def cpu_baseline(np, synth, masks, shift, pages, pools_desc, b_host, c_host, fractions,
                  passes, gpu_pages):
     """The CPU oracle (single-threaded C) on the headline workload: the full
     arrays, every colour set, ``passes`` passes; page tables from the oracle."""
@@ -397,6 +409,7 @@ def cpu_baseline(np, synth, masks, shift, pages, pool_pages, base, b_host, c_hos
     elems = 0
     check = None
     for nc in fractions:
+        base, pool_pages = pools_desc[nc]
         pt, found = oracle.pagetable(masks, base, shift, pool_pages, synth.colour_set_bits(range(nc)),
                                      3 * pages)
         assert found >= 3 * pages

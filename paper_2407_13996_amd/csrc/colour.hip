@@ -41,6 +41,10 @@ constexpr int kClsPerLane = 16;  // addresses per lane per step (128 bytes)
 constexpr int kClsSteps = 4;
 constexpr uint64_t kClsTile = (uint64_t)kClsThreads * kClsPerLane * kClsSteps;
 
+// Histogram bins are replicated 16 times in LDS (copy = lane % 16) so that
+// the LDS atomics of one wavefront rarely meet on one address.
+constexpr int kHistCopies = 16;
+
 template <int K, bool HIST>
 __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__restrict__ addrs,
                                                           uint64_t n, uint8_t *__restrict__ colours,
@@ -48,9 +52,12 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
                                                           uint64_t *hist_out, uint32_t n_tiles,
                                                           Gate g)
 {
-    __shared__ uint32_t s_hist[HIST ? 256 : 1];
+    constexpr uint32_t kBins = 1u << K;
+    __shared__ uint32_t s_hist[HIST ? kBins * kHistCopies : 1];
+    const uint32_t copy = threadIdx.x % kHistCopies;
     if (HIST) {
-        s_hist[threadIdx.x] = 0;
+        for (uint32_t i = threadIdx.x; i < kBins * kHistCopies; i += kClsThreads)
+            s_hist[i] = 0;
         __syncthreads();
     }
     auto body = [&](uint32_t t, uint32_t, uint32_t &) {
@@ -66,23 +73,23 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
                 uint32_t packed[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
                 for (int j = 0; j < kClsPerLane / 2; ++j) {
-                    uint32_t c0 = colour_of<K>(v[j].x, v[j].y, h);
-                    uint32_t c1 = colour_of<K>(v[j].z, v[j].w, h);
+                    const uint32_t c0 = colour_of<K>(v[j].x, v[j].y, h);
+                    const uint32_t c1 = colour_of<K>(v[j].z, v[j].w, h);
                     packed[j >> 1] |= (c0 | (c1 << 8)) << ((j & 1) * 16);
                     if (HIST) {
-                        atomicAdd(&s_hist[c0], 1u);
-                        atomicAdd(&s_hist[c1], 1u);
+                        atomicAdd(&s_hist[c0 * kHistCopies + copy], 1u);
+                        atomicAdd(&s_hist[c1 * kHistCopies + copy], 1u);
                     }
                 }
                 u32x4 out = {packed[0], packed[1], packed[2], packed[3]};
                 store_nt(colours + i0, out);
             } else if (i0 < n) {
                 for (uint64_t i = i0; i < n; ++i) {
-                    uint64_t a = addrs[i];
-                    uint32_t c = colour_of<K>((uint32_t)a, (uint32_t)(a >> 32), h);
+                    const uint64_t a = addrs[i];
+                    const uint32_t c = colour_of<K>((uint32_t)a, (uint32_t)(a >> 32), h);
                     colours[i] = (uint8_t)c;
                     if (HIST)
-                        atomicAdd(&s_hist[c], 1u);
+                        atomicAdd(&s_hist[c * kHistCopies + copy], 1u);
                 }
             }
         }
@@ -90,25 +97,27 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
     auto flush = [&]() {
         if (HIST) {
             __syncthreads();
-            const uint32_t bins = 1u << K;
-            if (threadIdx.x < bins) {
-                uint32_t v = s_hist[threadIdx.x];
+            for (uint32_t b = threadIdx.x; b < kBins; b += kClsThreads) {
+                uint32_t v = 0;
+#pragma unroll
+                for (int r = 0; r < kHistCopies; ++r) {
+                    v += s_hist[b * kHistCopies + r];
+                    s_hist[b * kHistCopies + r] = 0;
+                }
                 if (v)
-                    __hip_atomic_fetch_add(&hist_acc[threadIdx.x], (uint64_t)v, __ATOMIC_RELAXED,
+                    __hip_atomic_fetch_add(&hist_acc[b], (uint64_t)v, __ATOMIC_RELAXED,
                                            __HIP_MEMORY_SCOPE_AGENT);
-                s_hist[threadIdx.x] = 0;
             }
             __threadfence();
         }
     };
     auto epilogue = [&]() {
         if (HIST) {
-            const uint32_t bins = 1u << K;
-            if (threadIdx.x < bins) {
-                uint64_t v = __hip_atomic_load(&hist_acc[threadIdx.x], __ATOMIC_RELAXED,
-                                               __HIP_MEMORY_SCOPE_AGENT);
-                hist_out[threadIdx.x] = v;
-                __hip_atomic_store(&hist_acc[threadIdx.x], (uint64_t)0, __ATOMIC_RELAXED,
+            for (uint32_t b = threadIdx.x; b < kBins; b += kClsThreads) {
+                const uint64_t v = __hip_atomic_load(&hist_acc[b], __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+                hist_out[b] = v;
+                __hip_atomic_store(&hist_acc[b], (uint64_t)0, __ATOMIC_RELAXED,
                                    __HIP_MEMORY_SCOPE_AGENT);
             }
         }

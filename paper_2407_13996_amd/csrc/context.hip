@@ -80,6 +80,7 @@ int make_gate(Ctx *c, void *stream, uint64_t n_tiles, Gate *g, int *allowed_cus)
     std::memcpy(g->mask, st->mask.bits, sizeof g->mask);
     g->lut = c->d_lut;
     g->q = c->d_queues + st->slot;
+    g->n_allowed = (uint32_t)popcount_mask(st->mask);
     g->err = c->d_err;
     g->log_cu = c->log_cu;
     g->log_tile = c->log_tile;
@@ -91,11 +92,9 @@ int make_gate(Ctx *c, void *stream, uint64_t n_tiles, Gate *g, int *allowed_cus)
 
 uint32_t gated_grid(const Ctx *c, int blocks_per_cu, uint64_t n_tiles, int allowed_cus)
 {
-    uint64_t cap = (uint64_t)blocks_per_cu * (uint64_t)c->num_cus;
-    uint64_t want = (n_tiles * (uint64_t)c->num_cus + (uint64_t)allowed_cus - 1) /
-                    (uint64_t)std::max(allowed_cus, 1);
-    want = std::max<uint64_t>(want, (uint64_t)c->num_cus);
-    return (uint32_t)std::min(want, cap);
+    const uint64_t per_share = (n_tiles + (uint64_t)allowed_cus - 1) / (uint64_t)std::max(allowed_cus, 1);
+    const uint64_t per_cu = std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)blocks_per_cu, per_share));
+    return (uint32_t)(per_cu * (uint64_t)c->num_cus);
 }
 
 int check_hash(const sgdrc_hash *h)
@@ -242,8 +241,8 @@ int sgdrc_init(int device, sgdrc_ctx **out)
         }                                           \
     } while (0)
     TRY(hipMalloc(&c->d_lut, kLutSize * sizeof(uint16_t)));
-    TRY(hipMalloc(&c->d_queues, kMaxStreams * sizeof(TileQueue)));
-    TRY(hipMemset(c->d_queues, 0, kMaxStreams * sizeof(TileQueue)));
+    TRY(hipMalloc(&c->d_queues, kMaxStreams * sizeof(QueueSlot)));
+    TRY(hipMemset(c->d_queues, 0, kMaxStreams * sizeof(QueueSlot)));
     TRY(hipMalloc(&c->d_hist_acc, (size_t)kMaxStreams * kHistBins * sizeof(uint64_t)));
     TRY(hipMemset(c->d_hist_acc, 0, (size_t)kMaxStreams * kHistBins * sizeof(uint64_t)));
     TRY(hipMalloc(&c->d_err, sizeof(uint32_t)));

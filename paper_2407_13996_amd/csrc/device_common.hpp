@@ -1,5 +1,5 @@
 // Device-side building blocks shared by the kernels of libsgdrc:
-// the in-kernel CU gate, the self-resetting atomic tile queue, page-table
+// the in-kernel CU gate, the per-CU atomic tile queues, page-table
 // translation and 16-byte vector types.
 #pragma once
 
@@ -20,24 +20,35 @@ constexpr uint32_t kBadPage = 0xFFFFFFFFu;
 constexpr uint32_t kDevErrPtRange = 1u;
 constexpr uint32_t kDevFlagGateFallback = 2u;
 
-// One work queue per stream.  ``next`` hands out tile indices; ``done``
-// counts finished workgroups so that the last one can reset both, which
-// leaves the queue at zero for the next launch on the same stream.
-struct alignas(128) TileQueue {
-    uint32_t next;
-    uint32_t done;
-    uint32_t pad[30];
+constexpr int kMaxCus = 256;
+constexpr int kCounterStride = 32;  // 32-bit words between counters (128 bytes)
+constexpr int kDoneGroups = 8;
+
+// Work distribution state of one stream.  Tiles are split into contiguous
+// shares, one per allowed CU in logical order; the workgroups resident on a
+// CU take the tiles of its share through that CU's ticket counter, so
+// ticket atomics only contend among workgroups of one CU.  Arrivals are
+// counted in eight groups (blockIdx % 8, whose sizes are known) and then
+// once per group, so that the last workgroup of the grid can be found
+// without every workgroup hitting one address.  That workgroup finishes
+// any share that received no workgroup and zeroes the slot for the next
+// launch on the stream.
+struct QueueSlot {
+    uint32_t cu_next[kMaxCus * kCounterStride];
+    uint32_t done[kDoneGroups * kCounterStride];
+    uint32_t done_all[kCounterStride];
 };
 
 // Per-launch gate arguments (passed by value in the kernel arguments).
 struct Gate {
     uint64_t mask[4];         // logical CUs allowed to work
     const uint16_t *lut;      // hardware key -> logical CU
-    TileQueue *q;             // this stream's queue
+    QueueSlot *q;             // this stream's work distribution state
     uint32_t *err;            // device error / event flags
     uint32_t *log_cu;         // optional: tiles per logical CU
     uint32_t *log_tile;       // optional: visits per tile
     uint64_t log_cap;         // entries of log_tile
+    uint32_t n_allowed;       // number of set bits in mask
 };
 
 __device__ __forceinline__ uint32_t hw_key()
@@ -56,9 +67,30 @@ __device__ __forceinline__ uint32_t my_cu(const Gate &g)
 
 __device__ __forceinline__ bool cu_allowed(const Gate &g, uint32_t cu)
 {
-    if (cu >= 256u)
+    if (cu >= (uint32_t)kMaxCus)
         return false;
     return ((g.mask[cu >> 6] >> (cu & 63u)) & 1ull) != 0ull;
+}
+
+// Position of an allowed CU among the allowed CUs (0-based, logical order).
+__device__ __forceinline__ uint32_t cu_rank(const Gate &g, uint32_t cu)
+{
+    uint32_t r = 0;
+#pragma unroll
+    for (uint32_t w = 0; w < 4; ++w) {
+        const uint64_t m = g.mask[w];
+        if (w < (cu >> 6))
+            r += (uint32_t)__popcll(m);
+        else if (w == (cu >> 6))
+            r += (uint32_t)__popcll(m & ((1ull << (cu & 63u)) - 1ull));
+    }
+    return r;
+}
+
+// First tile of share r when n_tiles are split over n_shares shares.
+__device__ __forceinline__ uint32_t share_begin(uint32_t r, uint32_t n_tiles, uint32_t n_shares)
+{
+    return (uint32_t)(((uint64_t)r * n_tiles) / n_shares);
 }
 
 __device__ __forceinline__ void raise_flag(uint32_t *err, uint32_t bit)
@@ -66,16 +98,15 @@ __device__ __forceinline__ void raise_flag(uint32_t *err, uint32_t bit)
     __hip_atomic_fetch_or(err, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Claim the next tile for the whole workgroup (thread 0 takes the ticket).
-__device__ __forceinline__ uint32_t claim_tile(TileQueue *q, uint32_t *s_ticket)
+// Next ticket of a counter for the whole workgroup (thread 0 takes it).
+__device__ __forceinline__ uint32_t claim_ticket(uint32_t *ctr, uint32_t *s_ticket)
 {
     if (threadIdx.x == 0)
-        *s_ticket = __hip_atomic_fetch_add(&q->next, 1u, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
+        *s_ticket = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
     // the ticket is the same in every lane; make that visible to the
     // compiler so tile bases and page-table reads stay scalar
-    uint32_t t = __builtin_amdgcn_readfirstlane(*s_ticket);
+    const uint32_t t = __builtin_amdgcn_readfirstlane(*s_ticket);
     __syncthreads();
     return t;
 }
@@ -83,7 +114,7 @@ __device__ __forceinline__ uint32_t claim_tile(TileQueue *q, uint32_t *s_ticket)
 __device__ __forceinline__ void log_tile(const Gate &g, uint32_t cu, uint32_t tile)
 {
     if (threadIdx.x == 0) {
-        if (g.log_cu && cu < 256u)
+        if (g.log_cu && cu < (uint32_t)kMaxCus)
             __hip_atomic_fetch_add(&g.log_cu[cu], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (g.log_tile && tile < g.log_cap)
             __hip_atomic_fetch_add(&g.log_tile[tile], 1u, __ATOMIC_RELAXED,
@@ -91,40 +122,54 @@ __device__ __forceinline__ void log_tile(const Gate &g, uint32_t cu, uint32_t ti
     }
 }
 
-// Workgroup arrival at the end of its tile loop.  Returns true (to every
-// thread of the workgroup) for the last workgroup of the grid to arrive.
-// Every workgroup arrives after its last ticket, so the last one sees the
-// final state of the queue.
-__device__ __forceinline__ bool arrive_last(TileQueue *q, uint32_t *s_flag)
+// Workgroup arrival after its tile loop.  Returns true (to every thread of
+// the workgroup) for the last workgroup of the grid to arrive; every
+// workgroup arrives after its last ticket, so that one sees the final
+// state of all counters.
+__device__ __forceinline__ bool arrive_last(QueueSlot *q, uint32_t *s_flag)
 {
     __syncthreads();
     if (threadIdx.x == 0) {
         __threadfence();
-        uint32_t d = __hip_atomic_fetch_add(&q->done, 1u, __ATOMIC_ACQ_REL,
-                                            __HIP_MEMORY_SCOPE_AGENT);
-        *s_flag = (d == gridDim.x - 1u) ? 1u : 0u;
+        const uint32_t G = gridDim.x;
+        const uint32_t grp = blockIdx.x % (uint32_t)kDoneGroups;
+        const uint32_t expected = G / kDoneGroups + (grp < G % kDoneGroups ? 1u : 0u);
+        const uint32_t groups = G < (uint32_t)kDoneGroups ? G : (uint32_t)kDoneGroups;
+        uint32_t last = 0u;
+        const uint32_t d = __hip_atomic_fetch_add(&q->done[grp * kCounterStride], 1u,
+                                                  __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+        if (d == expected - 1u) {
+            const uint32_t e = __hip_atomic_fetch_add(&q->done_all[0], 1u, __ATOMIC_ACQ_REL,
+                                                      __HIP_MEMORY_SCOPE_AGENT);
+            last = e == groups - 1u ? 1u : 0u;
+        }
+        *s_flag = last;
     }
     __syncthreads();
     return *s_flag != 0u;
 }
 
-// Called by the last workgroup only, after all its work: zero the queue.
-__device__ __forceinline__ void reset_queue(TileQueue *q)
+// Called by the last workgroup only, after all its work: zero the slot.
+__device__ __forceinline__ void reset_slot(QueueSlot *q)
 {
     __syncthreads();
-    if (threadIdx.x == 0) {
-        __hip_atomic_store(&q->next, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&q->done, 0u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-    }
+    for (uint32_t i = threadIdx.x; i < (uint32_t)kMaxCus; i += blockDim.x)
+        __hip_atomic_store(&q->cu_next[i * kCounterStride], 0u, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x < (uint32_t)kDoneGroups)
+        __hip_atomic_store(&q->done[threadIdx.x * kCounterStride], 0u, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x == 0)
+        __hip_atomic_store(&q->done_all[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Runs ``body(tile, cu, err)`` for every tile this workgroup obtains, under
-// the gate.  Workgroups on CUs outside the mask take no tiles.  ``flush()``
-// runs after a workgroup's tile loop (to publish per-workgroup partials).
-// The last workgroup to arrive finishes any tiles left over (possible only
-// when no workgroup landed on an allowed CU; flagged), flushes again, calls
-// ``epilogue()`` with every other workgroup's work complete, and resets the
-// queue for the next launch on the stream.
+// Runs ``body(tile, cu, err)`` for every tile of this workgroup's CU share
+// that it obtains, under the gate.  Workgroups on CUs outside the mask take
+// no tiles.  ``flush()`` runs after a workgroup's tile loop (to publish
+// per-workgroup partials).  The last workgroup to arrive finishes the
+// tiles of any share that no workgroup took (possible only when an allowed
+// CU received no workgroup; flagged), flushes again, calls ``epilogue()``
+// with every other workgroup's work complete, and zeroes the slot.
 //
 // Bodies must not return early or branch around the rest of the tile on a
 // per-lane condition: the loop contains barriers, and a lane-dependent exit
@@ -137,35 +182,57 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
 {
     __shared__ uint32_t s_ticket;
     __shared__ uint32_t s_flag;
+    __shared__ uint32_t s_left_lo[kMaxCus], s_left_hi[kMaxCus];
     uint32_t err = 0u;
     const uint32_t cu = my_cu(g);
     if (cu_allowed(g, cu)) {
+        const uint32_t rank = cu_rank(g, cu);
+        const uint32_t lo = share_begin(rank, n_tiles, g.n_allowed);
+        const uint32_t hi = share_begin(rank + 1u, n_tiles, g.n_allowed);
+        uint32_t *ctr = &g.q->cu_next[cu * kCounterStride];
         for (;;) {
-            const uint32_t t = claim_tile(g.q, &s_ticket);
-            if (t >= n_tiles)
+            const uint32_t k = claim_ticket(ctr, &s_ticket);
+            if (k >= hi - lo)
                 break;
-            log_tile(g, cu, t);
-            body(t, cu, err);
+            log_tile(g, cu, lo + k);
+            body(lo + k, cu, err);
         }
         flush();
     }
     if (arrive_last(g.q, &s_flag)) {
-        uint32_t leftover = 0u;
-        for (;;) {
-            const uint32_t t = claim_tile(g.q, &s_ticket);
-            if (t >= n_tiles)
-                break;
-            leftover += 1u;
-            log_tile(g, cu, t);
-            body(t, cu, err);
+        // shares that no workgroup finished: [lo + tickets taken, hi)
+        bool left = false;
+        for (uint32_t c = threadIdx.x; c < (uint32_t)kMaxCus; c += blockDim.x) {
+            uint32_t a = 0u, b = 0u;
+            if (cu_allowed(g, c)) {
+                const uint32_t r = cu_rank(g, c);
+                const uint32_t lo = share_begin(r, n_tiles, g.n_allowed);
+                const uint32_t hi = share_begin(r + 1u, n_tiles, g.n_allowed);
+                const uint32_t taken = __hip_atomic_load(&g.q->cu_next[c * kCounterStride],
+                                                         __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT);
+                a = taken < hi - lo ? lo + taken : hi;
+                b = hi;
+            }
+            s_left_lo[c] = a;
+            s_left_hi[c] = b;
+            left = left || a < b;
         }
-        if (leftover != 0u) {
+        if (__syncthreads_or(left ? 1 : 0)) {
+            for (uint32_t c = 0; c < (uint32_t)kMaxCus; ++c) {
+                const uint32_t a = __builtin_amdgcn_readfirstlane(s_left_lo[c]);
+                const uint32_t b = __builtin_amdgcn_readfirstlane(s_left_hi[c]);
+                for (uint32_t t = a; t < b; ++t) {
+                    log_tile(g, cu, t);
+                    body(t, cu, err);
+                }
+            }
             flush();
             err |= threadIdx.x == 0 ? kDevFlagGateFallback : 0u;
         }
         __syncthreads();
         epilogue();
-        reset_queue(g.q);
+        reset_slot(g.q);
     }
     if (err != 0u)
         raise_flag(g.err, err);

@@ -16,7 +16,7 @@
 namespace sgdrc {
 
 constexpr uint32_t kCtxMagic = 0x53474452u;  // "SGDR"
-constexpr int kMaxStreams = 256;
+constexpr int kMaxStreams = 64;
 constexpr int kHistBins = 256;
 
 struct StreamState {
@@ -33,7 +33,7 @@ struct Ctx {
     sgdrc_cu_mask all_cus{};
 
     uint16_t *d_lut = nullptr;           // kLutSize entries
-    TileQueue *d_queues = nullptr;       // kMaxStreams
+    QueueSlot *d_queues = nullptr;       // kMaxStreams
     uint64_t *d_hist_acc = nullptr;      // kMaxStreams x kHistBins
     uint32_t *d_err = nullptr;           // one word
 
@@ -72,9 +72,10 @@ int stream_state(Ctx *c, void *stream, StreamState **out);
 // Gate arguments for a launch of ``n_tiles`` tiles on ``stream``.
 int make_gate(Ctx *c, void *stream, uint64_t n_tiles, Gate *g, int *allowed_cus);
 
-// Grid size for a gated persistent kernel: enough workgroups that the
-// allowed CUs see about one per tile, at least one per CU, at most what
-// fits on the device at once.
+// Grid size for a gated persistent kernel: the same number of workgroups
+// for every CU (the dispatcher spreads them over all CUs; those on CUs
+// outside the mask leave at once), as many as fit at once but no more than
+// the tiles of one allowed CU's share.
 uint32_t gated_grid(const Ctx *c, int blocks_per_cu, uint64_t n_tiles, int allowed_cus);
 
 int popcount_mask(const sgdrc_cu_mask &m);
