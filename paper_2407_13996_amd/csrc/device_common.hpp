@@ -219,12 +219,21 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
             left = left || a < b;
         }
         if (__syncthreads_or(left ? 1 : 0)) {
-            for (uint32_t c = 0; c < (uint32_t)kMaxCus; ++c) {
-                const uint32_t a = __builtin_amdgcn_readfirstlane(s_left_lo[c]);
-                const uint32_t b = __builtin_amdgcn_readfirstlane(s_left_hi[c]);
-                for (uint32_t t = a; t < b; ++t) {
+            // one flat loop over (share, tile) so that no barrier of the
+            // body ends up in a nested loop
+            uint32_t c = 0u;
+            uint32_t t = __builtin_amdgcn_readfirstlane(s_left_lo[0]);
+            uint32_t end = __builtin_amdgcn_readfirstlane(s_left_hi[0]);
+            while (c < (uint32_t)kMaxCus) {
+                if (t < end) {
                     log_tile(g, cu, t);
                     body(t, cu, err);
+                    t += 1u;
+                } else {
+                    c += 1u;
+                    const uint32_t cc = c < (uint32_t)kMaxCus ? c : 0u;
+                    t = __builtin_amdgcn_readfirstlane(s_left_lo[cc]);
+                    end = c < (uint32_t)kMaxCus ? __builtin_amdgcn_readfirstlane(s_left_hi[cc]) : 0u;
                 }
             }
             flush();
