@@ -108,7 +108,6 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
                     __hip_atomic_fetch_add(&hist_acc[b], (uint64_t)v, __ATOMIC_RELAXED,
                                            __HIP_MEMORY_SCOPE_AGENT);
             }
-            __threadfence();
         }
     };
     auto epilogue = [&]() {

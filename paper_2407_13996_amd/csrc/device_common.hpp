@@ -126,20 +126,29 @@ __device__ __forceinline__ void log_tile(const Gate &g, uint32_t cu, uint32_t ti
 // the workgroup) for the last workgroup of the grid to arrive; every
 // workgroup arrives after its last ticket, so that one sees the final
 // state of all counters.
+//
+// Ordering: every wave first waits for all of its memory operations to
+// complete (the barrier alone only waits for LDS), so the workgroup's
+// ticket and histogram atomics are done before the arrival atomic is
+// issued; the last workgroup reads the counters with device-scope atomic
+// loads issued after its arrival atomic has returned.  All of these are
+// device-scope atomics, coherent across XCDs by themselves, so no fence is
+// used: on gfx950 a device-scope fence writes back and invalidates the
+// whole L2 of the XCD.
 __device__ __forceinline__ bool arrive_last(QueueSlot *q, uint32_t *s_flag)
 {
+    __builtin_amdgcn_s_waitcnt(0);  // vmcnt, expcnt and lgkmcnt all zero
     __syncthreads();
     if (threadIdx.x == 0) {
-        __threadfence();
         const uint32_t G = gridDim.x;
         const uint32_t grp = blockIdx.x % (uint32_t)kDoneGroups;
         const uint32_t expected = G / kDoneGroups + (grp < G % kDoneGroups ? 1u : 0u);
         const uint32_t groups = G < (uint32_t)kDoneGroups ? G : (uint32_t)kDoneGroups;
         uint32_t last = 0u;
         const uint32_t d = __hip_atomic_fetch_add(&q->done[grp * kCounterStride], 1u,
-                                                  __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (d == expected - 1u) {
-            const uint32_t e = __hip_atomic_fetch_add(&q->done_all[0], 1u, __ATOMIC_ACQ_REL,
+            const uint32_t e = __hip_atomic_fetch_add(&q->done_all[0], 1u, __ATOMIC_RELAXED,
                                                       __HIP_MEMORY_SCOPE_AGENT);
             last = e == groups - 1u ? 1u : 0u;
         }
@@ -239,6 +248,7 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
             flush();
             err |= threadIdx.x == 0 ? kDevFlagGateFallback : 0u;
         }
+        __builtin_amdgcn_s_waitcnt(0);  // own partials complete before the epilogue reads
         __syncthreads();
         epilogue();
         reset_slot(g.q);

@@ -30,7 +30,7 @@ constexpr int kGemvRows = 4;     // rows per tile, vector-ALU path
 constexpr int kGemvU = 2;        // 16-byte slices per lane and row in flight
 constexpr int kMfmaRows = 16;    // rows per tile, MFMA path
 constexpr int kMfmaNI = 4;       // MFMAs per wave step
-constexpr int kPtCap = 64;       // page-table entries staged per tile
+constexpr int kPtCap = 256;      // page-table entries staged per tile (one per thread)
 
 template <int DT> struct Dt;
 template <> struct Dt<SGDRC_F32> { static constexpr int size = 4; };
@@ -71,10 +71,10 @@ __device__ __forceinline__ void decode(const uint32_t *w, float *f)
     }
 }
 
-// Page table entries of one tile: either staged in LDS or read directly.
+// Page-table entries of one tile, staged in LDS.  The host guarantees that
+// a tile spans at most kPtCap pages.
 struct TilePages {
     uint64_t p_lo;
-    uint32_t np;
 };
 
 __device__ __forceinline__ TilePages stage_pages(const uint32_t *pt, uint64_t pool_pages,
@@ -83,20 +83,16 @@ __device__ __forceinline__ TilePages stage_pages(const uint32_t *pt, uint64_t po
 {
     TilePages tp;
     tp.p_lo = byte_lo >> shift;
-    tp.np = (uint32_t)(((byte_hi - 1) >> shift) - tp.p_lo + 1);
-    if (tp.np <= (uint32_t)kPtCap && threadIdx.x < tp.np)
+    const uint32_t np = (uint32_t)(((byte_hi - 1) >> shift) - tp.p_lo + 1);
+    if (threadIdx.x < np)
         s_pt[threadIdx.x] = checked_page(pt, tp.p_lo + threadIdx.x, pool_pages, err);
     __syncthreads();
     return tp;
 }
 
-__device__ __forceinline__ uint32_t page_of(const TilePages &tp, const uint32_t *s_pt,
-                                            const uint32_t *pt, uint64_t pool_pages, uint64_t j,
-                                            uint32_t &err)
+__device__ __forceinline__ uint32_t page_of(const TilePages &tp, const uint32_t *s_pt, uint64_t j)
 {
-    if (tp.np <= (uint32_t)kPtCap)
-        return s_pt[j - tp.p_lo];
-    return checked_page(pt, j, pool_pages, err);
+    return s_pt[j - tp.p_lo];
 }
 
 template <int WT, int XT, int NB>
@@ -139,7 +135,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
                     wv[u][r] = u32x4{0u, 0u, 0u, 0u};
                     if (ok && m0 + r < M) {
                         const uint64_t off = (uint64_t)(m0 + r) * row_bytes + (uint64_t)kv * 16u;
-                        const uint32_t p = page_of(tp, s_pt, pt, pool_pages, off >> shift, err);
+                        const uint32_t p = page_of(tp, s_pt, off >> shift);
                         if (p != kBadPage)
                             wv[u][r] = load_nt(w_pool + ((uint64_t)p << shift) + (off & pmask));
                     }
@@ -269,7 +265,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemm_mfma(
                 if (kv < KV) {
                     if (row_ok) {
                         const uint64_t off = (uint64_t)row * row_bytes + (uint64_t)kv * 16u;
-                        const uint32_t p = page_of(tp, s_pt, pt, pool_pages, off >> shift, err);
+                        const uint32_t p = page_of(tp, s_pt, off >> shift);
                         if (p != kBadPage)
                             av[i] = load_nt(w_pool + ((uint64_t)p << shift) + (off & pmask));
                     }
@@ -382,6 +378,15 @@ int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, 
         return rc;
 
     const bool mfma = batch >= 5 && w_dtype == x_dtype && w_dtype != SGDRC_F32;
+    {
+        // a tile's rows must span at most kPtCap pages (they are staged in LDS)
+        const uint64_t rows = mfma ? kMfmaRows : kGemvRows;
+        const uint64_t span = rows * (uint64_t)K * dtype_size(w_dtype);
+        if ((span >> page_shift) + 2 > (uint64_t)kPtCap)
+            return set_error(SGDRC_EINVAL, "rows of %llu bytes span too many %u-byte pages",
+                             (unsigned long long)((uint64_t)K * dtype_size(w_dtype)),
+                             1u << page_shift);
+    }
     GemvKernel k;
     uint64_t n_tiles;
     if (mfma) {
