@@ -76,6 +76,30 @@ class Timer:
         return [a.elapsed_time(b) for t, a, b in self.pairs if tag is None or t == tag]
 
 
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "triad_3x1GiB_64KiB.pmc.md")
+
+
+def recorded_traffic():
+    """Calibrated HBM bytes per triad launch from the committed rocprofv3
+    FETCH_SIZE/WRITE_SIZE summary, or None if the kernel sources changed
+    since the counters were taken (their hash no longer matches)."""
+    import hashlib
+    try:
+        fields = {}
+        for line in open(PMC_SUMMARY):
+            if ":" in line and not line.startswith(("#", "|", "`")):
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
+        h = hashlib.sha256()
+        for f in fields["kernel_sources"].split():
+            h.update(open(os.path.join(ROOT, f), "rb").read())
+        if h.hexdigest()[:16] != fields["kernel_sources_sha256_16"]:
+            return None
+        return int(fields["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def aligned_pool(torch, n_pages, shift):
     """A device byte pool of n_pages pages whose base is page aligned."""
     P = 1 << shift
@@ -189,7 +213,8 @@ def main():
     avg_ms = float(np.mean(all_ms))
     achieved = bytes_per_pass / (avg_ms * 1e-3) / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": recorded_traffic(), "traffic_unit": "bytes per launch",
                 "kernel": "k_triad (64 KiB pages)", "avg_launch_ms": round(avg_ms, 4),
                 "bytes_per_launch": bytes_per_pass}
 
