@@ -43,9 +43,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--rows", default="classify,pagetable,relayout,gemv",
+    ap.add_argument("--rows", default="classify,pagetable,relayout,gemv,corun",
                     help="comma list of extra rows to measure ('' for none)")
     ap.add_argument("--gemv-launches", type=int, default=300)
+    ap.add_argument("--corun-launches", type=int, default=2000)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-passes", type=int, default=3)
     return ap.parse_args()
@@ -263,6 +264,8 @@ def main():
         rows["relayout"] = bench_relayout(torch, sg, synth, ctx, stream, timer)
     if "gemv" in want:
         rows["gemv"] = bench_gemv(torch, sg, synth, ctx, stream, timer, args.gemv_launches)
+    if "corun" in want:
+        rows["corun"] = bench_corun(torch, sg, synth, ctx, args.corun_launches)
     if rows:
         result["rows"] = rows
 
@@ -419,6 +422,129 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
     return {"what": "bf16 W on 48/64 colours in 2 MiB pages, bf16 x, fp32 y; "
                     f"{copies} rotated weight copies; {launches} launches per point",
             "bytes": "M*K*2 + B*K*2 + B*M*4", "points": out}
+
+
+def bench_corun(torch, sg, synth, ctx, ls_launches):
+    """Co-located pair: LS GEMV (bf16 4096x11008, batch 1) on colours 0..47 and
+    CUs 0..191, BE triad (three 2 GiB fp32 arrays, 64 KiB pages) on colours
+    48..63 and CUs 192..255, against the same two kernels uncoloured (identity
+    page tables over contiguous buffers) with the same CU split (the paper's
+    control group) and uncoloured with no CU split.  LS runs a closed loop of
+    ``ls_launches`` kernels; BE streams triads for the whole LS window."""
+    import numpy as np
+    dev = "cuda:0"
+    n_cus = ctx.num_cus
+    ls_cus, be_cus = list(range(n_cus * 3 // 4)), list(range(n_cus * 3 // 4, n_cus))
+    M, K = 4096, 11008
+    g = torch.Generator(device=dev)
+    g.manual_seed(11)
+    # ---- LS operands: W in 2 MiB pages on colours 0..47 (4 rotated copies) and contiguous
+    wshift = 21
+    WP = 1 << wshift
+    wm = synth.xor_masks(6, seed=1, min_bit=wshift)
+    w_bytes = M * K * 2
+    wpages = -(-w_bytes // WP)
+    copies = 4
+    w_lin = (torch.randn(M * K, generator=g, device=dev) * 0.02).to(torch.bfloat16)
+    w_ident = torch.arange(wpages, dtype=torch.int32, device=dev)
+    w_pool_pages = int(copies * wpages * 64 / 48 * 1.1) + 16
+    w_raw, w_base = aligned_pool(torch, w_pool_pages, wshift)
+    w_pt = torch.empty(copies * wpages, dtype=torch.int32, device=dev)
+    sg.colour_alloc_pagetable(ctx, wm, w_base, wshift, w_pool_pages, range(48), copies * wpages, w_pt)
+    W_col = []
+    for i in range(copies):
+        Wi = sg.paged(w_base, w_pt[i * wpages:(i + 1) * wpages], w_pool_pages)
+        sg.bimodal_relayout(ctx, Wi, sg.paged(w_lin, w_ident, wpages), w_bytes, wshift)
+        W_col.append(Wi)
+    w_plain = [torch.empty(wpages * WP // 2, dtype=torch.bfloat16, device=dev) for _ in range(copies)]
+    W_plain = []
+    for i in range(copies):
+        Wi = sg.paged(w_plain[i], w_ident, wpages)
+        sg.bimodal_relayout(ctx, Wi, sg.paged(w_lin, w_ident, wpages), w_bytes, wshift)
+        W_plain.append(Wi)
+    x = torch.randn(K, generator=g, device=dev).to(torch.bfloat16)
+    y = torch.empty(M, dtype=torch.float32, device=dev)
+    # ---- BE operands: three 2 GiB fp32 arrays, 64 KiB pages on colours 48..63, and contiguous
+    shift = 16
+    n = 1 << 29
+    pages = (n * 4) >> shift
+    tm = synth.xor_masks(6, seed=1, min_bit=shift)
+    be_pool_pages = int(3 * pages * 64 / 16 * 1.04) + 64
+    be_raw, be_base = aligned_pool(torch, be_pool_pages, shift)
+    be_pt = torch.empty(3 * pages, dtype=torch.int32, device=dev)
+    sg.colour_alloc_pagetable(ctx, tm, be_base, shift, be_pool_pages, range(48, 64), 3 * pages, be_pt)
+    ident = torch.arange(pages, dtype=torch.int32, device=dev)
+    lin = [torch.empty(n, dtype=torch.float32, device=dev) for _ in range(3)]
+    lin[1].uniform_(-1, 1, generator=g)
+    lin[2].uniform_(-1, 1, generator=g)
+    T_col = [sg.paged(be_base, be_pt[i * pages:(i + 1) * pages], be_pool_pages) for i in range(3)]
+    for i in (1, 2):
+        sg.bimodal_relayout(ctx, T_col[i], sg.paged(lin[i], ident, pages), n * 4, shift)
+    T_plain = [sg.paged(lin[i], ident, pages) for i in range(3)]
+    torch.cuda.synchronize()
+    log(f"corun: LS gemv {M}x{K} on {len(ls_cus)} CUs, BE triad 3x2 GiB on {len(be_cus)} CUs")
+
+    s_ls = torch.cuda.Stream(device=0)
+    s_be = torch.cuda.Stream(device=0)
+
+    def run(Ws, Ts, ls_mask, be_mask, with_be):
+        sg.set_cu_mask(ctx, s_ls, ls_mask)
+        sg.set_cu_mask(ctx, s_be, be_mask)
+        t_ls = Timer(torch, s_ls)
+        t_be = Timer(torch, s_be)
+        for i in range(10):
+            sg.colored_gemv(ctx, Ws[i % copies], sg.BF16, M, K, x, sg.BF16, 1, y, wshift, s_ls)
+        sg.colored_stream(ctx, Ts[0], Ts[1], Ts[2], 3.0, n, shift, s_be)
+        torch.cuda.synchronize()
+        pending = []          # completion events of queued BE launches
+
+        def top_up():
+            while pending and pending[0].query():
+                pending.pop(0)
+            while len(pending) < 2:
+                e0 = t_be.start()
+                sg.colored_stream(ctx, Ts[0], Ts[1], Ts[2], 3.0, n, shift, s_be)
+                t_be.stop(e0)
+                pending.append(t_be.pairs[-1][2])
+
+        if with_be:
+            top_up()
+        for i in range(ls_launches):
+            e0 = t_ls.start()
+            sg.colored_gemv(ctx, Ws[i % copies], sg.BF16, M, K, x, sg.BF16, 1, y, wshift, s_ls)
+            t_ls.stop(e0)
+            if with_be and i % 25 == 0:
+                top_up()
+        if with_be:
+            last_ls = t_ls.pairs[-1][2]
+            while not last_ls.query():
+                top_up()
+                time.sleep(0.0002)
+        torch.cuda.synchronize()
+        out = {}
+        d = np.array(t_ls.durations_ms()) * 1e3
+        out["ls_p50_us"] = round(float(np.percentile(d, 50)), 2)
+        out["ls_p99_us"] = round(float(np.percentile(d, 99)), 2)
+        if with_be:
+            bd = np.array(t_be.durations_ms())
+            out["be_GBps"] = round(12 * n / (float(np.median(bd)) * 1e-3) / 1e9, 1)
+            out["be_launches"] = len(bd)
+        sg.set_cu_mask(ctx, s_ls, None)
+        sg.set_cu_mask(ctx, s_be, None)
+        return out
+
+    res = {"what": "LS bf16 GEMV 4096x11008 batch 1 (closed loop) + BE fp32 triad 3x2 GiB",
+           "ls_launches": ls_launches}
+    res["isolated_ls_coloured_masked"] = run(W_col, T_col, ls_cus, be_cus, with_be=False)
+    res["corun_coloured_masked"] = run(W_col, T_col, ls_cus, be_cus, with_be=True)
+    res["corun_uncoloured_masked"] = run(W_plain, T_plain, ls_cus, be_cus, with_be=True)
+    res["corun_uncoloured_unmasked"] = run(W_plain, T_plain, None, None, with_be=True)
+    for k in ("isolated_ls_coloured_masked", "corun_coloured_masked", "corun_uncoloured_masked",
+              "corun_uncoloured_unmasked"):
+        log(f"corun {k}: {res[k]}")
+    del w_raw, be_raw, lin, w_plain
+    torch.cuda.empty_cache()
+    return res
 
 
 def cpu_baseline(np, synth, masks, shift, pages, pools_desc, b_host, c_host, fractions,
