@@ -80,7 +80,21 @@ int make_gate(Ctx *c, void *stream, uint64_t n_tiles, Gate *g, int *allowed_cus)
     std::memcpy(g->mask, st->mask.bits, sizeof g->mask);
     g->lut = c->d_lut;
     g->q = c->d_queues + st->slot;
-    g->n_allowed = (uint32_t)popcount_mask(st->mask);
+    // split the tiles over the CU groups in proportion to their allowed CUs
+    uint64_t allowed[kMaxGroups] = {};
+    uint64_t total = 0;
+    for (int grp = 0; grp < c->n_groups; ++grp) {
+        for (int cu = c->grp_first_cu[grp]; cu < c->grp_first_cu[grp + 1]; ++cu)
+            allowed[grp] += (st->mask.bits[cu >> 6] >> (cu & 63)) & 1ull;
+        total += allowed[grp];
+    }
+    uint64_t cum = 0;
+    g->grp_tile[0] = 0;
+    for (int grp = 0; grp < kMaxGroups; ++grp) {
+        cum += grp < c->n_groups ? allowed[grp] : 0;
+        g->grp_tile[grp + 1] = (uint32_t)(total ? n_tiles * cum / total : n_tiles);
+    }
+    g->n_groups = (uint32_t)c->n_groups;
     g->err = c->d_err;
     g->log_cu = c->log_cu;
     g->log_tile = c->log_tile;
@@ -175,18 +189,28 @@ static int probe_topology(Ctx *c, int expected)
     if (expected > SGDRC_MAX_CUS)
         return set_error(SGDRC_ENODEV, "device has %d CUs, more than %d", expected,
                          SGDRC_MAX_CUS);
-    std::vector<uint16_t> lut(kLutSize, kLutNone);
+    // groups: CUs of one XCC (key bits 11:8), in key order
+    std::vector<uint32_t> lut(kLutSize, kLutNone);
+    int n_groups = 0;
     for (int i = 0; i < expected; ++i) {
         if (uniq[i] >= (uint32_t)kLutSize)
             return set_error(SGDRC_ENODEV, "CU key 0x%x out of range", uniq[i]);
+        if (i == 0 || (uniq[i] >> 8) != (uniq[i - 1] >> 8)) {
+            if (n_groups == kMaxGroups)
+                return set_error(SGDRC_ENODEV, "more than %d XCCs", kMaxGroups);
+            c->grp_first_cu[n_groups++] = i;
+        }
         c->keys[i] = uniq[i];
-        lut[uniq[i]] = (uint16_t)i;
+        lut[uniq[i]] = (uint32_t)i | ((uint32_t)(n_groups - 1) << 16);
     }
+    c->n_groups = n_groups;
+    for (int grp = n_groups; grp <= kMaxGroups; ++grp)
+        c->grp_first_cu[grp] = expected;
     c->num_cus = expected;
     std::memset(&c->all_cus, 0, sizeof c->all_cus);
     for (int i = 0; i < expected; ++i)
         c->all_cus.bits[i >> 6] |= 1ull << (i & 63);
-    SGDRC_HIP(hipMemcpy(c->d_lut, lut.data(), kLutSize * sizeof(uint16_t), hipMemcpyHostToDevice));
+    SGDRC_HIP(hipMemcpy(c->d_lut, lut.data(), kLutSize * sizeof(uint32_t), hipMemcpyHostToDevice));
     return SGDRC_OK;
 }
 
@@ -240,7 +264,7 @@ int sgdrc_init(int device, sgdrc_ctx **out)
             return rc;                              \
         }                                           \
     } while (0)
-    TRY(hipMalloc(&c->d_lut, kLutSize * sizeof(uint16_t)));
+    TRY(hipMalloc(&c->d_lut, kLutSize * sizeof(uint32_t)));
     TRY(hipMalloc(&c->d_queues, kMaxStreams * sizeof(QueueSlot)));
     TRY(hipMemset(c->d_queues, 0, kMaxStreams * sizeof(QueueSlot)));
     TRY(hipMalloc(&c->d_hist_acc, (size_t)kMaxStreams * kHistBins * sizeof(uint64_t)));

@@ -14,41 +14,44 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kLutSize = 4096;          // (XCC_ID[3:0] << 8) | HW_ID[15:8]
-constexpr uint16_t kLutNone = 0xFFFFu;  // key never seen by the probe
+constexpr uint32_t kLutNone = 0xFFFFFFFFu;  // key never seen by the probe
 constexpr uint32_t kBadPage = 0xFFFFFFFFu;
 
 constexpr uint32_t kDevErrPtRange = 1u;
 constexpr uint32_t kDevFlagGateFallback = 2u;
 
 constexpr int kMaxCus = 256;
+constexpr int kMaxGroups = 16;      // CU groups = XCDs (XCC_ID has 4 bits)
 constexpr int kCounterStride = 32;  // 32-bit words between counters (128 bytes)
 constexpr int kDoneGroups = 8;
 
 // Work distribution state of one stream.  Tiles are split into contiguous
-// shares, one per allowed CU in logical order; the workgroups resident on a
-// CU take the tiles of its share through that CU's ticket counter, so
-// ticket atomics only contend among workgroups of one CU.  Arrivals are
-// counted in eight groups (blockIdx % 8, whose sizes are known) and then
-// once per group, so that the last workgroup of the grid can be found
-// without every workgroup hitting one address.  That workgroup finishes
-// any share that received no workgroup and zeroes the slot for the next
-// launch on the stream.
+// ranges, one per CU group (XCD) in proportion to the allowed CUs of the
+// group; the workgroups resident on a group's CUs claim that range in order
+// through the group's ticket counter, which balances load dynamically
+// inside an XCD while ticket atomics spread over one counter per XCD.
+// Arrivals are counted in eight groups (blockIdx % 8, whose sizes are
+// known) and then once per group, so that the last workgroup of the grid
+// can be found without every workgroup hitting one address.  That
+// workgroup finishes any range that no workgroup took and zeroes the slot
+// for the next launch on the stream.
 struct QueueSlot {
-    uint32_t cu_next[kMaxCus * kCounterStride];
+    uint32_t grp_next[kMaxGroups * kCounterStride];
     uint32_t done[kDoneGroups * kCounterStride];
     uint32_t done_all[kCounterStride];
 };
 
 // Per-launch gate arguments (passed by value in the kernel arguments).
 struct Gate {
-    uint64_t mask[4];         // logical CUs allowed to work
-    const uint16_t *lut;      // hardware key -> logical CU
-    QueueSlot *q;             // this stream's work distribution state
-    uint32_t *err;            // device error / event flags
-    uint32_t *log_cu;         // optional: tiles per logical CU
-    uint32_t *log_tile;       // optional: visits per tile
-    uint64_t log_cap;         // entries of log_tile
-    uint32_t n_allowed;       // number of set bits in mask
+    uint64_t mask[4];            // logical CUs allowed to work
+    const uint32_t *lut;         // hardware key -> logical CU | group << 16
+    QueueSlot *q;                // this stream's work distribution state
+    uint32_t *err;               // device error / event flags
+    uint32_t *log_cu;            // optional: tiles per logical CU
+    uint32_t *log_tile;          // optional: visits per tile
+    uint64_t log_cap;            // entries of log_tile
+    uint32_t grp_tile[kMaxGroups + 1];  // first tile of each group's range
+    uint32_t n_groups;
 };
 
 __device__ __forceinline__ uint32_t hw_key()
@@ -59,8 +62,9 @@ __device__ __forceinline__ uint32_t hw_key()
     return ((xcc & 0xFu) << 8) | ((hw >> 8) & 0xFFu);
 }
 
-// Logical CU of the executing workgroup, or kLutNone.
-__device__ __forceinline__ uint32_t my_cu(const Gate &g)
+// LUT entry of the executing workgroup's CU: logical CU | group << 16, or
+// kLutNone.  The key comes from scalar registers, so this is a scalar load.
+__device__ __forceinline__ uint32_t my_cu_entry(const Gate &g)
 {
     return g.lut[hw_key()];
 }
@@ -70,27 +74,6 @@ __device__ __forceinline__ bool cu_allowed(const Gate &g, uint32_t cu)
     if (cu >= (uint32_t)kMaxCus)
         return false;
     return ((g.mask[cu >> 6] >> (cu & 63u)) & 1ull) != 0ull;
-}
-
-// Position of an allowed CU among the allowed CUs (0-based, logical order).
-__device__ __forceinline__ uint32_t cu_rank(const Gate &g, uint32_t cu)
-{
-    uint32_t r = 0;
-#pragma unroll
-    for (uint32_t w = 0; w < 4; ++w) {
-        const uint64_t m = g.mask[w];
-        if (w < (cu >> 6))
-            r += (uint32_t)__popcll(m);
-        else if (w == (cu >> 6))
-            r += (uint32_t)__popcll(m & ((1ull << (cu & 63u)) - 1ull));
-    }
-    return r;
-}
-
-// First tile of share r when n_tiles are split over n_shares shares.
-__device__ __forceinline__ uint32_t share_begin(uint32_t r, uint32_t n_tiles, uint32_t n_shares)
-{
-    return (uint32_t)(((uint64_t)r * n_tiles) / n_shares);
 }
 
 __device__ __forceinline__ void raise_flag(uint32_t *err, uint32_t bit)
@@ -162,8 +145,8 @@ __device__ __forceinline__ bool arrive_last(QueueSlot *q, uint32_t *s_flag)
 __device__ __forceinline__ void reset_slot(QueueSlot *q)
 {
     __syncthreads();
-    for (uint32_t i = threadIdx.x; i < (uint32_t)kMaxCus; i += blockDim.x)
-        __hip_atomic_store(&q->cu_next[i * kCounterStride], 0u, __ATOMIC_RELAXED,
+    if (threadIdx.x < (uint32_t)kMaxGroups)
+        __hip_atomic_store(&q->grp_next[threadIdx.x * kCounterStride], 0u, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
     if (threadIdx.x < (uint32_t)kDoneGroups)
         __hip_atomic_store(&q->done[threadIdx.x * kCounterStride], 0u, __ATOMIC_RELAXED,
@@ -172,13 +155,14 @@ __device__ __forceinline__ void reset_slot(QueueSlot *q)
         __hip_atomic_store(&q->done_all[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Runs ``body(tile, cu, err)`` for every tile of this workgroup's CU share
-// that it obtains, under the gate.  Workgroups on CUs outside the mask take
-// no tiles.  ``flush()`` runs after a workgroup's tile loop (to publish
-// per-workgroup partials).  The last workgroup to arrive finishes the
-// tiles of any share that no workgroup took (possible only when an allowed
-// CU received no workgroup; flagged), flushes again, calls ``epilogue()``
-// with every other workgroup's work complete, and zeroes the slot.
+// Runs ``body(tile, cu, err)`` for every tile of this workgroup's group
+// range that it obtains, under the gate.  Workgroups on CUs outside the
+// mask take no tiles.  ``flush()`` runs after a workgroup's tile loop (to
+// publish per-workgroup partials).  The last workgroup to arrive finishes
+// the tiles of any range that no workgroup took (possible only when no
+// workgroup landed on an allowed CU of some group; flagged), flushes again,
+// calls ``epilogue()`` with every other workgroup's work complete, and
+// zeroes the slot.
 //
 // Bodies must not return early or branch around the rest of the tile on a
 // per-lane condition: the loop contains barriers, and a lane-dependent exit
@@ -191,58 +175,63 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
 {
     __shared__ uint32_t s_ticket;
     __shared__ uint32_t s_flag;
-    __shared__ uint32_t s_left_lo[kMaxCus], s_left_hi[kMaxCus];
+    __shared__ uint32_t s_left_lo[kMaxGroups], s_left_hi[kMaxGroups];
     uint32_t err = 0u;
-    const uint32_t cu = my_cu(g);
-    if (cu_allowed(g, cu)) {
-        const uint32_t rank = cu_rank(g, cu);
-        const uint32_t lo = share_begin(rank, n_tiles, g.n_allowed);
-        const uint32_t hi = share_begin(rank + 1u, n_tiles, g.n_allowed);
-        uint32_t *ctr = &g.q->cu_next[cu * kCounterStride];
-        for (;;) {
-            const uint32_t k = claim_ticket(ctr, &s_ticket);
-            if (k >= hi - lo)
-                break;
+    const uint32_t entry = my_cu_entry(g);
+    const uint32_t cu = entry & 0xFFFFu;
+    if (entry != kLutNone && cu_allowed(g, cu)) {
+        const uint32_t grp = entry >> 16;
+        const uint32_t lo = g.grp_tile[grp], hi = g.grp_tile[grp + 1u];
+        uint32_t *ctr = &g.q->grp_next[grp * kCounterStride];
+        // the next ticket is requested before the body runs, so its atomic
+        // round trip overlaps the tile's memory traffic
+        uint32_t k = claim_ticket(ctr, &s_ticket);
+        while (k < hi - lo) {
+            uint32_t next = 0u;
+            if (threadIdx.x == 0)
+                next = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             log_tile(g, cu, lo + k);
             body(lo + k, cu, err);
+            if (threadIdx.x == 0)
+                s_ticket = next;
+            __syncthreads();
+            k = __builtin_amdgcn_readfirstlane(s_ticket);
+            __syncthreads();
         }
         flush();
     }
     if (arrive_last(g.q, &s_flag)) {
-        // shares that no workgroup finished: [lo + tickets taken, hi)
+        // ranges that no workgroup finished: [lo + tickets taken, hi), then
+        // worked through in one flat loop so that no barrier of the body
+        // ends up in a nested loop
         bool left = false;
-        for (uint32_t c = threadIdx.x; c < (uint32_t)kMaxCus; c += blockDim.x) {
+        if (threadIdx.x < (uint32_t)kMaxGroups) {
             uint32_t a = 0u, b = 0u;
-            if (cu_allowed(g, c)) {
-                const uint32_t r = cu_rank(g, c);
-                const uint32_t lo = share_begin(r, n_tiles, g.n_allowed);
-                const uint32_t hi = share_begin(r + 1u, n_tiles, g.n_allowed);
-                const uint32_t taken = __hip_atomic_load(&g.q->cu_next[c * kCounterStride],
-                                                         __ATOMIC_RELAXED,
-                                                         __HIP_MEMORY_SCOPE_AGENT);
+            if (threadIdx.x < g.n_groups) {
+                const uint32_t lo = g.grp_tile[threadIdx.x], hi = g.grp_tile[threadIdx.x + 1u];
+                const uint32_t taken = __hip_atomic_load(&g.q->grp_next[threadIdx.x * kCounterStride],
+                                                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 a = taken < hi - lo ? lo + taken : hi;
                 b = hi;
             }
-            s_left_lo[c] = a;
-            s_left_hi[c] = b;
-            left = left || a < b;
+            s_left_lo[threadIdx.x] = a;
+            s_left_hi[threadIdx.x] = b;
+            left = a < b;
         }
         if (__syncthreads_or(left ? 1 : 0)) {
-            // one flat loop over (share, tile) so that no barrier of the
-            // body ends up in a nested loop
             uint32_t c = 0u;
             uint32_t t = __builtin_amdgcn_readfirstlane(s_left_lo[0]);
             uint32_t end = __builtin_amdgcn_readfirstlane(s_left_hi[0]);
-            while (c < (uint32_t)kMaxCus) {
+            while (c < (uint32_t)kMaxGroups) {
                 if (t < end) {
                     log_tile(g, cu, t);
                     body(t, cu, err);
                     t += 1u;
                 } else {
                     c += 1u;
-                    const uint32_t cc = c < (uint32_t)kMaxCus ? c : 0u;
+                    const uint32_t cc = c < (uint32_t)kMaxGroups ? c : 0u;
                     t = __builtin_amdgcn_readfirstlane(s_left_lo[cc]);
-                    end = c < (uint32_t)kMaxCus ? __builtin_amdgcn_readfirstlane(s_left_hi[cc]) : 0u;
+                    end = c < (uint32_t)kMaxGroups ? __builtin_amdgcn_readfirstlane(s_left_hi[cc]) : 0u;
                 }
             }
             flush();

@@ -27,7 +27,6 @@ typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 constexpr int kGemvThreads = 256;
 constexpr int kGemvWaves = kGemvThreads / 64;
 constexpr int kGemvRows = 4;     // rows per tile, vector-ALU path
-constexpr int kGemvU = 2;        // 16-byte slices per lane and row in flight
 constexpr int kMfmaRows = 16;    // rows per tile, MFMA path
 constexpr int kMfmaNI = 4;       // MFMAs per wave step
 constexpr int kPtCap = 256;      // page-table entries staged per tile (one per thread)
@@ -104,6 +103,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
     constexpr int WSZ = Dt<WT>::size, XSZ = Dt<XT>::size;
     constexpr int EPV = 16 / WSZ;                 // elements per 16-byte slice of W
     constexpr int XW = EPV * XSZ / 4;             // 32-bit words of x per slice and batch
+    constexpr int kGemvU = NB <= 2 ? 4 : 2;       // 16-byte slices per lane and row in flight
     __shared__ uint32_t s_pt[kPtCap];
     __shared__ float s_red[kGemvWaves][kGemvRows * NB];
     const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63u;

@@ -31,8 +31,10 @@ struct Ctx {
     int num_cus = 0;
     uint32_t keys[SGDRC_MAX_CUS] = {};   // logical CU -> hardware key
     sgdrc_cu_mask all_cus{};
+    int n_groups = 0;                    // CU groups (XCDs)
+    int grp_first_cu[kMaxGroups + 1] = {};  // logical CUs of group g: [first[g], first[g+1])
 
-    uint16_t *d_lut = nullptr;           // kLutSize entries
+    uint32_t *d_lut = nullptr;           // kLutSize entries: logical CU | group << 16
     QueueSlot *d_queues = nullptr;       // kMaxStreams
     uint64_t *d_hist_acc = nullptr;      // kMaxStreams x kHistBins
     uint32_t *d_err = nullptr;           // one word
