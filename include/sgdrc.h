@@ -127,6 +127,16 @@ int sgdrc_last_tiles(sgdrc_ctx *ctx, void *stream, uint64_t *tiles);
 
 /* ------------------------------------------------------------- operations */
 
+/* Cap on the workgroups that later launches on ``stream`` place on each CU
+ * (0 = as many as fit, the default).  The hardware sends workgroup i of a
+ * grid to XCD i mod (number of XCDs), whatever the CU mask, and a workgroup
+ * outside the mask only leaves after it has been placed.  A long persistent
+ * kernel that fills its CUs completely would therefore hold back the stray
+ * workgroups of short kernels on other streams until it ends; co-located
+ * streams give the long-running one a cap below its occupancy to leave room.
+ * Host-only.  EINVAL: cap above 64. */
+int sgdrc_set_stream_occupancy(sgdrc_ctx *ctx, void *stream, uint32_t max_wgs_per_cu);
+
 /* Tidal compute-unit masking (paper section 7.1, Elastic SM Scaling; the
  * per-launch TPC mask there is replaced by an in-kernel gate).  Sets the CU
  * set used by every later launch on ``stream``: each workgroup reads its
@@ -141,8 +151,9 @@ int set_cu_mask(sgdrc_ctx *ctx, void *stream, const sgdrc_cu_mask *mask);
  * colour; the hash is the linear XOR form discussed in section 3.2).
  * d_colours[i] = colour(d_addrs[i]) for i < n.  If d_hist != NULL it
  * receives the number of addresses of each colour (2^K uint64 entries,
- * overwritten).  d_addrs must be 8-byte aligned.  n == 0 is valid (hist is
- * zeroed).  EINVAL: bad hash, NULL pointers with n > 0. */
+ * overwritten).  d_addrs and d_colours must be 16-byte aligned, d_hist
+ * 8-byte aligned.  n == 0 is valid (hist is zeroed).  EINVAL: bad hash,
+ * NULL pointers with n > 0, misaligned pointers. */
 int colour_classify(sgdrc_ctx *ctx, const sgdrc_hash *hash, const uint64_t *d_addrs,
                     uint64_t n, uint8_t *d_colours, uint64_t *d_hist, void *stream);
 

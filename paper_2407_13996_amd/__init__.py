@@ -72,6 +72,7 @@ def lib() -> ctypes.CDLL:
             "sgdrc_set_worklog": ([vp, vp, vp, u64], i32),
             "sgdrc_last_tiles": ([vp, vp, P(u64)], i32),
             "set_cu_mask": ([vp, vp, P(CuMask)], i32),
+            "sgdrc_set_stream_occupancy": ([vp, vp, u32], i32),
             "colour_classify": ([vp, P(Hash), vp, u64, vp, vp, vp], i32),
             "colour_alloc_pagetable": ([vp, P(Hash), u64, u32, u64, P(ColourSet), u64, vp,
                                         P(u64), vp], i32),
@@ -195,6 +196,11 @@ def set_cu_mask(ctx, stream, cus) -> None:
     """cus: iterable of logical CU indices, or None for all CUs."""
     m = None if cus is None else ctypes.byref(make_set(words_of(cus), CuMask))
     _check(lib().set_cu_mask(_h(ctx), _stream(stream), m))
+
+
+def set_stream_occupancy(ctx, stream, max_wgs_per_cu: int) -> None:
+    """Cap the workgroups per CU of later launches on ``stream`` (0 = no cap)."""
+    _check(lib().sgdrc_set_stream_occupancy(_h(ctx), _stream(stream), int(max_wgs_per_cu)))
 
 
 def colour_classify(ctx, masks, addrs, colours, hist=None, stream=None) -> None:

@@ -227,20 +227,20 @@ static int launch_classify(Ctx *c, const HashArgs &h, const uint64_t *d_addrs, u
     if (n_tiles >= (1ull << 31))
         return set_error(SGDRC_EINVAL, "n too large");
     Gate g;
-    int allowed = 0;
-    int rc = make_gate(c, stream, n_tiles, &g, &allowed);
+    LaunchInfo li;
+    int rc = make_gate(c, stream, n_tiles, kStreamGroupCus, &g, &li);
     if (rc)
         return rc;
     uint64_t *acc = c->d_hist_acc + (size_t)(g.q - c->d_queues) * kHistBins;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (d_hist) {
         static const int occ = occupancy(k_classify<K, true>, kClsThreads);
-        uint32_t grid = gated_grid(c, occ, n_tiles, allowed);
+        uint32_t grid = gated_grid(c, occ, n_tiles, li);
         hipLaunchKernelGGL((k_classify<K, true>), dim3(grid), dim3(kClsThreads), 0, s, d_addrs, n,
                            d_colours, h, acc, d_hist, (uint32_t)n_tiles, g);
     } else {
         static const int occ = occupancy(k_classify<K, false>, kClsThreads);
-        uint32_t grid = gated_grid(c, occ, n_tiles, allowed);
+        uint32_t grid = gated_grid(c, occ, n_tiles, li);
         hipLaunchKernelGGL((k_classify<K, false>), dim3(grid), dim3(kClsThreads), 0, s, d_addrs,
                            n, d_colours, h, acc, d_hist, (uint32_t)n_tiles, g);
     }

@@ -70,7 +70,7 @@ int stream_state(Ctx *c, void *stream, StreamState **out)
     return SGDRC_OK;
 }
 
-int make_gate(Ctx *c, void *stream, uint64_t n_tiles, Gate *g, int *allowed_cus)
+int make_gate(Ctx *c, void *stream, uint64_t n_tiles, int group_cus, Gate *g, LaunchInfo *li)
 {
     StreamState *st = nullptr;
     int rc = stream_state(c, stream, &st);
@@ -80,34 +80,54 @@ int make_gate(Ctx *c, void *stream, uint64_t n_tiles, Gate *g, int *allowed_cus)
     std::memcpy(g->mask, st->mask.bits, sizeof g->mask);
     g->lut = c->d_lut;
     g->q = c->d_queues + st->slot;
-    // split the tiles over the CU groups in proportion to their allowed CUs
-    uint64_t allowed[kMaxGroups] = {};
-    uint64_t total = 0;
-    for (int grp = 0; grp < c->n_groups; ++grp) {
-        for (int cu = c->grp_first_cu[grp]; cu < c->grp_first_cu[grp + 1]; ++cu)
-            allowed[grp] += (st->mask.bits[cu >> 6] >> (cu & 63)) & 1ull;
-        total += allowed[grp];
-    }
-    uint64_t cum = 0;
-    g->grp_tile[0] = 0;
-    for (int grp = 0; grp < kMaxGroups; ++grp) {
-        cum += grp < c->n_groups ? allowed[grp] : 0;
-        g->grp_tile[grp + 1] = (uint32_t)(total ? n_tiles * cum / total : n_tiles);
-    }
-    g->n_groups = (uint32_t)c->n_groups;
     g->err = c->d_err;
     g->log_cu = c->log_cu;
     g->log_tile = c->log_tile;
     g->log_cap = c->log_cap;
+    // queue groups: runs of group_cus CUs inside each XCD
+    uint32_t shift = 0;
+    while ((1 << (shift + 1)) <= group_cus && shift < 5)
+        ++shift;
+    uint64_t allowed[kMaxGroups] = {};
+    uint64_t total = 0;
+    int n_groups = 0;
+    std::memset(g->grp_base, 0, sizeof g->grp_base);
+    for (int x = 0; x < c->n_xcds; ++x) {
+        const int first = c->xcd_first_cu[x], count = c->xcd_first_cu[x + 1] - first;
+        const int subs = (count + (1 << shift) - 1) >> shift;
+        if (n_groups + subs > kMaxGroups)
+            return set_error(SGDRC_EINVAL, "too many queue groups");
+        g->grp_base[x] = (uint8_t)n_groups;
+        for (int i = 0; i < count; ++i) {
+            const int cu = first + i;
+            const uint64_t bit = (st->mask.bits[cu >> 6] >> (cu & 63)) & 1ull;
+            allowed[n_groups + (i >> shift)] += bit;
+            total += bit;
+        }
+        n_groups += subs;
+    }
+    uint64_t cum = 0;
+    g->grp_tile[0] = 0;
+    for (int grp = 0; grp < kMaxGroups; ++grp) {
+        cum += allowed[grp];
+        g->grp_tile[grp + 1] = (uint32_t)(total ? n_tiles * cum / total : n_tiles);
+    }
+    g->n_groups = (uint32_t)n_groups;
+    g->grp_shift = shift;
     st->last_tiles = n_tiles;
-    *allowed_cus = popcount_mask(st->mask);
+    li->allowed = (int)total;
+    li->wg_cap = st->wg_cap;
     return SGDRC_OK;
 }
 
-uint32_t gated_grid(const Ctx *c, int blocks_per_cu, uint64_t n_tiles, int allowed_cus)
+uint32_t gated_grid(const Ctx *c, int blocks_per_cu, uint64_t n_tiles, const LaunchInfo &li)
 {
-    const uint64_t per_share = (n_tiles + (uint64_t)allowed_cus - 1) / (uint64_t)std::max(allowed_cus, 1);
-    const uint64_t per_cu = std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)blocks_per_cu, per_share));
+    uint64_t fit = (uint64_t)blocks_per_cu;
+    if (li.wg_cap)
+        fit = std::min<uint64_t>(fit, li.wg_cap);
+    const uint64_t allowed = (uint64_t)std::max(li.allowed, 1);
+    const uint64_t per_cu_tiles = (n_tiles + allowed - 1) / allowed;
+    const uint64_t per_cu = std::max<uint64_t>(1, std::min<uint64_t>(fit, per_cu_tiles));
     return (uint32_t)(per_cu * (uint64_t)c->num_cus);
 }
 
@@ -189,23 +209,26 @@ static int probe_topology(Ctx *c, int expected)
     if (expected > SGDRC_MAX_CUS)
         return set_error(SGDRC_ENODEV, "device has %d CUs, more than %d", expected,
                          SGDRC_MAX_CUS);
-    // groups: CUs of one XCC (key bits 11:8), in key order
+    // XCDs: CUs with the same XCC_ID (key bits 11:8), in key order
     std::vector<uint32_t> lut(kLutSize, kLutNone);
-    int n_groups = 0;
+    int n_xcds = 0;
     for (int i = 0; i < expected; ++i) {
         if (uniq[i] >= (uint32_t)kLutSize)
             return set_error(SGDRC_ENODEV, "CU key 0x%x out of range", uniq[i]);
         if (i == 0 || (uniq[i] >> 8) != (uniq[i - 1] >> 8)) {
-            if (n_groups == kMaxGroups)
-                return set_error(SGDRC_ENODEV, "more than %d XCCs", kMaxGroups);
-            c->grp_first_cu[n_groups++] = i;
+            if (n_xcds == kMaxXcds)
+                return set_error(SGDRC_ENODEV, "more than %d XCCs", kMaxXcds);
+            c->xcd_first_cu[n_xcds++] = i;
         }
+        const uint32_t in_xcd = (uint32_t)(i - c->xcd_first_cu[n_xcds - 1]);
+        if (in_xcd > 255u)
+            return set_error(SGDRC_ENODEV, "more than 256 CUs in one XCC");
         c->keys[i] = uniq[i];
-        lut[uniq[i]] = (uint32_t)i | ((uint32_t)(n_groups - 1) << 16);
+        lut[uniq[i]] = (uint32_t)i | ((uint32_t)(n_xcds - 1) << 16) | (in_xcd << 24);
     }
-    c->n_groups = n_groups;
-    for (int grp = n_groups; grp <= kMaxGroups; ++grp)
-        c->grp_first_cu[grp] = expected;
+    c->n_xcds = n_xcds;
+    for (int x = n_xcds; x <= kMaxXcds; ++x)
+        c->xcd_first_cu[x] = expected;
     c->num_cus = expected;
     std::memset(&c->all_cus, 0, sizeof c->all_cus);
     for (int i = 0; i < expected; ++i)
@@ -362,6 +385,24 @@ int sgdrc_last_tiles(sgdrc_ctx *ctx, void *stream, uint64_t *tiles)
     std::lock_guard<std::mutex> lock(c->mu);
     auto it = c->streams.find(stream);
     *tiles = it == c->streams.end() ? 0 : it->second.last_tiles;
+    return SGDRC_OK;
+}
+
+int sgdrc_set_stream_occupancy(sgdrc_ctx *ctx, void *stream, uint32_t max_wgs_per_cu)
+{
+    clear_error();
+    if (max_wgs_per_cu > 64)
+        return set_error(SGDRC_EINVAL, "max_wgs_per_cu %u above 64", max_wgs_per_cu);
+    Ctx *c = nullptr;
+    int rc = check_ctx(ctx, &c);
+    if (rc)
+        return rc;
+    StreamState *st = nullptr;
+    rc = stream_state(c, stream, &st);
+    if (rc)
+        return rc;
+    std::lock_guard<std::mutex> lock(c->mu);
+    st->wg_cap = max_wgs_per_cu;
     return SGDRC_OK;
 }
 

@@ -21,15 +21,19 @@ constexpr uint32_t kDevErrPtRange = 1u;
 constexpr uint32_t kDevFlagGateFallback = 2u;
 
 constexpr int kMaxCus = 256;
-constexpr int kMaxGroups = 16;      // CU groups = XCDs (XCC_ID has 4 bits)
+constexpr int kMaxXcds = 16;        // XCC_ID has 4 bits
+constexpr int kMaxGroups = 64;      // queue groups: runs of CUs inside one XCD
 constexpr int kCounterStride = 32;  // 32-bit words between counters (128 bytes)
 constexpr int kDoneGroups = 8;
 
-// Work distribution state of one stream.  Tiles are split into contiguous
-// ranges, one per CU group (XCD) in proportion to the allowed CUs of the
-// group; the workgroups resident on a group's CUs claim that range in order
-// through the group's ticket counter, which balances load dynamically
-// inside an XCD while ticket atomics spread over one counter per XCD.
+// Work distribution state of one stream.  The CUs of each XCD are cut into
+// runs of 2^grp_shift CUs ("queue groups"; a launch picks the run length:
+// a whole XCD for long streaming kernels, a few CUs for short ones).  Tiles
+// are split into contiguous ranges, one per group in proportion to the
+// group's allowed CUs; the workgroups resident on a group's CUs claim that
+// range in order through the group's ticket counter, which balances load
+// dynamically inside a group while the ticket atomics spread over many
+// counters.
 // Arrivals are counted in eight groups (blockIdx % 8, whose sizes are
 // known) and then once per group, so that the last workgroup of the grid
 // can be found without every workgroup hitting one address.  That
@@ -44,14 +48,16 @@ struct QueueSlot {
 // Per-launch gate arguments (passed by value in the kernel arguments).
 struct Gate {
     uint64_t mask[4];            // logical CUs allowed to work
-    const uint32_t *lut;         // hardware key -> logical CU | group << 16
+    const uint32_t *lut;         // hardware key -> logical CU | XCD << 16 | CU-in-XCD << 24
     QueueSlot *q;                // this stream's work distribution state
     uint32_t *err;               // device error / event flags
     uint32_t *log_cu;            // optional: tiles per logical CU
     uint32_t *log_tile;          // optional: visits per tile
     uint64_t log_cap;            // entries of log_tile
     uint32_t grp_tile[kMaxGroups + 1];  // first tile of each group's range
+    uint8_t grp_base[kMaxXcds];  // first queue group of each XCD
     uint32_t n_groups;
+    uint32_t grp_shift;          // log2 of CUs per queue group
 };
 
 __device__ __forceinline__ uint32_t hw_key()
@@ -62,8 +68,9 @@ __device__ __forceinline__ uint32_t hw_key()
     return ((xcc & 0xFu) << 8) | ((hw >> 8) & 0xFFu);
 }
 
-// LUT entry of the executing workgroup's CU: logical CU | group << 16, or
-// kLutNone.  The key comes from scalar registers, so this is a scalar load.
+// LUT entry of the executing workgroup's CU: logical CU | XCD << 16 |
+// CU-in-XCD << 24, or kLutNone.  The key comes from scalar registers, so
+// this is a scalar load.
 __device__ __forceinline__ uint32_t my_cu_entry(const Gate &g)
 {
     return g.lut[hw_key()];
@@ -180,7 +187,7 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
     const uint32_t entry = my_cu_entry(g);
     const uint32_t cu = entry & 0xFFFFu;
     if (entry != kLutNone && cu_allowed(g, cu)) {
-        const uint32_t grp = entry >> 16;
+        const uint32_t grp = g.grp_base[(entry >> 16) & 0xFFu] + ((entry >> 24) >> g.grp_shift);
         const uint32_t lo = g.grp_tile[grp], hi = g.grp_tile[grp + 1u];
         uint32_t *ctr = &g.q->grp_next[grp * kCounterStride];
         // the next ticket is requested before the body runs, so its atomic

@@ -401,11 +401,11 @@ int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, 
         n_tiles = (M + kGemvRows - 1) / kGemvRows;
     }
     Gate g;
-    int allowed = 0;
-    rc = make_gate(c, stream, n_tiles, &g, &allowed);
+    LaunchInfo li;
+    rc = make_gate(c, stream, n_tiles, kGemvGroupCus, &g, &li);
     if (rc)
         return rc;
-    const uint32_t grid = gated_grid(c, kernel_occupancy(k), n_tiles, allowed);
+    const uint32_t grid = gated_grid(c, kernel_occupancy(k), n_tiles, li);
     hipLaunchKernelGGL(k, dim3(grid), dim3(kGemvThreads), 0, reinterpret_cast<hipStream_t>(stream),
                        static_cast<const uint8_t *>(w->pool), w->pt, w->pool_pages, M, K,
                        static_cast<const uint8_t *>(d_x), batch, d_y, page_shift,

@@ -18,11 +18,23 @@ namespace sgdrc {
 constexpr uint32_t kCtxMagic = 0x53474452u;  // "SGDR"
 constexpr int kMaxStreams = 64;
 constexpr int kHistBins = 256;
+// CUs served by one work queue: a whole XCD for long streaming kernels
+// (dynamic balance across the XCD), a few CUs for short kernels such as the
+// GEMV (fewer workgroups contending on each counter).
+constexpr int kStreamGroupCus = 32;
+constexpr int kGemvGroupCus = 8;
 
 struct StreamState {
     int slot = -1;
     sgdrc_cu_mask mask{};
+    uint32_t wg_cap = 0;        // workgroups per CU at most (0 = as many as fit)
     uint64_t last_tiles = 0;
+};
+
+// What a gated launch needs besides the Gate itself.
+struct LaunchInfo {
+    int allowed = 0;            // allowed CUs
+    uint32_t wg_cap = 0;        // per-stream cap on workgroups per CU
 };
 
 struct Ctx {
@@ -31,8 +43,8 @@ struct Ctx {
     int num_cus = 0;
     uint32_t keys[SGDRC_MAX_CUS] = {};   // logical CU -> hardware key
     sgdrc_cu_mask all_cus{};
-    int n_groups = 0;                    // CU groups (XCDs)
-    int grp_first_cu[kMaxGroups + 1] = {};  // logical CUs of group g: [first[g], first[g+1])
+    int n_xcds = 0;
+    int xcd_first_cu[kMaxXcds + 1] = {};  // logical CUs of XCD x: [first[x], first[x+1])
 
     uint32_t *d_lut = nullptr;           // kLutSize entries: logical CU | group << 16
     QueueSlot *d_queues = nullptr;       // kMaxStreams
@@ -71,14 +83,15 @@ int check_ctx(const sgdrc_ctx *ctx, Ctx **out);
 // Per-stream state (creates it, with all CUs allowed, on first use).
 int stream_state(Ctx *c, void *stream, StreamState **out);
 
-// Gate arguments for a launch of ``n_tiles`` tiles on ``stream``.
-int make_gate(Ctx *c, void *stream, uint64_t n_tiles, Gate *g, int *allowed_cus);
+// Gate arguments for a launch of ``n_tiles`` tiles on ``stream`` whose work
+// queues serve runs of ``group_cus`` CUs (a power of two, at most 32).
+int make_gate(Ctx *c, void *stream, uint64_t n_tiles, int group_cus, Gate *g, LaunchInfo *li);
 
 // Grid size for a gated persistent kernel: the same number of workgroups
 // for every CU (the dispatcher spreads them over all CUs; those on CUs
-// outside the mask leave at once), as many as fit at once but no more than
-// the tiles of one allowed CU's share.
-uint32_t gated_grid(const Ctx *c, int blocks_per_cu, uint64_t n_tiles, int allowed_cus);
+// outside the mask leave at once), as many as fit at once (or the stream's
+// cap) but no more than the tiles that fall to one allowed CU.
+uint32_t gated_grid(const Ctx *c, int blocks_per_cu, uint64_t n_tiles, const LaunchInfo &li);
 
 int popcount_mask(const sgdrc_cu_mask &m);
 

@@ -246,15 +246,15 @@ int bimodal_relayout(sgdrc_ctx *ctx, const sgdrc_paged *dst, const sgdrc_paged *
     if (n_tiles >= (1ull << 31))
         return set_error(SGDRC_EINVAL, "n_bytes too large");
     Gate g;
-    int allowed = 0;
-    rc = make_gate(c, stream, n_tiles, &g, &allowed);
+    LaunchInfo li;
+    rc = make_gate(c, stream, n_tiles, kStreamGroupCus, &g, &li);
     if (rc)
         return rc;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const bool big = page_shift >= kStreamTileShift;
     static const int occ_big = occupancy(k_relayout<true>, kStreamThreads);
     static const int occ_small = occupancy(k_relayout<false>, kStreamThreads);
-    const uint32_t grid = gated_grid(c, big ? occ_big : occ_small, n_tiles, allowed);
+    const uint32_t grid = gated_grid(c, big ? occ_big : occ_small, n_tiles, li);
     auto kern = big ? k_relayout<true> : k_relayout<false>;
     hipLaunchKernelGGL(kern, dim3(grid), dim3(kStreamThreads), 0, s,
                        static_cast<uint8_t *>(dst->pool), dst->pt, dst->pool_pages,
@@ -285,15 +285,15 @@ int colored_stream(sgdrc_ctx *ctx, const sgdrc_paged *a, const sgdrc_paged *b,
     if (n_tiles >= (1ull << 31))
         return set_error(SGDRC_EINVAL, "n_elems too large");
     Gate g;
-    int allowed = 0;
-    rc = make_gate(c, stream, n_tiles, &g, &allowed);
+    LaunchInfo li;
+    rc = make_gate(c, stream, n_tiles, kStreamGroupCus, &g, &li);
     if (rc)
         return rc;
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
     const bool big = page_shift >= kStreamTileShift;
     static const int occ_big = occupancy(k_triad<true>, kStreamThreads);
     static const int occ_small = occupancy(k_triad<false>, kStreamThreads);
-    const uint32_t grid = gated_grid(c, big ? occ_big : occ_small, n_tiles, allowed);
+    const uint32_t grid = gated_grid(c, big ? occ_big : occ_small, n_tiles, li);
     auto kern = big ? k_triad<true> : k_triad<false>;
     hipLaunchKernelGGL(kern, dim3(grid), dim3(kStreamThreads), 0, hs,
                        static_cast<uint8_t *>(a->pool), a->pt, a->pool_pages,
