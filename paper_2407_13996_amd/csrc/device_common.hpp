@@ -24,7 +24,6 @@ constexpr int kMaxCus = 256;
 constexpr int kMaxXcds = 16;        // XCC_ID has 4 bits
 constexpr int kMaxGroups = 64;      // queue groups: runs of CUs inside one XCD
 constexpr int kCounterStride = 32;  // 32-bit words between counters (128 bytes)
-constexpr int kDoneGroups = 8;
 
 // Work distribution state of one stream.  The CUs of each XCD are cut into
 // runs of 2^grp_shift CUs ("queue groups"; a launch picks the run length:
@@ -34,14 +33,21 @@ constexpr int kDoneGroups = 8;
 // range in order through the group's ticket counter, which balances load
 // dynamically inside a group while the ticket atomics spread over many
 // counters.
-// Arrivals are counted in eight groups (blockIdx % 8, whose sizes are
-// known) and then once per group, so that the last workgroup of the grid
-// can be found without every workgroup hitting one address.  That
-// workgroup finishes any range that no workgroup took and zeroes the slot
-// for the next launch on the stream.
+// Arrivals are counted per class blockIdx % n_res (class sizes are known)
+// and then once per class, so that the last workgroup of the grid can be
+// found without every workgroup hitting one address.  That workgroup
+// finishes any range that no workgroup took and zeroes the slot for the
+// next launch on the stream.
+//
+// The dispatcher sends workgroup i to XCD i mod (number of XCDs).  When the
+// context has verified that mapping, n_res is the XCD count and classes
+// whose XCD has no allowed CU do not take part: their workgroups leave at
+// once, without touching memory.  This stays correct if the mapping does
+// not hold (work is claimed dynamically, and ranges that no taking-part
+// workgroup reached are finished by the last one); it only costs time.
 struct QueueSlot {
     uint32_t grp_next[kMaxGroups * kCounterStride];
-    uint32_t done[kDoneGroups * kCounterStride];
+    uint32_t done[kMaxXcds * kCounterStride];
     uint32_t done_all[kCounterStride];
 };
 
@@ -58,6 +64,8 @@ struct Gate {
     uint8_t grp_base[kMaxXcds];  // first queue group of each XCD
     uint32_t n_groups;
     uint32_t grp_shift;          // log2 of CUs per queue group
+    uint32_t n_res;              // arrival classes: blockIdx % n_res
+    uint32_t res_mask;           // classes that take part (bit r = class r)
 };
 
 __device__ __forceinline__ uint32_t hw_key()
@@ -125,22 +133,24 @@ __device__ __forceinline__ void log_tile(const Gate &g, uint32_t cu, uint32_t ti
 // device-scope atomics, coherent across XCDs by themselves, so no fence is
 // used: on gfx950 a device-scope fence writes back and invalidates the
 // whole L2 of the XCD.
-__device__ __forceinline__ bool arrive_last(QueueSlot *q, uint32_t *s_flag)
+__device__ __forceinline__ bool arrive_last(const Gate &g, uint32_t *s_flag)
 {
     __builtin_amdgcn_s_waitcnt(0);  // vmcnt, expcnt and lgkmcnt all zero
     __syncthreads();
     if (threadIdx.x == 0) {
         const uint32_t G = gridDim.x;
-        const uint32_t grp = blockIdx.x % (uint32_t)kDoneGroups;
-        const uint32_t expected = G / kDoneGroups + (grp < G % kDoneGroups ? 1u : 0u);
-        const uint32_t groups = G < (uint32_t)kDoneGroups ? G : (uint32_t)kDoneGroups;
+        const uint32_t grp = blockIdx.x % g.n_res;
+        const uint32_t expected = G / g.n_res + (grp < G % g.n_res ? 1u : 0u);
+        uint32_t classes = 0;
+        for (uint32_t r = 0; r < g.n_res; ++r)
+            classes += ((g.res_mask >> r) & 1u) && r < G ? 1u : 0u;
         uint32_t last = 0u;
-        const uint32_t d = __hip_atomic_fetch_add(&q->done[grp * kCounterStride], 1u,
+        const uint32_t d = __hip_atomic_fetch_add(&g.q->done[grp * kCounterStride], 1u,
                                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (d == expected - 1u) {
-            const uint32_t e = __hip_atomic_fetch_add(&q->done_all[0], 1u, __ATOMIC_RELAXED,
+            const uint32_t e = __hip_atomic_fetch_add(&g.q->done_all[0], 1u, __ATOMIC_RELAXED,
                                                       __HIP_MEMORY_SCOPE_AGENT);
-            last = e == groups - 1u ? 1u : 0u;
+            last = e == classes - 1u ? 1u : 0u;
         }
         *s_flag = last;
     }
@@ -155,7 +165,7 @@ __device__ __forceinline__ void reset_slot(QueueSlot *q)
     if (threadIdx.x < (uint32_t)kMaxGroups)
         __hip_atomic_store(&q->grp_next[threadIdx.x * kCounterStride], 0u, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
-    if (threadIdx.x < (uint32_t)kDoneGroups)
+    if (threadIdx.x < (uint32_t)kMaxXcds)
         __hip_atomic_store(&q->done[threadIdx.x * kCounterStride], 0u, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
     if (threadIdx.x == 0)
@@ -183,6 +193,8 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
     __shared__ uint32_t s_ticket;
     __shared__ uint32_t s_flag;
     __shared__ uint32_t s_left_lo[kMaxGroups], s_left_hi[kMaxGroups];
+    if (((g.res_mask >> (blockIdx.x % g.n_res)) & 1u) == 0u)
+        return;  // sent to an XCD without allowed CUs: leave without counting
     uint32_t err = 0u;
     const uint32_t entry = my_cu_entry(g);
     const uint32_t cu = entry & 0xFFFFu;
@@ -207,7 +219,7 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
         }
         flush();
     }
-    if (arrive_last(g.q, &s_flag)) {
+    if (arrive_last(g, &s_flag)) {
         // ranges that no workgroup finished: [lo + tickets taken, hi), then
         // worked through in one flat loop so that no barrier of the body
         // ends up in a nested loop

@@ -71,7 +71,8 @@ def test_topology(ctx):
     per_xcc = {}
     for k in keys:
         per_xcc[k >> 8] = per_xcc.get(k >> 8, 0) + 1
-    say("CUs per XCC:", per_xcc)
+    say("CUs per XCC:", per_xcc, "round-robin XCD dispatch:", ctx.xcd_round_robin)
+    assert sum(per_xcc.values()) == n
 
 
 # ---------------------------------------------------------------- classify
