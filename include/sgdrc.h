@@ -107,11 +107,6 @@ int sgdrc_num_cus(const sgdrc_ctx *ctx);
  * (the CU, shader-array and shader-engine fields). */
 int sgdrc_cu_key(const sgdrc_ctx *ctx, uint32_t cu, uint32_t *key);
 
-/* 1 if the probe found that workgroup i of a grid always runs on the XCD
- * of workgroup i mod (number of XCDs) (then workgroups sent to XCDs without
- * allowed CUs leave at once), 0 if not, or a negative code. */
-int sgdrc_xcd_round_robin(const sgdrc_ctx *ctx);
-
 /* Text of the calling thread's last error ("" if none). */
 const char *sgdrc_last_error(void);
 

@@ -67,7 +67,6 @@ def lib() -> ctypes.CDLL:
             "sgdrc_destroy": ([vp], i32),
             "sgdrc_num_cus": ([vp], i32),
             "sgdrc_cu_key": ([vp, u32, P(u32)], i32),
-            "sgdrc_xcd_round_robin": ([vp], i32),
             "sgdrc_last_error": ([], ctypes.c_char_p),
             "sgdrc_device_error": ([vp, P(u32)], i32),
             "sgdrc_set_worklog": ([vp, vp, vp, u64], i32),
@@ -168,13 +167,6 @@ class Context:
         k = ctypes.c_uint32()
         _check(lib().sgdrc_cu_key(self.handle, int(cu), ctypes.byref(k)))
         return k.value
-
-    @property
-    def xcd_round_robin(self) -> bool:
-        r = lib().sgdrc_xcd_round_robin(self.handle)
-        if r < 0:
-            _check(r)
-        return bool(r)
 
     def device_error(self) -> int:
         f = ctypes.c_uint32()

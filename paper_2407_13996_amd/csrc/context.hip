@@ -114,20 +114,14 @@ int make_gate(Ctx *c, void *stream, uint64_t n_tiles, int group_cus, Gate *g, La
     }
     g->n_groups = (uint32_t)n_groups;
     g->grp_shift = shift;
-    // arrival classes
-    if (c->rr_ok) {
-        g->n_res = (uint32_t)c->n_xcds;
-        g->res_mask = 0;
-        for (int r = 0; r < c->n_xcds; ++r) {
-            const int x = c->res_xcd[r];
-            bool any = false;
-            for (int cu = c->xcd_first_cu[x]; cu < c->xcd_first_cu[x + 1] && !any; ++cu)
-                any = (st->mask.bits[cu >> 6] >> (cu & 63)) & 1ull;
-            g->res_mask |= any ? (1u << r) : 0u;
-        }
-    } else {
-        g->n_res = 8;
-        g->res_mask = 0xFFu;
+    // physical XCC ids whose XCD has allowed CUs
+    g->xcc_allowed = 0;
+    for (int x = 0; x < c->n_xcds; ++x) {
+        bool any = false;
+        for (int cu = c->xcd_first_cu[x]; cu < c->xcd_first_cu[x + 1] && !any; ++cu)
+            any = (st->mask.bits[cu >> 6] >> (cu & 63)) & 1ull;
+        if (any)
+            g->xcc_allowed |= 1u << ((c->keys[c->xcd_first_cu[x]] >> 8) & 0xFu);
     }
     st->last_tiles = n_tiles;
     li->allowed = (int)total;
@@ -197,7 +191,7 @@ __global__ void k_cu_probe(uint32_t *keys, uint32_t n, uint32_t spins)
 
 static int probe_topology(Ctx *c, int expected)
 {
-    std::vector<uint32_t> uniq, by_block;
+    std::vector<uint32_t> uniq;
     for (int attempt = 0; attempt < 3; ++attempt) {
         const uint32_t n = (uint32_t)expected * (48u << attempt);
         uint32_t *d_keys = nullptr;
@@ -212,7 +206,6 @@ static int probe_topology(Ctx *c, int expected)
         (void)hipFree(d_keys);
         if (e != hipSuccess)
             return hip_fail(e, "CU probe");
-        by_block = keys;
         std::sort(keys.begin(), keys.end());
         keys.erase(std::unique(keys.begin(), keys.end()), keys.end());
         uniq = keys;
@@ -246,20 +239,6 @@ static int probe_topology(Ctx *c, int expected)
     for (int x = n_xcds; x <= kMaxXcds; ++x)
         c->xcd_first_cu[x] = expected;
     c->num_cus = expected;
-    // does workgroup i always run on the XCD of workgroup i mod n_xcds?
-    c->rr_ok = n_xcds > 0 && by_block.size() >= (size_t)n_xcds;
-    for (size_t i = 0; c->rr_ok && i < by_block.size(); ++i)
-        c->rr_ok = (by_block[i] >> 8) == (by_block[i % n_xcds] >> 8);
-    for (int r = 0; c->rr_ok && r < n_xcds; ++r) {
-        int x = 0;
-        while (x < n_xcds && (c->keys[c->xcd_first_cu[x]] >> 8) != (by_block[r] >> 8))
-            ++x;
-        c->rr_ok = x < n_xcds;
-        c->res_xcd[r] = x;
-    }
-    std::memset(&c->all_cus, 0, sizeof c->all_cus);
-    for (int i = 0; i < expected; ++i)
-        c->all_cus.bits[i >> 6] |= 1ull << (i & 63);
     SGDRC_HIP(hipMemcpy(c->d_lut, lut.data(), kLutSize * sizeof(uint32_t), hipMemcpyHostToDevice));
     return SGDRC_OK;
 }
@@ -352,14 +331,6 @@ int sgdrc_num_cus(const sgdrc_ctx *ctx)
     if (c->magic != kCtxMagic)
         return set_error(SGDRC_ENODEV, "not an initialised sgdrc context");
     return c->num_cus;
-}
-
-int sgdrc_xcd_round_robin(const sgdrc_ctx *ctx)
-{
-    int n = sgdrc_num_cus(ctx);
-    if (n < 0)
-        return n;
-    return reinterpret_cast<const Ctx *>(ctx)->rr_ok ? 1 : 0;
 }
 
 int sgdrc_cu_key(const sgdrc_ctx *ctx, uint32_t cu, uint32_t *key)

@@ -23,6 +23,7 @@ constexpr uint32_t kDevFlagGateFallback = 2u;
 constexpr int kMaxCus = 256;
 constexpr int kMaxXcds = 16;        // XCC_ID has 4 bits
 constexpr int kMaxGroups = 64;      // queue groups: runs of CUs inside one XCD
+constexpr int kArrivalClasses = 8;
 constexpr int kCounterStride = 32;  // 32-bit words between counters (128 bytes)
 
 // Work distribution state of one stream.  The CUs of each XCD are cut into
@@ -33,21 +34,14 @@ constexpr int kCounterStride = 32;  // 32-bit words between counters (128 bytes)
 // range in order through the group's ticket counter, which balances load
 // dynamically inside a group while the ticket atomics spread over many
 // counters.
-// Arrivals are counted per class blockIdx % n_res (class sizes are known)
-// and then once per class, so that the last workgroup of the grid can be
-// found without every workgroup hitting one address.  That workgroup
-// finishes any range that no workgroup took and zeroes the slot for the
-// next launch on the stream.
-//
-// The dispatcher sends workgroup i to XCD i mod (number of XCDs).  When the
-// context has verified that mapping, n_res is the XCD count and classes
-// whose XCD has no allowed CU do not take part: their workgroups leave at
-// once, without touching memory.  This stays correct if the mapping does
-// not hold (work is claimed dynamically, and ranges that no taking-part
-// workgroup reached are finished by the last one); it only costs time.
+// Arrivals are counted per class blockIdx % 8 (class sizes are known) and
+// then once per class, so that the last workgroup of the grid can be found
+// without every workgroup hitting one address.  That workgroup finishes any
+// range that no workgroup took and zeroes the slot for the next launch on
+// the stream.
 struct QueueSlot {
     uint32_t grp_next[kMaxGroups * kCounterStride];
-    uint32_t done[kMaxXcds * kCounterStride];
+    uint32_t done[kArrivalClasses * kCounterStride];
     uint32_t done_all[kCounterStride];
 };
 
@@ -64,8 +58,7 @@ struct Gate {
     uint8_t grp_base[kMaxXcds];  // first queue group of each XCD
     uint32_t n_groups;
     uint32_t grp_shift;          // log2 of CUs per queue group
-    uint32_t n_res;              // arrival classes: blockIdx % n_res
-    uint32_t res_mask;           // classes that take part (bit r = class r)
+    uint32_t xcc_allowed;        // bit x: XCC_ID x has allowed CUs
 };
 
 __device__ __forceinline__ uint32_t hw_key()
@@ -139,11 +132,9 @@ __device__ __forceinline__ bool arrive_last(const Gate &g, uint32_t *s_flag)
     __syncthreads();
     if (threadIdx.x == 0) {
         const uint32_t G = gridDim.x;
-        const uint32_t grp = blockIdx.x % g.n_res;
-        const uint32_t expected = G / g.n_res + (grp < G % g.n_res ? 1u : 0u);
-        uint32_t classes = 0;
-        for (uint32_t r = 0; r < g.n_res; ++r)
-            classes += ((g.res_mask >> r) & 1u) && r < G ? 1u : 0u;
+        const uint32_t grp = blockIdx.x % (uint32_t)kArrivalClasses;
+        const uint32_t expected = G / kArrivalClasses + (grp < G % kArrivalClasses ? 1u : 0u);
+        const uint32_t classes = G < (uint32_t)kArrivalClasses ? G : (uint32_t)kArrivalClasses;
         uint32_t last = 0u;
         const uint32_t d = __hip_atomic_fetch_add(&g.q->done[grp * kCounterStride], 1u,
                                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -165,7 +156,7 @@ __device__ __forceinline__ void reset_slot(QueueSlot *q)
     if (threadIdx.x < (uint32_t)kMaxGroups)
         __hip_atomic_store(&q->grp_next[threadIdx.x * kCounterStride], 0u, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
-    if (threadIdx.x < (uint32_t)kMaxXcds)
+    if (threadIdx.x < (uint32_t)kArrivalClasses)
         __hip_atomic_store(&q->done[threadIdx.x * kCounterStride], 0u, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
     if (threadIdx.x == 0)
@@ -193,10 +184,12 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
     __shared__ uint32_t s_ticket;
     __shared__ uint32_t s_flag;
     __shared__ uint32_t s_left_lo[kMaxGroups], s_left_hi[kMaxGroups];
-    if (((g.res_mask >> (blockIdx.x % g.n_res)) & 1u) == 0u)
-        return;  // sent to an XCD without allowed CUs: leave without counting
     uint32_t err = 0u;
-    const uint32_t entry = my_cu_entry(g);
+    // a workgroup on an XCD without allowed CUs skips even the table lookup
+    uint32_t xcc;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+    const bool xcd_on = ((g.xcc_allowed >> (xcc & 0xFu)) & 1u) != 0u;
+    const uint32_t entry = xcd_on ? my_cu_entry(g) : kLutNone;
     const uint32_t cu = entry & 0xFFFFu;
     if (entry != kLutNone && cu_allowed(g, cu)) {
         const uint32_t grp = g.grp_base[(entry >> 16) & 0xFFu] + ((entry >> 24) >> g.grp_shift);

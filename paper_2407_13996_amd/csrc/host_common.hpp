@@ -45,8 +45,6 @@ struct Ctx {
     sgdrc_cu_mask all_cus{};
     int n_xcds = 0;
     int xcd_first_cu[kMaxXcds + 1] = {};  // logical CUs of XCD x: [first[x], first[x+1])
-    bool rr_ok = false;                   // workgroup i runs on XCD res_xcd[i % n_xcds]
-    int res_xcd[kMaxXcds] = {};
 
     uint32_t *d_lut = nullptr;           // kLutSize entries: logical CU | group << 16
     QueueSlot *d_queues = nullptr;       // kMaxStreams

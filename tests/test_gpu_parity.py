@@ -71,7 +71,7 @@ def test_topology(ctx):
     per_xcc = {}
     for k in keys:
         per_xcc[k >> 8] = per_xcc.get(k >> 8, 0) + 1
-    say("CUs per XCC:", per_xcc, "round-robin XCD dispatch:", ctx.xcd_round_robin)
+    say("CUs per XCC:", per_xcc)
     assert sum(per_xcc.values()) == n
 
 
@@ -374,4 +374,50 @@ def test_out_of_range_page_entry_is_flagged_not_accessed(ctx):
     assert ctx.device_error() & sg.DEVERR_PT_RANGE
     d = to_host(dst).reshape(pages, 65536)
     assert (d[3] == 0).all() and (d[[0, 1, 2, 4, 5, 6, 7]] == 1).all()
+    assert ctx.device_error() == 0
+
+
+def test_two_streams_disjoint_masks_run_concurrently(ctx, orc):
+    """A GEMV stream on CUs 0..3/4 and a triad stream on the rest, launched
+    back to back so that they overlap; both results match the oracle and no
+    range needed the last-workgroup fallback (the fixture checks the flags)."""
+    n = ctx.num_cus
+    s_ls, s_be = torch.cuda.Stream(), torch.cuda.Stream()
+    sg.set_cu_mask(ctx, s_ls, range(3 * n // 4))
+    sg.set_cu_mask(ctx, s_be, range(3 * n // 4, n))
+    sg.set_stream_occupancy(ctx, s_be, 3)
+    # triad operands: 64 MiB arrays, identity pages
+    shift, elems = 16, 1 << 24
+    pages = elems * 4 >> shift
+    pt = torch.arange(pages, dtype=torch.int32, device=DEV)
+    b = synth.uniform_f32(elems, seed=31)
+    c = synth.uniform_f32(elems, seed=32)
+    d_b, d_c = to_dev(b), to_dev(c)
+    d_a = torch.zeros_like(d_b)
+    # GEMV operands: bf16 1024x4096 in 64 KiB pages
+    M, K = 1024, 4096
+    wb = synth.normal_bf16(M * K, seed=33, sigma=0.02)
+    xb = synth.normal_bf16(K, seed=34)
+    wpages = M * K * 2 >> shift
+    wpt = torch.arange(wpages, dtype=torch.int32, device=DEV)
+    d_w, d_x = to_dev(wb), to_dev(xb)
+    d_y = torch.zeros(M, dtype=torch.float32, device=DEV)
+    torch.cuda.synchronize()
+    for i in range(4):
+        sg.colored_stream(ctx, sg.paged(d_a, pt, pages), sg.paged(d_b, pt, pages),
+                          sg.paged(d_c, pt, pages), 3.0, elems, shift, s_be)
+        for _ in range(20):
+            sg.colored_gemv(ctx, sg.paged(d_w, wpt, wpages), sg.BF16, M, K, d_x, sg.BF16, 1, d_y,
+                            shift, s_ls)
+    torch.cuda.synchronize()
+    sg.set_cu_mask(ctx, s_ls, None)
+    sg.set_cu_mask(ctx, s_be, None)
+    sg.set_stream_occupancy(ctx, s_be, 0)
+    ident = np.arange(pages, dtype=np.uint32)
+    ref_a = np.zeros_like(b)
+    orc.triad(ref_a, ident, b, ident, c, ident, 3.0, elems, shift)
+    assert (to_host(d_a).view(np.uint32) == ref_a.view(np.uint32)).all()
+    y_ref, absdot = orc.gemv(wb, np.arange(wpages, dtype=np.uint32), orc.BF16, M, K, xb, orc.BF16,
+                             1, shift)
+    gemv_ok(to_host(d_y).reshape(1, M), y_ref, absdot)
     assert ctx.device_error() == 0
