@@ -163,14 +163,15 @@ __device__ __forceinline__ void reset_slot(QueueSlot *q)
         __hip_atomic_store(&q->done_all[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Runs ``body(tile, cu, err)`` for every tile of this workgroup's group
-// range that it obtains, under the gate.  Workgroups on CUs outside the
-// mask take no tiles.  ``flush()`` runs after a workgroup's tile loop (to
-// publish per-workgroup partials).  The last workgroup to arrive finishes
-// the tiles of any range that no workgroup took (possible only when no
-// workgroup landed on an allowed CU of some group; flagged), flushes again,
-// calls ``epilogue()`` with every other workgroup's work complete, and
-// zeroes the slot.
+// Runs ``body(tile, cu, err)`` for every tile that this workgroup obtains,
+// under the gate.  Workgroups on CUs outside the mask take no tiles; the
+// others take tiles of their own group's range, then steal from other
+// groups' ranges until every range is exhausted.  ``flush()`` runs after a
+// workgroup's tile loop (to publish per-workgroup partials).  The last
+// workgroup to arrive finishes the tiles of any range that no workgroup
+// took (only possible when no workgroup landed on any allowed CU; flagged),
+// flushes again, calls ``epilogue()`` with every other workgroup's work
+// complete, and zeroes the slot.
 //
 // Bodies must not return early or branch around the rest of the tile on a
 // per-lane condition: the loop contains barriers, and a lane-dependent exit
@@ -184,6 +185,10 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
     __shared__ uint32_t s_ticket;
     __shared__ uint32_t s_flag;
     __shared__ uint32_t s_left_lo[kMaxGroups], s_left_hi[kMaxGroups];
+    __shared__ uint32_t s_grp_tile[kMaxGroups + 1];
+    for (uint32_t i = threadIdx.x; i <= (uint32_t)kMaxGroups; i += blockDim.x)
+        s_grp_tile[i] = g.grp_tile[i];
+    __syncthreads();
     uint32_t err = 0u;
     // a workgroup on an XCD without allowed CUs skips even the table lookup
     uint32_t xcc;
@@ -192,23 +197,59 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
     const uint32_t entry = xcd_on ? my_cu_entry(g) : kLutNone;
     const uint32_t cu = entry & 0xFFFFu;
     if (entry != kLutNone && cu_allowed(g, cu)) {
-        const uint32_t grp = g.grp_base[(entry >> 16) & 0xFFu] + ((entry >> 24) >> g.grp_shift);
-        const uint32_t lo = g.grp_tile[grp], hi = g.grp_tile[grp + 1u];
-        uint32_t *ctr = &g.q->grp_next[grp * kCounterStride];
-        // the next ticket is requested before the body runs, so its atomic
-        // round trip overlaps the tile's memory traffic
-        uint32_t k = claim_ticket(ctr, &s_ticket);
-        while (k < hi - lo) {
-            uint32_t next = 0u;
-            if (threadIdx.x == 0)
-                next = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            log_tile(g, cu, lo + k);
-            body(lo + k, cu, err);
-            if (threadIdx.x == 0)
-                s_ticket = next;
-            __syncthreads();
-            k = __builtin_amdgcn_readfirstlane(s_ticket);
-            __syncthreads();
+        uint32_t grp = g.grp_base[(entry >> 16) & 0xFFu] + ((entry >> 24) >> g.grp_shift);
+        uint32_t lo = s_grp_tile[grp], hi = s_grp_tile[grp + 1u];
+        uint32_t k = claim_ticket(&g.q->grp_next[grp * kCounterStride], &s_ticket);
+        // One flat loop: work through the own group's range (the next ticket
+        // is requested before the body runs, so its round trip overlaps the
+        // tile), then steal from the next group in ring order that still has
+        // tiles, found by wave 0 reading every group's counter at once.
+        for (;;) {
+            if (k < hi - lo) {
+                uint32_t next = 0u;
+                if (threadIdx.x == 0)
+                    next = __hip_atomic_fetch_add(&g.q->grp_next[grp * kCounterStride], 1u,
+                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                log_tile(g, cu, lo + k);
+                body(lo + k, cu, err);
+                if (threadIdx.x == 0)
+                    s_ticket = next;
+                __syncthreads();
+                k = __builtin_amdgcn_readfirstlane(s_ticket);
+                __syncthreads();
+            } else {
+                if (threadIdx.x < 64u) {
+                    const uint32_t r = threadIdx.x;
+                    bool rem = false;
+                    if (r < g.n_groups) {
+                        const uint32_t size = s_grp_tile[r + 1u] - s_grp_tile[r];
+                        const uint32_t taken =
+                            size ? __hip_atomic_load(&g.q->grp_next[r * kCounterStride],
+                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                                 : 0u;
+                        rem = taken < size;
+                    }
+                    const uint64_t bits = __ballot(rem);
+                    if (threadIdx.x == 0) {
+                        uint32_t pick = kLutNone;
+                        if (bits) {
+                            const uint32_t sh = (grp + 1u) & 63u;
+                            const uint64_t rot = sh ? ((bits >> sh) | (bits << (64u - sh))) : bits;
+                            pick = (sh + (uint32_t)__builtin_ctzll(rot)) & 63u;
+                        }
+                        s_ticket = pick;
+                    }
+                }
+                __syncthreads();
+                const uint32_t pick = __builtin_amdgcn_readfirstlane(s_ticket);
+                __syncthreads();
+                if (pick == kLutNone)
+                    break;
+                grp = pick;
+                lo = s_grp_tile[grp];
+                hi = s_grp_tile[grp + 1u];
+                k = claim_ticket(&g.q->grp_next[grp * kCounterStride], &s_ticket);
+            }
         }
         flush();
     }
