@@ -112,6 +112,8 @@ int make_gate(Ctx *c, void *stream, uint64_t n_tiles, int group_cus, Gate *g, La
         cum += allowed[grp];
         g->grp_tile[grp + 1] = (uint32_t)(total ? n_tiles * cum / total : n_tiles);
     }
+    if (total == 0)
+        return set_error(SGDRC_EINVAL, "the stream's CU mask allows no CU of this device");
     g->n_groups = (uint32_t)n_groups;
     g->grp_shift = shift;
     // physical XCC ids whose XCD has allowed CUs
@@ -239,6 +241,9 @@ static int probe_topology(Ctx *c, int expected)
     for (int x = n_xcds; x <= kMaxXcds; ++x)
         c->xcd_first_cu[x] = expected;
     c->num_cus = expected;
+    std::memset(&c->all_cus, 0, sizeof c->all_cus);
+    for (int i = 0; i < expected; ++i)
+        c->all_cus.bits[i >> 6] |= 1ull << (i & 63);
     SGDRC_HIP(hipMemcpy(c->d_lut, lut.data(), kLutSize * sizeof(uint32_t), hipMemcpyHostToDevice));
     return SGDRC_OK;
 }
