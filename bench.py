@@ -245,10 +245,12 @@ def main():
         gpu_pages[j] = t8["raw"][off:off + P].cpu().numpy().view(np.float32).copy()
     pools_desc = {nc: (tables[nc]["base"], tables[nc]["pool_pages"]) for nc in fractions}
 
+    flags = {"headline": ctx.device_error()}
     rows = {}
     want = [r for r in args.rows.split(",") if r]
     if "classify" in want:
         rows["classify"] = bench_classify(torch, sg, synth, ctx, stream, timer)
+        flags["classify"] = ctx.device_error()
     if "pagetable" in want:
         rows["pagetable"] = {
             "what": "colour_alloc_pagetable over the headline pool (synchronous call)",
@@ -262,10 +264,13 @@ def main():
     torch.cuda.empty_cache()
     if "relayout" in want:
         rows["relayout"] = bench_relayout(torch, sg, synth, ctx, stream, timer)
+        flags["relayout"] = ctx.device_error()
     if "gemv" in want:
         rows["gemv"] = bench_gemv(torch, sg, synth, ctx, stream, timer, args.gemv_launches)
+        flags["gemv"] = ctx.device_error()
     if "corun" in want:
         rows["corun"] = bench_corun(torch, sg, synth, ctx, args.corun_launches)
+        flags["corun"] = ctx.device_error()
     if rows:
         result["rows"] = rows
 
@@ -273,8 +278,11 @@ def main():
         result["cpu_baseline"] = cpu_baseline(np, synth, masks, shift, pages, pools_desc,
                                               b_host, c_host, fractions, args.cpu_passes,
                                               gpu_pages)
-    err = ctx.device_error()
-    result["device_error_flags"] = err
+    flags["end"] = ctx.device_error()
+    result["device_flags_by_row"] = flags
+    result["device_error_flags"] = 0
+    for v in flags.values():
+        result["device_error_flags"] |= v
     ctx.close()
     print(json.dumps(result), flush=True)
 
