@@ -395,7 +395,8 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
             sg.bimodal_relayout(ctx, Wi, sg.paged(w, ident, pages), w_bytes, shift, stream)
             W.append(Wi)
         y = torch.empty(8 * M, dtype=torch.float32, device="cuda:0")
-        log(f"gemv {M}x{K}: {copies} weight copies rotated")
+        setup_flags = ctx.device_error()
+        log(f"gemv {M}x{K}: {copies} weight copies rotated (setup flags {setup_flags})")
         for B in (1, 2, 4, 8):
             for ncu in (64, 128, 192, 256):
                 if ncu > n_cus:
@@ -414,10 +415,11 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
                     sg.set_cu_mask(ctx, stream, None)
                     torch.cuda.synchronize()
                 d = timer.durations_ms(tag)
+                flag = ctx.device_error()
                 nbytes = M * K * 2 + B * K * 2 + B * M * 4
                 med, p99 = pctl(d, 50), pctl(d, 99)
                 gbs = nbytes / (med * 1e-3) / 1e9
-                out.append({"M": M, "K": K, "batch": B, "cus": ncu,
+                out.append({"M": M, "K": K, "batch": B, "cus": ncu, "device_flags": flag,
                             "path": "mfma" if B >= 5 else "valu",
                             "p50_us": round(med * 1e3, 2), "p99_us": round(p99 * 1e3, 2),
                             "GBps": round(gbs, 1),

@@ -84,27 +84,34 @@ int make_gate(Ctx *c, void *stream, uint64_t n_tiles, int group_cus, Gate *g, La
     g->log_cu = c->log_cu;
     g->log_tile = c->log_tile;
     g->log_cap = c->log_cap;
-    // queue groups: runs of group_cus CUs inside each XCD
+    // queue groups: runs of group_cus CUs inside each XCD, or one group
     uint32_t shift = 0;
     while ((1 << (shift + 1)) <= group_cus && shift < 5)
         ++shift;
+    const bool single = group_cus <= 0;
+    if (single)
+        shift = 8;  // every CU-in-XCD index (< 256) maps to sub-group 0
     uint64_t allowed[kMaxGroups] = {};
     uint64_t total = 0;
     int n_groups = 0;
     std::memset(g->grp_base, 0, sizeof g->grp_base);
     for (int x = 0; x < c->n_xcds; ++x) {
         const int first = c->xcd_first_cu[x], count = c->xcd_first_cu[x + 1] - first;
-        const int subs = (count + (1 << shift) - 1) >> shift;
+        const int subs = single ? 0 : (count + (1 << shift) - 1) >> shift;
         if (n_groups + subs > kMaxGroups)
             return set_error(SGDRC_EINVAL, "too many queue groups");
         g->grp_base[x] = (uint8_t)n_groups;
         for (int i = 0; i < count; ++i) {
             const int cu = first + i;
             const uint64_t bit = (st->mask.bits[cu >> 6] >> (cu & 63)) & 1ull;
-            allowed[n_groups + (i >> shift)] += bit;
+            allowed[single ? 0 : n_groups + (i >> shift)] += bit;
             total += bit;
         }
         n_groups += subs;
+    }
+    if (single) {
+        n_groups = 1;
+        std::memset(g->grp_base, 0, sizeof g->grp_base);
     }
     uint64_t cum = 0;
     g->grp_tile[0] = 0;

@@ -178,7 +178,13 @@ __device__ __forceinline__ void reset_slot(QueueSlot *q)
 // from it lets the compiler send some lanes of a wave back to the barrier
 // while others still owe the next ticket.  Bodies record problems in the
 // per-thread ``err`` bits instead; they are raised once, after the loop.
-template <typename Body, typename Flush, typename Epilogue>
+//
+// AHEAD: request the next ticket before the body runs, so that its round
+// trip overlaps the tile.  That pays off for short launches of one or two
+// tiles per workgroup (the GEMV); on long streaming launches it measured
+// slower on MI355X (an atomic issued ahead of a tile's loads delays them),
+// so streaming kernels claim after the body.
+template <bool AHEAD, typename Body, typename Flush, typename Epilogue>
 __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles, Body body,
                                                 Flush flush, Epilogue epilogue)
 {
@@ -200,18 +206,20 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
         uint32_t grp = g.grp_base[(entry >> 16) & 0xFFu] + ((entry >> 24) >> g.grp_shift);
         uint32_t lo = s_grp_tile[grp], hi = s_grp_tile[grp + 1u];
         uint32_t k = claim_ticket(&g.q->grp_next[grp * kCounterStride], &s_ticket);
-        // One flat loop: work through the own group's range (the next ticket
-        // is requested before the body runs, so its round trip overlaps the
-        // tile), then steal from the next group in ring order that still has
-        // tiles, found by wave 0 reading every group's counter at once.
+        // One flat loop: work through the own group's range, then steal from
+        // the next group in ring order that still has tiles, found by wave 0
+        // reading every group's counter at once.
         for (;;) {
             if (k < hi - lo) {
                 uint32_t next = 0u;
-                if (threadIdx.x == 0)
+                if (AHEAD && threadIdx.x == 0)
                     next = __hip_atomic_fetch_add(&g.q->grp_next[grp * kCounterStride], 1u,
                                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 log_tile(g, cu, lo + k);
                 body(lo + k, cu, err);
+                if (!AHEAD && threadIdx.x == 0)
+                    next = __hip_atomic_fetch_add(&g.q->grp_next[grp * kCounterStride], 1u,
+                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 if (threadIdx.x == 0)
                     s_ticket = next;
                 __syncthreads();

@@ -213,7 +213,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
         }
         __syncthreads();
     };
-    gated_tile_loop(g, n_tiles, body, NoOp(), NoOp());
+    gated_tile_loop<true>(g, n_tiles, body, NoOp(), NoOp());
 }
 
 template <int DT>
@@ -302,7 +302,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemm_mfma(
         }
         __syncthreads();
     };
-    gated_tile_loop(g, n_tiles, body, NoOp(), NoOp());
+    gated_tile_loop<true>(g, n_tiles, body, NoOp(), NoOp());
 }
 
 typedef void (*GemvKernel)(const uint8_t *, const uint32_t *, uint64_t, uint32_t, uint32_t,

@@ -18,10 +18,12 @@ namespace sgdrc {
 constexpr uint32_t kCtxMagic = 0x53474452u;  // "SGDR"
 constexpr int kMaxStreams = 64;
 constexpr int kHistBins = 256;
-// CUs served by one work queue: a whole XCD for long streaming kernels
-// (dynamic balance across the XCD), a few CUs for short kernels such as the
-// GEMV (fewer workgroups contending on each counter).
-constexpr int kStreamGroupCus = 32;
+// CUs served by one work queue.  Long streaming kernels use one queue for
+// the whole device (0): tiles are then taken in address order by all CUs
+// together, which measured faster on MI355X than splitting the address range
+// over per-XCD queues.  Short kernels such as the GEMV use queues of a few
+// CUs, so that fewer workgroups contend on each counter.
+constexpr int kStreamGroupCus = 0;
 constexpr int kGemvGroupCus = 8;
 
 struct StreamState {
@@ -84,7 +86,8 @@ int check_ctx(const sgdrc_ctx *ctx, Ctx **out);
 int stream_state(Ctx *c, void *stream, StreamState **out);
 
 // Gate arguments for a launch of ``n_tiles`` tiles on ``stream`` whose work
-// queues serve runs of ``group_cus`` CUs (a power of two, at most 32).
+// queues serve runs of ``group_cus`` CUs inside an XCD (a power of two, at
+// most 32), or the whole device (0).
 int make_gate(Ctx *c, void *stream, uint64_t n_tiles, int group_cus, Gate *g, LaunchInfo *li);
 
 // Grid size for a gated persistent kernel: the same number of workgroups

@@ -105,7 +105,7 @@ __global__ __launch_bounds__(kStreamThreads) void k_relayout(
             __syncthreads();
         }
     };
-    gated_tile_loop(g, n_tiles, body, NoOp(), NoOp());
+    gated_tile_loop<false>(g, n_tiles, body, NoOp(), NoOp());
 }
 
 __device__ __forceinline__ u32x4 fma4(float s, u32x4 c, u32x4 b)
@@ -220,7 +220,7 @@ __global__ __launch_bounds__(kStreamThreads) void k_triad(
             __syncthreads();
         }
     };
-    gated_tile_loop(g, n_tiles, body, NoOp(), NoOp());
+    gated_tile_loop<false>(g, n_tiles, body, NoOp(), NoOp());
 }
 
 }  // namespace sgdrc
