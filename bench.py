@@ -300,6 +300,7 @@ def bench_classify_one(torch, sg, synth, ctx, stream, timer, n, reps, hist):
     masks = synth.xor_masks(6, seed=1, min_bit=12)
     addrs = synth.page_addresses(n, seed=0)
     d_addrs = torch.from_numpy(addrs.view("int64")).to("cuda:0")
+    torch.cuda.synchronize()
     d_col = torch.empty(n, dtype=torch.uint8, device="cuda:0")
     d_hist = torch.empty(64, dtype=torch.int64, device="cuda:0") if hist else None
     tag = ("classify", hist)
@@ -339,6 +340,7 @@ def bench_relayout(torch, sg, synth, ctx, stream, timer, reps=10):
     pt = torch.empty(pages, dtype=torch.int32, device="cuda:0")
     sg.colour_alloc_pagetable(ctx, masks, base, shift, pool_pages, range(16), pages, pt, stream)
     back = torch.empty_like(all_form)
+    torch.cuda.synchronize()   # operands made on torch's stream, used on ``stream``
     A = sg.paged(all_form, ident, pages)
     S = sg.paged(base, pt, pool_pages)
     B = sg.paged(back, ident, pages)
@@ -380,6 +382,7 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
     g.manual_seed(7)
     x = (torch.randn(8 * 11008, generator=g, device="cuda:0")).to(torch.bfloat16)
     for (M, K) in [(4096, 11008), (11008, 4096)]:
+        torch.cuda.synchronize()   # operands made on torch's stream, used on ``stream``
         w_bytes = M * K * 2
         pages = -(-w_bytes // P)
         pool_pages = int(copies * pages * 64 / 48 * 1.1) + 16
@@ -389,6 +392,7 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
                                   pt, stream)
         w = (torch.randn(M * K, generator=g, device="cuda:0") * 0.02).to(torch.bfloat16)
         ident = torch.arange(pages, dtype=torch.int32, device="cuda:0")
+        torch.cuda.synchronize()
         W = []
         for i in range(copies):
             Wi = sg.paged(base, pt[i * pages:(i + 1) * pages], pool_pages)
