@@ -3,6 +3,13 @@
 Every HIP source is compiled with packed-fp32 instructions disabled
 (``-target-feature -packed-fp32-ops``); the host pass warns that it does not
 know the feature, which is harmless.
+
+The atomic optimizer is switched off (``-amdgpu-atomic-optimizer-strategy=
+None``).  Every atomic in the library is issued by one lane or by lanes with
+distinct addresses, so the pass has nothing to combine; what it does do is
+rewrite a one-lane ticket fetch-add into a wave-wide form whose result is
+read back at once, which makes the wavefront wait for all of its outstanding
+loads and stores right where the ticket is requested.
 """
 from __future__ import annotations
 
@@ -23,6 +30,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CFLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
     "-I", os.path.join(ROOT, "include"), "-I", CSRC,
 ]
 

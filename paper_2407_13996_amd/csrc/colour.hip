@@ -1,9 +1,11 @@
 // Batched XOR-hash colouring and the ordered page-table build.
 //
 // Colour bit k of an address is the parity of (address & M_k).  The
-// classify kernel streams 8-byte addresses with 16-byte non-temporal loads
-// (16 addresses per lane per step) and writes one colour byte each, packed
-// 16 to a lane store.  The page-table build is an ordered stream compaction
+// classify kernel streams 8-byte addresses with 16-byte non-temporal loads,
+// each wavefront instruction reading 1 KiB of consecutive addresses, and
+// writes one colour byte per address: every wavefront passes its 1024
+// colour bytes of a step through its own 1 KiB of LDS so that each lane
+// stores 16 consecutive colours with one 16-byte store.  The page-table build is an ordered stream compaction
 // over the pool's page addresses: a counting pass, a scan of per-workgroup
 // counts, and an emitting pass that places each qualifying page with a
 // wavefront ballot and a masked bit count, so the table comes out in
@@ -37,9 +39,10 @@ __device__ __forceinline__ uint32_t colour_of(uint32_t lo, uint32_t hi, const Ha
 }
 
 constexpr int kClsThreads = 256;
-constexpr int kClsPerLane = 16;  // addresses per lane per step (128 bytes)
+constexpr int kClsLoads = 8;                        // 16-byte loads per lane per step
+constexpr uint32_t kClsWaveStep = 64u * 2u * kClsLoads;  // 1024 addresses per wavefront step
 constexpr int kClsSteps = 4;
-constexpr uint64_t kClsTile = (uint64_t)kClsThreads * kClsPerLane * kClsSteps;
+constexpr uint64_t kClsTile = (uint64_t)kClsThreads / 64u * kClsWaveStep * kClsSteps;  // 16384
 
 // Histogram bins are replicated 16 times in LDS (copy = lane % 16) so that
 // the LDS atomics of one wavefront rarely meet on one address.
@@ -54,42 +57,57 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
 {
     constexpr uint32_t kBins = 1u << K;
     __shared__ uint32_t s_hist[HIST ? kBins * kHistCopies : 1];
-    const uint32_t copy = threadIdx.x % kHistCopies;
+    // per wavefront: the colour bytes of one step, 2 per lane and load
+    __shared__ __attribute__((aligned(16))) uint16_t s_col[kClsThreads / 64][kClsWaveStep / 2];
+    const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
+    const uint32_t copy = lane % kHistCopies;
     if (HIST) {
         for (uint32_t i = threadIdx.x; i < kBins * kHistCopies; i += kClsThreads)
             s_hist[i] = 0;
         __syncthreads();
     }
-    auto body = [&](uint32_t t, uint32_t, uint32_t &) {
+    auto body = [&](uint32_t t, uint32_t, uint32_t &, auto &&claim) {
         const uint64_t tile0 = (uint64_t)t * kClsTile;
 #pragma unroll 1
         for (int s = 0; s < kClsSteps; ++s) {
-            const uint64_t i0 = tile0 + ((uint64_t)s * kClsThreads + threadIdx.x) * kClsPerLane;
-            if (i0 + kClsPerLane <= n) {
-                u32x4 v[kClsPerLane / 2];
+            const bool last = s == kClsSteps - 1;
+            // first address of this wavefront's step (wave-uniform)
+            const uint64_t base = tile0 + ((uint64_t)s * (kClsThreads / 64) + wave) * kClsWaveStep;
+            if (base + kClsWaveStep <= n) {
+                u32x4 v[kClsLoads];
 #pragma unroll
-                for (int j = 0; j < kClsPerLane / 2; ++j)
-                    v[j] = load_nt(addrs + i0 + 2 * j);
-                uint32_t packed[4] = {0u, 0u, 0u, 0u};
+                for (int j = 0; j < kClsLoads; ++j)
+                    v[j] = load_nt(addrs + base + 2u * (j * 64u + lane));
+                if (last)
+                    claim();
 #pragma unroll
-                for (int j = 0; j < kClsPerLane / 2; ++j) {
+                for (int j = 0; j < kClsLoads; ++j) {
                     const uint32_t c0 = colour_of<K>(v[j].x, v[j].y, h);
                     const uint32_t c1 = colour_of<K>(v[j].z, v[j].w, h);
-                    packed[j >> 1] |= (c0 | (c1 << 8)) << ((j & 1) * 16);
+                    s_col[wave][j * 64u + lane] = (uint16_t)(c0 | (c1 << 8));
                     if (HIST) {
                         atomicAdd(&s_hist[c0 * kHistCopies + copy], 1u);
                         atomicAdd(&s_hist[c1 * kHistCopies + copy], 1u);
                     }
                 }
-                u32x4 out = {packed[0], packed[1], packed[2], packed[3]};
-                store_nt(colours + i0, out);
-            } else if (i0 < n) {
-                for (uint64_t i = i0; i < n; ++i) {
-                    const uint64_t a = addrs[i];
-                    const uint32_t c = colour_of<K>((uint32_t)a, (uint32_t)(a >> 32), h);
-                    colours[i] = (uint8_t)c;
-                    if (HIST)
-                        atomicAdd(&s_hist[c * kHistCopies + copy], 1u);
+                // LDS accesses of one wavefront complete in order; this
+                // only keeps the compiler from moving the read up
+                __builtin_amdgcn_wave_barrier();
+                const u32x4 out = *reinterpret_cast<const u32x4 *>(&s_col[wave][lane * 8u]);
+                __builtin_amdgcn_wave_barrier();
+                store_nt(colours + base + 16u * lane, out);
+            } else {
+                if (last)
+                    claim();
+                for (uint32_t r = 0; r < kClsWaveStep / 64u; ++r) {
+                    const uint64_t i = base + r * 64u + lane;
+                    if (i < n) {
+                        const uint64_t a = addrs[i];
+                        const uint32_t c = colour_of<K>((uint32_t)a, (uint32_t)(a >> 32), h);
+                        colours[i] = (uint8_t)c;
+                        if (HIST)
+                            atomicAdd(&s_hist[c * kHistCopies + copy], 1u);
+                    }
                 }
             }
         }
@@ -121,7 +139,7 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
             }
         }
     };
-    gated_tile_loop<false>(g, n_tiles, body, flush, epilogue);
+    gated_tile_loop<Claim::Mid>(g, n_tiles, body, flush, epilogue);
 }
 
 constexpr int kPtThreads = 256;

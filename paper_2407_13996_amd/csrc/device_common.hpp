@@ -12,6 +12,7 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kLutSize = 4096;          // (XCC_ID[3:0] << 8) | HW_ID[15:8]
 constexpr uint32_t kLutNone = 0xFFFFFFFFu;  // key never seen by the probe
@@ -163,28 +164,42 @@ __device__ __forceinline__ void reset_slot(QueueSlot *q)
         __hip_atomic_store(&q->done_all[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Runs ``body(tile, cu, err)`` for every tile that this workgroup obtains,
-// under the gate.  Workgroups on CUs outside the mask take no tiles; the
-// others take tiles of their own group's range, then steal from other
-// groups' ranges until every range is exhausted.  ``flush()`` runs after a
-// workgroup's tile loop (to publish per-workgroup partials).  The last
-// workgroup to arrive finishes the tiles of any range that no workgroup
-// took (only possible when no workgroup landed on any allowed CU; flagged),
-// flushes again, calls ``epilogue()`` with every other workgroup's work
-// complete, and zeroes the slot.
+struct NoOp {
+    __device__ void operator()() const {}
+};
+
+// When a workgroup takes its next ticket relative to the work of a tile.
+//  Ahead: before the tile, so that the round trip overlaps the whole tile;
+//    pays off for short launches of one or two tiles per workgroup (GEMV).
+//  Mid:   where the body calls ``claim()``: streaming bodies call it after
+//    issuing their loads and before their stores.  On gfx950 one counter
+//    tracks loads, stores and atomics of a wave in issue order, so waiting
+//    for a ticket taken after the stores also waits for the stores to be
+//    acknowledged by memory, and a ticket taken before the loads holds the
+//    loads back behind a contended atomic; between the two it costs neither.
+//  After: after the tile.
+enum class Claim { Ahead, Mid, After };
+
+// Runs ``body(tile, cu, err, claim)`` for every tile that this workgroup
+// obtains, under the gate.  Workgroups on CUs outside the mask take no
+// tiles; the others take tiles of their own group's range, then steal from
+// other groups' ranges until every range is exhausted.  ``flush()`` runs
+// after a workgroup's tile loop (to publish per-workgroup partials).  The
+// last workgroup to arrive finishes the tiles of any range that no
+// workgroup took (only possible when no workgroup landed on any allowed CU;
+// flagged), flushes again, calls ``epilogue()`` with every other
+// workgroup's work complete, and zeroes the slot.
+//
+// ``claim`` is a callable that every thread of the workgroup calls exactly
+// once per tile, on a workgroup-uniform path; only Claim::Mid gives it an
+// effect.
 //
 // Bodies must not return early or branch around the rest of the tile on a
 // per-lane condition: the loop contains barriers, and a lane-dependent exit
 // from it lets the compiler send some lanes of a wave back to the barrier
 // while others still owe the next ticket.  Bodies record problems in the
 // per-thread ``err`` bits instead; they are raised once, after the loop.
-//
-// AHEAD: request the next ticket before the body runs, so that its round
-// trip overlaps the tile.  That pays off for short launches of one or two
-// tiles per workgroup (the GEMV); on long streaming launches it measured
-// slower on MI355X (an atomic issued ahead of a tile's loads delays them),
-// so streaming kernels claim after the body.
-template <bool AHEAD, typename Body, typename Flush, typename Epilogue>
+template <Claim CL, typename Body, typename Flush, typename Epilogue>
 __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles, Body body,
                                                 Flush flush, Epilogue epilogue)
 {
@@ -209,17 +224,27 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
         // One flat loop: work through the own group's range, then steal from
         // the next group in ring order that still has tiles, found by wave 0
         // reading every group's counter at once.
+        //
+        // ``next`` lives across iterations and is written only by the ticket
+        // atomic: re-initialising it in the loop would be a vector-ALU write
+        // to the atomic's destination register, for which the compiler waits
+        // on the memory counter, stalling the tile's loads behind the
+        // previous tile's stores.
+        uint32_t next = 0u;
         for (;;) {
             if (k < hi - lo) {
-                uint32_t next = 0u;
-                if (AHEAD && threadIdx.x == 0)
-                    next = __hip_atomic_fetch_add(&g.q->grp_next[grp * kCounterStride], 1u,
-                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                uint32_t *const ctr = &g.q->grp_next[grp * kCounterStride];
+                if (CL == Claim::Ahead && threadIdx.x == 0)
+                    next = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                auto claim = [&]() {
+                    if (CL == Claim::Mid && threadIdx.x == 0)
+                        next = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT);
+                };
                 log_tile(g, cu, lo + k);
-                body(lo + k, cu, err);
-                if (!AHEAD && threadIdx.x == 0)
-                    next = __hip_atomic_fetch_add(&g.q->grp_next[grp * kCounterStride], 1u,
-                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                body(lo + k, cu, err, claim);
+                if (CL == Claim::After && threadIdx.x == 0)
+                    next = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 if (threadIdx.x == 0)
                     s_ticket = next;
                 __syncthreads();
@@ -286,7 +311,7 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
             while (c < (uint32_t)kMaxGroups) {
                 if (t < end) {
                     log_tile(g, cu, t);
-                    body(t, cu, err);
+                    body(t, cu, err, NoOp());
                     t += 1u;
                 } else {
                     c += 1u;
@@ -307,10 +332,6 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
         raise_flag(g.err, err);
 }
 
-struct NoOp {
-    __device__ void operator()() const {}
-};
-
 // Page-table lookup with the range check every kernel applies: an entry
 // outside the pool yields kBadPage and sets kDevErrPtRange in ``err``.
 __device__ __forceinline__ uint32_t checked_page(const uint32_t *pt, uint64_t j,
@@ -320,6 +341,32 @@ __device__ __forceinline__ uint32_t checked_page(const uint32_t *pt, uint64_t j,
     const bool bad = (uint64_t)p >= pool_pages;
     err |= bad ? kDevErrPtRange : 0u;
     return bad ? kBadPage : p;
+}
+
+// Buffer resources (gfx9 descriptor, raw addressing: stride 0, byte offsets,
+// data-format word as used for untyped buffers on this family).  Accesses at
+// byte offsets at or beyond ``bytes`` are dropped by the hardware: loads
+// return zero and stores write nothing.  Kernels keep every 16-byte access
+// 16-byte aligned and every range a multiple of 16 bytes, so an access is
+// either wholly inside or wholly outside its range.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr int kRsrcWord3 = 0x00020000;
+constexpr int kAuxNt = 2;  // cache policy: non-temporal
+
+__device__ __forceinline__ Rsrc make_rsrc(const void *base, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
+                                             kRsrcWord3);
+}
+
+__device__ __forceinline__ u32x4 buf_load_nt(Rsrc r, uint32_t off)
+{
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kAuxNt));
+}
+
+__device__ __forceinline__ void buf_store_nt(Rsrc r, uint32_t off, u32x4 v)
+{
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, v), r, off, 0, kAuxNt);
 }
 
 __device__ __forceinline__ u32x4 load_nt(const void *p)

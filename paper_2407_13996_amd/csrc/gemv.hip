@@ -111,7 +111,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
     const uint32_t KV = (uint32_t)(row_bytes / 16u);
     const uint64_t pmask = (1ull << shift) - 1ull;
 
-    auto body = [&](uint32_t t, uint32_t, uint32_t &err) {
+    auto body = [&](uint32_t t, uint32_t, uint32_t &err, auto &&) {
         const uint32_t m0 = t * kGemvRows;
         const uint32_t m_end = min(m0 + (uint32_t)kGemvRows, M);
         const TilePages tp = stage_pages(pt, pool_pages, (uint64_t)m0 * row_bytes,
@@ -213,7 +213,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
         }
         __syncthreads();
     };
-    gated_tile_loop<true>(g, n_tiles, body, NoOp(), NoOp());
+    gated_tile_loop<Claim::Ahead>(g, n_tiles, body, NoOp(), NoOp());
 }
 
 template <int DT>
@@ -246,7 +246,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemm_mfma(
     const uint32_t KV = (uint32_t)(row_bytes / 16u);
     const uint64_t pmask = (1ull << shift) - 1ull;
 
-    auto body = [&](uint32_t t, uint32_t, uint32_t &err) {
+    auto body = [&](uint32_t t, uint32_t, uint32_t &err, auto &&) {
         const uint32_t m0 = t * kMfmaRows;
         const uint32_t m_end = min(m0 + (uint32_t)kMfmaRows, M);
         const TilePages tp = stage_pages(pt, pool_pages, (uint64_t)m0 * row_bytes,
@@ -302,7 +302,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemm_mfma(
         }
         __syncthreads();
     };
-    gated_tile_loop<true>(g, n_tiles, body, NoOp(), NoOp());
+    gated_tile_loop<Claim::Ahead>(g, n_tiles, body, NoOp(), NoOp());
 }
 
 typedef void (*GemvKernel)(const uint8_t *, const uint32_t *, uint64_t, uint32_t, uint32_t,

@@ -1,72 +1,111 @@
 // Page-table-indirected streaming kernels: bimodal relayout (page-set to
 // page-set copy) and the colour-restricted triad a = b + s*c.
 //
-// Both run as gated persistent grids over a tile queue.  A tile is 32 KiB of
-// logical bytes per array; every lane moves 8 chunks of 16 bytes
-// (128 bytes in flight per lane and array) with non-temporal loads and
-// stores.  When a page is at least a tile, the tile's page-table entries are
-// wave-uniform scalar loads; for smaller pages the tile's entries are staged
-// in LDS once per tile and every chunk looks its page up there.
+// Both run as gated persistent grids over a tile queue, one workgroup per
+// CU.  A tile is 64 KiB of logical bytes per array; each of the four
+// wavefronts of a workgroup owns 16 KiB of it, and every lane moves 16
+// chunks of 16 bytes (256 bytes in flight per lane and array) with
+// non-temporal buffer loads and stores, each wavefront instruction covering
+// 1 KiB of consecutive bytes.
+//
+// Every access goes through a buffer resource whose base is a page address
+// and whose range is the number of bytes that may be touched there: zero
+// for a tile with an out-of-range page-table entry, the bytes left for the
+// last tile.  The hardware drops accesses outside the range, so the tile
+// body is the same straight-line code for full, ragged and skipped tiles.
+// That matters for speed as well as brevity: the next tile's ticket is
+// requested between the loads and the stores, and its result is waited for
+// only after the stores have been issued; a branch in the body would make
+// the compiler wait for the stores too on the way to the next tile.
+//
+// Tiles cover the largest multiple of 16 bytes; the last n_bytes mod 16
+// bytes are moved by the last workgroup of the grid after all tiles are
+// done (it may sit on any CU).
+#include <algorithm>
+
 #include "host_common.hpp"
 
 namespace sgdrc {
 
 constexpr int kStreamThreads = 256;
-constexpr int kStreamUnroll = 8;
-constexpr uint64_t kStreamTile = (uint64_t)kStreamThreads * 16u * kStreamUnroll;  // 32 KiB
-constexpr int kStreamTileShift = 15;
-constexpr int kTilePagesMax = (int)(kStreamTile >> SGDRC_MIN_PAGE_SHIFT);  // 8
+constexpr uint32_t kStepSpan = 64u * 16u;  // 1 KiB per wavefront instruction
 
-// Byte-wise copy of the ragged end of a 16-byte chunk.
-__device__ __forceinline__ void copy_tail(uint8_t *d, const uint8_t *s, uint32_t n)
+// Tile geometry for U 16-byte chunks per lane and array.
+template <int U>
+struct Geo {
+    static constexpr uint32_t kTile = (uint32_t)kStreamThreads * 16u * U;
+    static constexpr uint32_t kWaveSpan = 64u * 16u * U;
+    static constexpr int kPagesMax = (int)(kTile >> SGDRC_MIN_PAGE_SHIFT);
+};
+
+// Chunks per lane and array (tile = 4 KiB x U) and workgroups per CU.
+// Few deep workgroups measured fastest on MI355X: one 256-thread workgroup
+// per CU (one wavefront per SIMD) with 16 loads of 16 bytes per lane and
+// array in flight moves 1 GiB arrays at about 6.4 TB/s, for the triad and
+// for the copy alike; a second workgroup per CU, or 8 loads per lane, costs
+// 5 to 20 percent.  Unrolls stay powers of two so that a page of at least a
+// tile holds whole tiles.
+constexpr int kTriadUnroll = 16;
+constexpr int kRelayoutUnroll = 16;
+constexpr int kStreamWgsPerCu = 1;
+
+// Bytes of the span [from, from + span) that lie below n16.
+__device__ __forceinline__ uint32_t span_valid(uint64_t from, uint64_t n16, uint32_t span)
 {
-    for (uint32_t i = 0; i < n; ++i)
-        d[i] = s[i];
+    return n16 > from ? (uint32_t)(n16 - from < span ? n16 - from : span) : 0u;
 }
 
-template <bool BIG>
+// Wavefront index, known to the compiler to be uniform.
+__device__ __forceinline__ uint32_t wave_id()
+{
+    return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+}
+
+// Resource for the chunk of a small-page tile at tile offset cs (one page):
+// pool page p (kBadPage: empty range).
+__device__ __forceinline__ Rsrc chunk_rsrc(const uint8_t *pool, uint32_t p, uint32_t shift,
+                                           uint64_t pmask, uint64_t at, uint32_t valid)
+{
+    const bool ok = p != kBadPage;
+    return make_rsrc(pool + (ok ? ((uint64_t)p << shift) + (at & pmask) : 0u), ok ? valid : 0u);
+}
+
+template <int U, bool BIG>
 __global__ __launch_bounds__(kStreamThreads) void k_relayout(
     uint8_t *__restrict__ dst, const uint32_t *__restrict__ pt_d, uint64_t dst_pages,
     const uint8_t *__restrict__ src, const uint32_t *__restrict__ pt_s, uint64_t src_pages,
     uint64_t n_bytes, uint32_t shift, uint32_t n_tiles, Gate g)
 {
-    __shared__ uint32_t s_pd[kTilePagesMax], s_ps[kTilePagesMax];
+    __shared__ uint32_t s_pd[Geo<U>::kPagesMax], s_ps[Geo<U>::kPagesMax];
     const uint64_t pmask = (1ull << shift) - 1ull;
-    const uint64_t n_pages = (n_bytes + pmask) >> shift;
-    auto body = [&](uint32_t t, uint32_t, uint32_t &err) {
-        const uint64_t t0 = (uint64_t)t * kStreamTile;
-        const uint64_t tile_bytes = n_bytes - t0 < kStreamTile ? n_bytes - t0 : kStreamTile;
+    const uint64_t n16 = n_bytes & ~15ull;
+    const uint64_t n_pages = (n16 + pmask) >> shift;
+    const uint32_t lo = wave_id() * Geo<U>::kWaveSpan + (threadIdx.x & 63u) * 16u;
+    auto body = [&](uint32_t t, uint32_t, uint32_t &err, auto &&claim) {
+        const uint64_t t0 = (uint64_t)t * Geo<U>::kTile;
+        u32x4 v[U];
         if (BIG) {
             const uint64_t j = t0 >> shift;
             const uint32_t pd = pt_d[j], ps = pt_s[j];
             const bool bad = pd >= dst_pages || ps >= src_pages;
             err |= bad ? kDevErrPtRange : 0u;
-            uint8_t *d = dst + ((uint64_t)pd << shift) + (t0 & pmask);
-            const uint8_t *s = src + ((uint64_t)ps << shift) + (t0 & pmask);
-            if (bad) {
-                // skip the tile: nothing outside the pools is touched
-            } else if (tile_bytes == kStreamTile) {
-                u32x4 v[kStreamUnroll];
+            const uint32_t valid = bad ? 0u : span_valid(t0, n16, Geo<U>::kTile);
+            const uint64_t in = t0 & pmask;
+            const Rsrc rd = make_rsrc(dst + (bad ? 0u : ((uint64_t)pd << shift) + in), valid);
+            const Rsrc rs = make_rsrc(src + (bad ? 0u : ((uint64_t)ps << shift) + in), valid);
 #pragma unroll
-                for (int u = 0; u < kStreamUnroll; ++u)
-                    v[u] = load_nt(s + ((uint64_t)u * kStreamThreads + threadIdx.x) * 16u);
+            for (int u = 0; u < U; ++u)
+                v[u] = buf_load_nt(rs, lo + u * kStepSpan);
+            claim();
 #pragma unroll
-                for (int u = 0; u < kStreamUnroll; ++u)
-                    store_nt(d + ((uint64_t)u * kStreamThreads + threadIdx.x) * 16u, v[u]);
-            } else {
-                for (int u = 0; u < kStreamUnroll; ++u) {
-                    const uint64_t off = ((uint64_t)u * kStreamThreads + threadIdx.x) * 16u;
-                    if (off + 16u <= tile_bytes)
-                        store_nt(d + off, load_nt(s + off));
-                    else if (off < tile_bytes)
-                        copy_tail(d + off, s + off, (uint32_t)(tile_bytes - off));
-                }
-            }
+            for (int u = 0; u < U; ++u)
+                buf_store_nt(rd, lo + u * kStepSpan, v[u]);
         } else {
-            const uint64_t j0 = t0 >> shift;
-            const uint32_t np = (uint32_t)(kStreamTile >> shift);
+            // stage the tile's page-table entries; each wavefront
+            // instruction then covers 1 KiB inside one page
+            const uint32_t np = Geo<U>::kTile >> shift;
             if (threadIdx.x < np) {
-                const uint64_t j = j0 + threadIdx.x;
+                const uint64_t j = (t0 >> shift) + threadIdx.x;
                 uint32_t pd = kBadPage, ps = kBadPage;
                 if (j < n_pages) {
                     pd = checked_page(pt_d, j, dst_pages, err);
@@ -76,36 +115,49 @@ __global__ __launch_bounds__(kStreamThreads) void k_relayout(
                 s_ps[threadIdx.x] = ps;
             }
             __syncthreads();
-            u32x4 v[kStreamUnroll];
-            uint8_t *dp[kStreamUnroll];
+            const uint32_t lane16 = (threadIdx.x & 63u) * 16u;
+            const uint32_t wbase = wave_id() * Geo<U>::kWaveSpan;
 #pragma unroll
-            for (int u = 0; u < kStreamUnroll; ++u) {
-                const uint64_t off = ((uint64_t)u * kStreamThreads + threadIdx.x) * 16u;
-                dp[u] = nullptr;
-                if (off < tile_bytes) {
-                    const uint32_t jl = (uint32_t)(off >> shift);
-                    const uint32_t pd = s_pd[jl], ps = s_ps[jl];
-                    if (pd != kBadPage && ps != kBadPage) {
-                        const uint64_t in = (t0 + off) & pmask;
-                        dp[u] = dst + ((uint64_t)pd << shift) + in;
-                        const uint8_t *sp = src + ((uint64_t)ps << shift) + in;
-                        if (off + 16u <= tile_bytes) {
-                            v[u] = load_nt(sp);
-                        } else {
-                            copy_tail(dp[u], sp, (uint32_t)(tile_bytes - off));
-                            dp[u] = nullptr;
-                        }
-                    }
-                }
+            for (int u = 0; u < U; ++u) {
+                const uint32_t cs = wbase + u * kStepSpan;
+                const uint32_t jl = cs >> shift;
+                const uint32_t pd = __builtin_amdgcn_readfirstlane(s_pd[jl]);
+                const uint32_t ps = __builtin_amdgcn_readfirstlane(s_ps[jl]);
+                const uint32_t valid =
+                    pd == kBadPage ? 0u : span_valid(t0 + cs, n16, kStepSpan);
+                v[u] = buf_load_nt(chunk_rsrc(src, ps, shift, pmask, t0 + cs, valid), lane16);
             }
+            claim();
 #pragma unroll
-            for (int u = 0; u < kStreamUnroll; ++u)
-                if (dp[u])
-                    store_nt(dp[u], v[u]);
+            for (int u = 0; u < U; ++u) {
+                const uint32_t cs = wbase + u * kStepSpan;
+                const uint32_t jl = cs >> shift;
+                const uint32_t pd = __builtin_amdgcn_readfirstlane(s_pd[jl]);
+                const uint32_t ps = __builtin_amdgcn_readfirstlane(s_ps[jl]);
+                const uint32_t valid =
+                    ps == kBadPage ? 0u : span_valid(t0 + cs, n16, kStepSpan);
+                buf_store_nt(chunk_rsrc(dst, pd, shift, pmask, t0 + cs, valid), lane16, v[u]);
+            }
             __syncthreads();
         }
     };
-    gated_tile_loop<false>(g, n_tiles, body, NoOp(), NoOp());
+    // the last n_bytes mod 16 bytes, all inside the page that holds byte n16
+    auto epilogue = [&]() {
+        const uint32_t rem = (uint32_t)(n_bytes - n16);
+        if (threadIdx.x < rem) {
+            const uint64_t j = n16 >> shift;
+            uint32_t e = 0u;
+            const uint32_t pd = checked_page(pt_d, j, dst_pages, e);
+            const uint32_t ps = checked_page(pt_s, j, src_pages, e);
+            if (e == 0u) {
+                const uint64_t in = (n16 + threadIdx.x) & pmask;
+                dst[((uint64_t)pd << shift) + in] = src[((uint64_t)ps << shift) + in];
+            } else {
+                raise_flag(g.err, e);
+            }
+        }
+    };
+    gated_tile_loop<Claim::Mid>(g, n_tiles, body, NoOp(), epilogue);
 }
 
 __device__ __forceinline__ u32x4 fma4(float s, u32x4 c, u32x4 b)
@@ -118,109 +170,102 @@ __device__ __forceinline__ u32x4 fma4(float s, u32x4 c, u32x4 b)
     return r;
 }
 
-template <bool BIG>
+template <int U, bool BIG>
 __global__ __launch_bounds__(kStreamThreads) void k_triad(
     uint8_t *a, const uint32_t *__restrict__ pt_a, uint64_t a_pages,
     const uint8_t *b, const uint32_t *__restrict__ pt_b, uint64_t b_pages,
     const uint8_t *c, const uint32_t *__restrict__ pt_c, uint64_t c_pages, float s,
     uint64_t n_bytes, uint32_t shift, uint32_t n_tiles, Gate g)
 {
-    __shared__ uint32_t s_pa[kTilePagesMax], s_pb[kTilePagesMax], s_pc[kTilePagesMax];
+    __shared__ uint32_t s_pa[Geo<U>::kPagesMax], s_pb[Geo<U>::kPagesMax], s_pc[Geo<U>::kPagesMax];
     const uint64_t pmask = (1ull << shift) - 1ull;
-    const uint64_t n_pages = (n_bytes + pmask) >> shift;
-    auto body = [&](uint32_t t, uint32_t, uint32_t &err) {
-        const uint64_t t0 = (uint64_t)t * kStreamTile;
-        const uint64_t tile_bytes = n_bytes - t0 < kStreamTile ? n_bytes - t0 : kStreamTile;
+    const uint64_t n16 = n_bytes & ~15ull;
+    const uint64_t n_pages = (n16 + pmask) >> shift;
+    const uint32_t lo = wave_id() * Geo<U>::kWaveSpan + (threadIdx.x & 63u) * 16u;
+    auto body = [&](uint32_t t, uint32_t, uint32_t &err, auto &&claim) {
+        const uint64_t t0 = (uint64_t)t * Geo<U>::kTile;
+        u32x4 vb[U], vc[U];
         if (BIG) {
             const uint64_t j = t0 >> shift;
             const uint32_t pa = pt_a[j], pb = pt_b[j], pc = pt_c[j];
             const bool bad = pa >= a_pages || pb >= b_pages || pc >= c_pages;
             err |= bad ? kDevErrPtRange : 0u;
+            const uint32_t valid = bad ? 0u : span_valid(t0, n16, Geo<U>::kTile);
             const uint64_t in = t0 & pmask;
-            uint8_t *ap = a + ((uint64_t)pa << shift) + in;
-            const uint8_t *bp = b + ((uint64_t)pb << shift) + in;
-            const uint8_t *cp = c + ((uint64_t)pc << shift) + in;
-            if (bad) {
-                // skip the tile: nothing outside the pools is touched
-            } else if (tile_bytes == kStreamTile) {
-                u32x4 vb[kStreamUnroll], vc[kStreamUnroll];
+            const Rsrc ra = make_rsrc(a + (bad ? 0u : ((uint64_t)pa << shift) + in), valid);
+            const Rsrc rb = make_rsrc(b + (bad ? 0u : ((uint64_t)pb << shift) + in), valid);
+            const Rsrc rc = make_rsrc(c + (bad ? 0u : ((uint64_t)pc << shift) + in), valid);
 #pragma unroll
-                for (int u = 0; u < kStreamUnroll; ++u) {
-                    const uint64_t off = ((uint64_t)u * kStreamThreads + threadIdx.x) * 16u;
-                    vb[u] = load_nt(bp + off);
-                    vc[u] = load_nt(cp + off);
-                }
-#pragma unroll
-                for (int u = 0; u < kStreamUnroll; ++u) {
-                    const uint64_t off = ((uint64_t)u * kStreamThreads + threadIdx.x) * 16u;
-                    store_nt(ap + off, fma4(s, vc[u], vb[u]));
-                }
-            } else {
-                for (int u = 0; u < kStreamUnroll; ++u) {
-                    const uint64_t off = ((uint64_t)u * kStreamThreads + threadIdx.x) * 16u;
-                    if (off + 16u <= tile_bytes) {
-                        store_nt(ap + off, fma4(s, load_nt(cp + off), load_nt(bp + off)));
-                    } else if (off < tile_bytes) {
-                        for (uint64_t e = off; e < tile_bytes; e += 4) {
-                            const float r = __builtin_fmaf(s, *(const float *)(cp + e),
-                                                           *(const float *)(bp + e));
-                            *(float *)(ap + e) = r;
-                        }
-                    }
-                }
+            for (int u = 0; u < U; ++u) {
+                vb[u] = buf_load_nt(rb, lo + u * kStepSpan);
+                vc[u] = buf_load_nt(rc, lo + u * kStepSpan);
             }
+            claim();
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                buf_store_nt(ra, lo + u * kStepSpan, fma4(s, vc[u], vb[u]));
         } else {
-            const uint64_t j0 = t0 >> shift;
-            const uint32_t np = (uint32_t)(kStreamTile >> shift);
+            const uint32_t np = Geo<U>::kTile >> shift;
             if (threadIdx.x < np) {
-                const uint64_t j = j0 + threadIdx.x;
+                const uint64_t j = (t0 >> shift) + threadIdx.x;
                 uint32_t pa = kBadPage, pb = kBadPage, pc = kBadPage;
                 if (j < n_pages) {
                     pa = checked_page(pt_a, j, a_pages, err);
                     pb = checked_page(pt_b, j, b_pages, err);
                     pc = checked_page(pt_c, j, c_pages, err);
                 }
-                s_pa[threadIdx.x] = pa;
-                s_pb[threadIdx.x] = pb;
-                s_pc[threadIdx.x] = pc;
+                // a chunk is skipped unless all three of its pages are valid
+                const bool ok = pa != kBadPage && pb != kBadPage && pc != kBadPage;
+                s_pa[threadIdx.x] = ok ? pa : kBadPage;
+                s_pb[threadIdx.x] = ok ? pb : kBadPage;
+                s_pc[threadIdx.x] = ok ? pc : kBadPage;
             }
             __syncthreads();
-            u32x4 vb[kStreamUnroll], vc[kStreamUnroll];
-            uint8_t *ap[kStreamUnroll];
+            const uint32_t lane16 = (threadIdx.x & 63u) * 16u;
+            const uint32_t wbase = wave_id() * Geo<U>::kWaveSpan;
 #pragma unroll
-            for (int u = 0; u < kStreamUnroll; ++u) {
-                const uint64_t off = ((uint64_t)u * kStreamThreads + threadIdx.x) * 16u;
-                ap[u] = nullptr;
-                if (off < tile_bytes) {
-                    const uint32_t jl = (uint32_t)(off >> shift);
-                    const uint32_t pa = s_pa[jl], pb = s_pb[jl], pc = s_pc[jl];
-                    if (pa != kBadPage && pb != kBadPage && pc != kBadPage) {
-                        const uint64_t in = (t0 + off) & pmask;
-                        uint8_t *aq = a + ((uint64_t)pa << shift) + in;
-                        const uint8_t *bq = b + ((uint64_t)pb << shift) + in;
-                        const uint8_t *cq = c + ((uint64_t)pc << shift) + in;
-                        if (off + 16u <= tile_bytes) {
-                            vb[u] = load_nt(bq);
-                            vc[u] = load_nt(cq);
-                            ap[u] = aq;
-                        } else {
-                            for (uint64_t e = 0; e < tile_bytes - off; e += 4) {
-                                const float r = __builtin_fmaf(s, *(const float *)(cq + e),
-                                                               *(const float *)(bq + e));
-                                *(float *)(aq + e) = r;
-                            }
-                        }
-                    }
-                }
+            for (int u = 0; u < U; ++u) {
+                const uint32_t cs = wbase + u * kStepSpan;
+                const uint32_t jl = cs >> shift;
+                const uint32_t pb = __builtin_amdgcn_readfirstlane(s_pb[jl]);
+                const uint32_t pc = __builtin_amdgcn_readfirstlane(s_pc[jl]);
+                const uint32_t valid = span_valid(t0 + cs, n16, kStepSpan);
+                vb[u] = buf_load_nt(chunk_rsrc(b, pb, shift, pmask, t0 + cs, valid), lane16);
+                vc[u] = buf_load_nt(chunk_rsrc(c, pc, shift, pmask, t0 + cs, valid), lane16);
             }
+            claim();
 #pragma unroll
-            for (int u = 0; u < kStreamUnroll; ++u)
-                if (ap[u])
-                    store_nt(ap[u], fma4(s, vc[u], vb[u]));
+            for (int u = 0; u < U; ++u) {
+                const uint32_t cs = wbase + u * kStepSpan;
+                const uint32_t jl = cs >> shift;
+                const uint32_t pa = __builtin_amdgcn_readfirstlane(s_pa[jl]);
+                const uint32_t valid = span_valid(t0 + cs, n16, kStepSpan);
+                buf_store_nt(chunk_rsrc(a, pa, shift, pmask, t0 + cs, valid), lane16,
+                             fma4(s, vc[u], vb[u]));
+            }
             __syncthreads();
         }
     };
-    gated_tile_loop<false>(g, n_tiles, body, NoOp(), NoOp());
+    // the last (n_bytes mod 16) / 4 elements, all inside the page of byte n16
+    auto epilogue = [&]() {
+        const uint32_t rem = (uint32_t)(n_bytes - n16) / 4u;
+        if (threadIdx.x < rem) {
+            const uint64_t j = n16 >> shift;
+            uint32_t e = 0u;
+            const uint32_t pa = checked_page(pt_a, j, a_pages, e);
+            const uint32_t pb = checked_page(pt_b, j, b_pages, e);
+            const uint32_t pc = checked_page(pt_c, j, c_pages, e);
+            if (e == 0u) {
+                const uint64_t in = (n16 + 4u * threadIdx.x) & pmask;
+                const float r = __builtin_fmaf(s, *(const float *)(c + ((uint64_t)pc << shift) + in),
+                                               *(const float *)(b + ((uint64_t)pb << shift) + in));
+                *(float *)(a + ((uint64_t)pa << shift) + in) = r;
+            } else {
+                raise_flag(g.err, e);
+            }
+        }
+    };
+    gated_tile_loop<Claim::Mid>(g, n_tiles, body, NoOp(), epilogue);
 }
 
 }  // namespace sgdrc
@@ -242,7 +287,9 @@ int bimodal_relayout(sgdrc_ctx *ctx, const sgdrc_paged *dst, const sgdrc_paged *
     rc = check_ctx(ctx, &c);
     if (rc)
         return rc;
-    const uint64_t n_tiles = (n_bytes + kStreamTile - 1) / kStreamTile;
+    constexpr int U = kRelayoutUnroll;
+    constexpr uint32_t tile = Geo<U>::kTile;
+    const uint64_t n_tiles = ((n_bytes & ~15ull) + tile - 1) / tile;
     if (n_tiles >= (1ull << 31))
         return set_error(SGDRC_EINVAL, "n_bytes too large");
     Gate g;
@@ -251,11 +298,12 @@ int bimodal_relayout(sgdrc_ctx *ctx, const sgdrc_paged *dst, const sgdrc_paged *
     if (rc)
         return rc;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    const bool big = page_shift >= kStreamTileShift;
-    static const int occ_big = occupancy(k_relayout<true>, kStreamThreads);
-    static const int occ_small = occupancy(k_relayout<false>, kStreamThreads);
-    const uint32_t grid = gated_grid(c, big ? occ_big : occ_small, n_tiles, li);
-    auto kern = big ? k_relayout<true> : k_relayout<false>;
+    const bool big = (1ull << page_shift) >= tile;
+    auto kern = big ? k_relayout<U, true> : k_relayout<U, false>;
+    static const int occ_big = occupancy(k_relayout<U, true>, kStreamThreads);
+    static const int occ_small = occupancy(k_relayout<U, false>, kStreamThreads);
+    const int per_cu = std::min(big ? occ_big : occ_small, kStreamWgsPerCu);
+    const uint32_t grid = gated_grid(c, per_cu, n_tiles, li);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(kStreamThreads), 0, s,
                        static_cast<uint8_t *>(dst->pool), dst->pt, dst->pool_pages,
                        static_cast<const uint8_t *>(src->pool), src->pt, src->pool_pages, n_bytes,
@@ -281,7 +329,9 @@ int colored_stream(sgdrc_ctx *ctx, const sgdrc_paged *a, const sgdrc_paged *b,
     if (rc)
         return rc;
     const uint64_t n_bytes = n_elems * 4u;
-    const uint64_t n_tiles = (n_bytes + kStreamTile - 1) / kStreamTile;
+    constexpr int U = kTriadUnroll;
+    constexpr uint32_t tile = Geo<U>::kTile;
+    const uint64_t n_tiles = ((n_bytes & ~15ull) + tile - 1) / tile;
     if (n_tiles >= (1ull << 31))
         return set_error(SGDRC_EINVAL, "n_elems too large");
     Gate g;
@@ -290,11 +340,12 @@ int colored_stream(sgdrc_ctx *ctx, const sgdrc_paged *a, const sgdrc_paged *b,
     if (rc)
         return rc;
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
-    const bool big = page_shift >= kStreamTileShift;
-    static const int occ_big = occupancy(k_triad<true>, kStreamThreads);
-    static const int occ_small = occupancy(k_triad<false>, kStreamThreads);
-    const uint32_t grid = gated_grid(c, big ? occ_big : occ_small, n_tiles, li);
-    auto kern = big ? k_triad<true> : k_triad<false>;
+    const bool big = (1ull << page_shift) >= tile;
+    auto kern = big ? k_triad<U, true> : k_triad<U, false>;
+    static const int occ_big = occupancy(k_triad<U, true>, kStreamThreads);
+    static const int occ_small = occupancy(k_triad<U, false>, kStreamThreads);
+    const int per_cu = std::min(big ? occ_big : occ_small, kStreamWgsPerCu);
+    const uint32_t grid = gated_grid(c, per_cu, n_tiles, li);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(kStreamThreads), 0, hs,
                        static_cast<uint8_t *>(a->pool), a->pt, a->pool_pages,
                        static_cast<const uint8_t *>(b->pool), b->pt, b->pool_pages,

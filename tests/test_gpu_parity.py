@@ -178,7 +178,8 @@ def make_tables(orc, shift, n_pages, S, seed, K=6):
 
 @pytest.mark.parametrize("shift,n_bytes", [(12, 37 * 4096 + 1234), (16, 9 * 65536 + 17),
                                            (21, 2 * 2097152 + 4096 * 3 + 5), (15, 1),
-                                           (16, 64 * 65536)])
+                                           (16, 64 * 65536), (14, 11 * 16384 + 4015),
+                                           (13, 15), (17, 3 * 131072 + 65536 + 32)])
 def test_relayout_matches_oracle(ctx, orc, shift, n_bytes):
     say(f"relayout shift={shift} n_bytes={n_bytes}")
     P = 1 << shift
@@ -218,7 +219,8 @@ def test_relayout_round_trip_fp16_is_identity(ctx, orc):
 # ------------------------------------------------------------------- triad
 
 @pytest.mark.parametrize("shift,n", [(12, 5 * 1024 + 77), (16, 3 * 16384 + 5), (16, 40 * 16384),
-                                     (21, 524288 + 3), (13, 7)])
+                                     (21, 524288 + 3), (13, 7), (14, 9 * 4096 + 2),
+                                     (15, 5 * 8192 + 1), (16, 3)])
 def test_triad_matches_oracle(ctx, orc, shift, n):
     say(f"triad shift={shift} n={n}")
     P = 1 << shift
@@ -361,7 +363,7 @@ def test_cu_mask_confines_work_and_visits_each_tile_once(ctx, orc):
         sg.set_cu_mask(ctx, stream, None)
         assert ctx.device_error() & sg.DEVERR_PT_RANGE == 0
         cl, tl = to_host(cu_log), to_host(tile_log)
-        assert tiles == elems * 4 // 32768
+        assert tiles == elems * 4 // 65536  # 64 KiB stream tiles
         assert (tl[:tiles] == 1).all() and (tl[tiles:] == 0).all()
         worked = set(np.nonzero(cl)[0].tolist())
         assert worked <= set(cus)
