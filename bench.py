@@ -77,6 +77,28 @@ class Timer:
         return [a.elapsed_time(b) for t, a, b in self.pairs if tag is None or t == tag]
 
 
+class DevTimes:
+    """Kernel spans from the library's device time log: for each launch on
+    ``stream`` the ticks at which its first workgroup started and its last
+    workgroup finished, so no host launch overhead is included."""
+
+    def __init__(self, torch, ctx, stream, n):
+        self.torch, self.ctx, self.stream, self.n = torch, ctx, stream, n
+        self.slots = torch.zeros(2 * n, dtype=torch.int64, device="cuda:0")
+        torch.cuda.synchronize()
+        ctx.set_timelog(stream, self.slots)
+
+    def close_us(self, count=None):
+        """Switch the log off and return the spans (microseconds) of the
+        first ``count`` launches logged (at most n)."""
+        import numpy as np
+        self.torch.cuda.synchronize()
+        self.ctx.set_timelog(self.stream, None)
+        t = self.slots.cpu().numpy().reshape(-1, 2).astype(np.int64)
+        t = t[: self.n if count is None else min(count, self.n)]
+        return (t[:, 1] - t[:, 0]) * 1e3 / self.ctx.wallclock_khz
+
+
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "triad_3x1GiB_64KiB.pmc.md")
 
 
@@ -411,31 +433,39 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
                     for i in range(20):
                         sg.colored_gemv(ctx, W[i % copies], sg.BF16, M, K, x, sg.BF16, B, y,
                                         shift, stream)
+                    dev = DevTimes(torch, ctx, stream, launches)
                     for i in range(launches):
                         e0 = timer.start()
                         sg.colored_gemv(ctx, W[i % copies], sg.BF16, M, K, x, sg.BF16, B, y,
                                         shift, stream)
                         timer.stop(e0, tag)
+                    spans = dev.close_us()
                     sg.set_cu_mask(ctx, stream, None)
                     torch.cuda.synchronize()
                 d = timer.durations_ms(tag)
                 flag = ctx.device_error()
                 nbytes = M * K * 2 + B * K * 2 + B * M * 4
-                med, p99 = pctl(d, 50), pctl(d, 99)
-                gbs = nbytes / (med * 1e-3) / 1e9
+                med, p99 = pctl(list(spans), 50), pctl(list(spans), 99)
+                gbs = nbytes / (med * 1e-6) / 1e9
                 out.append({"M": M, "K": K, "batch": B, "cus": ncu, "device_flags": flag,
                             "path": "mfma" if B >= 5 else "valu",
-                            "p50_us": round(med * 1e3, 2), "p99_us": round(p99 * 1e3, 2),
+                            "p50_us": round(med, 2), "p99_us": round(p99, 2),
                             "GBps": round(gbs, 1),
                             "pct_of_colour_scaled_peak": round(100 * gbs / (0.75 * HBM_PEAK_GBS), 1),
-                            "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1)})
-                log(f"gemv {M}x{K} B={B} cus={ncu}: p50 {med * 1e3:.1f} us p99 {p99 * 1e3:.1f} us "
-                    f"{gbs:.0f} GB/s")
+                            "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1),
+                            "launch_p50_us": round(pctl(d, 50) * 1e3, 2),
+                            "launch_p99_us": round(pctl(d, 99) * 1e3, 2)})
+                log(f"gemv {M}x{K} B={B} cus={ncu}: kernel p50 {med:.1f} us p99 {p99:.1f} us "
+                    f"{gbs:.0f} GB/s; with launch p50 {pctl(d, 50) * 1e3:.1f} us")
         del raw, W
         torch.cuda.empty_cache()
     return {"what": "bf16 W on 48/64 colours in 2 MiB pages, bf16 x, fp32 y; "
                     f"{copies} rotated weight copies; {launches} launches per point",
-            "bytes": "M*K*2 + B*K*2 + B*M*4", "points": out}
+            "bytes": "M*K*2 + B*K*2 + B*M*4",
+            "timing": "p50/p99_us and GBps: kernel spans from the device time log (first "
+                      "workgroup start to last workgroup end); launch_p50/p99_us: host events "
+                      "around each call, including launch overhead",
+            "points": out}
 
 
 def bench_corun(torch, sg, synth, ctx, ls_launches):
@@ -501,9 +531,10 @@ def bench_corun(torch, sg, synth, ctx, ls_launches):
     s_ls = torch.cuda.Stream(device=0)
     s_be = torch.cuda.Stream(device=0)
 
-    # The long-running BE triad leaves one workgroup slot per CU free, so that
-    # the LS kernels' workgroups that the hardware sends to BE's XCDs can be
-    # placed (and leave) without waiting for a BE kernel to end.
+    # The long-running BE triad must leave workgroup slots free on its CUs,
+    # so that the LS kernels' workgroups that the hardware sends to BE's XCDs
+    # can be placed (and leave) without waiting for a BE kernel to end.  The
+    # triad already runs one workgroup per CU; the cap states the bound.
     be_cap = 3
 
     def run(Ws, Ts, ls_mask, be_mask, with_be):
@@ -527,6 +558,8 @@ def bench_corun(torch, sg, synth, ctx, ls_launches):
                 t_be.stop(e0)
                 pending.append(t_be.pairs[-1][2])
 
+        dev_ls = DevTimes(torch, ctx, s_ls, ls_launches)
+        dev_be = DevTimes(torch, ctx, s_be, 4096) if with_be else None
         if with_be:
             top_up()
         for i in range(ls_launches):
@@ -542,20 +575,26 @@ def bench_corun(torch, sg, synth, ctx, ls_launches):
                 time.sleep(0.0002)
         torch.cuda.synchronize()
         out = {}
-        d = np.array(t_ls.durations_ms()) * 1e3
+        d = dev_ls.close_us()
         out["ls_p50_us"] = round(float(np.percentile(d, 50)), 2)
         out["ls_p99_us"] = round(float(np.percentile(d, 99)), 2)
+        hd = np.array(t_ls.durations_ms()) * 1e3
+        out["ls_launch_p50_us"] = round(float(np.percentile(hd, 50)), 2)
+        out["ls_launch_p99_us"] = round(float(np.percentile(hd, 99)), 2)
         if with_be:
-            bd = np.array(t_be.durations_ms())
-            out["be_GBps"] = round(12 * n / (float(np.median(bd)) * 1e-3) / 1e9, 1)
-            out["be_launches"] = len(bd)
+            nb = len(t_be.pairs)
+            bd = dev_be.close_us(nb)
+            out["be_GBps"] = round(12 * n / (float(np.median(bd)) * 1e-6) / 1e9, 1)
+            out["be_launches"] = nb
         sg.set_cu_mask(ctx, s_ls, None)
         sg.set_cu_mask(ctx, s_be, None)
         sg.set_stream_occupancy(ctx, s_be, 0)
         return out
 
     res = {"what": "LS bf16 GEMV 4096x11008 batch 1 (closed loop) + BE fp32 triad 3x2 GiB",
-           "ls_launches": ls_launches, "be_workgroups_per_cu_cap": be_cap}
+           "ls_launches": ls_launches, "be_workgroups_per_cu_cap": be_cap,
+           "timing": "ls_p50/p99_us and be_GBps from the device time log (kernel spans); "
+                     "ls_launch_p50/p99_us from host events around each LS call"}
     res["isolated_ls_coloured_masked"] = run(W_col, T_col, ls_cus, be_cus, with_be=False)
     res["corun_coloured_masked"] = run(W_col, T_col, ls_cus, be_cus, with_be=True)
     res["corun_uncoloured_masked"] = run(W_plain, T_plain, ls_cus, be_cus, with_be=True)

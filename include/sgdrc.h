@@ -125,6 +125,20 @@ int sgdrc_set_worklog(sgdrc_ctx *ctx, uint32_t *d_cu_tiles, uint32_t *d_tile_vis
  * context (0 if none); lets a caller size and read the work log. */
 int sgdrc_last_tiles(sgdrc_ctx *ctx, void *stream, uint64_t *tiles);
 
+/* Optional per-launch device time log, for measuring kernel latency without
+ * host launch overhead.  Launch i on ``stream`` (counted from this call) of
+ * colour_classify, bimodal_relayout, colored_stream or colored_gemv writes
+ * two uint64 ticks of the device wall clock to d_slots[2*(i % n_slots)]:
+ * the time workgroup 0 (the first one dispatched) started and the time the
+ * last workgroup finished.  d_slots: device memory, 2 * n_slots entries,
+ * 8-byte aligned, owned by the caller.  d_slots == NULL switches the log
+ * off.  Host-only.  EINVAL: n_slots == 0 with d_slots != NULL, misaligned
+ * slots. */
+int sgdrc_set_timelog(sgdrc_ctx *ctx, void *stream, uint64_t *d_slots, uint32_t n_slots);
+
+/* Rate of the device wall clock used by the time log, in kHz. */
+int sgdrc_wallclock_khz(const sgdrc_ctx *ctx, uint32_t *khz);
+
 /* ------------------------------------------------------------- operations */
 
 /* Cap on the workgroups that later launches on ``stream`` place on each CU

@@ -71,6 +71,8 @@ def lib() -> ctypes.CDLL:
             "sgdrc_device_error": ([vp, P(u32)], i32),
             "sgdrc_set_worklog": ([vp, vp, vp, u64], i32),
             "sgdrc_last_tiles": ([vp, vp, P(u64)], i32),
+            "sgdrc_set_timelog": ([vp, vp, vp, u32], i32),
+            "sgdrc_wallclock_khz": ([vp, P(u32)], i32),
             "set_cu_mask": ([vp, vp, P(CuMask)], i32),
             "sgdrc_set_stream_occupancy": ([vp, vp, u32], i32),
             "colour_classify": ([vp, P(Hash), vp, u64, vp, vp, vp], i32),
@@ -181,6 +183,21 @@ class Context:
         t = ctypes.c_uint64()
         _check(lib().sgdrc_last_tiles(self.handle, _stream(stream), ctypes.byref(t)))
         return t.value
+
+    def set_timelog(self, stream=None, slots=None) -> None:
+        """Log {start, end} device-clock ticks of each later launch on
+        ``stream`` into ``slots`` (int64 device tensor of 2 * n entries,
+        used cyclically); None switches the log off."""
+        n = 0 if slots is None else int(slots.numel()) // 2
+        if slots is not None and n == 0:
+            raise ValueError("slots must hold at least one {start, end} pair")
+        _check(lib().sgdrc_set_timelog(self.handle, _stream(stream), _addr(slots), n))
+
+    @property
+    def wallclock_khz(self) -> int:
+        k = ctypes.c_uint32()
+        _check(lib().sgdrc_wallclock_khz(self.handle, ctypes.byref(k)))
+        return k.value
 
     def close(self) -> None:
         if self.handle is not None and self.handle.value:

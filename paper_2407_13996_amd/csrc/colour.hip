@@ -1,15 +1,22 @@
 // Batched XOR-hash colouring and the ordered page-table build.
 //
 // Colour bit k of an address is the parity of (address & M_k).  The
-// classify kernel streams 8-byte addresses with 16-byte non-temporal loads,
-// each wavefront instruction reading 1 KiB of consecutive addresses, and
-// writes one colour byte per address: every wavefront passes its 1024
-// colour bytes of a step through its own 1 KiB of LDS so that each lane
-// stores 16 consecutive colours with one 16-byte store.  The page-table build is an ordered stream compaction
-// over the pool's page addresses: a counting pass, a scan of per-workgroup
-// counts, and an emitting pass that places each qualifying page with a
-// wavefront ballot and a masked bit count, so the table comes out in
-// ascending page order regardless of scheduling.
+// classify kernel streams 8-byte addresses through buffer loads, each
+// wavefront instruction reading 1 KiB of consecutive addresses and each
+// lane keeping 32 such loads (64 addresses) in flight per tile, and writes
+// one colour byte per address: every wavefront passes its 4096 colour bytes
+// of a tile through its own 4 KiB of LDS so that each lane stores 16
+// consecutive colours per 16-byte store.  Tiles cover the largest multiple
+// of 16 addresses, through buffer ranges that end there (so the tile body
+// has no branch around its memory accesses); the last n mod 16 addresses
+// are coloured by the grid's last workgroup.
+//
+// The page-table build is an ordered stream compaction over the pool's page
+// addresses: a counting pass, a scan of per-workgroup counts, and an
+// emitting pass that places each qualifying page with a wavefront ballot
+// and a masked bit count, so the table comes out in ascending page order
+// regardless of scheduling.
+#include <algorithm>
 #include <cstring>
 #include <mutex>
 
@@ -39,10 +46,13 @@ __device__ __forceinline__ uint32_t colour_of(uint32_t lo, uint32_t hi, const Ha
 }
 
 constexpr int kClsThreads = 256;
-constexpr int kClsLoads = 8;                        // 16-byte loads per lane per step
-constexpr uint32_t kClsWaveStep = 64u * 2u * kClsLoads;  // 1024 addresses per wavefront step
-constexpr int kClsSteps = 4;
-constexpr uint64_t kClsTile = (uint64_t)kClsThreads / 64u * kClsWaveStep * kClsSteps;  // 16384
+constexpr int kClsLoads = 32;                            // 16-byte loads per lane per tile
+constexpr uint32_t kClsWaveTile = 64u * 2u * kClsLoads;  // 4096 addresses per wavefront
+constexpr uint64_t kClsTile = (uint64_t)kClsThreads / 64u * kClsWaveTile;  // 16384
+// Workgroups per CU: one deep workgroup streams fastest; with the histogram
+// a second one overlaps its LDS atomics with the first one's loads.
+constexpr int kClsWgsPerCu = 1;
+constexpr int kClsHistWgsPerCu = 2;
 
 // Histogram bins are replicated 16 times in LDS (copy = lane % 16) so that
 // the LDS atomics of one wavefront rarely meet on one address.
@@ -57,60 +67,52 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
 {
     constexpr uint32_t kBins = 1u << K;
     __shared__ uint32_t s_hist[HIST ? kBins * kHistCopies : 1];
-    // per wavefront: the colour bytes of one step, 2 per lane and load
-    __shared__ __attribute__((aligned(16))) uint16_t s_col[kClsThreads / 64][kClsWaveStep / 2];
-    const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
+    // per wavefront: the colour bytes of one tile, 2 per lane and load
+    __shared__ __attribute__((aligned(16))) uint16_t s_col[kClsThreads / 64][kClsWaveTile / 2];
+    const uint32_t lane = threadIdx.x & 63u;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const uint32_t copy = lane % kHistCopies;
+    const uint64_t n16 = n & ~15ull;
     if (HIST) {
         for (uint32_t i = threadIdx.x; i < kBins * kHistCopies; i += kClsThreads)
             s_hist[i] = 0;
         __syncthreads();
     }
     auto body = [&](uint32_t t, uint32_t, uint32_t &, auto &&claim) {
-        const uint64_t tile0 = (uint64_t)t * kClsTile;
-#pragma unroll 1
-        for (int s = 0; s < kClsSteps; ++s) {
-            const bool last = s == kClsSteps - 1;
-            // first address of this wavefront's step (wave-uniform)
-            const uint64_t base = tile0 + ((uint64_t)s * (kClsThreads / 64) + wave) * kClsWaveStep;
-            if (base + kClsWaveStep <= n) {
-                u32x4 v[kClsLoads];
+        // first address of this wavefront's part of the tile, and how many
+        // of its addresses lie below n16 (a multiple of 16, possibly 0)
+        const uint64_t base = (uint64_t)t * kClsTile + (uint64_t)wave * kClsWaveTile;
+        const uint32_t valid =
+            n16 > base ? (uint32_t)(n16 - base < kClsWaveTile ? n16 - base : kClsWaveTile) : 0u;
+        const Rsrc ra = make_rsrc(addrs + base, valid * 8u);
+        u32x4 v[kClsLoads];
 #pragma unroll
-                for (int j = 0; j < kClsLoads; ++j)
-                    v[j] = load_nt(addrs + base + 2u * (j * 64u + lane));
-                if (last)
-                    claim();
+        for (int j = 0; j < kClsLoads; ++j)
+            v[j] = buf_load_nt(ra, (j * 64u + lane) * 16u);
+        claim();
 #pragma unroll
-                for (int j = 0; j < kClsLoads; ++j) {
-                    const uint32_t c0 = colour_of<K>(v[j].x, v[j].y, h);
-                    const uint32_t c1 = colour_of<K>(v[j].z, v[j].w, h);
-                    s_col[wave][j * 64u + lane] = (uint16_t)(c0 | (c1 << 8));
-                    if (HIST) {
-                        atomicAdd(&s_hist[c0 * kHistCopies + copy], 1u);
-                        atomicAdd(&s_hist[c1 * kHistCopies + copy], 1u);
-                    }
-                }
-                // LDS accesses of one wavefront complete in order; this
-                // only keeps the compiler from moving the read up
-                __builtin_amdgcn_wave_barrier();
-                const u32x4 out = *reinterpret_cast<const u32x4 *>(&s_col[wave][lane * 8u]);
-                __builtin_amdgcn_wave_barrier();
-                store_nt(colours + base + 16u * lane, out);
-            } else {
-                if (last)
-                    claim();
-                for (uint32_t r = 0; r < kClsWaveStep / 64u; ++r) {
-                    const uint64_t i = base + r * 64u + lane;
-                    if (i < n) {
-                        const uint64_t a = addrs[i];
-                        const uint32_t c = colour_of<K>((uint32_t)a, (uint32_t)(a >> 32), h);
-                        colours[i] = (uint8_t)c;
-                        if (HIST)
-                            atomicAdd(&s_hist[c * kHistCopies + copy], 1u);
-                    }
-                }
+        for (int j = 0; j < kClsLoads; ++j) {
+            const uint32_t c0 = colour_of<K>(v[j].x, v[j].y, h);
+            const uint32_t c1 = colour_of<K>(v[j].z, v[j].w, h);
+            s_col[wave][j * 64u + lane] = (uint16_t)(c0 | (c1 << 8));
+            // both addresses of the load are valid or neither (valid is even)
+            if (HIST && 2u * (j * 64u + lane) < valid) {
+                atomicAdd(&s_hist[c0 * kHistCopies + copy], 1u);
+                atomicAdd(&s_hist[c1 * kHistCopies + copy], 1u);
             }
         }
+        // LDS accesses of one wavefront complete in order; the wave
+        // barriers only keep the compiler from moving these accesses
+        __builtin_amdgcn_wave_barrier();
+        u32x4 out[kClsLoads / 8];
+#pragma unroll
+        for (int q = 0; q < kClsLoads / 8; ++q)
+            out[q] = *reinterpret_cast<const u32x4 *>(&s_col[wave][q * 512u + lane * 8u]);
+        __builtin_amdgcn_wave_barrier();
+        const Rsrc rc = make_rsrc(colours + base, valid);
+#pragma unroll
+        for (int q = 0; q < kClsLoads / 8; ++q)
+            buf_store_nt(rc, q * 1024u + lane * 16u, out[q]);
     };
     auto flush = [&]() {
         if (HIST) {
@@ -128,8 +130,21 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
             }
         }
     };
+    // runs in the last workgroup with every other workgroup's histogram in
+    // hist_acc: colour the last n mod 16 addresses, then publish the counts
     auto epilogue = [&]() {
+        const uint64_t i = n16 + threadIdx.x;
+        if (i < n) {
+            const uint64_t a = addrs[i];
+            const uint32_t c = colour_of<K>((uint32_t)a, (uint32_t)(a >> 32), h);
+            colours[i] = (uint8_t)c;
+            if (HIST)
+                __hip_atomic_fetch_add(&hist_acc[c], (uint64_t)1, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+        }
         if (HIST) {
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
             for (uint32_t b = threadIdx.x; b < kBins; b += kClsThreads) {
                 const uint64_t v = __hip_atomic_load(&hist_acc[b], __ATOMIC_RELAXED,
                                                      __HIP_MEMORY_SCOPE_AGENT);
@@ -241,7 +256,7 @@ template <int K>
 static int launch_classify(Ctx *c, const HashArgs &h, const uint64_t *d_addrs, uint64_t n,
                            uint8_t *d_colours, uint64_t *d_hist, void *stream)
 {
-    const uint64_t n_tiles = (n + kClsTile - 1) / kClsTile;
+    const uint64_t n_tiles = ((n & ~15ull) + kClsTile - 1) / kClsTile;
     if (n_tiles >= (1ull << 31))
         return set_error(SGDRC_EINVAL, "n too large");
     Gate g;
@@ -253,12 +268,12 @@ static int launch_classify(Ctx *c, const HashArgs &h, const uint64_t *d_addrs, u
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (d_hist) {
         static const int occ = occupancy(k_classify<K, true>, kClsThreads);
-        uint32_t grid = gated_grid(c, occ, n_tiles, li);
+        uint32_t grid = gated_grid(c, std::min(occ, kClsHistWgsPerCu), n_tiles, li);
         hipLaunchKernelGGL((k_classify<K, true>), dim3(grid), dim3(kClsThreads), 0, s, d_addrs, n,
                            d_colours, h, acc, d_hist, (uint32_t)n_tiles, g);
     } else {
         static const int occ = occupancy(k_classify<K, false>, kClsThreads);
-        uint32_t grid = gated_grid(c, occ, n_tiles, li);
+        uint32_t grid = gated_grid(c, std::min(occ, kClsWgsPerCu), n_tiles, li);
         hipLaunchKernelGGL((k_classify<K, false>), dim3(grid), dim3(kClsThreads), 0, s, d_addrs,
                            n, d_colours, h, acc, d_hist, (uint32_t)n_tiles, g);
     }

@@ -84,6 +84,11 @@ int make_gate(Ctx *c, void *stream, uint64_t n_tiles, int group_cus, Gate *g, La
     g->log_cu = c->log_cu;
     g->log_tile = c->log_tile;
     g->log_cap = c->log_cap;
+    g->tlog = nullptr;
+    if (st->tlog) {
+        g->tlog = st->tlog + 2u * (st->tlog_next % st->tlog_slots);
+        ++st->tlog_next;
+    }
     // queue groups: runs of group_cus CUs inside each XCD, or one group
     uint32_t shift = 0;
     while ((1 << (shift + 1)) <= group_cus && shift < 5)
@@ -294,6 +299,11 @@ int sgdrc_init(int device, sgdrc_ctx **out)
     if (!c)
         return set_error(SGDRC_EHIP, "out of host memory");
     c->device = device;
+    {
+        int khz = 0;
+        SGDRC_HIP(hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, device));
+        c->wallclock_khz = khz > 0 ? (uint32_t)khz : 0u;
+    }
     int rc = SGDRC_OK;
     hipError_t e = hipSuccess;
 #define TRY(call)                                   \
@@ -403,6 +413,41 @@ int sgdrc_last_tiles(sgdrc_ctx *ctx, void *stream, uint64_t *tiles)
     std::lock_guard<std::mutex> lock(c->mu);
     auto it = c->streams.find(stream);
     *tiles = it == c->streams.end() ? 0 : it->second.last_tiles;
+    return SGDRC_OK;
+}
+
+int sgdrc_set_timelog(sgdrc_ctx *ctx, void *stream, uint64_t *d_slots, uint32_t n_slots)
+{
+    clear_error();
+    if (d_slots && n_slots == 0)
+        return set_error(SGDRC_EINVAL, "n_slots is 0");
+    if (reinterpret_cast<uintptr_t>(d_slots) & 7u)
+        return set_error(SGDRC_EINVAL, "time-log slots not 8-byte aligned");
+    Ctx *c = nullptr;
+    int rc = check_ctx(ctx, &c);
+    if (rc)
+        return rc;
+    StreamState *st = nullptr;
+    rc = stream_state(c, stream, &st);
+    if (rc)
+        return rc;
+    std::lock_guard<std::mutex> lock(c->mu);
+    st->tlog = d_slots;
+    st->tlog_slots = d_slots ? n_slots : 0;
+    st->tlog_next = 0;
+    return SGDRC_OK;
+}
+
+int sgdrc_wallclock_khz(const sgdrc_ctx *ctx, uint32_t *khz)
+{
+    clear_error();
+    if (!khz)
+        return set_error(SGDRC_EINVAL, "khz is NULL");
+    Ctx *c = nullptr;
+    int rc = check_ctx(const_cast<sgdrc_ctx *>(ctx), &c);
+    if (rc)
+        return rc;
+    *khz = c->wallclock_khz;
     return SGDRC_OK;
 }
 

@@ -55,6 +55,7 @@ struct Gate {
     uint32_t *log_cu;            // optional: tiles per logical CU
     uint32_t *log_tile;          // optional: visits per tile
     uint64_t log_cap;            // entries of log_tile
+    uint64_t *tlog;              // optional: {start, end} wall-clock ticks of this launch
     uint32_t grp_tile[kMaxGroups + 1];  // first tile of each group's range
     uint8_t grp_base[kMaxXcds];  // first queue group of each XCD
     uint32_t n_groups;
@@ -207,6 +208,11 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
     __shared__ uint32_t s_flag;
     __shared__ uint32_t s_left_lo[kMaxGroups], s_left_hi[kMaxGroups];
     __shared__ uint32_t s_grp_tile[kMaxGroups + 1];
+    // time log: workgroup 0, the first one the hardware dispatches, stamps
+    // the start; the last workgroup to finish stamps the end
+    if (g.tlog && blockIdx.x == 0 && threadIdx.x == 0)
+        __hip_atomic_store(&g.tlog[0], __builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
     for (uint32_t i = threadIdx.x; i <= (uint32_t)kMaxGroups; i += blockDim.x)
         s_grp_tile[i] = g.grp_tile[i];
     __syncthreads();
@@ -327,6 +333,11 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
         __syncthreads();
         epilogue();
         reset_slot(g.q);
+        if (g.tlog && threadIdx.x == 0) {
+            __builtin_amdgcn_s_waitcnt(0);
+            __hip_atomic_store(&g.tlog[1], __builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
     }
     if (err != 0u)
         raise_flag(g.err, err);

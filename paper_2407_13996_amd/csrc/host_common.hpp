@@ -31,6 +31,9 @@ struct StreamState {
     sgdrc_cu_mask mask{};
     uint32_t wg_cap = 0;        // workgroups per CU at most (0 = as many as fit)
     uint64_t last_tiles = 0;
+    uint64_t *tlog = nullptr;   // time-log slots ({start, end} pairs) or NULL
+    uint32_t tlog_slots = 0;
+    uint64_t tlog_next = 0;     // launches logged since the log was set
 };
 
 // What a gated launch needs besides the Gate itself.
@@ -43,6 +46,7 @@ struct Ctx {
     uint32_t magic = kCtxMagic;
     int device = -1;
     int num_cus = 0;
+    uint32_t wallclock_khz = 0;          // rate of the counter read by s_memrealtime
     uint32_t keys[SGDRC_MAX_CUS] = {};   // logical CU -> hardware key
     sgdrc_cu_mask all_cus{};
     int n_xcds = 0;

@@ -134,6 +134,13 @@ def test_context_calls_reject_null(L):
     f = ctypes.c_uint32()
     assert L.sgdrc_device_error(NULL, ctypes.byref(f)) == sg.ENODEV
     assert L.sgdrc_init(0, None) == sg.EINVAL
+    assert L.sgdrc_set_timelog(NULL, None, 256, 0) == sg.EINVAL        # slots but n_slots 0
+    assert L.sgdrc_set_timelog(NULL, None, 260, 4) == sg.EINVAL        # misaligned slots
+    assert L.sgdrc_set_timelog(NULL, None, 256, 4) == sg.ENODEV
+    assert L.sgdrc_set_timelog(NULL, None, None, 0) == sg.ENODEV       # off, but no context
+    k = ctypes.c_uint32()
+    assert L.sgdrc_wallclock_khz(NULL, None) == sg.EINVAL
+    assert L.sgdrc_wallclock_khz(NULL, ctypes.byref(k)) == sg.ENODEV
 
 
 def test_binding_raises_with_message():

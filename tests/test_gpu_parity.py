@@ -90,7 +90,8 @@ def test_topology(ctx):
 # ---------------------------------------------------------------- classify
 
 @pytest.mark.parametrize("n,K,hist", [(65536, 4, True), (65536 + 13, 6, True), (5, 8, True),
-                                      (100003, 3, False), (0, 4, True)])
+                                      (100003, 3, False), (0, 4, True), (16, 6, True),
+                                      (3 * 8192 + 2048 + 31, 6, True), (8192 * 40 + 15, 1, True)])
 def test_classify_matches_oracle(ctx, orc, n, K, hist):
     say(f"classify n={n} K={K} hist={hist}")
     masks = synth.xor_masks(K, seed=1, min_bit=12)
@@ -335,6 +336,45 @@ def test_gemv_bitwise_identical_across_cu_masks(ctx, orc):
         same = [y for b, y in ys if b == B]
         for y in same[1:]:
             assert (y.view(np.uint32) == same[0].view(np.uint32)).all()
+
+
+# ------------------------------------------------------------- time log
+
+def test_timelog_brackets_each_launch(ctx):
+    """Each gated launch stamps {start, end} device-clock ticks into its slot
+    (slots used cyclically); the span is positive and no longer than the
+    host-event time around the same launch."""
+    import torch
+    shift, elems = 16, 64 * 16384
+    pages = elems * 4 >> shift
+    pt = torch.arange(pages, dtype=torch.int32, device=DEV)
+    b = to_dev(synth.uniform_f32(elems, seed=1))
+    c = to_dev(synth.uniform_f32(elems, seed=2))
+    a = torch.zeros_like(b)
+    stream = torch.cuda.current_stream()
+    slots = torch.zeros(2 * 3, dtype=torch.int64, device=DEV)
+    khz = ctx.wallclock_khz
+    assert khz > 0
+    ctx.set_timelog(stream, slots)
+    spans = []
+    for i in range(5):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        sg.colored_stream(ctx, sg.paged(a, pt, pages), sg.paged(b, pt, pages),
+                          sg.paged(c, pt, pages), 2.0, elems, shift, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t = to_host(slots).astype(np.int64).reshape(3, 2)[i % 3]
+        span_ms = (int(t[1]) - int(t[0])) / khz
+        spans.append(span_ms)
+        assert 0 < span_ms <= e0.elapsed_time(e1) + 0.05, (span_ms, e0.elapsed_time(e1))
+    ctx.set_timelog(stream, None)
+    before = to_host(slots).copy()
+    sg.colored_stream(ctx, sg.paged(a, pt, pages), sg.paged(b, pt, pages),
+                      sg.paged(c, pt, pages), 2.0, elems, shift, stream)
+    torch.cuda.synchronize()
+    assert (to_host(slots) == before).all()
+    say(f"  time-log spans (ms): {[round(x, 4) for x in spans]}")
 
 
 # ------------------------------------------------------- CU gate and queue
