@@ -256,6 +256,121 @@ def test_triad_in_place_alias(ctx, orc):
     assert (to_host(d_b).view(np.uint32) == ref.view(np.uint32)).all()
 
 
+# ----------------------------------------------- full-size configurations
+
+def aligned_pool(n_pages, shift):
+    """A device byte pool of n_pages pages whose base is page aligned."""
+    P = 1 << shift
+    raw = torch.empty(n_pages * P + P, dtype=torch.uint8, device=DEV)
+    off = (-raw.data_ptr()) % P
+    return raw, raw.data_ptr() + off, off
+
+
+def test_classify_full_size_config5(ctx, orc):
+    """2^26 random 4 KiB-aligned addresses, 6 masks: every colour and the
+    histogram equal the oracle's."""
+    n = 1 << 26
+    masks = synth.xor_masks(6, seed=1, min_bit=12)
+    addrs = synth.page_addresses(n, seed=0)
+    d_col = torch.full((n + 16,), 0xEE, dtype=torch.uint8, device=DEV)
+    d_hist = torch.zeros(64, dtype=torch.int64, device=DEV)
+    say("classify 2^26 addresses")
+    sg.colour_classify(ctx, masks, to_dev(addrs), d_col, d_hist)
+    ref, ref_hist = orc.classify(addrs, masks)
+    got = to_host(d_col)
+    assert (got[:n] == ref).all() and (got[n:] == 0xEE).all()
+    assert (to_host(d_hist).astype(np.uint64) == ref_hist).all()
+
+
+@pytest.mark.parametrize("elems,colours,cus", [
+    (1 << 28, range(8), None),               # C2 at the smallest colour set, all CUs
+    (1 << 29, range(48, 64), range(192, 256)),  # C4's BE stream: 2 GiB arrays, 64 CUs
+])
+def test_triad_full_size_sampled(ctx, orc, elems, colours, cus):
+    """Full-size triad through GPU-built page tables (compared with the
+    oracle's in full); 2^18 sampled elements of a against the oracle's fmaf."""
+    shift, P = 16, 1 << 16
+    epp = P // 4
+    pages = elems // epp
+    masks = synth.xor_masks(6, seed=1, min_bit=shift)
+    colours = list(colours)
+    pool_pages = int(3 * pages * 64 / len(colours) * 1.04) + 64
+    raw, base, off = aligned_pool(pool_pages, shift)
+    say(f"triad {elems} elements, {len(colours)}/64 colours, pool {pool_pages} pages")
+    d_pt = torch.empty(3 * pages, dtype=torch.int32, device=DEV)
+    sg.colour_alloc_pagetable(ctx, masks, base, shift, pool_pages, colours, 3 * pages, d_pt)
+    ref_pt, found = orc.pagetable(masks, base, shift, pool_pages, synth.colour_set_bits(colours),
+                                  3 * pages)
+    assert found >= 3 * pages
+    assert (to_host(d_pt).view(np.uint32) == ref_pt).all()
+    pts = [d_pt[i * pages:(i + 1) * pages] for i in range(3)]
+    arr = [sg.paged(base, pts[i], pool_pages) for i in range(3)]
+    b = synth.uniform_f32(elems, seed=2)
+    c = synth.uniform_f32(elems, seed=3)
+    ident = torch.arange(pages, dtype=torch.int32, device=DEV)
+    d_b, d_c = to_dev(b), to_dev(c)
+    sg.bimodal_relayout(ctx, arr[1], sg.paged(d_b, ident, pages), elems * 4, shift)
+    sg.bimodal_relayout(ctx, arr[2], sg.paged(d_c, ident, pages), elems * 4, shift)
+    del d_b, d_c
+    stream = torch.cuda.current_stream()
+    if cus is not None:
+        sg.set_cu_mask(ctx, stream, cus)
+    try:
+        sg.colored_stream(ctx, arr[0], arr[1], arr[2], 3.0, elems, shift, stream)
+    finally:
+        sg.set_cu_mask(ctx, stream, None)
+    rng = np.random.default_rng(11)
+    idx = np.sort(rng.choice(elems, size=1 << 18, replace=False)).astype(np.int64)
+    pa = ref_pt[:pages].astype(np.int64)
+    where = off // 4 + pa[idx // epp] * epp + idx % epp       # float index into raw
+    got = to_host(raw.view(torch.float32)[torch.from_numpy(where).to(DEV)])
+    k = idx.size
+    kp = -(-k // epp)
+    bs = np.zeros(kp * epp, np.float32); bs[:k] = b[idx]
+    cs = np.zeros(kp * epp, np.float32); cs[:k] = c[idx]
+    ref = np.zeros(kp * epp, np.float32)
+    ident_h = np.arange(kp, dtype=np.uint32)
+    orc.triad(ref, ident_h, bs, ident_h, cs, ident_h, 3.0, k, shift)
+    assert (got.view(np.uint32) == ref[:k].view(np.uint32)).all()
+
+
+def test_relayout_full_size_config5(ctx, orc):
+    """4 GiB fp16 tensor (65,536 pages of 64 KiB) from the all-colour page set
+    to 16 of 64 colours and back: every restricted page holds its source page
+    at the oracle table's position, and the round trip is the identity."""
+    shift, P = 16, 1 << 16
+    pages = 65536
+    n_bytes = pages * P
+    masks = synth.xor_masks(6, seed=1, min_bit=shift)
+    colours = list(range(16))
+    pool_pages = int(pages * 4 * 1.04) + 64
+    raw, base, off = aligned_pool(pool_pages, shift)
+    ref_pt, found = orc.pagetable(masks, base, shift, pool_pages, synth.colour_set_bits(colours),
+                                  pages)
+    assert found >= pages
+    d_pt = to_dev(ref_pt)
+    g = torch.Generator(device=DEV)
+    g.manual_seed(5)
+    src = torch.randint(-32768, 32768, (n_bytes // 2,), generator=g, dtype=torch.int16, device=DEV)
+    ident = torch.arange(pages, dtype=torch.int32, device=DEV)
+    say("relayout 4 GiB all -> 16/64 -> all")
+    sg.bimodal_relayout(ctx, sg.paged(base, d_pt, pool_pages), sg.paged(src, ident, pages),
+                        n_bytes, shift)
+    pool_pages_view = raw[off:off + pool_pages * P].view(pool_pages, P)
+    rows = torch.from_numpy(ref_pt.astype(np.int64)).to(DEV)
+    same = 0
+    for j0 in range(0, pages, 8192):      # compare in 512 MiB slices
+        sel = rows[j0:j0 + 8192]
+        same += int((pool_pages_view.index_select(0, sel)
+                     == src.view(torch.uint8).view(pages, P)[j0:j0 + 8192]).all().item())
+    assert same == pages // 8192
+    back = torch.zeros_like(src)
+    sg.bimodal_relayout(ctx, sg.paged(back, ident, pages), sg.paged(base, d_pt, pool_pages),
+                        n_bytes, shift)
+    torch.cuda.synchronize()
+    assert bool(torch.equal(back, src))
+
+
 # -------------------------------------------------------------------- GEMV
 
 def w_bits(dt, n, seed):
