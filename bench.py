@@ -543,10 +543,11 @@ def bench_corun(torch, sg, synth, ctx, ls_launches):
     # triad already runs one workgroup per CU; the cap states the bound.
     be_cap = 3
 
-    def run(Ws, Ts, ls_mask, be_mask, with_be):
+    def run(Ws, Ts, ls_mask, be_mask, with_be, ls_cap=0):
         sg.set_cu_mask(ctx, s_ls, ls_mask)
         sg.set_cu_mask(ctx, s_be, be_mask)
         sg.set_stream_occupancy(ctx, s_be, be_cap)
+        sg.set_stream_occupancy(ctx, s_ls, ls_cap)
         t_ls = Timer(torch, s_ls)
         t_be = Timer(torch, s_be)
         for i in range(10):
@@ -595,6 +596,7 @@ def bench_corun(torch, sg, synth, ctx, ls_launches):
         sg.set_cu_mask(ctx, s_ls, None)
         sg.set_cu_mask(ctx, s_be, None)
         sg.set_stream_occupancy(ctx, s_be, 0)
+        sg.set_stream_occupancy(ctx, s_ls, 0)
         return out
 
     res = {"what": "LS bf16 GEMV 4096x11008 batch 1 (closed loop) + BE fp32 triad 3x2 GiB",
@@ -605,8 +607,10 @@ def bench_corun(torch, sg, synth, ctx, ls_launches):
     res["corun_coloured_masked"] = run(W_col, T_col, ls_cus, be_cus, with_be=True)
     res["corun_uncoloured_masked"] = run(W_plain, T_plain, ls_cus, be_cus, with_be=True)
     res["corun_uncoloured_unmasked"] = run(W_plain, T_plain, None, None, with_be=True)
+    res["corun_coloured_masked_ls_cap3"] = run(W_col, T_col, ls_cus, be_cus, with_be=True,
+                                               ls_cap=3)
     for k in ("isolated_ls_coloured_masked", "corun_coloured_masked", "corun_uncoloured_masked",
-              "corun_uncoloured_unmasked"):
+              "corun_uncoloured_unmasked", "corun_coloured_masked_ls_cap3"):
         log(f"corun {k}: {res[k]}")
     del w_raw, be_raw, lin, w_plain
     torch.cuda.empty_cache()

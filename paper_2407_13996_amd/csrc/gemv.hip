@@ -15,7 +15,7 @@
 //
 // Batches 5..8 with bf16 x bf16 or f16 x f16 operands use the gfx950
 // 16x16x32 MFMA: a 16-row block of W is the A operand, x (batch padded to 16
-// columns with zeros) the B operand.
+// columns with zeros) the B operand; eight wavefronts split K.
 #include "host_common.hpp"
 
 namespace sgdrc {
@@ -29,6 +29,11 @@ constexpr int kGemvWaves = kGemvThreads / 64;
 constexpr int kGemvRows = 4;     // rows per tile, vector-ALU path
 constexpr int kMfmaRows = 16;    // rows per tile, MFMA path
 constexpr int kMfmaNI = 4;       // MFMAs per wave step
+// MFMA path: 8 waves split K, so that a 16-row tile keeps twice the loads of
+// a 4-wave workgroup in flight (measured best of 4, 8 and 16 waves for both
+// 4096x11008 and 11008x4096 at batch 8)
+constexpr int kMfmaThreads = 512;
+constexpr int kMfmaWaves = kMfmaThreads / 64;
 constexpr int kPtCap = 256;      // page-table entries staged per tile (one per thread)
 
 template <int DT> struct Dt;
@@ -233,13 +238,13 @@ __device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c)
 // k order inside the instruction matches between the operands.  The
 // accumulator holds rows 4g..4g+3 of batch column l % 16.
 template <int DT>
-__global__ __launch_bounds__(kGemvThreads) void k_gemm_mfma(
+__global__ __launch_bounds__(kMfmaThreads) void k_gemm_mfma(
     const uint8_t *__restrict__ w_pool, const uint32_t *__restrict__ pt, uint64_t pool_pages,
     uint32_t M, uint32_t K, const uint8_t *__restrict__ x, uint32_t nb, float *__restrict__ y,
     uint32_t shift, uint32_t n_tiles, Gate g)
 {
     __shared__ uint32_t s_pt[kPtCap];
-    __shared__ f32x4 s_red[kGemvWaves][64];
+    __shared__ f32x4 s_red[kMfmaWaves][64];
     const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63u;
     const uint32_t rl = lane & 15u, grp = lane >> 4;
     const uint64_t row_bytes = (uint64_t)K * 2u;
@@ -255,11 +260,11 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemm_mfma(
         const bool row_ok = row < M;
         const bool col_ok = rl < nb;
         f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-        for (uint32_t j = 0; (j * kGemvWaves + wave) * kMfmaNI * 4u < KV; ++j) {
+        for (uint32_t j = 0; (j * kMfmaWaves + wave) * kMfmaNI * 4u < KV; ++j) {
             u32x4 av[kMfmaNI], bv[kMfmaNI];
 #pragma unroll
             for (int i = 0; i < kMfmaNI; ++i) {
-                const uint32_t kv = ((j * kGemvWaves + wave) * kMfmaNI + i) * 4u + grp;
+                const uint32_t kv = ((j * kMfmaWaves + wave) * kMfmaNI + i) * 4u + grp;
                 av[i] = u32x4{0u, 0u, 0u, 0u};
                 bv[i] = u32x4{0u, 0u, 0u, 0u};
                 if (kv < KV) {
@@ -283,7 +288,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemm_mfma(
         if (wave == 0) {
             f32x4 v = s_red[0][lane];
 #pragma unroll
-            for (int w = 1; w < kGemvWaves; ++w) {
+            for (int w = 1; w < kMfmaWaves; ++w) {
                 f32x4 o = s_red[w][lane];
                 v.x += o.x;
                 v.y += o.y;
@@ -327,7 +332,7 @@ static GemvKernel pick_valu_x(int x_dtype, uint32_t batch)
     }
 }
 
-static int kernel_occupancy(GemvKernel k)
+static int kernel_occupancy(GemvKernel k, int threads)
 {
     static std::mutex mu;
     static std::unordered_map<const void *, int> cache;
@@ -335,7 +340,7 @@ static int kernel_occupancy(GemvKernel k)
     auto it = cache.find((const void *)k);
     if (it != cache.end())
         return it->second;
-    int n = occupancy(k, kGemvThreads);
+    int n = occupancy(k, threads);
     cache[(const void *)k] = n;
     return n;
 }
@@ -405,8 +410,9 @@ int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, 
     rc = make_gate(c, stream, n_tiles, kGemvGroupCus, &g, &li);
     if (rc)
         return rc;
-    const uint32_t grid = gated_grid(c, kernel_occupancy(k), n_tiles, li);
-    hipLaunchKernelGGL(k, dim3(grid), dim3(kGemvThreads), 0, reinterpret_cast<hipStream_t>(stream),
+    const int threads = mfma ? kMfmaThreads : kGemvThreads;
+    const uint32_t grid = gated_grid(c, kernel_occupancy(k, threads), n_tiles, li);
+    hipLaunchKernelGGL(k, dim3(grid), dim3(threads), 0, reinterpret_cast<hipStream_t>(stream),
                        static_cast<const uint8_t *>(w->pool), w->pt, w->pool_pages, M, K,
                        static_cast<const uint8_t *>(d_x), batch, d_y, page_shift,
                        (uint32_t)n_tiles, g);

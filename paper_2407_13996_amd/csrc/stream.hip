@@ -8,21 +8,23 @@
 // non-temporal buffer loads and stores, each wavefront instruction covering
 // 1 KiB of consecutive bytes.
 //
-// Every access goes through a buffer resource whose base is a page address
-// and whose range is the number of bytes that may be touched there: zero
-// for a tile with an out-of-range page-table entry, the bytes left for the
-// last tile.  The hardware drops accesses outside the range, so the tile
-// body is the same straight-line code for full, ragged and skipped tiles.
-// That matters for speed as well as brevity: the next tile's ticket is
-// requested between the loads and the stores, and its result is waited for
-// only after the stores have been issued; a branch in the body would make
-// the compiler wait for the stores too on the way to the next tile.
+// The tile's page-table entries (one to sixteen pages) are staged in LDS.
+// Every 1 KiB wavefront chunk lies inside one page, and each gets its own
+// buffer resource: base = the chunk's address in its page, range = the
+// bytes the chunk may touch (zero for an out-of-range page-table entry,
+// fewer for the last tile).  The hardware drops accesses outside the range,
+// so the tile body is the same straight-line code for full, ragged and
+// skipped chunks.  That matters for speed as well as brevity: the next
+// tile's ticket is requested between the loads and the stores, and its
+// result is waited for only after the stores have been issued; a branch in
+// the body would make the compiler wait for the stores too on the way to
+// the next tile.  (One resource per chunk also measured faster than one
+// resource per tile and array with offsets up to 64 KiB: 6.5-6.7 against
+// 5.9-6.5 TB/s for the triad on 64 KiB pages.)
 //
 // Tiles cover the largest multiple of 16 bytes; the last n_bytes mod 16
 // bytes are moved by the last workgroup of the grid after all tiles are
 // done (it may sit on any CU).
-#include <algorithm>
-
 #include "host_common.hpp"
 
 namespace sgdrc {
@@ -41,10 +43,9 @@ struct Geo {
 // Chunks per lane and array (tile = 4 KiB x U) and workgroups per CU.
 // Few deep workgroups measured fastest on MI355X: one 256-thread workgroup
 // per CU (one wavefront per SIMD) with 16 loads of 16 bytes per lane and
-// array in flight moves 1 GiB arrays at about 6.4 TB/s, for the triad and
-// for the copy alike; a second workgroup per CU, or 8 loads per lane, costs
-// 5 to 20 percent.  Unrolls stay powers of two so that a page of at least a
-// tile holds whole tiles.
+// array in flight moves 1 GiB arrays at 6.4-6.7 TB/s, for the triad and for
+// the copy alike; a second workgroup per CU, or 8 loads per lane, costs 5
+// to 20 percent.
 constexpr int kTriadUnroll = 16;
 constexpr int kRelayoutUnroll = 16;
 constexpr int kStreamWgsPerCu = 1;
@@ -61,8 +62,8 @@ __device__ __forceinline__ uint32_t wave_id()
     return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 }
 
-// Resource for the chunk of a small-page tile at tile offset cs (one page):
-// pool page p (kBadPage: empty range).
+// Resource for the 1 KiB chunk at logical byte ``at`` (inside pool page p;
+// kBadPage gives an empty range).
 __device__ __forceinline__ Rsrc chunk_rsrc(const uint8_t *pool, uint32_t p, uint32_t shift,
                                            uint64_t pmask, uint64_t at, uint32_t valid)
 {
@@ -70,76 +71,74 @@ __device__ __forceinline__ Rsrc chunk_rsrc(const uint8_t *pool, uint32_t p, uint
     return make_rsrc(pool + (ok ? ((uint64_t)p << shift) + (at & pmask) : 0u), ok ? valid : 0u);
 }
 
-template <int U, bool BIG>
+// Stages the entries of the pages that tile [t0, t0 + tile) touches: entry
+// i of each table is for logical page (t0 >> shift) + i.  Pages at or beyond
+// n_pages, and entries out of range of their pool, become kBadPage (the
+// latter also set the error bit).  ALL3: a page is kept only if it is valid
+// in every table.
+template <int N, bool ALL3>
+__device__ __forceinline__ void stage_tile_pages(uint64_t t0, uint32_t tile, uint32_t shift,
+                                                 uint64_t n_pages, const uint32_t *const pts[N],
+                                                 const uint64_t pool_pages[N], uint32_t *const s[N],
+                                                 uint32_t &err)
+{
+    const uint64_t p0 = t0 >> shift;
+    const uint32_t np = (uint32_t)(((t0 + tile - 1u) >> shift) - p0 + 1u);
+    if (threadIdx.x < np) {
+        const uint64_t j = p0 + threadIdx.x;
+        uint32_t p[N];
+        bool ok = true;
+#pragma unroll
+        for (int a = 0; a < N; ++a) {
+            p[a] = j < n_pages ? checked_page(pts[a], j, pool_pages[a], err) : kBadPage;
+            ok = ok && p[a] != kBadPage;
+        }
+#pragma unroll
+        for (int a = 0; a < N; ++a)
+            s[a][threadIdx.x] = (ALL3 && !ok) ? kBadPage : p[a];
+    }
+    __syncthreads();
+}
+
+template <int U>
 __global__ __launch_bounds__(kStreamThreads) void k_relayout(
     uint8_t *__restrict__ dst, const uint32_t *__restrict__ pt_d, uint64_t dst_pages,
     const uint8_t *__restrict__ src, const uint32_t *__restrict__ pt_s, uint64_t src_pages,
     uint64_t n_bytes, uint32_t shift, uint32_t n_tiles, Gate g)
 {
+    constexpr uint32_t kTile = Geo<U>::kTile;
     __shared__ uint32_t s_pd[Geo<U>::kPagesMax], s_ps[Geo<U>::kPagesMax];
     const uint64_t pmask = (1ull << shift) - 1ull;
     const uint64_t n16 = n_bytes & ~15ull;
     const uint64_t n_pages = (n16 + pmask) >> shift;
-    const uint32_t lo = wave_id() * Geo<U>::kWaveSpan + (threadIdx.x & 63u) * 16u;
+    const uint32_t lane16 = (threadIdx.x & 63u) * 16u;
+    const uint32_t wbase = wave_id() * Geo<U>::kWaveSpan;
+    const uint32_t *const pts[2] = {pt_d, pt_s};
+    const uint64_t pools[2] = {dst_pages, src_pages};
+    uint32_t *const stg[2] = {s_pd, s_ps};
     auto body = [&](uint32_t t, uint32_t, uint32_t &err, auto &&claim) {
-        const uint64_t t0 = (uint64_t)t * Geo<U>::kTile;
+        const uint64_t t0 = (uint64_t)t * kTile;
+        const uint64_t p0 = t0 >> shift;
+        stage_tile_pages<2, true>(t0, kTile, shift, n_pages, pts, pools, stg, err);
         u32x4 v[U];
-        if (BIG) {
-            const uint64_t j = t0 >> shift;
-            const uint32_t pd = pt_d[j], ps = pt_s[j];
-            const bool bad = pd >= dst_pages || ps >= src_pages;
-            err |= bad ? kDevErrPtRange : 0u;
-            const uint32_t valid = bad ? 0u : span_valid(t0, n16, Geo<U>::kTile);
-            const uint64_t in = t0 & pmask;
-            const Rsrc rd = make_rsrc(dst + (bad ? 0u : ((uint64_t)pd << shift) + in), valid);
-            const Rsrc rs = make_rsrc(src + (bad ? 0u : ((uint64_t)ps << shift) + in), valid);
 #pragma unroll
-            for (int u = 0; u < U; ++u)
-                v[u] = buf_load_nt(rs, lo + u * kStepSpan);
-            claim();
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-                buf_store_nt(rd, lo + u * kStepSpan, v[u]);
-        } else {
-            // stage the tile's page-table entries; each wavefront
-            // instruction then covers 1 KiB inside one page
-            const uint32_t np = Geo<U>::kTile >> shift;
-            if (threadIdx.x < np) {
-                const uint64_t j = (t0 >> shift) + threadIdx.x;
-                uint32_t pd = kBadPage, ps = kBadPage;
-                if (j < n_pages) {
-                    pd = checked_page(pt_d, j, dst_pages, err);
-                    ps = checked_page(pt_s, j, src_pages, err);
-                }
-                s_pd[threadIdx.x] = pd;
-                s_ps[threadIdx.x] = ps;
-            }
-            __syncthreads();
-            const uint32_t lane16 = (threadIdx.x & 63u) * 16u;
-            const uint32_t wbase = wave_id() * Geo<U>::kWaveSpan;
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const uint32_t cs = wbase + u * kStepSpan;
-                const uint32_t jl = cs >> shift;
-                const uint32_t pd = __builtin_amdgcn_readfirstlane(s_pd[jl]);
-                const uint32_t ps = __builtin_amdgcn_readfirstlane(s_ps[jl]);
-                const uint32_t valid =
-                    pd == kBadPage ? 0u : span_valid(t0 + cs, n16, kStepSpan);
-                v[u] = buf_load_nt(chunk_rsrc(src, ps, shift, pmask, t0 + cs, valid), lane16);
-            }
-            claim();
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const uint32_t cs = wbase + u * kStepSpan;
-                const uint32_t jl = cs >> shift;
-                const uint32_t pd = __builtin_amdgcn_readfirstlane(s_pd[jl]);
-                const uint32_t ps = __builtin_amdgcn_readfirstlane(s_ps[jl]);
-                const uint32_t valid =
-                    ps == kBadPage ? 0u : span_valid(t0 + cs, n16, kStepSpan);
-                buf_store_nt(chunk_rsrc(dst, pd, shift, pmask, t0 + cs, valid), lane16, v[u]);
-            }
-            __syncthreads();
+        for (int u = 0; u < U; ++u) {
+            const uint64_t at = t0 + wbase + u * kStepSpan;
+            const uint32_t jl = (uint32_t)((at >> shift) - p0);
+            const uint32_t ps = __builtin_amdgcn_readfirstlane(s_ps[jl]);
+            v[u] = buf_load_nt(chunk_rsrc(src, ps, shift, pmask, at, span_valid(at, n16, kStepSpan)),
+                               lane16);
         }
+        claim();
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint64_t at = t0 + wbase + u * kStepSpan;
+            const uint32_t jl = (uint32_t)((at >> shift) - p0);
+            const uint32_t pd = __builtin_amdgcn_readfirstlane(s_pd[jl]);
+            buf_store_nt(chunk_rsrc(dst, pd, shift, pmask, at, span_valid(at, n16, kStepSpan)),
+                         lane16, v[u]);
+        }
+        __syncthreads();
     };
     // the last n_bytes mod 16 bytes, all inside the page that holds byte n16
     auto epilogue = [&]() {
@@ -170,81 +169,49 @@ __device__ __forceinline__ u32x4 fma4(float s, u32x4 c, u32x4 b)
     return r;
 }
 
-template <int U, bool BIG>
+template <int U>
 __global__ __launch_bounds__(kStreamThreads) void k_triad(
     uint8_t *a, const uint32_t *__restrict__ pt_a, uint64_t a_pages,
     const uint8_t *b, const uint32_t *__restrict__ pt_b, uint64_t b_pages,
     const uint8_t *c, const uint32_t *__restrict__ pt_c, uint64_t c_pages, float s,
     uint64_t n_bytes, uint32_t shift, uint32_t n_tiles, Gate g)
 {
+    constexpr uint32_t kTile = Geo<U>::kTile;
     __shared__ uint32_t s_pa[Geo<U>::kPagesMax], s_pb[Geo<U>::kPagesMax], s_pc[Geo<U>::kPagesMax];
     const uint64_t pmask = (1ull << shift) - 1ull;
     const uint64_t n16 = n_bytes & ~15ull;
     const uint64_t n_pages = (n16 + pmask) >> shift;
-    const uint32_t lo = wave_id() * Geo<U>::kWaveSpan + (threadIdx.x & 63u) * 16u;
+    const uint32_t lane16 = (threadIdx.x & 63u) * 16u;
+    const uint32_t wbase = wave_id() * Geo<U>::kWaveSpan;
+    const uint32_t *const pts[3] = {pt_a, pt_b, pt_c};
+    const uint64_t pools[3] = {a_pages, b_pages, c_pages};
+    uint32_t *const stg[3] = {s_pa, s_pb, s_pc};
     auto body = [&](uint32_t t, uint32_t, uint32_t &err, auto &&claim) {
-        const uint64_t t0 = (uint64_t)t * Geo<U>::kTile;
+        const uint64_t t0 = (uint64_t)t * kTile;
+        const uint64_t p0 = t0 >> shift;
+        // a chunk is skipped unless all three of its pages are valid
+        stage_tile_pages<3, true>(t0, kTile, shift, n_pages, pts, pools, stg, err);
         u32x4 vb[U], vc[U];
-        if (BIG) {
-            const uint64_t j = t0 >> shift;
-            const uint32_t pa = pt_a[j], pb = pt_b[j], pc = pt_c[j];
-            const bool bad = pa >= a_pages || pb >= b_pages || pc >= c_pages;
-            err |= bad ? kDevErrPtRange : 0u;
-            const uint32_t valid = bad ? 0u : span_valid(t0, n16, Geo<U>::kTile);
-            const uint64_t in = t0 & pmask;
-            const Rsrc ra = make_rsrc(a + (bad ? 0u : ((uint64_t)pa << shift) + in), valid);
-            const Rsrc rb = make_rsrc(b + (bad ? 0u : ((uint64_t)pb << shift) + in), valid);
-            const Rsrc rc = make_rsrc(c + (bad ? 0u : ((uint64_t)pc << shift) + in), valid);
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                vb[u] = buf_load_nt(rb, lo + u * kStepSpan);
-                vc[u] = buf_load_nt(rc, lo + u * kStepSpan);
-            }
-            claim();
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-                buf_store_nt(ra, lo + u * kStepSpan, fma4(s, vc[u], vb[u]));
-        } else {
-            const uint32_t np = Geo<U>::kTile >> shift;
-            if (threadIdx.x < np) {
-                const uint64_t j = (t0 >> shift) + threadIdx.x;
-                uint32_t pa = kBadPage, pb = kBadPage, pc = kBadPage;
-                if (j < n_pages) {
-                    pa = checked_page(pt_a, j, a_pages, err);
-                    pb = checked_page(pt_b, j, b_pages, err);
-                    pc = checked_page(pt_c, j, c_pages, err);
-                }
-                // a chunk is skipped unless all three of its pages are valid
-                const bool ok = pa != kBadPage && pb != kBadPage && pc != kBadPage;
-                s_pa[threadIdx.x] = ok ? pa : kBadPage;
-                s_pb[threadIdx.x] = ok ? pb : kBadPage;
-                s_pc[threadIdx.x] = ok ? pc : kBadPage;
-            }
-            __syncthreads();
-            const uint32_t lane16 = (threadIdx.x & 63u) * 16u;
-            const uint32_t wbase = wave_id() * Geo<U>::kWaveSpan;
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const uint32_t cs = wbase + u * kStepSpan;
-                const uint32_t jl = cs >> shift;
-                const uint32_t pb = __builtin_amdgcn_readfirstlane(s_pb[jl]);
-                const uint32_t pc = __builtin_amdgcn_readfirstlane(s_pc[jl]);
-                const uint32_t valid = span_valid(t0 + cs, n16, kStepSpan);
-                vb[u] = buf_load_nt(chunk_rsrc(b, pb, shift, pmask, t0 + cs, valid), lane16);
-                vc[u] = buf_load_nt(chunk_rsrc(c, pc, shift, pmask, t0 + cs, valid), lane16);
-            }
-            claim();
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const uint32_t cs = wbase + u * kStepSpan;
-                const uint32_t jl = cs >> shift;
-                const uint32_t pa = __builtin_amdgcn_readfirstlane(s_pa[jl]);
-                const uint32_t valid = span_valid(t0 + cs, n16, kStepSpan);
-                buf_store_nt(chunk_rsrc(a, pa, shift, pmask, t0 + cs, valid), lane16,
-                             fma4(s, vc[u], vb[u]));
-            }
-            __syncthreads();
+        for (int u = 0; u < U; ++u) {
+            const uint64_t at = t0 + wbase + u * kStepSpan;
+            const uint32_t jl = (uint32_t)((at >> shift) - p0);
+            const uint32_t pb = __builtin_amdgcn_readfirstlane(s_pb[jl]);
+            const uint32_t pc = __builtin_amdgcn_readfirstlane(s_pc[jl]);
+            const uint32_t valid = span_valid(at, n16, kStepSpan);
+            vb[u] = buf_load_nt(chunk_rsrc(b, pb, shift, pmask, at, valid), lane16);
+            vc[u] = buf_load_nt(chunk_rsrc(c, pc, shift, pmask, at, valid), lane16);
         }
+        claim();
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint64_t at = t0 + wbase + u * kStepSpan;
+            const uint32_t jl = (uint32_t)((at >> shift) - p0);
+            const uint32_t pa = __builtin_amdgcn_readfirstlane(s_pa[jl]);
+            buf_store_nt(chunk_rsrc(a, pa, shift, pmask, at, span_valid(at, n16, kStepSpan)),
+                         lane16, fma4(s, vc[u], vb[u]));
+        }
+        __syncthreads();
     };
     // the last (n_bytes mod 16) / 4 elements, all inside the page of byte n16
     auto epilogue = [&]() {
@@ -298,11 +265,9 @@ int bimodal_relayout(sgdrc_ctx *ctx, const sgdrc_paged *dst, const sgdrc_paged *
     if (rc)
         return rc;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    const bool big = (1ull << page_shift) >= tile;
-    auto kern = big ? k_relayout<U, true> : k_relayout<U, false>;
-    static const int occ_big = occupancy(k_relayout<U, true>, kStreamThreads);
-    static const int occ_small = occupancy(k_relayout<U, false>, kStreamThreads);
-    const int per_cu = std::min(big ? occ_big : occ_small, kStreamWgsPerCu);
+    auto kern = k_relayout<U>;
+    static const int occ = occupancy(k_relayout<U>, kStreamThreads);
+    const int per_cu = std::min(occ, kStreamWgsPerCu);
     const uint32_t grid = gated_grid(c, per_cu, n_tiles, li);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(kStreamThreads), 0, s,
                        static_cast<uint8_t *>(dst->pool), dst->pt, dst->pool_pages,
@@ -340,11 +305,9 @@ int colored_stream(sgdrc_ctx *ctx, const sgdrc_paged *a, const sgdrc_paged *b,
     if (rc)
         return rc;
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
-    const bool big = (1ull << page_shift) >= tile;
-    auto kern = big ? k_triad<U, true> : k_triad<U, false>;
-    static const int occ_big = occupancy(k_triad<U, true>, kStreamThreads);
-    static const int occ_small = occupancy(k_triad<U, false>, kStreamThreads);
-    const int per_cu = std::min(big ? occ_big : occ_small, kStreamWgsPerCu);
+    auto kern = k_triad<U>;
+    static const int occ = occupancy(k_triad<U>, kStreamThreads);
+    const int per_cu = std::min(occ, kStreamWgsPerCu);
     const uint32_t grid = gated_grid(c, per_cu, n_tiles, li);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(kStreamThreads), 0, hs,
                        static_cast<uint8_t *>(a->pool), a->pt, a->pool_pages,
