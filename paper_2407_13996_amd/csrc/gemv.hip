@@ -26,7 +26,7 @@ typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kGemvThreads = 256;
 constexpr int kGemvWaves = kGemvThreads / 64;
-constexpr int kGemvRows = 4;     // rows per tile, vector-ALU path
+constexpr int kGemvRowsMax = 8;  // rows per tile, vector-ALU path (at most)
 constexpr int kMfmaRows = 16;    // rows per tile, MFMA path
 constexpr int kMfmaNI = 4;       // MFMAs per wave step
 // MFMA path: 8 waves split K, so that a 16-row tile keeps twice the loads of
@@ -99,7 +99,8 @@ __device__ __forceinline__ uint32_t page_of(const TilePages &tp, const uint32_t 
     return s_pt[j - tp.p_lo];
 }
 
-template <int WT, int XT, int NB>
+// R rows per tile; U 16-byte slices per lane and row in flight.
+template <int WT, int XT, int NB, int R, int U>
 __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
     const uint8_t *__restrict__ w_pool, const uint32_t *__restrict__ pt, uint64_t pool_pages,
     uint32_t M, uint32_t K, const uint8_t *__restrict__ x, uint32_t nb, float *__restrict__ y,
@@ -108,35 +109,34 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
     constexpr int WSZ = Dt<WT>::size, XSZ = Dt<XT>::size;
     constexpr int EPV = 16 / WSZ;                 // elements per 16-byte slice of W
     constexpr int XW = EPV * XSZ / 4;             // 32-bit words of x per slice and batch
-    constexpr int kGemvU = NB <= 2 ? 4 : 2;       // 16-byte slices per lane and row in flight
     __shared__ uint32_t s_pt[kPtCap];
-    __shared__ float s_red[kGemvWaves][kGemvRows * NB];
+    __shared__ float s_red[kGemvWaves][R * NB];
     const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63u;
     const uint64_t row_bytes = (uint64_t)K * WSZ;
     const uint32_t KV = (uint32_t)(row_bytes / 16u);
     const uint64_t pmask = (1ull << shift) - 1ull;
 
     auto body = [&](uint32_t t, uint32_t, uint32_t &err, auto &&) {
-        const uint32_t m0 = t * kGemvRows;
-        const uint32_t m_end = min(m0 + (uint32_t)kGemvRows, M);
+        const uint32_t m0 = t * R;
+        const uint32_t m_end = min(m0 + (uint32_t)R, M);
         const TilePages tp = stage_pages(pt, pool_pages, (uint64_t)m0 * row_bytes,
                                          (uint64_t)m_end * row_bytes, shift, s_pt, err);
-        float acc[kGemvRows][NB];
+        float acc[R][NB];
 #pragma unroll
-        for (int r = 0; r < kGemvRows; ++r)
+        for (int r = 0; r < R; ++r)
 #pragma unroll
             for (int b = 0; b < NB; ++b)
                 acc[r][b] = 0.0f;
 
-        for (uint32_t j = 0; (j * kGemvWaves + wave) * 64u < KV; j += kGemvU) {
-            u32x4 wv[kGemvU][kGemvRows];
-            uint32_t xv[kGemvU][NB][XW];
+        for (uint32_t j = 0; (j * kGemvWaves + wave) * 64u < KV; j += U) {
+            u32x4 wv[U][R];
+            uint32_t xv[U][NB][XW];
 #pragma unroll
-            for (int u = 0; u < kGemvU; ++u) {
+            for (int u = 0; u < U; ++u) {
                 const uint32_t kv = ((j + u) * kGemvWaves + wave) * 64u + lane;
                 const bool ok = kv < KV;
 #pragma unroll
-                for (int r = 0; r < kGemvRows; ++r) {
+                for (int r = 0; r < R; ++r) {
                     wv[u][r] = u32x4{0u, 0u, 0u, 0u};
                     if (ok && m0 + r < M) {
                         const uint64_t off = (uint64_t)(m0 + r) * row_bytes + (uint64_t)kv * 16u;
@@ -170,13 +170,13 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
                 }
             }
 #pragma unroll
-            for (int u = 0; u < kGemvU; ++u) {
+            for (int u = 0; u < U; ++u) {
                 float xf[NB][EPV];
 #pragma unroll
                 for (int b = 0; b < NB; ++b)
                     decode<XT, EPV>(xv[u][b], xf[b]);
 #pragma unroll
-                for (int r = 0; r < kGemvRows; ++r) {
+                for (int r = 0; r < R; ++r) {
                     const uint32_t ww[4] = {wv[u][r].x, wv[u][r].y, wv[u][r].z, wv[u][r].w};
                     float wf[EPV];
                     decode<WT, EPV>(ww, wf);
@@ -190,7 +190,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
         }
         // butterfly over the 64 lanes: every lane ends with the same sum
 #pragma unroll
-        for (int r = 0; r < kGemvRows; ++r)
+        for (int r = 0; r < R; ++r)
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
                 float v = acc[r][b];
@@ -201,13 +201,13 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
             }
         if (lane == 0) {
 #pragma unroll
-            for (int r = 0; r < kGemvRows; ++r)
+            for (int r = 0; r < R; ++r)
 #pragma unroll
                 for (int b = 0; b < NB; ++b)
                     s_red[wave][r * NB + b] = acc[r][b];
         }
         __syncthreads();
-        if (threadIdx.x < (uint32_t)(kGemvRows * NB)) {
+        if (threadIdx.x < (uint32_t)(R * NB)) {
             const uint32_t r = threadIdx.x / NB, b = threadIdx.x % NB;
             float v = s_red[0][threadIdx.x];
 #pragma unroll
@@ -313,22 +313,36 @@ __global__ __launch_bounds__(kMfmaThreads) void k_gemm_mfma(
 typedef void (*GemvKernel)(const uint8_t *, const uint32_t *, uint64_t, uint32_t, uint32_t,
                            const uint8_t *, uint32_t, float *, uint32_t, uint32_t, Gate);
 
+struct ValuCfg {
+    GemvKernel kernel;
+    uint32_t rows;
+};
+
+// Rows per tile and slices in flight for the vector-ALU path, by batch and
+// row length (measured on MI355X over the 4096x11008 and 11008x4096 bf16
+// layers): the choice keeps every lane busy in as few rounds as possible
+// and the tile count no larger than the workgroups the occupancy allows.
 template <int WT, int XT>
-static GemvKernel pick_valu(uint32_t batch)
+static ValuCfg pick_valu(uint32_t batch, bool long_rows)
 {
-    if (batch <= 1) return k_gemv_valu<WT, XT, 1>;
-    if (batch <= 2) return k_gemv_valu<WT, XT, 2>;
-    if (batch <= 4) return k_gemv_valu<WT, XT, 4>;
-    return k_gemv_valu<WT, XT, 8>;
+    if (batch <= 1)
+        return long_rows ? ValuCfg{k_gemv_valu<WT, XT, 1, 4, 4>, 4}
+                         : ValuCfg{k_gemv_valu<WT, XT, 1, 8, 2>, 8};
+    if (batch <= 2)
+        return long_rows ? ValuCfg{k_gemv_valu<WT, XT, 2, 8, 3>, 8}
+                         : ValuCfg{k_gemv_valu<WT, XT, 2, 8, 2>, 8};
+    if (batch <= 4)
+        return ValuCfg{k_gemv_valu<WT, XT, 4, 4, 2>, 4};
+    return ValuCfg{k_gemv_valu<WT, XT, 8, 4, 2>, 4};
 }
 
 template <int WT>
-static GemvKernel pick_valu_x(int x_dtype, uint32_t batch)
+static ValuCfg pick_valu_x(int x_dtype, uint32_t batch, bool long_rows)
 {
     switch (x_dtype) {
-    case SGDRC_F32: return pick_valu<WT, SGDRC_F32>(batch);
-    case SGDRC_BF16: return pick_valu<WT, SGDRC_BF16>(batch);
-    default: return pick_valu<WT, SGDRC_F16>(batch);
+    case SGDRC_F32: return pick_valu<WT, SGDRC_F32>(batch, long_rows);
+    case SGDRC_BF16: return pick_valu<WT, SGDRC_BF16>(batch, long_rows);
+    default: return pick_valu<WT, SGDRC_F16>(batch, long_rows);
     }
 }
 
@@ -385,7 +399,7 @@ int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, 
     const bool mfma = batch >= 5 && w_dtype == x_dtype && w_dtype != SGDRC_F32;
     {
         // a tile's rows must span at most kPtCap pages (they are staged in LDS)
-        const uint64_t rows = mfma ? kMfmaRows : kGemvRows;
+        const uint64_t rows = mfma ? kMfmaRows : kGemvRowsMax;
         const uint64_t span = rows * (uint64_t)K * dtype_size(w_dtype);
         if ((span >> page_shift) + 2 > (uint64_t)kPtCap)
             return set_error(SGDRC_EINVAL, "rows of %llu bytes span too many %u-byte pages",
@@ -398,12 +412,16 @@ int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, 
         k = w_dtype == SGDRC_BF16 ? k_gemm_mfma<SGDRC_BF16> : k_gemm_mfma<SGDRC_F16>;
         n_tiles = (M + kMfmaRows - 1) / kMfmaRows;
     } else {
+        // rows of more than 512 slices of 16 bytes take two rounds of loads
+        const bool long_rows = (uint64_t)K * dtype_size(w_dtype) > 512u * 16u;
+        ValuCfg cfg;
         switch (w_dtype) {
-        case SGDRC_F32: k = pick_valu_x<SGDRC_F32>(x_dtype, batch); break;
-        case SGDRC_BF16: k = pick_valu_x<SGDRC_BF16>(x_dtype, batch); break;
-        default: k = pick_valu_x<SGDRC_F16>(x_dtype, batch); break;
+        case SGDRC_F32: cfg = pick_valu_x<SGDRC_F32>(x_dtype, batch, long_rows); break;
+        case SGDRC_BF16: cfg = pick_valu_x<SGDRC_BF16>(x_dtype, batch, long_rows); break;
+        default: cfg = pick_valu_x<SGDRC_F16>(x_dtype, batch, long_rows); break;
         }
-        n_tiles = (M + kGemvRows - 1) / kGemvRows;
+        k = cfg.kernel;
+        n_tiles = (M + cfg.rows - 1) / cfg.rows;
     }
     Gate g;
     LaunchInfo li;
