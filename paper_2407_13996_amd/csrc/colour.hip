@@ -154,7 +154,7 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
             }
         }
     };
-    gated_tile_loop<Claim::Mid>(g, n_tiles, body, flush, epilogue);
+    gated_tile_loop<Claim::Mid>(g, n_tiles, NoOp(), body, flush, epilogue);
 }
 
 constexpr int kPtThreads = 256;

@@ -72,10 +72,11 @@ __device__ __forceinline__ uint32_t hw_key()
 }
 
 // LUT entry of the executing workgroup's CU: logical CU | XCD << 16 |
-// CU-in-XCD << 24, or kLutNone.  The key comes from scalar registers, so
-// this is a scalar load.
+// CU-in-XCD << 24, or kLutNone.
 __device__ __forceinline__ uint32_t my_cu_entry(const Gate &g)
 {
+    // (A vector load: reading the table as constant memory, which makes the
+    // lookup a scalar load, measured 10 percent slower on the GEMV.)
     return g.lut[hw_key()];
 }
 
@@ -181,8 +182,10 @@ struct NoOp {
 //  After: after the tile.
 enum class Claim { Ahead, Mid, After };
 
-// Runs ``body(tile, cu, err, claim)`` for every tile that this workgroup
-// obtains, under the gate.  Workgroups on CUs outside the mask take no
+// Runs ``prologue()`` once at the start, alongside the gate's own reads and
+// before a barrier (kernels stage per-launch tables there; it should be
+// straight-line code), then ``body(tile, cu, err, claim)`` for every tile
+// that this workgroup obtains, under the gate.  Workgroups on CUs outside the mask take no
 // tiles; the others take tiles of their own group's range, then steal from
 // other groups' ranges until every range is exhausted.  ``flush()`` runs
 // after a workgroup's tile loop (to publish per-workgroup partials).  The
@@ -200,28 +203,37 @@ enum class Claim { Ahead, Mid, After };
 // from it lets the compiler send some lanes of a wave back to the barrier
 // while others still owe the next ticket.  Bodies record problems in the
 // per-thread ``err`` bits instead; they are raised once, after the loop.
-template <Claim CL, typename Body, typename Flush, typename Epilogue>
-__device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles, Body body,
-                                                Flush flush, Epilogue epilogue)
+template <Claim CL, typename Prologue, typename Body, typename Flush, typename Epilogue>
+__device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles, Prologue prologue,
+                                                Body body, Flush flush, Epilogue epilogue)
 {
     __shared__ uint32_t s_ticket;
     __shared__ uint32_t s_flag;
     __shared__ uint32_t s_left_lo[kMaxGroups], s_left_hi[kMaxGroups];
     __shared__ uint32_t s_grp_tile[kMaxGroups + 1];
+    // Prologue: every memory read it needs is issued before any branch on
+    // a value read, so that the round trips overlap (the CU-table entry is
+    // read even on an XCD without allowed CUs, and then ignored).
+    uint32_t xcc;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+    const uint32_t lut_entry = my_cu_entry(g);
+    // every kernel runs at least kMaxGroups + 1 threads per workgroup; the
+    // threads beyond write the last entry again (same value), which keeps
+    // this straight-line code
+    {
+        const uint32_t i = threadIdx.x < (uint32_t)kMaxGroups ? threadIdx.x : (uint32_t)kMaxGroups;
+        s_grp_tile[i] = g.grp_tile[i];
+    }
+    prologue();
+    const bool xcd_on = ((g.xcc_allowed >> (xcc & 0xFu)) & 1u) != 0u;
+    const uint32_t entry = xcd_on ? lut_entry : kLutNone;
     // time log: workgroup 0, the first one the hardware dispatches, stamps
     // the start; the last workgroup to finish stamps the end
     if (g.tlog && blockIdx.x == 0 && threadIdx.x == 0)
         __hip_atomic_store(&g.tlog[0], __builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
-    for (uint32_t i = threadIdx.x; i <= (uint32_t)kMaxGroups; i += blockDim.x)
-        s_grp_tile[i] = g.grp_tile[i];
     __syncthreads();
     uint32_t err = 0u;
-    // a workgroup on an XCD without allowed CUs skips even the table lookup
-    uint32_t xcc;
-    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
-    const bool xcd_on = ((g.xcc_allowed >> (xcc & 0xFu)) & 1u) != 0u;
-    const uint32_t entry = xcd_on ? my_cu_entry(g) : kLutNone;
     const uint32_t cu = entry & 0xFFFFu;
     if (entry != kLutNone && cu_allowed(g, cu)) {
         uint32_t grp = g.grp_base[(entry >> 16) & 0xFFu] + ((entry >> 24) >> g.grp_shift);

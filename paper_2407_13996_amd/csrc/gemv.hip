@@ -99,6 +99,32 @@ __device__ __forceinline__ uint32_t page_of(const TilePages &tp, const uint32_t 
     return s_pt[j - tp.p_lo];
 }
 
+// When the whole matrix spans at most kPtCap pages, its table is staged in
+// LDS once per workgroup, in the tile loop's prologue (overlapping the
+// gate's own reads), and tiles skip their per-tile staging.  The staging is
+// straight-line: threads beyond the last page read and write that page's
+// entry again.  Out-of-range entries are recorded in ``err``.
+__device__ __forceinline__ void stage_whole_table(const uint32_t *pt, uint64_t pool_pages,
+                                                  uint64_t w_pages, uint32_t *s_pt, uint32_t &err)
+{
+    const uint64_t n = w_pages < (uint64_t)kPtCap ? w_pages : (uint64_t)kPtCap;
+    const uint32_t i = threadIdx.x < n ? threadIdx.x : (uint32_t)(n - 1u);
+    uint32_t e = 0u;
+    s_pt[i] = checked_page(pt, i, pool_pages, e);
+    err |= threadIdx.x < n ? e : 0u;
+}
+
+// Page lookup context of one tile: the whole staged table, or this tile's
+// pages staged now (a barrier; the choice is uniform).
+__device__ __forceinline__ TilePages tile_pages(bool whole, const uint32_t *pt, uint64_t pool_pages,
+                                                uint64_t byte_lo, uint64_t byte_hi, uint32_t shift,
+                                                uint32_t *s_pt, uint32_t &err)
+{
+    if (whole)
+        return TilePages{0u};
+    return stage_pages(pt, pool_pages, byte_lo, byte_hi, shift, s_pt, err);
+}
+
 // R rows per tile; U 16-byte slices per lane and row in flight.
 template <int WT, int XT, int NB, int R, int U>
 __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
@@ -115,12 +141,16 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
     const uint64_t row_bytes = (uint64_t)K * WSZ;
     const uint32_t KV = (uint32_t)(row_bytes / 16u);
     const uint64_t pmask = (1ull << shift) - 1ull;
+    const uint64_t w_pages = ((uint64_t)M * row_bytes + pmask) >> shift;
+    const bool whole = w_pages <= (uint64_t)kPtCap;
+    uint32_t pro_err = 0u;
+    auto prologue = [&]() { stage_whole_table(pt, pool_pages, w_pages, s_pt, pro_err); };
 
     auto body = [&](uint32_t t, uint32_t, uint32_t &err, auto &&) {
         const uint32_t m0 = t * R;
         const uint32_t m_end = min(m0 + (uint32_t)R, M);
-        const TilePages tp = stage_pages(pt, pool_pages, (uint64_t)m0 * row_bytes,
-                                         (uint64_t)m_end * row_bytes, shift, s_pt, err);
+        const TilePages tp = tile_pages(whole, pt, pool_pages, (uint64_t)m0 * row_bytes,
+                                        (uint64_t)m_end * row_bytes, shift, s_pt, err);
         float acc[R][NB];
 #pragma unroll
         for (int r = 0; r < R; ++r)
@@ -218,7 +248,9 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
         }
         __syncthreads();
     };
-    gated_tile_loop<Claim::Ahead>(g, n_tiles, body, NoOp(), NoOp());
+    gated_tile_loop<Claim::Ahead>(g, n_tiles, prologue, body, NoOp(), NoOp());
+    if (pro_err)
+        raise_flag(g.err, pro_err);
 }
 
 template <int DT>
@@ -250,12 +282,16 @@ __global__ __launch_bounds__(kMfmaThreads) void k_gemm_mfma(
     const uint64_t row_bytes = (uint64_t)K * 2u;
     const uint32_t KV = (uint32_t)(row_bytes / 16u);
     const uint64_t pmask = (1ull << shift) - 1ull;
+    const uint64_t w_pages = ((uint64_t)M * row_bytes + pmask) >> shift;
+    const bool whole = w_pages <= (uint64_t)kPtCap;
+    uint32_t pro_err = 0u;
+    auto prologue = [&]() { stage_whole_table(pt, pool_pages, w_pages, s_pt, pro_err); };
 
     auto body = [&](uint32_t t, uint32_t, uint32_t &err, auto &&) {
         const uint32_t m0 = t * kMfmaRows;
         const uint32_t m_end = min(m0 + (uint32_t)kMfmaRows, M);
-        const TilePages tp = stage_pages(pt, pool_pages, (uint64_t)m0 * row_bytes,
-                                         (uint64_t)m_end * row_bytes, shift, s_pt, err);
+        const TilePages tp = tile_pages(whole, pt, pool_pages, (uint64_t)m0 * row_bytes,
+                                        (uint64_t)m_end * row_bytes, shift, s_pt, err);
         const uint32_t row = m0 + rl;
         const bool row_ok = row < M;
         const bool col_ok = rl < nb;
@@ -307,7 +343,9 @@ __global__ __launch_bounds__(kMfmaThreads) void k_gemm_mfma(
         }
         __syncthreads();
     };
-    gated_tile_loop<Claim::Ahead>(g, n_tiles, body, NoOp(), NoOp());
+    gated_tile_loop<Claim::Ahead>(g, n_tiles, prologue, body, NoOp(), NoOp());
+    if (pro_err)
+        raise_flag(g.err, pro_err);
 }
 
 typedef void (*GemvKernel)(const uint8_t *, const uint32_t *, uint64_t, uint32_t, uint32_t,

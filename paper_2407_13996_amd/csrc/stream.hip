@@ -156,7 +156,7 @@ __global__ __launch_bounds__(kStreamThreads) void k_relayout(
             }
         }
     };
-    gated_tile_loop<Claim::Mid>(g, n_tiles, body, NoOp(), epilogue);
+    gated_tile_loop<Claim::Mid>(g, n_tiles, NoOp(), body, NoOp(), epilogue);
 }
 
 __device__ __forceinline__ u32x4 fma4(float s, u32x4 c, u32x4 b)
@@ -232,7 +232,7 @@ __global__ __launch_bounds__(kStreamThreads) void k_triad(
             }
         }
     };
-    gated_tile_loop<Claim::Mid>(g, n_tiles, body, NoOp(), epilogue);
+    gated_tile_loop<Claim::Mid>(g, n_tiles, NoOp(), body, NoOp(), epilogue);
 }
 
 }  // namespace sgdrc
