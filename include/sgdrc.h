@@ -30,6 +30,11 @@
  *  - A context serves one device.  It may be used from several host
  *    threads; operations on one stream are ordered, operations on different
  *    streams may run concurrently (each stream gets its own work queue).
+ *  - CU masks (set_cu_mask) confine every tile of work to the allowed CUs.
+ *    The grid's last workgroup, which may sit on any CU, also handles a
+ *    launch's remainder below the 16-byte access granularity (the last
+ *    n mod 16 bytes of a relayout or triad, the last n mod 16 addresses of
+ *    a classify) and any tiles left if no workgroup reached an allowed CU.
  */
 #ifndef SGDRC_H
 #define SGDRC_H
