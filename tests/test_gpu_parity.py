@@ -433,6 +433,14 @@ def test_gemv_dtype_mix(ctx, orc, wd, xd, B):
     run_gemv(ctx, orc, 517, 264, B, wd, xd, 12, seed=10 + B)
 
 
+@pytest.mark.parametrize("M,B", [(512, 1), (512, 8), (513, 1), (513, 8), (511, 3)])
+def test_gemv_page_table_staging_boundary(ctx, orc, M, B):
+    """W of 256 pages (its table staged once per workgroup) and of 257 pages
+    (staged per tile), on both the vector and the MFMA path."""
+    say(f"gemv bf16 {M}x1024 B={B}, 4 KiB pages")
+    run_gemv(ctx, orc, M, 1024, B, sg.BF16, sg.BF16, 12, seed=M + B)
+
+
 @pytest.mark.parametrize("M,K,B", [(4096, 11008, 1), (11008, 4096, 8)])
 def test_gemv_config3_full_size(ctx, orc, M, K, B):
     say(f"gemv bf16 {M}x{K} B={B}, 2 MiB pages, colours 0..47 of 64")
