@@ -454,7 +454,7 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
                 med, p99 = pctl(list(spans), 50), pctl(list(spans), 99)
                 gbs = nbytes / (med * 1e-6) / 1e9
                 out.append({"M": M, "K": K, "batch": B, "cus": ncu, "device_flags": flag,
-                            "path": "mfma" if B >= 5 else "valu",
+                            "path": "mfma" if B >= 3 else "valu",
                             "p50_us": round(med, 2), "p99_us": round(p99, 2),
                             "GBps": round(gbs, 1),
                             "pct_of_colour_scaled_peak": round(100 * gbs / (0.75 * HBM_PEAK_GBS), 1),

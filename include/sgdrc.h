@@ -217,12 +217,13 @@ int colored_stream(sgdrc_ctx *ctx, const sgdrc_paged *a, const sgdrc_paged *b,
  * products summed in fp32.  W is row-major [M x K] of w_dtype, stored
  * through w's page table (ceil(M K esize / 2^page_shift) entries); d_x is
  * contiguous [batch x K] of x_dtype (16-byte aligned); d_y is contiguous
- * [batch x M] fp32.  Batches 5..8 with bf16 x bf16 or f16 x f16 operands
+ * [batch x M] fp32.  Batches 3..8 with bf16 x bf16 or f16 x f16 operands
  * run on MFMA; all other cases on the vector ALUs.  The sum order depends
  * only on (M, K, batch, dtypes), never on the CU mask, so results are
  * bitwise reproducible.  EINVAL: batch outside 1..8, M or K zero, K *
- * esize(w_dtype) not a multiple of 16, unknown dtype, NULL pointers,
- * unaligned pointers. */
+ * esize(w_dtype) not a multiple of 16, x of 4 GiB or more, a tile's rows
+ * (8, or 16 on MFMA) spanning more pages than one tile may stage, unknown
+ * dtype, NULL pointers, unaligned pointers. */
 int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, uint32_t K,
                  const void *d_x, int x_dtype, uint32_t batch, float *d_y,
                  uint32_t page_shift, void *stream);

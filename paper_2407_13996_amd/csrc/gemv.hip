@@ -13,9 +13,10 @@
 // reads the table directly), and every 16-byte slice is mapped with one LDS
 // read plus a shift and an add.
 //
-// Batches 5..8 with bf16 x bf16 or f16 x f16 operands use the gfx950
+// Batches 3..8 with bf16 x bf16 or f16 x f16 operands use the gfx950
 // 16x16x32 MFMA: a 16-row block of W is the A operand, x (batch padded to 16
-// columns with zeros) the B operand; eight wavefronts split K.
+// columns) the B operand; eight wavefronts split each chunk of K.  From batch
+// 3 on it measured faster than the vector path on MI355X.
 #include "host_common.hpp"
 
 namespace sgdrc {
@@ -28,7 +29,6 @@ constexpr int kGemvThreads = 256;
 constexpr int kGemvWaves = kGemvThreads / 64;
 constexpr int kGemvRowsMax = 8;  // rows per tile, vector-ALU path (at most)
 constexpr int kMfmaRows = 16;    // rows per tile, MFMA path
-constexpr int kMfmaNI = 4;       // MFMAs per wave step
 // MFMA path: 8 waves split K, so that a 16-row tile keeps twice the loads of
 // a 4-wave workgroup in flight (measured best of 4, 8 and 16 waves for both
 // 4096x11008 and 11008x4096 at batch 8)
@@ -264,11 +264,32 @@ __device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c)
                                                       __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
 }
 
-// Batch 5..8 on MFMA.  Lane l supplies row (l % 16) of the 16-row W block
-// and batch column (l % 16) of x, both for the k-slice of its lane group
-// g = l / 16; lanes of one group read the same k-slice of W and x, so the
-// k order inside the instruction matches between the operands.  The
-// accumulator holds rows 4g..4g+3 of batch column l % 16.
+// Batch 3..8 on MFMA.  A tile (16 rows x K) is consumed in chunks of
+// kMfmaChunk bytes per row.  Each chunk of W (16 rows) and of x (8 batch
+// rows) is read with row-contiguous 16-byte loads (each wavefront
+// instruction covers 1 KiB of one row) and staged in LDS; the MFMAs then
+// read their operands from LDS: lane l supplies row (l % 16) of the W block
+// and batch column (l % 16) of x, both for the 16-byte k-slice of its lane
+// group g = l / 16, so the k order inside the instruction matches between
+// the operands, and the accumulator holds rows 4g..4g+3 of batch column
+// l % 16.  The eight waves take the chunk's 32 k-steps four each.  The
+// two chunks that follow are in flight during the current chunk's MFMAs;
+// beyond the last chunk the loads read a valid address and are discarded.
+constexpr uint32_t kMfmaChunk = 2048;                  // bytes per row per chunk
+constexpr uint32_t kMfmaChunkSlices = kMfmaChunk / 16u;  // 128
+constexpr uint32_t kMfmaLdsRow = kMfmaChunk + 16u;     // padded LDS row
+constexpr int kMfmaBatchRows = 8;                      // x rows staged (batch <= 8)
+constexpr int kMfmaWLoads = kMfmaRows * (int)kMfmaChunkSlices / kMfmaThreads;       // 4
+constexpr int kMfmaXLoads = kMfmaBatchRows * (int)kMfmaChunkSlices / kMfmaThreads;  // 2
+constexpr int kMfmaStepsPerWave = (int)(kMfmaChunk / 64u) / kMfmaWaves;             // 4
+
+// x through a buffer resource, cached (every workgroup reads all of x).
+constexpr uint32_t kXOutside = 0xFFFFFFF0u;  // offset past any x resource
+__device__ __forceinline__ u32x4 buf_load(Rsrc r, uint32_t off)
+{
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
 template <int DT>
 __global__ __launch_bounds__(kMfmaThreads) void k_gemm_mfma(
     const uint8_t *__restrict__ w_pool, const uint32_t *__restrict__ pt, uint64_t pool_pages,
@@ -277,13 +298,20 @@ __global__ __launch_bounds__(kMfmaThreads) void k_gemm_mfma(
 {
     __shared__ uint32_t s_pt[kPtCap];
     __shared__ f32x4 s_red[kMfmaWaves][64];
-    const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63u;
+    __shared__ __attribute__((aligned(16))) uint8_t s_w[kMfmaRows][kMfmaLdsRow];
+    __shared__ __attribute__((aligned(16))) uint8_t s_x[kMfmaBatchRows][kMfmaLdsRow];
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t lane = threadIdx.x & 63u;
     const uint32_t rl = lane & 15u, grp = lane >> 4;
     const uint64_t row_bytes = (uint64_t)K * 2u;
     const uint32_t KV = (uint32_t)(row_bytes / 16u);
+    const uint32_t n_chunks = (KV + kMfmaChunkSlices - 1u) / kMfmaChunkSlices;
     const uint64_t pmask = (1ull << shift) - 1ull;
     const uint64_t w_pages = ((uint64_t)M * row_bytes + pmask) >> shift;
     const bool whole = w_pages <= (uint64_t)kPtCap;
+    // x is below 4 GiB (checked by the host), so 32-bit offsets reach it
+    const uint32_t x_row = K * 2u;
+    const Rsrc x_rsrc = make_rsrc(x, nb * x_row);
     uint32_t pro_err = 0u;
     auto prologue = [&]() { stage_whole_table(pt, pool_pages, w_pages, s_pt, pro_err); };
 
@@ -292,32 +320,77 @@ __global__ __launch_bounds__(kMfmaThreads) void k_gemm_mfma(
         const uint32_t m_end = min(m0 + (uint32_t)kMfmaRows, M);
         const TilePages tp = tile_pages(whole, pt, pool_pages, (uint64_t)m0 * row_bytes,
                                         (uint64_t)m_end * row_bytes, shift, s_pt, err);
-        const uint32_t row = m0 + rl;
-        const bool row_ok = row < M;
-        const bool col_ok = rl < nb;
-        f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-        for (uint32_t j = 0; (j * kMfmaWaves + wave) * kMfmaNI * 4u < KV; ++j) {
-            u32x4 av[kMfmaNI], bv[kMfmaNI];
+        // Two register sets of chunk loads, so that two chunks are in flight
+        // while a third feeds the MFMAs.  Loads are always issued and are zero
+        // where out of range (rows beyond M, slices beyond K, batch rows
+        // beyond nb), so chunks are taken in pairs without a branch; the pad
+        // chunk of an odd count adds zeros.
+        // The in-range test of each load travels beside its data as a bit of
+        // ``okv`` and is applied where the data goes to LDS: a select right
+        // after the load would make the loop wait for the data there.
+        u32x4 wa[kMfmaWLoads], xa[kMfmaXLoads], wb[kMfmaWLoads], xb[kMfmaXLoads];
+        uint32_t oka = 0u, okb = 0u;
+        auto load_chunk = [&](uint32_t c, u32x4 *wv, u32x4 *xv, uint32_t &okv) __attribute__((always_inline)) {
+            okv = 0u;
 #pragma unroll
-            for (int i = 0; i < kMfmaNI; ++i) {
-                const uint32_t kv = ((j * kMfmaWaves + wave) * kMfmaNI + i) * 4u + grp;
-                av[i] = u32x4{0u, 0u, 0u, 0u};
-                bv[i] = u32x4{0u, 0u, 0u, 0u};
-                if (kv < KV) {
-                    if (row_ok) {
-                        const uint64_t off = (uint64_t)row * row_bytes + (uint64_t)kv * 16u;
-                        const uint32_t p = page_of(tp, s_pt, off >> shift);
-                        if (p != kBadPage)
-                            av[i] = load_nt(w_pool + ((uint64_t)p << shift) + (off & pmask));
-                    }
-                    if (col_ok)
-                        bv[i] = *reinterpret_cast<const u32x4 *>(
-                            x + ((uint64_t)rl * K + (uint64_t)kv * 8u) * 2u);
-                }
+            for (int q = 0; q < kMfmaWLoads; ++q) {
+                const uint32_t L = (uint32_t)q * kMfmaThreads + threadIdx.x;
+                const uint32_t r = L / kMfmaChunkSlices, sl = L % kMfmaChunkSlices;
+                const uint32_t kv = c * kMfmaChunkSlices + sl;
+                const uint32_t row = m0 + r;
+                const bool in = kv < KV && row < M;
+                const uint64_t off = (uint64_t)(in ? row : m0) * row_bytes + (uint64_t)(in ? kv : 0u) * 16u;
+                const uint32_t p = page_of(tp, s_pt, off >> shift);
+                const bool ok = in && p != kBadPage;
+                wv[q] = load_nt(w_pool + (ok ? ((uint64_t)p << shift) + (off & pmask) : 0u));
+                okv |= (uint32_t)ok << q;
             }
 #pragma unroll
-            for (int i = 0; i < kMfmaNI; ++i)
-                acc = mfma16x16x32<DT>(av[i], bv[i], acc);
+            for (int q = 0; q < kMfmaXLoads; ++q) {
+                const uint32_t L = (uint32_t)q * kMfmaThreads + threadIdx.x;
+                const uint32_t b = L / kMfmaChunkSlices, sl = L % kMfmaChunkSlices;
+                const uint32_t kv = c * kMfmaChunkSlices + sl;
+                // out of range: an offset beyond the resource, which reads zero
+                xv[q] = buf_load(x_rsrc, b < nb && kv < KV ? b * x_row + kv * 16u : kXOutside);
+            }
+        };
+        auto store_chunk = [&](const u32x4 *wv, const u32x4 *xv, uint32_t okv) __attribute__((always_inline)) {
+            const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int q = 0; q < kMfmaWLoads; ++q) {
+                const uint32_t L = (uint32_t)q * kMfmaThreads + threadIdx.x;
+                *reinterpret_cast<u32x4 *>(&s_w[L / kMfmaChunkSlices][(L % kMfmaChunkSlices) * 16u]) =
+                    (okv >> q) & 1u ? wv[q] : z;
+            }
+#pragma unroll
+            for (int q = 0; q < kMfmaXLoads; ++q) {
+                const uint32_t L = (uint32_t)q * kMfmaThreads + threadIdx.x;
+                *reinterpret_cast<u32x4 *>(&s_x[L / kMfmaChunkSlices][(L % kMfmaChunkSlices) * 16u]) = xv[q];
+            }
+        };
+        f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        auto mfma_chunk = [&]() __attribute__((always_inline)) {
+#pragma unroll
+            for (int i = 0; i < kMfmaStepsPerWave; ++i) {
+                const uint32_t j = wave * (uint32_t)kMfmaStepsPerWave + (uint32_t)i;
+                const u32x4 a = *reinterpret_cast<const u32x4 *>(&s_w[rl][j * 64u + grp * 16u]);
+                const u32x4 bx = *reinterpret_cast<const u32x4 *>(&s_x[rl & 7u][j * 64u + grp * 16u]);
+                acc = mfma16x16x32<DT>(a, rl < (uint32_t)kMfmaBatchRows ? bx : u32x4{0u, 0u, 0u, 0u}, acc);
+            }
+        };
+        load_chunk(0u, wa, xa, oka);
+        load_chunk(1u, wb, xb, okb);
+        for (uint32_t c = 0; c < n_chunks; c += 2u) {
+            __syncthreads();  // the previous chunk's MFMAs have read the LDS
+            store_chunk(wa, xa, oka);
+            __syncthreads();
+            load_chunk(c + 2u, wa, xa, oka);
+            mfma_chunk();
+            __syncthreads();
+            store_chunk(wb, xb, okb);
+            __syncthreads();
+            load_chunk(c + 3u, wb, xb, okb);
+            mfma_chunk();
         }
         s_red[wave][lane] = acc;
         __syncthreads();
@@ -331,7 +404,7 @@ __global__ __launch_bounds__(kMfmaThreads) void k_gemm_mfma(
                 v.z += o.z;
                 v.w += o.w;
             }
-            if (col_ok) {
+            if (rl < nb) {
                 const float vals[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
@@ -425,6 +498,8 @@ int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, 
         return set_error(SGDRC_EINVAL, "K * element size must be a multiple of 16 bytes");
     if ((uint64_t)K * dtype_size(w_dtype) / 16u >= (1ull << 31))
         return set_error(SGDRC_EINVAL, "K too large");
+    if ((uint64_t)batch * K * dtype_size(x_dtype) > 0xFFFFFFF0ull)
+        return set_error(SGDRC_EINVAL, "x must be smaller than 4 GiB");
     if (!d_x || !d_y)
         return set_error(SGDRC_EINVAL, "NULL x or y");
     if ((reinterpret_cast<uintptr_t>(d_x) & 15u) || (reinterpret_cast<uintptr_t>(d_y) & 3u))
@@ -434,7 +509,7 @@ int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, 
     if (rc)
         return rc;
 
-    const bool mfma = batch >= 5 && w_dtype == x_dtype && w_dtype != SGDRC_F32;
+    const bool mfma = batch >= 3 && w_dtype == x_dtype && w_dtype != SGDRC_F32;
     {
         // a tile's rows must span at most kPtCap pages (they are staged in LDS)
         const uint64_t rows = mfma ? kMfmaRows : kGemvRowsMax;

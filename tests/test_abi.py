@@ -123,6 +123,8 @@ def test_gemv_argument_errors(L):
     assert call(x=0) == sg.EINVAL
     assert call(x=264) == sg.EINVAL         # x not 16-byte aligned
     assert call(shift=40) == sg.EINVAL
+    assert call(K=1 << 28, b=8) == sg.EINVAL  # x of 4 GiB
+    assert call(K=1 << 28, b=7) == sg.ENODEV
 
 
 def test_context_calls_reject_null(L):

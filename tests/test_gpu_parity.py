@@ -441,6 +441,16 @@ def test_gemv_page_table_staging_boundary(ctx, orc, M, B):
     run_gemv(ctx, orc, M, 1024, B, sg.BF16, sg.BF16, 12, seed=M + B)
 
 
+@pytest.mark.parametrize("M,K,B,dt", [(300, 11008, 8, sg.BF16), (37, 3000, 3, sg.F16),
+                                      (64, 1024, 4, sg.BF16), (17, 8, 8, sg.F16)])
+def test_gemv_mfma_k_chunks(ctx, orc, M, K, B, dt):
+    """The MFMA path takes rows in chunks of 2 KiB, two chunks per loop trip:
+    an odd chunk count (11, 3, 1), a ragged last chunk and a row far shorter
+    than a chunk."""
+    say(f"gemv mfma {M}x{K} B={B} dtype {dt}, 4 KiB pages")
+    run_gemv(ctx, orc, M, K, B, dt, dt, 12, seed=M + K + B)
+
+
 @pytest.mark.parametrize("M,K,B", [(4096, 11008, 1), (11008, 4096, 8)])
 def test_gemv_config3_full_size(ctx, orc, M, K, B):
     say(f"gemv bf16 {M}x{K} B={B}, 2 MiB pages, colours 0..47 of 64")
