@@ -48,7 +48,7 @@ def parse():
     ap.add_argument("--gemv-launches", type=int, default=300)
     ap.add_argument("--corun-launches", type=int, default=2000)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--cpu-passes", type=int, default=3)
+    ap.add_argument("--cpu-passes", type=int, default=8)
     return ap.parse_args()
 
 
