@@ -1,15 +1,16 @@
 // Batched XOR-hash colouring and the ordered page-table build.
 //
 // Colour bit k of an address is the parity of (address & M_k).  The
-// classify kernel streams 8-byte addresses through buffer loads, each
-// wavefront instruction reading 1 KiB of consecutive addresses and each
-// lane keeping 32 such loads (64 addresses) in flight per tile, and writes
-// one colour byte per address: every wavefront passes its 4096 colour bytes
-// of a tile through its own 4 KiB of LDS so that each lane stores 16
-// consecutive colours per 16-byte store.  Tiles cover the largest multiple
-// of 16 addresses, through buffer ranges that end there (so the tile body
-// has no branch around its memory accesses); the last n mod 16 addresses
-// are coloured by the grid's last workgroup.
+// classify kernel hands out tiles to single wavefronts.  A wavefront
+// streams its tile's 8-byte addresses through buffer loads, each
+// instruction reading 1 KiB of consecutive addresses and each lane keeping
+// 16 such loads (32 addresses) in flight, colours them by table lookups
+// (the hash is linear over GF(2)), and writes one colour byte per address:
+// it passes its tile's 2048 colour bytes through its own 2 KiB of LDS so
+// that each lane stores 16 consecutive colours per 16-byte store.  Tiles
+// cover the largest multiple of 16 addresses, through buffer ranges that end
+// there (so the tile body has no branch around its memory accesses); the
+// last n mod 16 addresses are coloured by the grid's last workgroup.
 //
 // The page-table build is an ordered stream compaction over the pool's page
 // addresses: a counting pass, a scan of per-workgroup counts, and an
@@ -45,14 +46,33 @@ __device__ __forceinline__ uint32_t colour_of(uint32_t lo, uint32_t hi, const Ha
     return c;
 }
 
+// The hash is linear over GF(2): colour(a ^ b) = colour(a) ^ colour(b).  So
+// the colour of an address is the XOR of the colours of its six bytes in
+// place, colour(byte_t << 8t), each read from a 256-entry table.  One copy
+// of a table spans 64 LDS dwords (one per bank on gfx950), so a wavefront's
+// lookups into it never meet on a bank with different addresses.  Six
+// lookups and eleven integer ops replace the popcount form's 6 K.
+constexpr int kLutBytes = 6;  // address bits 0..47
+
+__device__ __forceinline__ uint32_t colour_lut(const uint8_t (*lut)[256], uint32_t lo, uint32_t hi)
+{
+    return (uint32_t)lut[0][lo & 0xffu] ^ (uint32_t)lut[1][(lo >> 8) & 0xffu] ^
+           (uint32_t)lut[2][(lo >> 16) & 0xffu] ^ (uint32_t)lut[3][lo >> 24] ^
+           (uint32_t)lut[4][hi & 0xffu] ^ (uint32_t)lut[5][(hi >> 8) & 0xffu];
+}
+
 constexpr int kClsThreads = 256;
-constexpr int kClsLoads = 32;                            // 16-byte loads per lane per tile
-constexpr uint32_t kClsWaveTile = 64u * 2u * kClsLoads;  // 4096 addresses per wavefront
-constexpr uint64_t kClsTile = (uint64_t)kClsThreads / 64u * kClsWaveTile;  // 16384
-// Workgroups per CU: one deep workgroup streams fastest; with the histogram
-// a second one overlaps its LDS atomics with the first one's loads.
+constexpr int kClsLoads = 16;                            // 16-byte loads per lane per tile
+constexpr uint32_t kClsWaveTile = 64u * 2u * kClsLoads;  // 2048 addresses per wavefront
+constexpr uint32_t kClsWaves = kClsThreads / 64;
+// Each wavefront takes its own tiles of kClsWaveTile addresses (32,768
+// tickets for 2^26 addresses), so the work queues serve runs of 8 CUs: one
+// device-wide counter serialises its atomics at about 12 ns each.
+constexpr int kClsGroupCus = 8;
+// Workgroups per CU: one, with or without the histogram (two or more, or
+// 32 or 8 loads per lane, measured slower on MI355X).
 constexpr int kClsWgsPerCu = 1;
-constexpr int kClsHistWgsPerCu = 2;
+constexpr int kClsHistWgsPerCu = 1;
 
 // Histogram bins are replicated 16 times in LDS (copy = lane % 16) so that
 // the LDS atomics of one wavefront rarely meet on one address.
@@ -69,6 +89,7 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
     __shared__ uint32_t s_hist[HIST ? kBins * kHistCopies : 1];
     // per wavefront: the colour bytes of one tile, 2 per lane and load
     __shared__ __attribute__((aligned(16))) uint16_t s_col[kClsThreads / 64][kClsWaveTile / 2];
+    __shared__ __attribute__((aligned(16))) uint8_t s_lut[kLutBytes][256];
     const uint32_t lane = threadIdx.x & 63u;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const uint32_t copy = lane % kHistCopies;
@@ -79,9 +100,9 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
         __syncthreads();
     }
     auto body = [&](uint32_t t, uint32_t, uint32_t &, auto &&claim) {
-        // first address of this wavefront's part of the tile, and how many
-        // of its addresses lie below n16 (a multiple of 16, possibly 0)
-        const uint64_t base = (uint64_t)t * kClsTile + (uint64_t)wave * kClsWaveTile;
+        // a tile is one wavefront's: its first address, and how many of its
+        // addresses lie below n16 (a multiple of 16, possibly 0)
+        const uint64_t base = (uint64_t)t * kClsWaveTile;
         const uint32_t valid =
             n16 > base ? (uint32_t)(n16 - base < kClsWaveTile ? n16 - base : kClsWaveTile) : 0u;
         const Rsrc ra = make_rsrc(addrs + base, valid * 8u);
@@ -92,8 +113,8 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
         claim();
 #pragma unroll
         for (int j = 0; j < kClsLoads; ++j) {
-            const uint32_t c0 = colour_of<K>(v[j].x, v[j].y, h);
-            const uint32_t c1 = colour_of<K>(v[j].z, v[j].w, h);
+            const uint32_t c0 = colour_lut(s_lut, v[j].x, v[j].y);
+            const uint32_t c1 = colour_lut(s_lut, v[j].z, v[j].w);
             s_col[wave][j * 64u + lane] = (uint16_t)(c0 | (c1 << 8));
             // both addresses of the load are valid or neither (valid is even)
             if (HIST && 2u * (j * 64u + lane) < valid) {
@@ -154,7 +175,18 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
             }
         }
     };
-    gated_tile_loop<Claim::Mid>(g, n_tiles, NoOp(), body, flush, epilogue);
+    // the byte tables, visible to the whole workgroup after the loop's
+    // opening barrier
+    auto prologue = [&]() {
+#pragma unroll
+        for (int r = 0; r < kLutBytes * 256 / kClsThreads; ++r) {
+            const uint32_t i = (uint32_t)r * kClsThreads + threadIdx.x;
+            const uint32_t t = i >> 8, e = i & 0xffu;
+            const uint64_t a = (uint64_t)e << (8u * t);
+            s_lut[t][e] = (uint8_t)colour_of<K>((uint32_t)a, (uint32_t)(a >> 32), h);
+        }
+    };
+    gated_wave_loop(g, n_tiles, prologue, body, flush, epilogue);
 }
 
 constexpr int kPtThreads = 256;
@@ -256,24 +288,26 @@ template <int K>
 static int launch_classify(Ctx *c, const HashArgs &h, const uint64_t *d_addrs, uint64_t n,
                            uint8_t *d_colours, uint64_t *d_hist, void *stream)
 {
-    const uint64_t n_tiles = ((n & ~15ull) + kClsTile - 1) / kClsTile;
+    const uint64_t n_tiles = ((n & ~15ull) + kClsWaveTile - 1) / kClsWaveTile;
     if (n_tiles >= (1ull << 31))
         return set_error(SGDRC_EINVAL, "n too large");
+    // grid sizing counts workgroups' worth of tiles
+    const uint64_t wg_tiles = (n_tiles + kClsWaves - 1) / kClsWaves;
     Gate g;
     LaunchInfo li;
-    int rc = make_gate(c, stream, n_tiles, kStreamGroupCus, &g, &li);
+    int rc = make_gate(c, stream, n_tiles, kClsGroupCus, &g, &li);
     if (rc)
         return rc;
     uint64_t *acc = c->d_hist_acc + (size_t)(g.q - c->d_queues) * kHistBins;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (d_hist) {
         static const int occ = occupancy(k_classify<K, true>, kClsThreads);
-        uint32_t grid = gated_grid(c, std::min(occ, kClsHistWgsPerCu), n_tiles, li);
+        uint32_t grid = gated_grid(c, std::min(occ, kClsHistWgsPerCu), wg_tiles, li);
         hipLaunchKernelGGL((k_classify<K, true>), dim3(grid), dim3(kClsThreads), 0, s, d_addrs, n,
                            d_colours, h, acc, d_hist, (uint32_t)n_tiles, g);
     } else {
         static const int occ = occupancy(k_classify<K, false>, kClsThreads);
-        uint32_t grid = gated_grid(c, std::min(occ, kClsWgsPerCu), n_tiles, li);
+        uint32_t grid = gated_grid(c, std::min(occ, kClsWgsPerCu), wg_tiles, li);
         hipLaunchKernelGGL((k_classify<K, false>), dim3(grid), dim3(kClsThreads), 0, s, d_addrs,
                            n, d_colours, h, acc, d_hist, (uint32_t)n_tiles, g);
     }

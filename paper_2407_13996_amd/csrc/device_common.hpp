@@ -355,6 +355,151 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
         raise_flag(g.err, err);
 }
 
+// Wavefront-granular form of gated_tile_loop, for bodies whose work is
+// private to one wavefront (they share no LDS between the waves of a
+// workgroup and contain no barrier).  Each wavefront takes its own tickets
+// (lane 0 runs the atomic, the value reaches the other lanes by
+// readfirstlane), so the loop holds no barrier: the waves of a workgroup
+// drift apart and keep loads in flight while a neighbour finishes a tile,
+// instead of draining the memory pipe together at every tile.  ``claim`` has
+// the Claim::Mid meaning.  Gate, queue groups, stealing, ``flush`` (per
+// workgroup, after all of its waves leave the loop), the last workgroup's
+// leftover ranges (spread over its waves) and ``epilogue`` are as in
+// gated_tile_loop.
+__device__ __forceinline__ void log_tile_wave(const Gate &g, uint32_t cu, uint32_t tile)
+{
+    if ((threadIdx.x & 63u) == 0u) {
+        if (g.log_cu && cu < (uint32_t)kMaxCus)
+            __hip_atomic_fetch_add(&g.log_cu[cu], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (g.log_tile && tile < g.log_cap)
+            __hip_atomic_fetch_add(&g.log_tile[tile], 1u, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+template <typename Prologue, typename Body, typename Flush, typename Epilogue>
+__device__ __forceinline__ void gated_wave_loop(const Gate &g, uint32_t n_tiles, Prologue prologue,
+                                                Body body, Flush flush, Epilogue epilogue)
+{
+    __shared__ uint32_t s_flag;
+    __shared__ uint32_t s_left_lo[kMaxGroups], s_left_hi[kMaxGroups];
+    __shared__ uint32_t s_grp_tile[kMaxGroups + 1];
+    uint32_t xcc;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+    const uint32_t lut_entry = my_cu_entry(g);
+    {
+        const uint32_t i = threadIdx.x < (uint32_t)kMaxGroups ? threadIdx.x : (uint32_t)kMaxGroups;
+        s_grp_tile[i] = g.grp_tile[i];
+    }
+    prologue();
+    const bool xcd_on = ((g.xcc_allowed >> (xcc & 0xFu)) & 1u) != 0u;
+    const uint32_t entry = xcd_on ? lut_entry : kLutNone;
+    if (g.tlog && blockIdx.x == 0 && threadIdx.x == 0)
+        __hip_atomic_store(&g.tlog[0], __builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    uint32_t err = 0u;
+    const uint32_t cu = entry & 0xFFFFu;
+    const uint32_t lane = threadIdx.x & 63u;
+    if (entry != kLutNone && cu_allowed(g, cu)) {
+        uint32_t grp = g.grp_base[(entry >> 16) & 0xFFu] + ((entry >> 24) >> g.grp_shift);
+        uint32_t lo = s_grp_tile[grp], hi = s_grp_tile[grp + 1u];
+        // ``next`` holds the ticket in lane 0; written only by the atomic
+        // (see gated_tile_loop)
+        uint32_t next = 0u;
+        if (lane == 0u)
+            next = __hip_atomic_fetch_add(&g.q->grp_next[grp * kCounterStride], 1u,
+                                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        uint32_t k = __builtin_amdgcn_readfirstlane(next);
+        for (;;) {
+            if (k < hi - lo) {
+                uint32_t *const ctr = &g.q->grp_next[grp * kCounterStride];
+                auto claim = [&]() {
+                    if (lane == 0u)
+                        next = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT);
+                };
+                log_tile_wave(g, cu, lo + k);
+                body(lo + k, cu, err, claim);
+                k = __builtin_amdgcn_readfirstlane(next);
+            } else {
+                // steal: the next group in ring order that still has tiles
+                bool rem = false;
+                if (lane < g.n_groups) {
+                    const uint32_t size = s_grp_tile[lane + 1u] - s_grp_tile[lane];
+                    const uint32_t taken =
+                        size ? __hip_atomic_load(&g.q->grp_next[lane * kCounterStride],
+                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                             : 0u;
+                    rem = taken < size;
+                }
+                const uint64_t bits = __ballot(rem);
+                if (bits == 0ull)
+                    break;
+                const uint32_t sh = (grp + 1u) & 63u;
+                const uint64_t rot = sh ? ((bits >> sh) | (bits << (64u - sh))) : bits;
+                grp = __builtin_amdgcn_readfirstlane((sh + (uint32_t)__builtin_ctzll(rot)) & 63u);
+                lo = s_grp_tile[grp];
+                hi = s_grp_tile[grp + 1u];
+                if (lane == 0u)
+                    next = __hip_atomic_fetch_add(&g.q->grp_next[grp * kCounterStride], 1u,
+                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                k = __builtin_amdgcn_readfirstlane(next);
+            }
+        }
+        flush();
+    }
+    if (arrive_last(g, &s_flag)) {
+        bool left = false;
+        if (threadIdx.x < (uint32_t)kMaxGroups) {
+            uint32_t a = 0u, b = 0u;
+            if (threadIdx.x < g.n_groups) {
+                const uint32_t lo = g.grp_tile[threadIdx.x], hi = g.grp_tile[threadIdx.x + 1u];
+                const uint32_t taken = __hip_atomic_load(&g.q->grp_next[threadIdx.x * kCounterStride],
+                                                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                a = taken < hi - lo ? lo + taken : hi;
+                b = hi;
+            }
+            s_left_lo[threadIdx.x] = a;
+            s_left_hi[threadIdx.x] = b;
+            left = a < b;
+        }
+        if (__syncthreads_or(left ? 1 : 0)) {
+            // wave w takes tiles lo + w, lo + w + waves, ... of each range
+            const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+            const uint32_t waves = blockDim.x >> 6;
+            uint32_t c = 0u;
+            uint32_t t = __builtin_amdgcn_readfirstlane(s_left_lo[0]) + wave;
+            uint32_t end = __builtin_amdgcn_readfirstlane(s_left_hi[0]);
+            while (c < (uint32_t)kMaxGroups) {
+                if (t < end) {
+                    log_tile_wave(g, cu, t);
+                    body(t, cu, err, NoOp());
+                    t += waves;
+                } else {
+                    c += 1u;
+                    const uint32_t cc = c < (uint32_t)kMaxGroups ? c : 0u;
+                    t = __builtin_amdgcn_readfirstlane(s_left_lo[cc]) + wave;
+                    end = c < (uint32_t)kMaxGroups ? __builtin_amdgcn_readfirstlane(s_left_hi[cc]) : 0u;
+                }
+            }
+            flush();
+            err |= threadIdx.x == 0 ? kDevFlagGateFallback : 0u;
+        }
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        epilogue();
+        reset_slot(g.q);
+        if (g.tlog && threadIdx.x == 0) {
+            __builtin_amdgcn_s_waitcnt(0);
+            __hip_atomic_store(&g.tlog[1], __builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+    if (err != 0u)
+        raise_flag(g.err, err);
+}
+
 // Page-table lookup with the range check every kernel applies: an entry
 // outside the pool yields kBadPage and sets kDevErrPtRange in ``err``.
 __device__ __forceinline__ uint32_t checked_page(const uint32_t *pt, uint64_t j,

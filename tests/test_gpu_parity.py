@@ -548,6 +548,43 @@ def test_cu_mask_confines_work_and_visits_each_tile_once(ctx, orc):
         assert (out.view(np.uint32) == ref.view(np.uint32)).all()
 
 
+def test_classify_wavefront_tiles_under_cu_masks(ctx, orc):
+    """Classify hands its tiles (2048 addresses) to single wavefronts: under
+    every mask each tile is taken once, only allowed CUs work, and colours
+    and histogram equal the oracle's."""
+    n_cu = ctx.num_cus
+    n = (1 << 20) + 37
+    masks = synth.xor_masks(6, seed=5, min_bit=12)
+    addrs = synth.page_addresses(n, seed=6)
+    ref, ref_hist = orc.classify(addrs, masks)
+    d_addrs = to_dev(addrs)
+    stream = torch.cuda.current_stream()
+    tiles_expected = (n & ~15) // 2048 + (1 if (n & ~15) % 2048 else 0)
+    for cus in [list(range(64)), synth.random_cu_subset(n_cu, 20, seed=8), [5], [n_cu - 1],
+                list(range(n_cu))]:
+        say(f"classify under a mask of {len(cus)} CUs")
+        d_col = torch.full((n + 16,), 0xEE, dtype=torch.uint8, device=DEV)
+        d_hist = torch.zeros(64, dtype=torch.int64, device=DEV)
+        cu_log = torch.zeros(n_cu, dtype=torch.int32, device=DEV)
+        tile_log = torch.zeros(4096, dtype=torch.int32, device=DEV)
+        ctx.set_worklog(cu_log, tile_log)
+        sg.set_cu_mask(ctx, stream, cus)
+        sg.colour_classify(ctx, masks, d_addrs, d_col, d_hist, stream)
+        tiles = ctx.last_tiles(stream)
+        ctx.set_worklog(None, None)
+        sg.set_cu_mask(ctx, stream, None)
+        cl, tl = to_host(cu_log), to_host(tile_log)
+        assert tiles == tiles_expected
+        assert (tl[:tiles] == 1).all() and (tl[tiles:] == 0).all()
+        assert set(np.nonzero(cl)[0].tolist()) <= set(cus)
+        assert cl.sum() == tiles
+        got = to_host(d_col)
+        assert (got[:n] == ref).all() and (got[n:] == 0xEE).all()
+        assert (to_host(d_hist).astype(np.uint64) == ref_hist).all()
+    # the gate's fallback (no workgroup resident on an allowed CU) is legal
+    assert ctx.device_error() & ~sg.DEVFLAG_GATE_FALLBACK == 0
+
+
 def test_out_of_range_page_entry_is_flagged_not_accessed(ctx):
     shift = 16
     pages = 8
