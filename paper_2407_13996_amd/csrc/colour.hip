@@ -48,10 +48,10 @@ __device__ __forceinline__ uint32_t colour_of(uint32_t lo, uint32_t hi, const Ha
 
 // The hash is linear over GF(2): colour(a ^ b) = colour(a) ^ colour(b).  So
 // the colour of an address is the XOR of the colours of its six bytes in
-// place, colour(byte_t << 8t), each read from a 256-entry table.  One copy
-// of a table spans 64 LDS dwords (one per bank on gfx950), so a wavefront's
-// lookups into it never meet on a bank with different addresses.  Six
-// lookups and eleven integer ops replace the popcount form's 6 K.
+// place, colour(byte_t << 8t), each read from a 256-entry table.  A table
+// is 64 LDS dwords, so a wavefront's lookups into one table conflict at most
+// two ways on a bank (none with 64 banks), without replicated copies.  Six
+// lookups and about ten integer ops replace the popcount form's 6 K.
 constexpr int kLutBytes = 6;  // address bits 0..47
 
 __device__ __forceinline__ uint32_t colour_lut(const uint8_t (*lut)[256], uint32_t lo, uint32_t hi)
