@@ -59,6 +59,8 @@ extern "C" {
 
 /* device error flags (bitwise OR, sticky until read) */
 #define SGDRC_DEVERR_PT_RANGE 1u
+#define SGDRC_DEVFLAG_GATE_FALLBACK 2u     /* no workgroup reached an allowed CU; the last did the tiles */
+#define SGDRC_DEVERR_SUSPENDED_DROPPED 4u  /* a suspended launch was discarded unresumed */
 
 /* element encodings */
 enum { SGDRC_F32 = 0, SGDRC_BF16 = 1, SGDRC_F16 = 2 };
@@ -165,6 +167,56 @@ int sgdrc_set_stream_occupancy(sgdrc_ctx *ctx, void *stream, uint32_t max_wgs_pe
  * next launch, never recreates the stream.  EINVAL: empty mask or a bit at
  * or above sgdrc_num_cus(). */
 int set_cu_mask(sgdrc_ctx *ctx, void *stream, const sgdrc_cu_mask *mask);
+
+/* Preemptible best-effort launches (paper section 7.1: a latency-sensitive
+ * task preempts the compute units of a best-effort kernel by writing an
+ * eviction flag that the persistent kernel polls; the kernel then restarts
+ * on fewer units).  With a flag set, later colored_stream and
+ * bimodal_relayout launches on ``stream`` are preemptible: each workgroup
+ * reads *d_flag with every tile it claims and, once it reads non-zero,
+ * finishes the tile it holds and leaves.  If tiles remain unclaimed, the
+ * launch ends "suspended": the rest of the work, including the last n mod
+ * 16 bytes, waits for sgdrc_resume.  Every tile is processed exactly once
+ * over a launch and its resumptions, so the result equals an uninterrupted
+ * launch.  d_flag: device memory, 4-byte aligned, owned by the caller, who
+ * writes it (from the host or from a kernel on another stream) and keeps it
+ * alive while such launches may run; a launch started with the flag set
+ * does no work.  Preemptible launches use a second work queue of their
+ * own; a fresh preemptible launch on a stream whose last one is still
+ * suspended first discards that one (and raises SGDRC_DEVERR_SUSPENDED_DROPPED).
+ * d_flag == NULL makes later launches non-preemptible (a suspended launch
+ * can still be resumed).  Host-only.  EINVAL: misaligned flag, or no work
+ * queue left (64 per context, shared with the streams). */
+int sgdrc_set_eviction_flag(sgdrc_ctx *ctx, void *stream, const uint32_t *d_flag);
+
+/* Enqueues on ``stream`` the continuation of the stream's last preemptible
+ * launch, under the stream's current CU mask and eviction flag, with the
+ * same arguments (the caller keeps their buffers alive).  If that launch
+ * (with its earlier resumptions) has completed, the enqueued kernel does
+ * nothing; a resumption can itself be evicted and resumed again.
+ * Asynchronous.  EINVAL: no preemptible launch on the stream, or the mask
+ * allows no CU. */
+int sgdrc_resume(sgdrc_ctx *ctx, void *stream);
+
+/* Waits for ``stream``, then sets *tiles_left to the number of tiles that
+ * the stream's last preemptible launch still has to process: 0 when it has
+ * completed, otherwise it is suspended.  EINVAL: no preemptible launch on
+ * the stream, NULL tiles_left. */
+int sgdrc_suspended(sgdrc_ctx *ctx, void *stream, uint64_t *tiles_left);
+
+/* Sliding-window CU reservation (paper section 7.1): the CUs reserved for
+ * the latency-sensitive side are the most that any of the next ``window``
+ * queued latency-sensitive kernels needs (ls_cus[i] = CUs that kernel i,
+ * in queue order, needs for its best latency; found offline), rounded up
+ * to a multiple of ``granule`` CUs (32 = whole XCDs, each with its own L2)
+ * and capped at num_cus.  *ls_mask receives the first R logical CUs and
+ * *be_mask the others (empty when R = num_cus: the best-effort side is
+ * then to be evicted, not masked).  n_queued == 0 gives R = 0.  Pure host
+ * computation, no context.  EINVAL: num_cus outside 1..256, window or
+ * granule 0, an ls_cus entry above num_cus, NULL pointers. */
+int sgdrc_tidal_masks(uint32_t num_cus, const uint32_t *ls_cus, uint32_t n_queued,
+                      uint32_t window, uint32_t granule, sgdrc_cu_mask *ls_mask,
+                      sgdrc_cu_mask *be_mask);
 
 /* Batched colouring (paper section 6, SPT step 1, marking each page's
  * colour; the hash is the linear XOR form discussed in section 3.2).

@@ -21,6 +21,7 @@ OK, EINVAL, ENOMEM, ENODEV, EHIP = 0, -22, -12, -19, -5
 F32, BF16, F16 = 0, 1, 2
 DEVERR_PT_RANGE = 1
 DEVFLAG_GATE_FALLBACK = 2
+DEVERR_SUSPENDED_DROPPED = 4
 MAX_MASKS = 8
 
 
@@ -75,6 +76,10 @@ def lib() -> ctypes.CDLL:
             "sgdrc_wallclock_khz": ([vp, P(u32)], i32),
             "set_cu_mask": ([vp, vp, P(CuMask)], i32),
             "sgdrc_set_stream_occupancy": ([vp, vp, u32], i32),
+            "sgdrc_set_eviction_flag": ([vp, vp, vp], i32),
+            "sgdrc_resume": ([vp, vp], i32),
+            "sgdrc_suspended": ([vp, vp, P(u64)], i32),
+            "sgdrc_tidal_masks": ([u32, P(u32), u32, u32, u32, P(CuMask), P(CuMask)], i32),
             "colour_classify": ([vp, P(Hash), vp, u64, vp, vp, vp], i32),
             "colour_alloc_pagetable": ([vp, P(Hash), u64, u32, u64, P(ColourSet), u64, vp,
                                         P(u64), vp], i32),
@@ -218,6 +223,40 @@ def set_cu_mask(ctx, stream, cus) -> None:
 def set_stream_occupancy(ctx, stream, max_wgs_per_cu: int) -> None:
     """Cap the workgroups per CU of later launches on ``stream`` (0 = no cap)."""
     _check(lib().sgdrc_set_stream_occupancy(_h(ctx), _stream(stream), int(max_wgs_per_cu)))
+
+
+def set_eviction_flag(ctx, stream, flag) -> None:
+    """Make later colored_stream / bimodal_relayout launches on ``stream``
+    preemptible by the device word ``flag`` (an int32 CUDA tensor of at
+    least one element, or a raw address); None switches it off."""
+    _check(lib().sgdrc_set_eviction_flag(_h(ctx), _stream(stream), _addr(flag)))
+
+
+def resume(ctx, stream=None) -> None:
+    """Enqueue the continuation of the stream's last preemptible launch."""
+    _check(lib().sgdrc_resume(_h(ctx), _stream(stream)))
+
+
+def suspended(ctx, stream=None) -> int:
+    """Wait for ``stream``; tiles its last preemptible launch has left (0 = done)."""
+    t = ctypes.c_uint64()
+    _check(lib().sgdrc_suspended(_h(ctx), _stream(stream), ctypes.byref(t)))
+    return t.value
+
+
+def _cus_of(m: CuMask, n: int) -> list:
+    return [i for i in range(n) if (m.bits[i >> 6] >> (i & 63)) & 1]
+
+
+def tidal_masks(num_cus: int, ls_cus, window: int, granule: int = 1):
+    """Sliding-window CU reservation: (LS CUs, BE CUs) as lists of logical CUs
+    for the queued latency-sensitive kernels' CU needs ``ls_cus``."""
+    q = [int(x) for x in ls_cus]
+    arr = (ctypes.c_uint32 * max(len(q), 1))(*q)
+    ls, be = CuMask(), CuMask()
+    _check(lib().sgdrc_tidal_masks(int(num_cus), arr, len(q), int(window), int(granule),
+                                   ctypes.byref(ls), ctypes.byref(be)))
+    return _cus_of(ls, num_cus), _cus_of(be, num_cus)
 
 
 def colour_classify(ctx, masks, addrs, colours, hist=None, stream=None) -> None:

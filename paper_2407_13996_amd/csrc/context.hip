@@ -1,5 +1,6 @@
 // Context management, CU-topology probe, per-stream CU masks and errors.
 #include <algorithm>
+#include <cstddef>
 #include <cstdio>
 #include <cstring>
 #include <new>
@@ -70,16 +71,39 @@ int stream_state(Ctx *c, void *stream, StreamState **out)
     return SGDRC_OK;
 }
 
-int make_gate(Ctx *c, void *stream, uint64_t n_tiles, int group_cus, Gate *g, LaunchInfo *li)
+// Physical XCC ids whose XCD has CUs allowed by ``m``.
+static uint32_t xcc_allowed(const Ctx *c, const sgdrc_cu_mask &m)
+{
+    uint32_t bits = 0;
+    for (int x = 0; x < c->n_xcds; ++x) {
+        bool any = false;
+        for (int cu = c->xcd_first_cu[x]; cu < c->xcd_first_cu[x + 1] && !any; ++cu)
+            any = (m.bits[cu >> 6] >> (cu & 63)) & 1ull;
+        if (any)
+            bits |= 1u << ((c->keys[c->xcd_first_cu[x]] >> 8) & 0xFu);
+    }
+    return bits;
+}
+
+int make_gate(Ctx *c, void *stream, uint64_t n_tiles, int group_cus, Gate *g, LaunchInfo *li,
+              bool preemptible)
 {
     StreamState *st = nullptr;
     int rc = stream_state(c, stream, &st);
     if (rc)
         return rc;
     std::lock_guard<std::mutex> lock(c->mu);
+    if (preemptible && st->slot_ev < 0)
+        return set_error(SGDRC_EINVAL, "stream has no preemptible queue");
     std::memcpy(g->mask, st->mask.bits, sizeof g->mask);
     g->lut = c->d_lut;
-    g->q = c->d_queues + st->slot;
+    g->q = c->d_queues + (preemptible ? st->slot_ev : st->slot);
+    g->evict = nullptr;
+    g->resume = 0;
+    if (preemptible)
+        g->evict = st->evict ? st->evict
+                             : reinterpret_cast<const uint32_t *>(
+                                   reinterpret_cast<const char *>(g->q) + offsetof(QueueSlot, zero));
     g->err = c->d_err;
     g->log_cu = c->log_cu;
     g->log_tile = c->log_tile;
@@ -128,19 +152,63 @@ int make_gate(Ctx *c, void *stream, uint64_t n_tiles, int group_cus, Gate *g, La
         return set_error(SGDRC_EINVAL, "the stream's CU mask allows no CU of this device");
     g->n_groups = (uint32_t)n_groups;
     g->grp_shift = shift;
-    // physical XCC ids whose XCD has allowed CUs
-    g->xcc_allowed = 0;
-    for (int x = 0; x < c->n_xcds; ++x) {
-        bool any = false;
-        for (int cu = c->xcd_first_cu[x]; cu < c->xcd_first_cu[x + 1] && !any; ++cu)
-            any = (st->mask.bits[cu >> 6] >> (cu & 63)) & 1ull;
-        if (any)
-            g->xcc_allowed |= 1u << ((c->keys[c->xcd_first_cu[x]] >> 8) & 0xFu);
-    }
+    g->xcc_allowed = xcc_allowed(c, st->mask);
     st->last_tiles = n_tiles;
     li->allowed = (int)total;
     li->wg_cap = st->wg_cap;
     return SGDRC_OK;
+}
+
+// One workgroup: if the slot holds a suspended launch, drop it (zero its
+// group counters and state) and raise kDevErrSuspendedDropped.  The
+// arrival counters are already zero (the suspended launch reset them).
+__global__ __launch_bounds__(64) void k_slot_discard(QueueSlot *q, uint32_t *err)
+{
+    const uint32_t st = __hip_atomic_load(&q->state[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (st != kSlotSuspended)
+        return;
+    __hip_atomic_store(&q->grp_next[threadIdx.x * kCounterStride], 0u, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x == 0) {
+        __hip_atomic_store(&q->stopped[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&q->state[0], kSlotIdle, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        raise_flag(err, kDevErrSuspendedDropped);
+    }
+}
+
+int discard_suspended(Ctx *c, void *stream)
+{
+    int slot;
+    {
+        std::lock_guard<std::mutex> lock(c->mu);
+        auto it = c->streams.find(stream);
+        if (it == c->streams.end() || it->second.slot_ev < 0)
+            return set_error(SGDRC_EINVAL, "stream has no preemptible queue");
+        slot = it->second.slot_ev;
+    }
+    static_assert(kMaxGroups == 64, "one thread per queue group");
+    hipLaunchKernelGGL(k_slot_discard, dim3(1), dim3(64), 0, reinterpret_cast<hipStream_t>(stream),
+                       c->d_queues + slot, c->d_err);
+    SGDRC_HIP(hipGetLastError());
+    return SGDRC_OK;
+}
+
+bool stream_preemptible(Ctx *c, void *stream)
+{
+    std::lock_guard<std::mutex> lock(c->mu);
+    auto it = c->streams.find(stream);
+    return it != c->streams.end() && it->second.ev_on;
+}
+
+void record_preemptible(Ctx *c, void *stream, const Gate &g, uint64_t n_tiles, int per_cu,
+                        Relaunch fn)
+{
+    std::lock_guard<std::mutex> lock(c->mu);
+    StreamState &st = c->streams[stream];
+    st.ev_gate = g;
+    st.ev_tiles = n_tiles;
+    st.ev_per_cu = per_cu;
+    st.ev_relaunch = std::move(fn);
 }
 
 uint32_t gated_grid(const Ctx *c, int blocks_per_cu, uint64_t n_tiles, const LaunchInfo &li)
@@ -490,6 +558,152 @@ int set_cu_mask(sgdrc_ctx *ctx, void *stream, const sgdrc_cu_mask *mask)
         return rc;
     std::lock_guard<std::mutex> lock(c->mu);
     st->mask = mask ? *mask : c->all_cus;
+    return SGDRC_OK;
+}
+
+int sgdrc_set_eviction_flag(sgdrc_ctx *ctx, void *stream, const uint32_t *d_flag)
+{
+    clear_error();
+    if (reinterpret_cast<uintptr_t>(d_flag) & 3u)
+        return set_error(SGDRC_EINVAL, "eviction flag not 4-byte aligned");
+    Ctx *c = nullptr;
+    int rc = check_ctx(ctx, &c);
+    if (rc)
+        return rc;
+    StreamState *st = nullptr;
+    rc = stream_state(c, stream, &st);
+    if (rc)
+        return rc;
+    std::lock_guard<std::mutex> lock(c->mu);
+    if (d_flag && st->slot_ev < 0) {
+        if (c->next_slot >= kMaxStreams)
+            return set_error(SGDRC_EINVAL, "more than %d work queues used with one context",
+                             kMaxStreams);
+        st->slot_ev = c->next_slot++;
+    }
+    st->ev_on = d_flag != nullptr;
+    st->evict = d_flag;
+    return SGDRC_OK;
+}
+
+int sgdrc_resume(sgdrc_ctx *ctx, void *stream)
+{
+    clear_error();
+    Ctx *c = nullptr;
+    int rc = check_ctx(ctx, &c);
+    if (rc)
+        return rc;
+    StreamState *st = nullptr;
+    rc = stream_state(c, stream, &st);
+    if (rc)
+        return rc;
+    Relaunch fn;
+    Gate g;
+    LaunchInfo li;
+    uint64_t tiles = 0;
+    int per_cu = 1;
+    {
+        std::lock_guard<std::mutex> lock(c->mu);
+        if (!st->ev_relaunch)
+            return set_error(SGDRC_EINVAL, "no preemptible launch on this stream to resume");
+        const int allowed = popcount_mask(st->mask);
+        if (allowed == 0)
+            return set_error(SGDRC_EINVAL, "the stream's CU mask allows no CU of this device");
+        // the suspended launch's tile ranges and group layout, the current
+        // mask, flag and logs
+        g = st->ev_gate;
+        std::memcpy(g.mask, st->mask.bits, sizeof g.mask);
+        g.xcc_allowed = xcc_allowed(c, st->mask);
+        g.q = c->d_queues + st->slot_ev;
+        g.evict = st->evict ? st->evict
+                            : reinterpret_cast<const uint32_t *>(
+                                  reinterpret_cast<const char *>(g.q) + offsetof(QueueSlot, zero));
+        g.resume = 1;
+        g.log_cu = c->log_cu;
+        g.log_tile = c->log_tile;
+        g.log_cap = c->log_cap;
+        g.tlog = nullptr;
+        if (st->tlog) {
+            g.tlog = st->tlog + 2u * (st->tlog_next % st->tlog_slots);
+            ++st->tlog_next;
+        }
+        tiles = st->ev_tiles;
+        per_cu = st->ev_per_cu;
+        st->last_tiles = tiles;
+        li.allowed = allowed;
+        li.wg_cap = st->wg_cap;
+        fn = st->ev_relaunch;
+    }
+    SGDRC_HIP(fn(g, gated_grid(c, per_cu, tiles, li)));
+    return SGDRC_OK;
+}
+
+int sgdrc_suspended(sgdrc_ctx *ctx, void *stream, uint64_t *tiles_left)
+{
+    clear_error();
+    if (!tiles_left)
+        return set_error(SGDRC_EINVAL, "tiles_left is NULL");
+    Ctx *c = nullptr;
+    int rc = check_ctx(ctx, &c);
+    if (rc)
+        return rc;
+    StreamState *st = nullptr;
+    rc = stream_state(c, stream, &st);
+    if (rc)
+        return rc;
+    int slot;
+    Gate g;
+    {
+        std::lock_guard<std::mutex> lock(c->mu);
+        if (!st->ev_relaunch)
+            return set_error(SGDRC_EINVAL, "no preemptible launch on this stream");
+        slot = st->slot_ev;
+        g = st->ev_gate;
+    }
+    SGDRC_HIP(hipStreamSynchronize(reinterpret_cast<hipStream_t>(stream)));
+    QueueSlot q;
+    SGDRC_HIP(hipMemcpy(&q, c->d_queues + slot, sizeof q, hipMemcpyDeviceToHost));
+    uint64_t left = 0;
+    if (q.state[0] == kSlotSuspended) {
+        for (uint32_t i = 0; i < g.n_groups; ++i) {
+            const uint32_t size = g.grp_tile[i + 1] - g.grp_tile[i];
+            const uint32_t taken = q.grp_next[i * kCounterStride];
+            left += taken < size ? size - taken : 0u;
+        }
+    }
+    *tiles_left = left;
+    return SGDRC_OK;
+}
+
+int sgdrc_tidal_masks(uint32_t num_cus, const uint32_t *ls_cus, uint32_t n_queued,
+                      uint32_t window, uint32_t granule, sgdrc_cu_mask *ls_mask,
+                      sgdrc_cu_mask *be_mask)
+{
+    clear_error();
+    if (num_cus < 1 || num_cus > SGDRC_MAX_CUS)
+        return set_error(SGDRC_EINVAL, "num_cus %u outside 1..%d", num_cus, SGDRC_MAX_CUS);
+    if (window < 1 || granule < 1)
+        return set_error(SGDRC_EINVAL, "window and granule must be positive");
+    if (n_queued > 0 && !ls_cus)
+        return set_error(SGDRC_EINVAL, "ls_cus is NULL");
+    if (!ls_mask || !be_mask)
+        return set_error(SGDRC_EINVAL, "NULL mask");
+    uint32_t need = 0;
+    for (uint32_t i = 0; i < n_queued && i < window; ++i) {
+        if (ls_cus[i] > num_cus)
+            return set_error(SGDRC_EINVAL, "queued kernel %u needs %u CUs, device has %u", i,
+                             ls_cus[i], num_cus);
+        need = std::max(need, ls_cus[i]);
+    }
+    uint64_t r = ((uint64_t)need + granule - 1) / granule * granule;
+    if (r > num_cus)
+        r = num_cus;
+    std::memset(ls_mask, 0, sizeof *ls_mask);
+    std::memset(be_mask, 0, sizeof *be_mask);
+    for (uint32_t cu = 0; cu < num_cus; ++cu) {
+        sgdrc_cu_mask *m = cu < r ? ls_mask : be_mask;
+        m->bits[cu >> 6] |= 1ull << (cu & 63);
+    }
     return SGDRC_OK;
 }
 

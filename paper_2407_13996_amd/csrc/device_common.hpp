@@ -20,6 +20,11 @@ constexpr uint32_t kBadPage = 0xFFFFFFFFu;
 
 constexpr uint32_t kDevErrPtRange = 1u;
 constexpr uint32_t kDevFlagGateFallback = 2u;
+constexpr uint32_t kDevErrSuspendedDropped = 4u;  // a suspended launch was discarded unresumed
+
+// Queue slot states (QueueSlot::state).
+constexpr uint32_t kSlotIdle = 0u;
+constexpr uint32_t kSlotSuspended = 1u;
 
 constexpr int kMaxCus = 256;
 constexpr int kMaxXcds = 16;        // XCC_ID has 4 bits
@@ -40,10 +45,20 @@ constexpr int kCounterStride = 32;  // 32-bit words between counters (128 bytes)
 // without every workgroup hitting one address.  That workgroup finishes any
 // range that no workgroup took and zeroes the slot for the next launch on
 // the stream.
+//
+// Preemptible launches (see gated_tile_loop) use three more words: the
+// slot's state (kSlotIdle, or kSlotSuspended while an evicted launch still
+// has unclaimed tiles, whose group counters are then kept for the resuming
+// launch), a mark set by every workgroup that stopped on the eviction flag,
+// and a word that stays zero (the flag of a preemptible launch that has
+// none).
 struct QueueSlot {
     uint32_t grp_next[kMaxGroups * kCounterStride];
     uint32_t done[kArrivalClasses * kCounterStride];
     uint32_t done_all[kCounterStride];
+    uint32_t state[kCounterStride];
+    uint32_t stopped[kCounterStride];
+    uint32_t zero[kCounterStride];
 };
 
 // Per-launch gate arguments (passed by value in the kernel arguments).
@@ -61,6 +76,8 @@ struct Gate {
     uint32_t n_groups;
     uint32_t grp_shift;          // log2 of CUs per queue group
     uint32_t xcc_allowed;        // bit x: XCC_ID x has allowed CUs
+    const uint32_t *evict;       // preemptible launches: eviction flag (non-zero = stop)
+    uint32_t resume;             // preemptible launches: 1 = continue a suspended launch
 };
 
 __device__ __forceinline__ uint32_t hw_key()
@@ -152,11 +169,13 @@ __device__ __forceinline__ bool arrive_last(const Gate &g, uint32_t *s_flag)
     return *s_flag != 0u;
 }
 
-// Called by the last workgroup only, after all its work: zero the slot.
-__device__ __forceinline__ void reset_slot(QueueSlot *q)
+// Called by the last workgroup only, after all its work: zero the slot
+// (the group counters too unless ``keep_counters``, which leaves them to a
+// resuming launch).
+__device__ __forceinline__ void reset_slot(QueueSlot *q, bool keep_counters = false)
 {
     __syncthreads();
-    if (threadIdx.x < (uint32_t)kMaxGroups)
+    if (!keep_counters && threadIdx.x < (uint32_t)kMaxGroups)
         __hip_atomic_store(&q->grp_next[threadIdx.x * kCounterStride], 0u, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
     if (threadIdx.x < (uint32_t)kArrivalClasses)
@@ -198,16 +217,33 @@ enum class Claim { Ahead, Mid, After };
 // once per tile, on a workgroup-uniform path; only Claim::Mid gives it an
 // effect.
 //
+// Preemptible launches (EV, Claim::Mid only): a workgroup reads the
+// eviction flag ``*g.evict`` together with each ticket it claims (and once
+// at its start).  Once it has seen the flag set it takes no more tickets:
+// it finishes the tile it already holds and leaves, and marks the slot.
+// If tiles are left unclaimed when the last workgroup arrives and some
+// workgroup stopped on the flag, the launch is suspended instead of
+// completed: the last workgroup leaves the remaining tiles and the
+// epilogue alone, keeps the group counters and sets the slot's state to
+// kSlotSuspended.  A resuming launch (``g.resume``, same kernel arguments
+// and tile ranges, any mask) continues from those counters, stealing
+// across groups as usual, and does nothing if the slot is idle (the
+// launch it resumes had completed).  Fresh launches start on an idle slot
+// (the host discards a suspended launch first, see k_slot_discard).
+//
 // Bodies must not return early or branch around the rest of the tile on a
 // per-lane condition: the loop contains barriers, and a lane-dependent exit
 // from it lets the compiler send some lanes of a wave back to the barrier
 // while others still owe the next ticket.  Bodies record problems in the
 // per-thread ``err`` bits instead; they are raised once, after the loop.
-template <Claim CL, typename Prologue, typename Body, typename Flush, typename Epilogue>
+template <Claim CL, bool EV = false, typename Prologue, typename Body, typename Flush,
+          typename Epilogue>
 __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles, Prologue prologue,
                                                 Body body, Flush flush, Epilogue epilogue)
 {
+    static_assert(!EV || CL == Claim::Mid, "preemptible launches claim mid-tile");
     __shared__ uint32_t s_ticket;
+    __shared__ uint32_t s_stop;
     __shared__ uint32_t s_flag;
     __shared__ uint32_t s_left_lo[kMaxGroups], s_left_hi[kMaxGroups];
     __shared__ uint32_t s_grp_tile[kMaxGroups + 1];
@@ -217,6 +253,14 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
     uint32_t xcc;
     asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
     const uint32_t lut_entry = my_cu_entry(g);
+    // preemptible: thread 0 reads the slot state and the flag; both reach
+    // the other threads through LDS, so the whole workgroup decides alike
+    // even if the flag changes meanwhile
+    uint32_t slot_state = 0u, flag0 = 0u;
+    if (EV && threadIdx.x == 0) {
+        slot_state = __hip_atomic_load(&g.q->state[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        flag0 = __hip_atomic_load(g.evict, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     // every kernel runs at least kMaxGroups + 1 threads per workgroup; the
     // threads beyond write the last entry again (same value), which keeps
     // this straight-line code
@@ -227,18 +271,30 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
     prologue();
     const bool xcd_on = ((g.xcc_allowed >> (xcc & 0xFu)) & 1u) != 0u;
     const uint32_t entry = xcd_on ? lut_entry : kLutNone;
+    if (EV && threadIdx.x == 0) {
+        // a launch with nothing to do: a resume of a completed launch
+        s_flag = (g.resume && slot_state != kSlotSuspended) ? 1u : 0u;
+        s_stop = flag0 != 0u ? 1u : 0u;
+    }
     // time log: workgroup 0, the first one the hardware dispatches, stamps
     // the start; the last workgroup to finish stamps the end
     if (g.tlog && blockIdx.x == 0 && threadIdx.x == 0)
         __hip_atomic_store(&g.tlog[0], __builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
+    const bool dead = EV && __builtin_amdgcn_readfirstlane(s_flag) != 0u;
+    const bool stop0 = EV && __builtin_amdgcn_readfirstlane(s_stop) != 0u;
+    // s_flag and s_stop are written again only after the barriers that
+    // follow (arrival, first ticket or first tile)
     uint32_t err = 0u;
     const uint32_t cu = entry & 0xFFFFu;
-    if (entry != kLutNone && cu_allowed(g, cu)) {
+    if (!dead && entry != kLutNone && cu_allowed(g, cu)) {
         uint32_t grp = g.grp_base[(entry >> 16) & 0xFFu] + ((entry >> 24) >> g.grp_shift);
         uint32_t lo = s_grp_tile[grp], hi = s_grp_tile[grp + 1u];
-        uint32_t k = claim_ticket(&g.q->grp_next[grp * kCounterStride], &s_ticket);
+        // preemptible: a workgroup that sees the flag at its start takes no
+        // ticket at all
+        bool stop = stop0;
+        uint32_t k = stop ? kLutNone : claim_ticket(&g.q->grp_next[grp * kCounterStride], &s_ticket);
         // One flat loop: work through the own group's range, then steal from
         // the next group in ring order that still has tiles, found by wave 0
         // reading every group's counter at once.
@@ -252,23 +308,37 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
         for (;;) {
             if (k < hi - lo) {
                 uint32_t *const ctr = &g.q->grp_next[grp * kCounterStride];
+                uint32_t fl = 0u;
                 if (CL == Claim::Ahead && threadIdx.x == 0)
                     next = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 auto claim = [&]() {
-                    if (CL == Claim::Mid && threadIdx.x == 0)
-                        next = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED,
-                                                      __HIP_MEMORY_SCOPE_AGENT);
+                    if (CL == Claim::Mid && threadIdx.x == 0) {
+                        if (!stop)
+                            next = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED,
+                                                          __HIP_MEMORY_SCOPE_AGENT);
+                        if (EV)
+                            fl = __hip_atomic_load(g.evict, __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_AGENT);
+                    }
                 };
                 log_tile(g, cu, lo + k);
                 body(lo + k, cu, err, claim);
                 if (CL == Claim::After && threadIdx.x == 0)
                     next = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                if (threadIdx.x == 0)
-                    s_ticket = next;
+                if (threadIdx.x == 0) {
+                    // after a stop, the ticket taken before it is the last
+                    s_ticket = stop ? kLutNone : next;
+                    if (EV)
+                        s_stop = (stop || fl != 0u) ? 1u : 0u;
+                }
                 __syncthreads();
                 k = __builtin_amdgcn_readfirstlane(s_ticket);
+                if (EV)
+                    stop = __builtin_amdgcn_readfirstlane(s_stop) != 0u;
                 __syncthreads();
             } else {
+                if (EV && stop)
+                    break;
                 if (threadIdx.x < 64u) {
                     const uint32_t r = threadIdx.x;
                     bool rem = false;
@@ -280,6 +350,9 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
                                  : 0u;
                         rem = taken < size;
                     }
+                    uint32_t fl = 0u;
+                    if (EV && r == 0u)
+                        fl = __hip_atomic_load(g.evict, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     const uint64_t bits = __ballot(rem);
                     if (threadIdx.x == 0) {
                         uint32_t pick = kLutNone;
@@ -289,12 +362,16 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
                             pick = (sh + (uint32_t)__builtin_ctzll(rot)) & 63u;
                         }
                         s_ticket = pick;
+                        if (EV)
+                            s_stop = fl != 0u ? 1u : 0u;
                     }
                 }
                 __syncthreads();
                 const uint32_t pick = __builtin_amdgcn_readfirstlane(s_ticket);
+                if (EV)
+                    stop = __builtin_amdgcn_readfirstlane(s_stop) != 0u;
                 __syncthreads();
-                if (pick == kLutNone)
+                if (pick == kLutNone || (EV && stop))
                     break;
                 grp = pick;
                 lo = s_grp_tile[grp];
@@ -302,12 +379,12 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
                 k = claim_ticket(&g.q->grp_next[grp * kCounterStride], &s_ticket);
             }
         }
+        if (EV && stop && threadIdx.x == 0)
+            __hip_atomic_store(&g.q->stopped[0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         flush();
     }
     if (arrive_last(g, &s_flag)) {
-        // ranges that no workgroup finished: [lo + tickets taken, hi), then
-        // worked through in one flat loop so that no barrier of the body
-        // ends up in a nested loop
+        // ranges that no workgroup finished: [lo + tickets taken, hi)
         bool left = false;
         if (threadIdx.x < (uint32_t)kMaxGroups) {
             uint32_t a = 0u, b = 0u;
@@ -322,29 +399,55 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
             s_left_hi[threadIdx.x] = b;
             left = a < b;
         }
-        if (__syncthreads_or(left ? 1 : 0)) {
-            uint32_t c = 0u;
-            uint32_t t = __builtin_amdgcn_readfirstlane(s_left_lo[0]);
-            uint32_t end = __builtin_amdgcn_readfirstlane(s_left_hi[0]);
-            while (c < (uint32_t)kMaxGroups) {
-                if (t < end) {
-                    log_tile(g, cu, t);
-                    body(t, cu, err, NoOp());
-                    t += 1u;
-                } else {
-                    c += 1u;
-                    const uint32_t cc = c < (uint32_t)kMaxGroups ? c : 0u;
-                    t = __builtin_amdgcn_readfirstlane(s_left_lo[cc]);
-                    end = c < (uint32_t)kMaxGroups ? __builtin_amdgcn_readfirstlane(s_left_hi[cc]) : 0u;
-                }
+        if (threadIdx.x == 0)
+            s_stop = EV ? __hip_atomic_load(&g.q->stopped[0], __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT)
+                        : 0u;
+        const bool any_left = __syncthreads_or(left ? 1 : 0) != 0;
+        const bool stopped = EV && __builtin_amdgcn_readfirstlane(s_stop) != 0u;
+        if (EV && dead) {
+            // nothing ran: only the arrival counters are reset
+            reset_slot(g.q, true);
+        } else if (EV && any_left && stopped) {
+            // suspended: the unclaimed tiles wait for a resuming launch
+            reset_slot(g.q, true);
+            if (threadIdx.x == 0) {
+                __hip_atomic_store(&g.q->stopped[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&g.q->state[0], kSlotSuspended, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
             }
-            flush();
-            err |= threadIdx.x == 0 ? kDevFlagGateFallback : 0u;
+        } else {
+            if (any_left) {
+                // worked through in one flat loop so that no barrier of the
+                // body ends up in a nested loop
+                uint32_t c = 0u;
+                uint32_t t = __builtin_amdgcn_readfirstlane(s_left_lo[0]);
+                uint32_t end = __builtin_amdgcn_readfirstlane(s_left_hi[0]);
+                while (c < (uint32_t)kMaxGroups) {
+                    if (t < end) {
+                        log_tile(g, cu, t);
+                        body(t, cu, err, NoOp());
+                        t += 1u;
+                    } else {
+                        c += 1u;
+                        const uint32_t cc = c < (uint32_t)kMaxGroups ? c : 0u;
+                        t = __builtin_amdgcn_readfirstlane(s_left_lo[cc]);
+                        end = c < (uint32_t)kMaxGroups ? __builtin_amdgcn_readfirstlane(s_left_hi[cc]) : 0u;
+                    }
+                }
+                flush();
+                err |= threadIdx.x == 0 ? kDevFlagGateFallback : 0u;
+            }
+            __builtin_amdgcn_s_waitcnt(0);  // own partials complete before the epilogue reads
+            __syncthreads();
+            epilogue();
+            reset_slot(g.q);
+            if (EV && threadIdx.x == 0) {
+                __hip_atomic_store(&g.q->stopped[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&g.q->state[0], kSlotIdle, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            }
         }
-        __builtin_amdgcn_s_waitcnt(0);  // own partials complete before the epilogue reads
-        __syncthreads();
-        epilogue();
-        reset_slot(g.q);
         if (g.tlog && threadIdx.x == 0) {
             __builtin_amdgcn_s_waitcnt(0);
             __hip_atomic_store(&g.tlog[1], __builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,

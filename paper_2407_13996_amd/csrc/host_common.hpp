@@ -6,6 +6,7 @@
 
 #include <cstdarg>
 #include <cstdint>
+#include <functional>
 #include <mutex>
 #include <string>
 #include <unordered_map>
@@ -26,6 +27,9 @@ constexpr int kHistBins = 256;
 constexpr int kStreamGroupCus = 0;
 constexpr int kGemvGroupCus = 8;
 
+// Re-issues a preemptible launch with a given gate and grid size.
+typedef std::function<hipError_t(const Gate &, uint32_t grid)> Relaunch;
+
 struct StreamState {
     int slot = -1;
     sgdrc_cu_mask mask{};
@@ -34,6 +38,16 @@ struct StreamState {
     uint64_t *tlog = nullptr;   // time-log slots ({start, end} pairs) or NULL
     uint32_t tlog_slots = 0;
     uint64_t tlog_next = 0;     // launches logged since the log was set
+    // preemptible launches: their own queue slot (so that a suspended
+    // launch never meets another kernel of the stream), the eviction flag,
+    // and the last such launch, kept for sgdrc_resume
+    int slot_ev = -1;
+    bool ev_on = false;
+    const uint32_t *evict = nullptr;
+    Relaunch ev_relaunch;
+    Gate ev_gate{};             // tile ranges and queue-group layout of that launch
+    uint64_t ev_tiles = 0;
+    int ev_per_cu = 1;
 };
 
 // What a gated launch needs besides the Gate itself.
@@ -91,8 +105,24 @@ int stream_state(Ctx *c, void *stream, StreamState **out);
 
 // Gate arguments for a launch of ``n_tiles`` tiles on ``stream`` whose work
 // queues serve runs of ``group_cus`` CUs inside an XCD (a power of two, at
-// most 32), or the whole device (0).
-int make_gate(Ctx *c, void *stream, uint64_t n_tiles, int group_cus, Gate *g, LaunchInfo *li);
+// most 32), or the whole device (0).  ``preemptible``: the launch uses the
+// stream's preemptible queue slot and eviction flag (the stream must have
+// eviction on).
+int make_gate(Ctx *c, void *stream, uint64_t n_tiles, int group_cus, Gate *g, LaunchInfo *li,
+              bool preemptible = false);
+
+// Whether launches on ``stream`` are to be preemptible (eviction flag set).
+bool stream_preemptible(Ctx *c, void *stream);
+
+// Enqueues, before a fresh preemptible launch on ``stream``, the discard of
+// a suspended launch that was never resumed (raising
+// kDevErrSuspendedDropped), so that the new launch starts on an idle slot.
+int discard_suspended(Ctx *c, void *stream);
+
+// Records ``fn`` (which has just launched with ``g``) as the stream's last
+// preemptible launch, for sgdrc_resume.
+void record_preemptible(Ctx *c, void *stream, const Gate &g, uint64_t n_tiles, int per_cu,
+                        Relaunch fn);
 
 // Grid size for a gated persistent kernel: the same number of workgroups
 // for every CU (the dispatcher spreads them over all CUs; those on CUs

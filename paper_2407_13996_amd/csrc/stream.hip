@@ -100,7 +100,7 @@ __device__ __forceinline__ void stage_tile_pages(uint64_t t0, uint32_t tile, uin
     __syncthreads();
 }
 
-template <int U>
+template <int U, bool EV>
 __global__ __launch_bounds__(kStreamThreads) void k_relayout(
     uint8_t *__restrict__ dst, const uint32_t *__restrict__ pt_d, uint64_t dst_pages,
     const uint8_t *__restrict__ src, const uint32_t *__restrict__ pt_s, uint64_t src_pages,
@@ -156,7 +156,7 @@ __global__ __launch_bounds__(kStreamThreads) void k_relayout(
             }
         }
     };
-    gated_tile_loop<Claim::Mid>(g, n_tiles, NoOp(), body, NoOp(), epilogue);
+    gated_tile_loop<Claim::Mid, EV>(g, n_tiles, NoOp(), body, NoOp(), epilogue);
 }
 
 __device__ __forceinline__ u32x4 fma4(float s, u32x4 c, u32x4 b)
@@ -169,7 +169,7 @@ __device__ __forceinline__ u32x4 fma4(float s, u32x4 c, u32x4 b)
     return r;
 }
 
-template <int U>
+template <int U, bool EV>
 __global__ __launch_bounds__(kStreamThreads) void k_triad(
     uint8_t *a, const uint32_t *__restrict__ pt_a, uint64_t a_pages,
     const uint8_t *b, const uint32_t *__restrict__ pt_b, uint64_t b_pages,
@@ -232,7 +232,7 @@ __global__ __launch_bounds__(kStreamThreads) void k_triad(
             }
         }
     };
-    gated_tile_loop<Claim::Mid>(g, n_tiles, NoOp(), body, NoOp(), epilogue);
+    gated_tile_loop<Claim::Mid, EV>(g, n_tiles, NoOp(), body, NoOp(), epilogue);
 }
 
 }  // namespace sgdrc
@@ -259,21 +259,36 @@ int bimodal_relayout(sgdrc_ctx *ctx, const sgdrc_paged *dst, const sgdrc_paged *
     const uint64_t n_tiles = ((n_bytes & ~15ull) + tile - 1) / tile;
     if (n_tiles >= (1ull << 31))
         return set_error(SGDRC_EINVAL, "n_bytes too large");
+    const bool ev = stream_preemptible(c, stream);
+    if (ev && (rc = discard_suspended(c, stream)))
+        return rc;
     Gate g;
     LaunchInfo li;
-    rc = make_gate(c, stream, n_tiles, kStreamGroupCus, &g, &li);
+    rc = make_gate(c, stream, n_tiles, kStreamGroupCus, &g, &li, ev);
     if (rc)
         return rc;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    auto kern = k_relayout<U>;
-    static const int occ = occupancy(k_relayout<U>, kStreamThreads);
+    static const int occ = occupancy(k_relayout<U, false>, kStreamThreads);
     const int per_cu = std::min(occ, kStreamWgsPerCu);
     const uint32_t grid = gated_grid(c, per_cu, n_tiles, li);
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(kStreamThreads), 0, s,
-                       static_cast<uint8_t *>(dst->pool), dst->pt, dst->pool_pages,
-                       static_cast<const uint8_t *>(src->pool), src->pt, src->pool_pages, n_bytes,
-                       page_shift, (uint32_t)n_tiles, g);
-    SGDRC_HIP(hipGetLastError());
+    uint8_t *const d = static_cast<uint8_t *>(dst->pool);
+    const uint8_t *const sp = static_cast<const uint8_t *>(src->pool);
+    const uint32_t *const dpt = dst->pt, *const spt = src->pt;
+    const uint64_t dpages = dst->pool_pages, spages = src->pool_pages;
+    auto launch = [=](const Gate &gg, uint32_t gr, bool preempt) {
+        if (preempt)
+            hipLaunchKernelGGL((k_relayout<U, true>), dim3(gr), dim3(kStreamThreads), 0, s, d, dpt,
+                               dpages, sp, spt, spages, n_bytes, page_shift, (uint32_t)n_tiles, gg);
+        else
+            hipLaunchKernelGGL((k_relayout<U, false>), dim3(gr), dim3(kStreamThreads), 0, s, d,
+                               dpt, dpages, sp, spt, spages, n_bytes, page_shift,
+                               (uint32_t)n_tiles, gg);
+        return hipGetLastError();
+    };
+    SGDRC_HIP(launch(g, grid, ev));
+    if (ev)
+        record_preemptible(c, stream, g, n_tiles, per_cu,
+                           [launch](const Gate &gg, uint32_t gr) { return launch(gg, gr, true); });
     return SGDRC_OK;
 }
 
@@ -299,22 +314,38 @@ int colored_stream(sgdrc_ctx *ctx, const sgdrc_paged *a, const sgdrc_paged *b,
     const uint64_t n_tiles = ((n_bytes & ~15ull) + tile - 1) / tile;
     if (n_tiles >= (1ull << 31))
         return set_error(SGDRC_EINVAL, "n_elems too large");
+    const bool ev = stream_preemptible(c, stream);
+    if (ev && (rc = discard_suspended(c, stream)))
+        return rc;
     Gate g;
     LaunchInfo li;
-    rc = make_gate(c, stream, n_tiles, kStreamGroupCus, &g, &li);
+    rc = make_gate(c, stream, n_tiles, kStreamGroupCus, &g, &li, ev);
     if (rc)
         return rc;
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
-    auto kern = k_triad<U>;
-    static const int occ = occupancy(k_triad<U>, kStreamThreads);
+    static const int occ = occupancy(k_triad<U, false>, kStreamThreads);
     const int per_cu = std::min(occ, kStreamWgsPerCu);
     const uint32_t grid = gated_grid(c, per_cu, n_tiles, li);
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(kStreamThreads), 0, hs,
-                       static_cast<uint8_t *>(a->pool), a->pt, a->pool_pages,
-                       static_cast<const uint8_t *>(b->pool), b->pt, b->pool_pages,
-                       static_cast<const uint8_t *>(c_arr->pool), c_arr->pt, c_arr->pool_pages, s,
-                       n_bytes, page_shift, (uint32_t)n_tiles, g);
-    SGDRC_HIP(hipGetLastError());
+    uint8_t *const ap = static_cast<uint8_t *>(a->pool);
+    const uint8_t *const bp = static_cast<const uint8_t *>(b->pool);
+    const uint8_t *const cp = static_cast<const uint8_t *>(c_arr->pool);
+    const uint32_t *const apt = a->pt, *const bpt = b->pt, *const cpt = c_arr->pt;
+    const uint64_t an = a->pool_pages, bn = b->pool_pages, cn = c_arr->pool_pages;
+    auto launch = [=](const Gate &gg, uint32_t gr, bool preempt) {
+        if (preempt)
+            hipLaunchKernelGGL((k_triad<U, true>), dim3(gr), dim3(kStreamThreads), 0, hs, ap, apt,
+                               an, bp, bpt, bn, cp, cpt, cn, s, n_bytes, page_shift,
+                               (uint32_t)n_tiles, gg);
+        else
+            hipLaunchKernelGGL((k_triad<U, false>), dim3(gr), dim3(kStreamThreads), 0, hs, ap, apt,
+                               an, bp, bpt, bn, cp, cpt, cn, s, n_bytes, page_shift,
+                               (uint32_t)n_tiles, gg);
+        return hipGetLastError();
+    };
+    SGDRC_HIP(launch(g, grid, ev));
+    if (ev)
+        record_preemptible(c, stream, g, n_tiles, per_cu,
+                           [launch](const Gate &gg, uint32_t gr) { return launch(gg, gr, true); });
     return SGDRC_OK;
 }
 

@@ -149,3 +149,66 @@ def test_binding_raises_with_message():
     with pytest.raises(sg.SgdrcError) as e:
         sg.set_cu_mask(None, 0, [])
     assert e.value.code == sg.EINVAL and "empty" in str(e.value)
+
+
+def test_preemption_argument_errors(L):
+    t = ctypes.c_uint64()
+    assert L.sgdrc_set_eviction_flag(NULL, None, 258) == sg.EINVAL     # misaligned flag
+    assert L.sgdrc_set_eviction_flag(NULL, None, 256) == sg.ENODEV
+    assert L.sgdrc_set_eviction_flag(NULL, None, None) == sg.ENODEV
+    assert L.sgdrc_resume(NULL, None) == sg.ENODEV
+    assert L.sgdrc_suspended(NULL, None, None) == sg.EINVAL
+    assert L.sgdrc_suspended(NULL, None, ctypes.byref(t)) == sg.ENODEV
+
+
+# ------------------------------------------------- sliding-window reservation
+# The CUs reserved for latency-sensitive kernels are the most that any
+# kernel in the window of the next queued ones needs (paper section 7.1),
+# here rounded up to a granule and given as the first logical CUs.
+
+def test_tidal_masks_hand_worked():
+    # queue needs 24, 64, 8 CUs: a window of 1 sees 24, of 2 or more 64
+    assert sg.tidal_masks(256, [24, 64, 8], window=1)[0] == list(range(24))
+    assert sg.tidal_masks(256, [24, 64, 8], window=2)[0] == list(range(64))
+    assert sg.tidal_masks(256, [24, 64, 8], window=9)[0] == list(range(64))
+    # whole XCDs: 24 -> 32, 65 -> 96
+    assert sg.tidal_masks(256, [24], window=1, granule=32)[0] == list(range(32))
+    assert sg.tidal_masks(256, [65, 3], window=2, granule=32)[0] == list(range(96))
+    # nothing queued: everything to the best-effort side
+    ls, be = sg.tidal_masks(256, [], window=4)
+    assert ls == [] and be == list(range(256))
+    # a need of the whole device leaves the best-effort side empty
+    ls, be = sg.tidal_masks(256, [10, 256], window=2)
+    assert ls == list(range(256)) and be == []
+    # rounding never exceeds the device
+    assert sg.tidal_masks(250, [249], window=1, granule=32)[0] == list(range(250))
+
+
+def test_tidal_masks_partition_random_queues():
+    import numpy as np
+    rng = np.random.default_rng(11)
+    for _ in range(200):
+        n = int(rng.integers(1, 257))
+        q = [int(x) for x in rng.integers(0, n + 1, size=int(rng.integers(0, 12)))]
+        w = int(rng.integers(1, 6))
+        gr = int(rng.choice([1, 8, 32]))
+        ls, be = sg.tidal_masks(n, q, window=w, granule=gr)
+        assert sorted(ls + be) == list(range(n))           # a partition of the CUs
+        assert ls == list(range(len(ls)))                   # LS holds a prefix
+        r = len(ls)
+        need = max(q[:w], default=0)
+        assert r >= need and (r == n or r % gr == 0) and r - need < gr
+
+
+def test_tidal_masks_argument_errors(L):
+    ls, be = sg.CuMask(), sg.CuMask()
+    r = ctypes.byref
+    q = (ctypes.c_uint32 * 2)(4, 8)
+    assert L.sgdrc_tidal_masks(0, q, 2, 1, 1, r(ls), r(be)) == sg.EINVAL
+    assert L.sgdrc_tidal_masks(257, q, 2, 1, 1, r(ls), r(be)) == sg.EINVAL
+    assert L.sgdrc_tidal_masks(256, q, 2, 0, 1, r(ls), r(be)) == sg.EINVAL
+    assert L.sgdrc_tidal_masks(256, q, 2, 1, 0, r(ls), r(be)) == sg.EINVAL
+    assert L.sgdrc_tidal_masks(256, None, 2, 1, 1, r(ls), r(be)) == sg.EINVAL
+    assert L.sgdrc_tidal_masks(4, q, 2, 2, 1, r(ls), r(be)) == sg.EINVAL   # 8 > 4 CUs
+    assert L.sgdrc_tidal_masks(256, q, 2, 1, 1, None, r(be)) == sg.EINVAL
+    assert L.sgdrc_tidal_masks(256, q, 2, 1, 1, r(ls), r(be)) == sg.OK

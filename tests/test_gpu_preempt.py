@@ -1,0 +1,325 @@
+"""Preemptible best-effort launches (paper section 7.1) on the GPU: an
+eviction flag stops a persistent triad or relayout at a tile boundary, the
+launch ends suspended, and sgdrc_resume finishes it under another CU mask.
+The interrupted and resumed launches together must equal one uninterrupted
+launch (the oracle's result, bit for bit), with every tile processed
+exactly once and the resumed tiles only on the new mask's CUs."""
+import sys
+
+import numpy as np
+import pytest
+
+import synth
+import paper_2407_13996_amd as sg
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+DEV = "cuda:0"
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def ctx(orc):
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    c = sg.Context(0)
+    yield c
+    c.close()
+
+
+@pytest.fixture(autouse=True)
+def no_device_flags(ctx):
+    ctx.device_error()
+    yield
+    assert ctx.device_error() == 0
+
+
+def to_dev(a):
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint32:
+        a = a.view(np.int32)
+    elif a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(a).to(DEV)
+
+
+def to_host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+class Triad:
+    """Three coloured arrays of n fp32 elements (oracle page tables) and the
+    oracle's a = b + 3 c."""
+
+    def __init__(self, orc, shift, n, seed):
+        P = 1 << shift
+        self.shift, self.n = shift, n
+        n_pages = -(-n * 4 // P)
+        self.pools = int(n_pages * 64 / 16 * 1.5) + 64
+        self.pts = []
+        for i in range(3):
+            masks = synth.xor_masks(6, seed=seed + i, min_bit=shift)
+            pt, found = orc.pagetable(masks, 0, shift, self.pools,
+                                      synth.colour_set_bits(range(8 * i, 8 * i + 16)), n_pages)
+            assert found >= n_pages
+            self.pts.append(pt)
+        epp = P // 4
+        self.a0 = synth.uniform_f32(self.pools * epp, seed=seed + 5)
+        b = synth.uniform_f32(self.pools * epp, seed=seed + 6)
+        c = synth.uniform_f32(self.pools * epp, seed=seed + 7)
+        self.d_a, self.d_b, self.d_c = to_dev(self.a0), to_dev(b), to_dev(c)
+        self.ref = self.a0.copy()
+        orc.triad(self.ref, self.pts[0], b, self.pts[1], c, self.pts[2], 3.0, n, shift)
+        self.tiles = -(-(n * 4 & ~15) // 65536)
+
+    def reset(self):
+        self.d_a.copy_(to_dev(self.a0))
+        torch.cuda.synchronize()
+
+    def launch(self, ctx, stream):
+        d_pts = [to_dev(p) for p in self.pts]
+        self._keep = d_pts
+        sg.colored_stream(ctx, sg.paged(self.d_a, d_pts[0], self.pools),
+                          sg.paged(self.d_b, d_pts[1], self.pools),
+                          sg.paged(self.d_c, d_pts[2], self.pools), 3.0, self.n, self.shift,
+                          stream)
+
+    def check(self):
+        assert (to_host(self.d_a).view(np.uint32) == self.ref.view(np.uint32)).all()
+
+
+class Logs:
+    def __init__(self, ctx, n_tiles):
+        self.ctx = ctx
+        self.cu = torch.zeros(ctx.num_cus, dtype=torch.int32, device=DEV)
+        self.tile = torch.zeros(max(n_tiles, 1), dtype=torch.int32, device=DEV)
+        ctx.set_worklog(self.cu, self.tile)
+
+    def snapshot(self):
+        return to_host(self.cu).copy(), to_host(self.tile).copy()
+
+    def close(self):
+        self.ctx.set_worklog(None, None)
+
+
+def test_triad_evicted_before_start_resumes_on_other_cus(ctx, orc):
+    n_cu = ctx.num_cus
+    tr = Triad(orc, 16, 600 * 16384 + 7, seed=40)
+    st = torch.cuda.Stream()
+    flag = torch.ones(1, dtype=torch.int32, device=DEV)
+    logs = Logs(ctx, tr.tiles)
+    try:
+        sg.set_eviction_flag(ctx, st, flag)
+        tr.launch(ctx, st)
+        left = sg.suspended(ctx, st)
+        say(f"evicted before start: {left} of {tr.tiles} tiles left")
+        assert left == tr.tiles
+        assert (to_host(tr.d_a).view(np.uint32) == tr.a0.view(np.uint32)).all()
+        cl, tl = logs.snapshot()
+        assert tl.sum() == 0
+        flag.zero_()
+        torch.cuda.synchronize()
+        sg.set_cu_mask(ctx, st, range(n_cu // 2, n_cu))
+        sg.resume(ctx, st)
+        assert sg.suspended(ctx, st) == 0
+        cl, tl = logs.snapshot()
+    finally:
+        logs.close()
+        sg.set_cu_mask(ctx, st, None)
+        sg.set_eviction_flag(ctx, st, None)
+    tr.check()
+    assert (tl == 1).all()
+    assert set(np.nonzero(cl)[0].tolist()) <= set(range(n_cu // 2, n_cu))
+
+
+def _delay(stream, us):
+    """Enqueue on ``stream`` work that takes roughly ``us`` microseconds."""
+    with torch.cuda.stream(stream):
+        if hasattr(torch.cuda, "_sleep"):
+            torch.cuda._sleep(int(us * 100))
+        else:
+            x = torch.empty(int(us * 2e5), device=DEV)
+            x.normal_()
+
+
+def test_triad_evicted_mid_run_every_tile_once(ctx, orc):
+    """The flag is raised from another stream while the triad runs; after
+    resumptions on a smaller mask, every tile was processed once."""
+    n_cu = ctx.num_cus
+    tr = Triad(orc, 16, 64 * 1024 * 1024 + 3, seed=50)    # 256 MiB arrays, 4097 tiles
+    st, st2 = torch.cuda.Stream(), torch.cuda.Stream()
+    flag = torch.zeros(1, dtype=torch.int32, device=DEV)
+    mid = 0
+    for delay_us in (5, 20, 40, 80, 160):
+        tr.reset()
+        flag.zero_()
+        torch.cuda.synchronize()
+        logs = Logs(ctx, tr.tiles)
+        try:
+            sg.set_eviction_flag(ctx, st, flag)
+            tr.launch(ctx, st)
+            _delay(st2, delay_us)
+            with torch.cuda.stream(st2):
+                flag.fill_(1)
+            left = sg.suspended(ctx, st)
+            torch.cuda.synchronize()
+            say(f"flag after ~{delay_us} us: {left} of {tr.tiles} tiles left")
+            mid += 0 < left < tr.tiles
+            flag.zero_()
+            torch.cuda.synchronize()
+            sg.set_cu_mask(ctx, st, range(n_cu // 4))
+            rounds = 0
+            while sg.suspended(ctx, st) and rounds < 4:
+                sg.resume(ctx, st)
+                rounds += 1
+            assert sg.suspended(ctx, st) == 0
+            cl, tl = logs.snapshot()
+        finally:
+            logs.close()
+            sg.set_cu_mask(ctx, st, None)
+            sg.set_eviction_flag(ctx, st, None)
+        tr.check()
+        assert (tl == 1).all(), np.unique(tl, return_counts=True)
+        assert cl.sum() == tr.tiles
+    assert mid >= 1, "no attempt was evicted mid-run"
+
+
+def test_resume_after_completion_does_nothing(ctx, orc):
+    tr = Triad(orc, 12, 5 * 1024 + 77, seed=60)
+    st = torch.cuda.Stream()
+    flag = torch.zeros(1, dtype=torch.int32, device=DEV)
+    logs = Logs(ctx, tr.tiles)
+    try:
+        sg.set_eviction_flag(ctx, st, flag)
+        tr.launch(ctx, st)
+        assert sg.suspended(ctx, st) == 0
+        sg.resume(ctx, st)
+        sg.resume(ctx, st)
+        assert sg.suspended(ctx, st) == 0
+        cl, tl = logs.snapshot()
+    finally:
+        logs.close()
+        sg.set_eviction_flag(ctx, st, None)
+    tr.check()
+    assert (tl == 1).all()
+
+
+def test_evicted_resumption_stays_suspended(ctx, orc):
+    tr = Triad(orc, 16, 40 * 16384, seed=70)
+    st = torch.cuda.Stream()
+    flag = torch.ones(1, dtype=torch.int32, device=DEV)
+    try:
+        sg.set_eviction_flag(ctx, st, flag)
+        tr.launch(ctx, st)
+        assert sg.suspended(ctx, st) == tr.tiles
+        sg.resume(ctx, st)                      # flag still set: no progress
+        assert sg.suspended(ctx, st) == tr.tiles
+        flag.zero_()
+        torch.cuda.synchronize()
+        sg.resume(ctx, st)
+        assert sg.suspended(ctx, st) == 0
+    finally:
+        sg.set_eviction_flag(ctx, st, None)
+    tr.check()
+
+
+def test_fresh_launch_drops_unresumed_suspension(ctx, orc):
+    first = Triad(orc, 16, 20 * 16384 + 1, seed=80)
+    second = Triad(orc, 16, 30 * 16384 + 2, seed=90)
+    st = torch.cuda.Stream()
+    flag = torch.ones(1, dtype=torch.int32, device=DEV)
+    try:
+        sg.set_eviction_flag(ctx, st, flag)
+        first.launch(ctx, st)
+        assert sg.suspended(ctx, st) == first.tiles
+        flag.zero_()
+        torch.cuda.synchronize()
+        second.launch(ctx, st)                  # discards the first launch's rest
+        assert sg.suspended(ctx, st) == 0
+    finally:
+        sg.set_eviction_flag(ctx, st, None)
+    assert ctx.device_error() == sg.DEVERR_SUSPENDED_DROPPED
+    second.check()
+    assert (to_host(first.d_a).view(np.uint32) == first.a0.view(np.uint32)).all()
+
+
+@pytest.mark.parametrize("shift,n_bytes", [(16, 64 * 65536 + 17), (12, 37 * 4096 + 1234)])
+def test_relayout_evicted_then_resumed(ctx, orc, shift, n_bytes):
+    P = 1 << shift
+    n_pages = -(-n_bytes // P)
+    pool = int(n_pages * 4 * 1.5) + 64
+    masks = synth.xor_masks(6, seed=3, min_bit=shift)
+    pt_s, f1 = orc.pagetable(masks, 0, shift, pool, synth.colour_set_bits(range(16)), n_pages)
+    pt_d, f2 = orc.pagetable(masks, 0, shift, pool, synth.colour_set_bits(range(16, 32)), n_pages)
+    assert min(f1, f2) >= n_pages
+    src = synth.random_u16(pool * P // 2, seed=4)
+    d_src = to_dev(src)
+    d_dst = torch.zeros(pool * P // 2, dtype=torch.int16, device=DEV)
+    ref = np.zeros(pool * P, dtype=np.uint8)
+    orc.relayout(ref, pt_d, src.view(np.uint8), pt_s, n_bytes, shift)
+    st = torch.cuda.Stream()
+    flag = torch.ones(1, dtype=torch.int32, device=DEV)
+    dpt_s, dpt_d = to_dev(pt_s), to_dev(pt_d)
+    try:
+        sg.set_eviction_flag(ctx, st, flag)
+        sg.bimodal_relayout(ctx, sg.paged(d_dst, dpt_d, pool), sg.paged(d_src, dpt_s, pool),
+                            n_bytes, shift, st)
+        assert sg.suspended(ctx, st) > 0
+        assert (to_host(d_dst) == 0).all()
+        flag.zero_()
+        torch.cuda.synchronize()
+        sg.set_cu_mask(ctx, st, range(0, ctx.num_cus, 3))
+        sg.resume(ctx, st)
+        assert sg.suspended(ctx, st) == 0
+    finally:
+        sg.set_cu_mask(ctx, st, None)
+        sg.set_eviction_flag(ctx, st, None)
+    assert (to_host(d_dst).view(np.uint8) == ref).all()
+
+
+def test_tidal_handover_ls_gemv_and_evicted_triad(ctx, orc):
+    """The section 7.1 sequence on one GPU: a best-effort triad runs on all
+    CUs; a latency-sensitive GEMV arrives, the triad is evicted, the
+    sliding-window policy splits the CUs, the GEMV runs on its share while
+    the triad resumes on the rest; both results are exact."""
+    n_cu = ctx.num_cus
+    tr = Triad(orc, 16, 64 * 1024 * 1024, seed=100)
+    be, ls = torch.cuda.Stream(), torch.cuda.Stream()
+    flag = torch.zeros(1, dtype=torch.int32, device=DEV)
+    M, K, B = 1024, 4096, 1
+    w = (synth.normal_f32(M * K, seed=9) * 0.02).astype(np.float32)
+    x = synth.normal_f32(B * K, seed=10).astype(np.float32)
+    wpt = np.arange(-(-M * K * 4 // 65536), dtype=np.uint32)
+    d_w, d_x = to_dev(w), to_dev(x)
+    d_y = torch.zeros(B * M, dtype=torch.float32, device=DEV)
+    ls_cus, be_cus = sg.tidal_masks(n_cu, [40, 96, 64], window=2, granule=32)
+    assert len(ls_cus) == 96 and len(be_cus) == n_cu - 96
+    try:
+        sg.set_eviction_flag(ctx, be, flag)
+        tr.launch(ctx, be)
+        _delay(ls, 20)
+        with torch.cuda.stream(ls):
+            flag.fill_(1)                       # the LS task evicts the BE kernel
+        be.synchronize()
+        left = sg.suspended(ctx, be)
+        say(f"handover: triad suspended with {left} of {tr.tiles} tiles left")
+        sg.set_cu_mask(ctx, be, be_cus)
+        sg.set_cu_mask(ctx, ls, ls_cus)
+        flag.zero_()
+        torch.cuda.synchronize()
+        sg.resume(ctx, be)
+        sg.colored_gemv(ctx, sg.paged(d_w, to_dev(wpt), len(wpt)), sg.F32, M, K, d_x, sg.F32, B,
+                        d_y, 16, ls)
+        torch.cuda.synchronize()
+        assert sg.suspended(ctx, be) == 0
+    finally:
+        sg.set_cu_mask(ctx, be, None)
+        sg.set_cu_mask(ctx, ls, None)
+        sg.set_eviction_flag(ctx, be, None)
+    tr.check()
+    ref, absdot = orc.gemv(w, wpt, sg.F32, M, K, x, sg.F32, B, 16)
+    y = to_host(d_y).reshape(B, M).astype(np.float64)
+    assert np.all(np.abs(y - ref) <= 1e-3 * absdot + 1e-30)
