@@ -43,10 +43,11 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--rows", default="classify,pagetable,relayout,gemv,corun",
+    ap.add_argument("--rows", default="classify,pagetable,relayout,gemv,corun,preempt",
                     help="comma list of extra rows to measure ('' for none)")
     ap.add_argument("--gemv-launches", type=int, default=300)
     ap.add_argument("--corun-launches", type=int, default=2000)
+    ap.add_argument("--preempt-trials", type=int, default=40)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-passes", type=int, default=8)
     return ap.parse_args()
@@ -88,14 +89,19 @@ class DevTimes:
         torch.cuda.synchronize()
         ctx.set_timelog(stream, self.slots)
 
-    def close_us(self, count=None):
-        """Switch the log off and return the spans (microseconds) of the
-        first ``count`` launches logged (at most n)."""
+    def close_ticks(self, count=None):
+        """Switch the log off and return the {start, end} ticks of the first
+        ``count`` launches logged (at most n), shape [launches, 2]."""
         import numpy as np
         self.torch.cuda.synchronize()
         self.ctx.set_timelog(self.stream, None)
         t = self.slots.cpu().numpy().reshape(-1, 2).astype(np.int64)
-        t = t[: self.n if count is None else min(count, self.n)]
+        return t[: self.n if count is None else min(count, self.n)]
+
+    def close_us(self, count=None):
+        """Switch the log off and return the spans (microseconds) of the
+        first ``count`` launches logged (at most n)."""
+        t = self.close_ticks(count)
         return (t[:, 1] - t[:, 0]) * 1e3 / self.ctx.wallclock_khz
 
 
@@ -296,9 +302,15 @@ def main():
     if "gemv" in want:
         rows["gemv"] = bench_gemv(torch, sg, synth, ctx, stream, timer, args.gemv_launches)
         flags["gemv"] = ctx.device_error()
+    ops = corun_operands(torch, sg, synth, ctx) if ("corun" in want or "preempt" in want) else None
     if "corun" in want:
-        rows["corun"] = bench_corun(torch, sg, synth, ctx, args.corun_launches)
+        rows["corun"] = bench_corun(torch, sg, synth, ctx, args.corun_launches, ops)
         flags["corun"] = ctx.device_error()
+    if "preempt" in want:
+        rows["preempt"] = bench_preempt(torch, sg, synth, ctx, ops, args.preempt_trials)
+        flags["preempt"] = ctx.device_error()
+    del ops
+    torch.cuda.empty_cache()
     if rows:
         result["rows"] = rows
 
@@ -474,17 +486,12 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
             "points": out}
 
 
-def bench_corun(torch, sg, synth, ctx, ls_launches):
-    """Co-located pair: LS GEMV (bf16 4096x11008, batch 1) on colours 0..47 and
-    CUs 0..191, BE triad (three 2 GiB fp32 arrays, 64 KiB pages) on colours
-    48..63 and CUs 192..255, against the same two kernels uncoloured (identity
-    page tables over contiguous buffers) with the same CU split (the paper's
-    control group) and uncoloured with no CU split.  LS runs a closed loop of
-    ``ls_launches`` kernels; BE streams triads for the whole LS window."""
-    import numpy as np
+def corun_operands(torch, sg, synth, ctx):
+    """Operands of the co-located pair (C4): the LS GEMV's bf16 W (4096 x
+    11008) in 2 MiB pages on colours 0..47 (4 rotated copies) and contiguous,
+    x and y; the BE triad's three 2 GiB fp32 arrays in 64 KiB pages on
+    colours 48..63 and contiguous."""
     dev = "cuda:0"
-    n_cus = ctx.num_cus
-    ls_cus, be_cus = list(range(n_cus * 3 // 4)), list(range(n_cus * 3 // 4, n_cus))
     M, K = 4096, 11008
     g = torch.Generator(device=dev)
     g.manual_seed(11)
@@ -532,6 +539,24 @@ def bench_corun(torch, sg, synth, ctx, ls_launches):
         sg.bimodal_relayout(ctx, T_col[i], sg.paged(lin[i], ident, pages), n * 4, shift)
     T_plain = [sg.paged(lin[i], ident, pages) for i in range(3)]
     torch.cuda.synchronize()
+    return {"M": M, "K": K, "wshift": wshift, "copies": copies, "W_col": W_col,
+            "W_plain": W_plain, "x": x, "y": y, "shift": shift, "n": n, "T_col": T_col,
+            "T_plain": T_plain, "_keep": (w_raw, w_plain, be_raw, lin, w_pt, be_pt, w_ident, ident)}
+
+
+def bench_corun(torch, sg, synth, ctx, ls_launches, ops):
+    """Co-located pair: LS GEMV (bf16 4096x11008, batch 1) on colours 0..47 and
+    CUs 0..191, BE triad (three 2 GiB fp32 arrays, 64 KiB pages) on colours
+    48..63 and CUs 192..255, against the same two kernels uncoloured (identity
+    page tables over contiguous buffers) with the same CU split (the paper's
+    control group) and uncoloured with no CU split.  LS runs a closed loop of
+    ``ls_launches`` kernels; BE streams triads for the whole LS window."""
+    import numpy as np
+    n_cus = ctx.num_cus
+    ls_cus, be_cus = list(range(n_cus * 3 // 4)), list(range(n_cus * 3 // 4, n_cus))
+    M, K, wshift, copies = ops["M"], ops["K"], ops["wshift"], ops["copies"]
+    W_col, W_plain, x, y = ops["W_col"], ops["W_plain"], ops["x"], ops["y"]
+    shift, n, T_col, T_plain = ops["shift"], ops["n"], ops["T_col"], ops["T_plain"]
     log(f"corun: LS gemv {M}x{K} on {len(ls_cus)} CUs, BE triad 3x2 GiB on {len(be_cus)} CUs")
 
     s_ls = torch.cuda.Stream(device=0)
@@ -612,8 +637,116 @@ def bench_corun(torch, sg, synth, ctx, ls_launches):
     for k in ("isolated_ls_coloured_masked", "corun_coloured_masked", "corun_uncoloured_masked",
               "corun_uncoloured_unmasked", "corun_coloured_masked_ls_cap3"):
         log(f"corun {k}: {res[k]}")
-    del w_raw, be_raw, lin, w_plain
-    torch.cuda.empty_cache()
+    return res
+
+
+def bench_preempt(torch, sg, synth, ctx, ops, trials):
+    """Tidal handover (paper section 7.1) at the C4 sizes.  The BE triad
+    (3 x 2 GiB, colours 48..63) starts on all CUs as a preemptible launch.
+    After a random delay the LS side raises the eviction flag in its own
+    stream order (a device store stamped with the device clock), takes the
+    CUs of the sliding-window policy and launches its GEMV (bf16 4096x11008,
+    colours 0..47); the BE stream clears the flag after its evicted kernel
+    and resumes on the CUs left.  Everything is enqueued without host waits.
+    Reported from the device time log: eviction latency (flag store -> end
+    of the BE kernel), LS latency from the flag store to the GEMV's end and
+    the GEMV's own span, the BE makespan (first start -> resumed end)
+    against an uninterrupted triad on all CUs; and the cost of the
+    preemptible triad kernel when nothing evicts it."""
+    import numpy as np
+    dev = "cuda:0"
+    khz = ctx.wallclock_khz
+    n_cus = ctx.num_cus
+    M, K, wshift, copies = ops["M"], ops["K"], ops["wshift"], ops["copies"]
+    Ws, x, y = ops["W_col"], ops["x"], ops["y"]
+    shift, n, T = ops["shift"], ops["n"], ops["T_col"]
+    ls_need = [n_cus * 3 // 4]
+    ls_cus, be_cus = sg.tidal_masks(n_cus, ls_need, window=4, granule=32)
+    s_ls, s_be = torch.cuda.Stream(device=0), torch.cuda.Stream(device=0)
+    flag = torch.zeros(1, dtype=torch.int32, device=dev)
+    stamps = torch.zeros(trials, dtype=torch.int64, device=dev)
+    us = lambda t: t * 1e3 / khz
+
+    def triad(stream):
+        sg.colored_stream(ctx, T[0], T[1], T[2], 3.0, n, shift, stream)
+
+    # the cost of the preemptible kernel (flag never raised) against the
+    # plain one, interleaved on all CUs
+    spans = {False: [], True: []}
+    for rep in range(6):
+        for pre in (False, True):
+            sg.set_eviction_flag(ctx, s_be, flag if pre else None)
+            d = DevTimes(torch, ctx, s_be, 1)
+            triad(s_be)
+            spans[pre].append(float(d.close_us()[0]))
+    plain_us, pre_us = np.median(spans[False][1:]), np.median(spans[True][1:])
+    log(f"preempt: triad plain {plain_us:.1f} us, preemptible {pre_us:.1f} us")
+
+    # delay calibration of torch's sleep kernel (cycles per microsecond)
+    with torch.cuda.stream(s_ls):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(s_ls)
+        torch.cuda._sleep(1000000)
+        e1.record(s_ls)
+    torch.cuda.synchronize()
+    cyc_per_us = 1000000 / max(e0.elapsed_time(e1) * 1e3, 1.0)
+
+    sg.set_eviction_flag(ctx, s_be, flag)
+    sg.set_stream_occupancy(ctx, s_be, 3)
+    for i in range(3):        # warm both kernels on their masks
+        sg.colored_gemv(ctx, Ws[i % copies], sg.BF16, M, K, x, sg.BF16, 1, y, wshift, s_ls)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(3)
+    dev_be = DevTimes(torch, ctx, s_be, 2 * trials)
+    dev_ls = DevTimes(torch, ctx, s_ls, trials)
+    for i in range(trials):
+        flag.zero_()
+        torch.cuda.synchronize()
+        sg.set_cu_mask(ctx, s_be, None)
+        triad(s_be)
+        with torch.cuda.stream(s_ls):
+            torch.cuda._sleep(int(rng.uniform(0.1, 0.8) * plain_us * cyc_per_us))
+        sg.signal_flag(ctx, s_ls, flag, 1, stamps[i:i + 1])
+        sg.set_cu_mask(ctx, s_ls, ls_cus)
+        sg.colored_gemv(ctx, Ws[i % copies], sg.BF16, M, K, x, sg.BF16, 1, y, wshift, s_ls)
+        sg.signal_flag(ctx, s_be, flag, 0)
+        sg.set_cu_mask(ctx, s_be, be_cus)
+        sg.resume(ctx, s_be)
+        torch.cuda.synchronize()
+    tb = dev_be.close_ticks(2 * trials).reshape(trials, 2, 2)
+    tl = dev_ls.close_ticks(trials)
+    sig = stamps.cpu().numpy()
+    left = sg.suspended(ctx, s_be)
+    sg.set_eviction_flag(ctx, s_be, None)
+    sg.set_cu_mask(ctx, s_be, None)
+    sg.set_cu_mask(ctx, s_ls, None)
+    sg.set_stream_occupancy(ctx, s_be, 0)
+    first_end, first_start, resume_end = tb[:, 0, 1], tb[:, 0, 0], tb[:, 1, 1]
+    hit = first_end > sig           # the flag landed while the BE kernel ran
+    evict = us(first_end - sig)[hit]
+    ls_from_flag = us(tl[:, 1] - sig)[hit]
+    ls_span = us(tl[:, 1] - tl[:, 0])[hit]
+    makespan = us(resume_end - first_start)[hit]
+
+    def p(a, q):
+        return round(float(np.percentile(a, q)), 2) if len(a) else None
+
+    res = {"what": "BE fp32 triad 3x2 GiB (colours 48..63) evicted from all CUs by an LS bf16 "
+                   "GEMV 4096x11008 batch 1 (colours 0..47); sliding-window split "
+                   f"{len(ls_cus)} LS / {len(be_cus)} BE CUs",
+           "trials": trials, "evicted_trials": int(hit.sum()), "left_after_last_trial": int(left),
+           "eviction_latency_p50_us": p(evict, 50), "eviction_latency_p99_us": p(evict, 99),
+           "ls_from_flag_p50_us": p(ls_from_flag, 50), "ls_from_flag_p99_us": p(ls_from_flag, 99),
+           "ls_gemv_span_p50_us": p(ls_span, 50), "ls_gemv_span_p99_us": p(ls_span, 99),
+           "be_makespan_p50_us": p(makespan, 50),
+           "be_uninterrupted_us": round(float(plain_us), 2),
+           "triad_plain_us": round(float(plain_us), 2),
+           "triad_preemptible_us": round(float(pre_us), 2),
+           "preemptible_overhead_pct": round(100 * (pre_us / plain_us - 1), 2),
+           "timing": "device time log and device clock stamps of the flag store; p50/p99 over "
+                     "the trials whose flag landed while the BE kernel ran"}
+    log(f"preempt: {res}")
     return res
 
 

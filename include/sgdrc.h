@@ -173,8 +173,8 @@ int set_cu_mask(sgdrc_ctx *ctx, void *stream, const sgdrc_cu_mask *mask);
  * eviction flag that the persistent kernel polls; the kernel then restarts
  * on fewer units).  With a flag set, later colored_stream and
  * bimodal_relayout launches on ``stream`` are preemptible: each workgroup
- * reads *d_flag with every tile it claims and, once it reads non-zero,
- * finishes the tile it holds and leaves.  If tiles remain unclaimed, the
+ * reads *d_flag at the start of every tile and, once it reads non-zero,
+ * finishes that tile and leaves.  If tiles remain unclaimed, the
  * launch ends "suspended": the rest of the work, including the last n mod
  * 16 bytes, waits for sgdrc_resume.  Every tile is processed exactly once
  * over a launch and its resumptions, so the result equals an uninterrupted
@@ -197,6 +197,17 @@ int sgdrc_set_eviction_flag(sgdrc_ctx *ctx, void *stream, const uint32_t *d_flag
  * Asynchronous.  EINVAL: no preemptible launch on the stream, or the mask
  * allows no CU. */
 int sgdrc_resume(sgdrc_ctx *ctx, void *stream);
+
+/* Enqueues on ``stream`` a one-thread kernel that stores ``value`` to
+ * *d_flag (a device-scope store, seen by kernels running on other streams)
+ * and, if d_stamp is not NULL, writes the device wall-clock tick of the
+ * store to *d_stamp (the clock of sgdrc_set_timelog).  This is how a
+ * latency-sensitive stream evicts a best-effort one in stream order (value
+ * 1 before its own kernels), and how the best-effort stream clears the
+ * flag before resuming (value 0).  EINVAL: d_flag NULL or misaligned,
+ * d_stamp misaligned. */
+int sgdrc_signal_flag(sgdrc_ctx *ctx, void *stream, uint32_t *d_flag, uint32_t value,
+                      uint64_t *d_stamp);
 
 /* Waits for ``stream``, then sets *tiles_left to the number of tiles that
  * the stream's last preemptible launch still has to process: 0 when it has

@@ -78,6 +78,7 @@ def lib() -> ctypes.CDLL:
             "sgdrc_set_stream_occupancy": ([vp, vp, u32], i32),
             "sgdrc_set_eviction_flag": ([vp, vp, vp], i32),
             "sgdrc_resume": ([vp, vp], i32),
+            "sgdrc_signal_flag": ([vp, vp, vp, u32, vp], i32),
             "sgdrc_suspended": ([vp, vp, P(u64)], i32),
             "sgdrc_tidal_masks": ([u32, P(u32), u32, u32, u32, P(CuMask), P(CuMask)], i32),
             "colour_classify": ([vp, P(Hash), vp, u64, vp, vp, vp], i32),
@@ -235,6 +236,13 @@ def set_eviction_flag(ctx, stream, flag) -> None:
 def resume(ctx, stream=None) -> None:
     """Enqueue the continuation of the stream's last preemptible launch."""
     _check(lib().sgdrc_resume(_h(ctx), _stream(stream)))
+
+
+def signal_flag(ctx, stream, flag, value: int, stamp=None) -> None:
+    """Enqueue on ``stream`` a device store of ``value`` to ``flag`` (and of
+    the device clock to ``stamp``, an int64 tensor element, if given)."""
+    _check(lib().sgdrc_signal_flag(_h(ctx), _stream(stream), _addr(flag), int(value),
+                                   _addr(stamp)))
 
 
 def suspended(ctx, stream=None) -> int:

@@ -193,6 +193,17 @@ int discard_suspended(Ctx *c, void *stream)
     return SGDRC_OK;
 }
 
+// One thread: store ``value`` to the flag and stamp the device wall clock.
+__global__ __launch_bounds__(64) void k_signal_flag(uint32_t *flag, uint32_t value, uint64_t *stamp)
+{
+    if (threadIdx.x != 0)
+        return;
+    __hip_atomic_store(flag, value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (stamp)
+        __hip_atomic_store(stamp, __builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+
 bool stream_preemptible(Ctx *c, void *stream)
 {
     std::lock_guard<std::mutex> lock(c->mu);
@@ -704,6 +715,24 @@ int sgdrc_tidal_masks(uint32_t num_cus, const uint32_t *ls_cus, uint32_t n_queue
         sgdrc_cu_mask *m = cu < r ? ls_mask : be_mask;
         m->bits[cu >> 6] |= 1ull << (cu & 63);
     }
+    return SGDRC_OK;
+}
+
+int sgdrc_signal_flag(sgdrc_ctx *ctx, void *stream, uint32_t *d_flag, uint32_t value,
+                      uint64_t *d_stamp)
+{
+    clear_error();
+    if (!d_flag || (reinterpret_cast<uintptr_t>(d_flag) & 3u))
+        return set_error(SGDRC_EINVAL, "flag NULL or not 4-byte aligned");
+    if (reinterpret_cast<uintptr_t>(d_stamp) & 7u)
+        return set_error(SGDRC_EINVAL, "stamp not 8-byte aligned");
+    Ctx *c = nullptr;
+    int rc = check_ctx(ctx, &c);
+    if (rc)
+        return rc;
+    hipLaunchKernelGGL(k_signal_flag, dim3(1), dim3(64), 0, reinterpret_cast<hipStream_t>(stream),
+                       d_flag, value, d_stamp);
+    SGDRC_HIP(hipGetLastError());
     return SGDRC_OK;
 }
 

@@ -218,9 +218,9 @@ enum class Claim { Ahead, Mid, After };
 // effect.
 //
 // Preemptible launches (EV, Claim::Mid only): a workgroup reads the
-// eviction flag ``*g.evict`` together with each ticket it claims (and once
-// at its start).  Once it has seen the flag set it takes no more tickets:
-// it finishes the tile it already holds and leaves, and marks the slot.
+// eviction flag ``*g.evict`` at its start and at the start of each tile.
+// Once it has seen the flag set it takes no more tickets: it finishes the
+// tile it is working on and leaves, and marks the slot.
 // If tiles are left unclaimed when the last workgroup arrives and some
 // workgroup stopped on the flag, the launch is suspended instead of
 // completed: the last workgroup leaves the remaining tiles and the
@@ -308,28 +308,29 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
         for (;;) {
             if (k < hi - lo) {
                 uint32_t *const ctr = &g.q->grp_next[grp * kCounterStride];
+                // preemptible: the flag is read before the tile's loads, so
+                // that its value is back when the next ticket is claimed; once
+                // it is set, the claim adds 0 (no branch around the atomic)
+                // and this tile is the workgroup's last
                 uint32_t fl = 0u;
+                if (EV && threadIdx.x == 0)
+                    fl = __hip_atomic_load(g.evict, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 if (CL == Claim::Ahead && threadIdx.x == 0)
                     next = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 auto claim = [&]() {
-                    if (CL == Claim::Mid && threadIdx.x == 0) {
-                        if (!stop)
-                            next = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED,
-                                                          __HIP_MEMORY_SCOPE_AGENT);
-                        if (EV)
-                            fl = __hip_atomic_load(g.evict, __ATOMIC_RELAXED,
-                                                   __HIP_MEMORY_SCOPE_AGENT);
-                    }
+                    if (CL == Claim::Mid && threadIdx.x == 0)
+                        next = __hip_atomic_fetch_add(ctr, (EV && fl != 0u) ? 0u : 1u,
+                                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 };
                 log_tile(g, cu, lo + k);
                 body(lo + k, cu, err, claim);
                 if (CL == Claim::After && threadIdx.x == 0)
                     next = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 if (threadIdx.x == 0) {
-                    // after a stop, the ticket taken before it is the last
-                    s_ticket = stop ? kLutNone : next;
+                    const bool halt = EV && fl != 0u;
+                    s_ticket = halt ? kLutNone : next;
                     if (EV)
-                        s_stop = (stop || fl != 0u) ? 1u : 0u;
+                        s_stop = halt ? 1u : 0u;
                 }
                 __syncthreads();
                 k = __builtin_amdgcn_readfirstlane(s_ticket);

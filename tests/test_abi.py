@@ -159,6 +159,10 @@ def test_preemption_argument_errors(L):
     assert L.sgdrc_resume(NULL, None) == sg.ENODEV
     assert L.sgdrc_suspended(NULL, None, None) == sg.EINVAL
     assert L.sgdrc_suspended(NULL, None, ctypes.byref(t)) == sg.ENODEV
+    assert L.sgdrc_signal_flag(NULL, None, None, 1, None) == sg.EINVAL    # NULL flag
+    assert L.sgdrc_signal_flag(NULL, None, 258, 1, None) == sg.EINVAL     # misaligned flag
+    assert L.sgdrc_signal_flag(NULL, None, 256, 1, 260) == sg.EINVAL      # misaligned stamp
+    assert L.sgdrc_signal_flag(NULL, None, 256, 1, 264) == sg.ENODEV
 
 
 # ------------------------------------------------- sliding-window reservation

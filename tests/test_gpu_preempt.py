@@ -293,28 +293,28 @@ def test_tidal_handover_ls_gemv_and_evicted_triad(ctx, orc):
     w = (synth.normal_f32(M * K, seed=9) * 0.02).astype(np.float32)
     x = synth.normal_f32(B * K, seed=10).astype(np.float32)
     wpt = np.arange(-(-M * K * 4 // 65536), dtype=np.uint32)
-    d_w, d_x = to_dev(w), to_dev(x)
+    d_w, d_x, d_wpt = to_dev(w), to_dev(x), to_dev(wpt)
     d_y = torch.zeros(B * M, dtype=torch.float32, device=DEV)
     ls_cus, be_cus = sg.tidal_masks(n_cu, [40, 96, 64], window=2, granule=32)
     assert len(ls_cus) == 96 and len(be_cus) == n_cu - 96
+    stamp = torch.zeros(1, dtype=torch.int64, device=DEV)
     try:
+        # all of it enqueued without waiting on the host: LS raises the flag
+        # in its own stream order, BE clears it after its evicted kernel and
+        # resumes on the CUs that the window leaves it
         sg.set_eviction_flag(ctx, be, flag)
         tr.launch(ctx, be)
         _delay(ls, 20)
-        with torch.cuda.stream(ls):
-            flag.fill_(1)                       # the LS task evicts the BE kernel
-        be.synchronize()
-        left = sg.suspended(ctx, be)
-        say(f"handover: triad suspended with {left} of {tr.tiles} tiles left")
-        sg.set_cu_mask(ctx, be, be_cus)
+        sg.signal_flag(ctx, ls, flag, 1, stamp)
         sg.set_cu_mask(ctx, ls, ls_cus)
-        flag.zero_()
-        torch.cuda.synchronize()
-        sg.resume(ctx, be)
-        sg.colored_gemv(ctx, sg.paged(d_w, to_dev(wpt), len(wpt)), sg.F32, M, K, d_x, sg.F32, B,
+        sg.colored_gemv(ctx, sg.paged(d_w, d_wpt, len(wpt)), sg.F32, M, K, d_x, sg.F32, B,
                         d_y, 16, ls)
+        sg.signal_flag(ctx, be, flag, 0)
+        sg.set_cu_mask(ctx, be, be_cus)
+        sg.resume(ctx, be)
         torch.cuda.synchronize()
         assert sg.suspended(ctx, be) == 0
+        assert int(to_host(stamp)[0]) > 0
     finally:
         sg.set_cu_mask(ctx, be, None)
         sg.set_cu_mask(ctx, ls, None)
