@@ -43,7 +43,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--rows", default="classify,pagetable,relayout,gemv,corun,preempt",
+    ap.add_argument("--rows", default="classify,pagetable,relayout,gemv,corun,preempt,bimodal",
                     help="comma list of extra rows to measure ('' for none)")
     ap.add_argument("--gemv-launches", type=int, default=300)
     ap.add_argument("--corun-launches", type=int, default=2000)
@@ -311,6 +311,9 @@ def main():
         flags["preempt"] = ctx.device_error()
     del ops
     torch.cuda.empty_cache()
+    if "bimodal" in want:
+        rows["bimodal"] = bench_bimodal(torch, sg, synth, ctx, stream)
+        flags["bimodal"] = ctx.device_error()
     if rows:
         result["rows"] = rows
 
@@ -748,6 +751,80 @@ def bench_preempt(torch, sg, synth, ctx, ops, trials):
                      "the trials whose flag landed while the BE kernel ran"}
     log(f"preempt: {res}")
     return res
+
+
+def bench_bimodal(torch, sg, synth, ctx, stream, reps=20, launches=100):
+    """Bimodal LS tensors (paper section 7.2) at the C3 shapes: both bf16
+    matrices (4096x11008, 11008x4096; 2 MiB pages) registered as
+    latency-sensitive tensors with an all-channel form and a form on colours
+    0..47.  Reported: the time of a state change (the runtime relays both
+    matrices between the forms; device time of the change on one stream)
+    and the batch-1 GEMV latency on the form the runtime hands out in each
+    state."""
+    import numpy as np
+    dev = "cuda:0"
+    shift = 21
+    P = 1 << shift
+    masks = synth.xor_masks(6, seed=1, min_bit=shift)
+    g = torch.Generator(device=dev)
+    g.manual_seed(13)
+    shapes = [(4096, 11008), (11008, 4096)]
+    keep = []
+    bm = sg.Bimodal(ctx)
+    ids = []
+    total = 0
+    for (M, K) in shapes:
+        nbytes = M * K * 2
+        pages = -(-nbytes // P)
+        w = (torch.randn(pages * P // 2, generator=g, device=dev) * 0.02).to(torch.bfloat16)
+        ident = torch.arange(pages, dtype=torch.int32, device=dev)
+        pool_pages = int(pages * 64 / 48 * 1.2) + 8
+        raw, base = aligned_pool(torch, pool_pages, shift)
+        pt = torch.empty(pages, dtype=torch.int32, device=dev)
+        sg.colour_alloc_pagetable(ctx, masks, base, shift, pool_pages, range(48), pages, pt)
+        ids.append(bm.register(sg.BM_LS_TENSOR, sg.paged(w, ident, pages),
+                               sg.paged(base, pt, pool_pages), nbytes, shift, stream))
+        keep += [w, ident, raw, pt]
+        total += nbytes
+    x = torch.randn(11008, generator=g, device=dev).to(torch.bfloat16)
+    y = torch.empty(11008, dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    trans = {sg.BM_COLOCATED: [], sg.BM_MONOPOLY: []}
+    for _ in range(reps):
+        for st in (sg.BM_COLOCATED, sg.BM_MONOPOLY):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            bm.set_state(st, stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            trans[st].append(e0.elapsed_time(e1))
+    out = {"what": "two bf16 C3 matrices as LS tensors: all-channel form vs colours 0..47 "
+                   "(2 MiB pages)", "bytes_moved_per_change": total}
+    for st, name in ((sg.BM_COLOCATED, "to_colocated"), (sg.BM_MONOPOLY, "to_monopoly")):
+        ms = float(np.median(trans[st]))
+        out[name + "_ms"] = round(ms, 4)
+        out[name + "_GBps"] = round(2 * total / (ms * 1e-3) / 1e9, 1)
+    for st, name in ((sg.BM_MONOPOLY, "monopoly"), (sg.BM_COLOCATED, "colocated")):
+        bm.set_state(st, stream)
+        for (M, K), tid in zip(shapes, ids):
+            desc, form = bm.input(tid)
+            with torch.cuda.stream(stream):
+                for _ in range(10):
+                    sg.colored_gemv(ctx, desc, sg.BF16, M, K, x, sg.BF16, 1, y, shift, stream)
+                d = DevTimes(torch, ctx, stream, launches)
+                for _ in range(launches):
+                    sg.colored_gemv(ctx, desc, sg.BF16, M, K, x, sg.BF16, 1, y, shift, stream)
+                spans = d.close_us()
+            out[f"gemv_{M}x{K}_{name}_p50_us"] = round(float(np.median(spans)), 2)
+            out[f"gemv_{M}x{K}_{name}_form"] = "all" if form == sg.BM_ALL else "colours 0..47"
+    bm.set_state(sg.BM_MONOPOLY, stream)
+    torch.cuda.synchronize()
+    bm.close()
+    log(f"bimodal: {out}")
+    del keep
+    torch.cuda.empty_cache()
+    return out
 
 
 def cpu_baseline(np, synth, masks, shift, pages, pools_desc, b_host, c_host, fractions,

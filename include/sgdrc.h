@@ -291,6 +291,75 @@ int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, 
                  const void *d_x, int x_dtype, uint32_t batch, float *d_y,
                  uint32_t page_shift, void *stream);
 
+/* ---------------------------------------------------- bimodal tensors
+ *
+ * Host runtime for the paper's bimodal tensors (section 7.2): which page
+ * set every tensor argument of a kernel uses, by tensor class and by the
+ * co-location state, and the moves between page sets when the state
+ * changes.  Each tensor has two forms given by the caller: ``all_form``
+ * (a page set over all channels, e.g. an identity table over a plain
+ * buffer) and ``part_form`` (a coloured page set: the best-effort colours
+ * for best-effort tensors, the latency-sensitive colours for
+ * latency-sensitive ones), both able to hold n_bytes.
+ *
+ *  SGDRC_BM_BE_WEIGHT   memory-bound best-effort input: two resident copies
+ *                       (registration fills part_form from all_form); read
+ *                       from all_form in SGDRC_BM_MONOPOLY, from part_form
+ *                       in SGDRC_BM_COLOCATED; never written.
+ *  SGDRC_BM_LS_TENSOR   memory-bound latency-sensitive tensor: one copy,
+ *                       given in all_form at registration, kept in
+ *                       part_form while COLOCATED and in all_form while
+ *                       MONOPOLY (sgdrc_bm_set_state moves it).
+ *  SGDRC_BM_ACTIVATION  intermediate result buffer (capacity n_bytes):
+ *                       written in the form of the writing kernel's state
+ *                       and read from where it was last written; reused
+ *                       through sgdrc_bm_acquire / sgdrc_bm_release.
+ *
+ * Moves are bimodal_relayout launches on the given stream; the caller
+ * orders them against the kernels that use the tensors and keeps all
+ * buffers alive.  Thread-safe.  Errors as elsewhere; a NULL or destroyed
+ * runtime gives EINVAL. */
+typedef struct sgdrc_bimodal sgdrc_bimodal;
+enum { SGDRC_BM_BE_WEIGHT = 0, SGDRC_BM_LS_TENSOR = 1, SGDRC_BM_ACTIVATION = 2 };
+enum { SGDRC_BM_MONOPOLY = 0, SGDRC_BM_COLOCATED = 1 };  /* states */
+enum { SGDRC_BM_ALL = 0, SGDRC_BM_PART = 1 };            /* forms */
+
+/* New runtime in state SGDRC_BM_MONOPOLY.  ctx may be NULL: such a runtime
+ * holds activations only (no moves).  Host-only. */
+int sgdrc_bm_create(sgdrc_ctx *ctx, sgdrc_bimodal **out);
+int sgdrc_bm_destroy(sgdrc_bimodal *bm);
+
+/* Registers a tensor of class ``cls`` (see above); *id receives its index
+ * (0, 1, ... in registration order).  A BE weight's part_form copy, and an
+ * LS tensor's move when the runtime is COLOCATED, are enqueued on
+ * ``stream``.  EINVAL: unknown class, bad forms or page_shift, n_bytes 0,
+ * NULL id; ENODEV: a weight or LS tensor on a runtime without context. */
+int sgdrc_bm_register(sgdrc_bimodal *bm, uint32_t cls, const sgdrc_paged *all_form,
+                      const sgdrc_paged *part_form, uint64_t n_bytes, uint32_t page_shift,
+                      void *stream, uint32_t *id);
+
+/* Changes the state; on a change every LS tensor moves to its form for the
+ * new state (relayouts on ``stream``).  EINVAL: unknown state. */
+int sgdrc_bm_set_state(sgdrc_bimodal *bm, int state, void *stream);
+int sgdrc_bm_state(sgdrc_bimodal *bm, int *state);
+
+/* The descriptor a kernel reads tensor ``id`` through, and (if ``where``
+ * is not NULL) which form it is.  EINVAL: unknown id, or an activation not
+ * written since it was acquired. */
+int sgdrc_bm_input(sgdrc_bimodal *bm, uint32_t id, sgdrc_paged *out, int *where);
+
+/* The descriptor a kernel writes tensor ``id`` through: for an activation
+ * the form of the current state, recorded as where it now lives; for an
+ * LS tensor its current form.  EINVAL: unknown id, a BE weight. */
+int sgdrc_bm_output(sgdrc_bimodal *bm, uint32_t id, sgdrc_paged *out, int *where);
+
+/* Takes the free activation with the smallest capacity of at least
+ * n_bytes (lowest id among equals); its contents count as unwritten.
+ * ENOMEM: none free.  Release returns it to the free list (EINVAL if it is
+ * not an acquired activation). */
+int sgdrc_bm_acquire(sgdrc_bimodal *bm, uint64_t n_bytes, uint32_t *id);
+int sgdrc_bm_release(sgdrc_bimodal *bm, uint32_t id);
+
 #ifdef __cplusplus
 }
 #endif

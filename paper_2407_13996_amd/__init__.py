@@ -23,6 +23,9 @@ DEVERR_PT_RANGE = 1
 DEVFLAG_GATE_FALLBACK = 2
 DEVERR_SUSPENDED_DROPPED = 4
 MAX_MASKS = 8
+BM_BE_WEIGHT, BM_LS_TENSOR, BM_ACTIVATION = 0, 1, 2
+BM_MONOPOLY, BM_COLOCATED = 0, 1
+BM_ALL, BM_PART = 0, 1
 
 
 class SgdrcError(RuntimeError):
@@ -81,6 +84,15 @@ def lib() -> ctypes.CDLL:
             "sgdrc_signal_flag": ([vp, vp, vp, u32, vp], i32),
             "sgdrc_suspended": ([vp, vp, P(u64)], i32),
             "sgdrc_tidal_masks": ([u32, P(u32), u32, u32, u32, P(CuMask), P(CuMask)], i32),
+            "sgdrc_bm_create": ([vp, P(vp)], i32),
+            "sgdrc_bm_destroy": ([vp], i32),
+            "sgdrc_bm_register": ([vp, u32, P(Paged), P(Paged), u64, u32, vp, P(u32)], i32),
+            "sgdrc_bm_set_state": ([vp, i32, vp], i32),
+            "sgdrc_bm_state": ([vp, P(i32)], i32),
+            "sgdrc_bm_input": ([vp, u32, P(Paged), P(i32)], i32),
+            "sgdrc_bm_output": ([vp, u32, P(Paged), P(i32)], i32),
+            "sgdrc_bm_acquire": ([vp, u64, P(u32)], i32),
+            "sgdrc_bm_release": ([vp, u32], i32),
             "colour_classify": ([vp, P(Hash), vp, u64, vp, vp, vp], i32),
             "colour_alloc_pagetable": ([vp, P(Hash), u64, u32, u64, P(ColourSet), u64, vp,
                                         P(u64), vp], i32),
@@ -302,3 +314,62 @@ def colored_gemv(ctx, w: Paged, w_dtype: int, M: int, K: int, x, x_dtype: int, b
     _check(lib().colored_gemv(_h(ctx), ctypes.byref(w), int(w_dtype), int(M), int(K), _addr(x),
                               int(x_dtype), int(batch), _addr(y), int(page_shift),
                               _stream(stream)))
+
+
+class Bimodal:
+    """The bimodal tensor runtime: tensor forms by class and co-location
+    state.  ``ctx`` may be None (activations only)."""
+
+    def __init__(self, ctx=None):
+        h = ctypes.c_void_p()
+        _check(lib().sgdrc_bm_create(_h(ctx) if ctx is not None else None, ctypes.byref(h)))
+        self.handle = h
+        self.has_ctx = ctx is not None
+        self._keep = []
+
+    def _st(self, stream):
+        # a runtime without context never moves data: no stream needed
+        return _stream(stream) if (self.has_ctx or stream is not None) else None
+
+    def register(self, cls: int, all_form: Paged, part_form: Paged, n_bytes: int,
+                 page_shift: int, stream=None) -> int:
+        i = ctypes.c_uint32()
+        _check(lib().sgdrc_bm_register(self.handle, int(cls), ctypes.byref(all_form),
+                                       ctypes.byref(part_form), int(n_bytes), int(page_shift),
+                                       self._st(stream), ctypes.byref(i)))
+        self._keep.append((all_form, part_form))
+        return i.value
+
+    def set_state(self, state: int, stream=None) -> None:
+        _check(lib().sgdrc_bm_set_state(self.handle, int(state), self._st(stream)))
+
+    @property
+    def state(self) -> int:
+        v = ctypes.c_int()
+        _check(lib().sgdrc_bm_state(self.handle, ctypes.byref(v)))
+        return v.value
+
+    def input(self, tid: int):
+        """(descriptor, form) a kernel reads tensor ``tid`` through."""
+        p, w = Paged(), ctypes.c_int()
+        _check(lib().sgdrc_bm_input(self.handle, int(tid), ctypes.byref(p), ctypes.byref(w)))
+        return p, w.value
+
+    def output(self, tid: int):
+        """(descriptor, form) a kernel writes tensor ``tid`` through."""
+        p, w = Paged(), ctypes.c_int()
+        _check(lib().sgdrc_bm_output(self.handle, int(tid), ctypes.byref(p), ctypes.byref(w)))
+        return p, w.value
+
+    def acquire(self, n_bytes: int) -> int:
+        i = ctypes.c_uint32()
+        _check(lib().sgdrc_bm_acquire(self.handle, int(n_bytes), ctypes.byref(i)))
+        return i.value
+
+    def release(self, tid: int) -> None:
+        _check(lib().sgdrc_bm_release(self.handle, int(tid)))
+
+    def close(self) -> None:
+        if self.handle is not None and self.handle.value:
+            _check(lib().sgdrc_bm_destroy(self.handle))
+        self.handle = None

@@ -23,7 +23,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libsgdrc.so")
-SOURCES = ["context.hip", "colour.hip", "stream.hip", "gemv.hip"]
+SOURCES = ["context.hip", "colour.hip", "stream.hip", "gemv.hip", "bimodal.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -216,3 +216,82 @@ def test_tidal_masks_argument_errors(L):
     assert L.sgdrc_tidal_masks(4, q, 2, 2, 1, r(ls), r(be)) == sg.EINVAL   # 8 > 4 CUs
     assert L.sgdrc_tidal_masks(256, q, 2, 1, 1, None, r(be)) == sg.EINVAL
     assert L.sgdrc_tidal_masks(256, q, 2, 1, 1, r(ls), r(be)) == sg.OK
+
+
+# ------------------------------------------------------ bimodal runtime (host)
+# A runtime without context holds activations only, which is enough to check
+# the section 7.2 rules that need no data movement: an intermediate result is
+# written in the form of the writing kernel's state and read from where it
+# was last written, and buffers are reused smallest-fit.
+
+def _forms(base):
+    return sg.Paged(base, base + 4096, 8), sg.Paged(base + (1 << 20), base + (1 << 20) + 4096, 8)
+
+
+def test_bimodal_activation_follows_its_writer():
+    bm = sg.Bimodal(None)
+    try:
+        a, p = _forms(1 << 32)
+        t = bm.register(sg.BM_ACTIVATION, a, p, 4096, 12)
+        with pytest.raises(sg.SgdrcError):
+            bm.input(t)                                    # never written
+        assert bm.state == sg.BM_MONOPOLY
+        desc, w = bm.output(t)
+        assert w == sg.BM_ALL and desc.pool == a.pool and desc.pt == a.pt
+        bm.set_state(sg.BM_COLOCATED)
+        assert bm.input(t)[1] == sg.BM_ALL                 # read where written
+        desc, w = bm.output(t)
+        assert w == sg.BM_PART and desc.pool == p.pool
+        bm.set_state(sg.BM_MONOPOLY)
+        assert bm.input(t)[1] == sg.BM_PART
+        bm.set_state(sg.BM_MONOPOLY)                       # no change, no effect
+        assert bm.state == sg.BM_MONOPOLY
+    finally:
+        bm.close()
+
+
+def test_bimodal_activation_reuse_smallest_fit():
+    bm = sg.Bimodal(None)
+    try:
+        ids = [bm.register(sg.BM_ACTIVATION, *_forms(1 << 32), cap, 12)
+               for cap in (1 << 20, 4 << 20, 2 << 20, 2 << 20)]
+        assert ids == [0, 1, 2, 3]
+        assert bm.acquire(3 << 19) == 2                    # 1.5 MiB -> first 2 MiB buffer
+        assert bm.acquire(3 << 19) == 3
+        assert bm.acquire(3 << 19) == 1                    # then the 4 MiB one
+        with pytest.raises(sg.SgdrcError) as e:
+            bm.acquire(3 << 19)
+        assert e.value.code == sg.ENOMEM
+        assert bm.acquire(1) == 0
+        bm.output(2)
+        bm.release(2)
+        assert bm.acquire(100) == 2                        # reused, contents unwritten
+        with pytest.raises(sg.SgdrcError):
+            bm.input(2)
+        with pytest.raises(sg.SgdrcError):
+            bm.release(0) or bm.release(0)                 # second release of 0 fails
+    finally:
+        bm.close()
+
+
+def test_bimodal_argument_errors(L):
+    r = ctypes.byref
+    h = ctypes.c_void_p()
+    assert L.sgdrc_bm_create(NULL, None) == sg.EINVAL
+    assert L.sgdrc_bm_create(NULL, r(h)) == sg.OK
+    i = ctypes.c_uint32()
+    a, p = _forms(1 << 32)
+    assert L.sgdrc_bm_register(h, 3, r(a), r(p), 64, 12, None, r(i)) == sg.EINVAL      # class
+    assert L.sgdrc_bm_register(h, 2, r(a), r(p), 0, 12, None, r(i)) == sg.EINVAL       # 0 bytes
+    assert L.sgdrc_bm_register(h, 2, r(a), r(p), 64, 11, None, r(i)) == sg.EINVAL      # shift
+    assert L.sgdrc_bm_register(h, 2, None, r(p), 64, 12, None, r(i)) == sg.EINVAL
+    assert L.sgdrc_bm_register(h, 0, r(a), r(p), 64, 12, None, r(i)) == sg.ENODEV      # no ctx
+    assert L.sgdrc_bm_register(h, 1, r(a), r(p), 64, 12, None, r(i)) == sg.ENODEV
+    assert L.sgdrc_bm_set_state(h, 2, None) == sg.EINVAL
+    out = sg.Paged()
+    assert L.sgdrc_bm_input(h, 0, r(out), None) == sg.EINVAL                           # no id 0
+    assert L.sgdrc_bm_register(h, 2, r(a), r(p), 64, 12, None, r(i)) == sg.OK
+    assert L.sgdrc_bm_output(h, 0, None, None) == sg.EINVAL
+    assert L.sgdrc_bm_release(h, 0) == sg.EINVAL                                       # not acquired
+    assert L.sgdrc_bm_destroy(h) == sg.OK
+    assert L.sgdrc_bm_input(None, 0, r(out), None) == sg.EINVAL
