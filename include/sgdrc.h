@@ -53,7 +53,7 @@ extern "C" {
 
 #define SGDRC_MAX_MASKS 8
 #define SGDRC_MAX_CUS 256
-#define SGDRC_MIN_PAGE_SHIFT 12 /* 4 KiB */
+#define SGDRC_MIN_PAGE_SHIFT 10 /* 1 KiB: the paper's finest colouring granularity (section 6) */
 #define SGDRC_MAX_PAGE_SHIFT 30 /* 1 GiB */
 #define SGDRC_MAX_BATCH 8
 
@@ -247,7 +247,7 @@ int colour_classify(sgdrc_ctx *ctx, const sgdrc_hash *hash, const uint64_t *d_ad
  * qualifying pages in the whole pool.  Returns SGDRC_ENOMEM when
  * found < n_needed (d_pt then holds all ``found`` pages).  Synchronous:
  * returns after the result is in d_pt.  EINVAL: bad hash, page_shift
- * outside [12, 30], addr_origin not page aligned, pool beyond 2^48 bytes of
+ * outside [10, 30], addr_origin not page aligned, pool beyond 2^48 bytes of
  * address space, pool_pages > 2^32, n_needed > pool_pages, empty set or
  * a colour >= 2^K in it. */
 int colour_alloc_pagetable(sgdrc_ctx *ctx, const sgdrc_hash *hash, uint64_t addr_origin,
@@ -261,7 +261,7 @@ int colour_alloc_pagetable(sgdrc_ctx *ctx, const sgdrc_hash *hash, uint64_t addr
  * pt[b >> s] at the same in-page offset.  Both tables hold
  * ceil(n_bytes / 2^page_shift) entries.  Bytes of dst pages beyond n_bytes
  * are not written.  src and dst must not overlap.  EINVAL: NULL pointers,
- * pools not 256-byte aligned, page_shift outside [12, 30]. */
+ * pools not 256-byte aligned, page_shift outside [10, 30]. */
 int bimodal_relayout(sgdrc_ctx *ctx, const sgdrc_paged *dst, const sgdrc_paged *src,
                      uint64_t n_bytes, uint32_t page_shift, void *stream);
 

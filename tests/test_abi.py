@@ -73,7 +73,7 @@ def test_pagetable_argument_errors(L):
     h = good_hash(4)
     assert call_pt(L, h) == sg.ENODEV
     assert call_pt(L, None) == sg.EINVAL
-    assert call_pt(L, h, shift=11) == sg.EINVAL
+    assert call_pt(L, h, shift=9) == sg.EINVAL
     assert call_pt(L, h, shift=31) == sg.EINVAL
     assert call_pt(L, h, origin=4096, shift=16) == sg.EINVAL          # origin not page aligned
     assert call_pt(L, h, colours=(16,)) == sg.EINVAL                  # colour >= 2^K
@@ -93,7 +93,7 @@ def pg(pool=256, pt=256, pages=4):
 def test_relayout_and_stream_argument_errors(L):
     r = ctypes.byref
     assert L.bimodal_relayout(NULL, r(pg()), r(pg()), 100, 16, None) == sg.ENODEV
-    assert L.bimodal_relayout(NULL, r(pg()), r(pg()), 100, 11, None) == sg.EINVAL
+    assert L.bimodal_relayout(NULL, r(pg()), r(pg()), 100, 9, None) == sg.EINVAL
     assert L.bimodal_relayout(NULL, r(pg(pool=128)), r(pg()), 100, 16, None) == sg.EINVAL
     assert L.bimodal_relayout(NULL, r(pg(pt=0)), r(pg()), 100, 16, None) == sg.EINVAL
     assert L.bimodal_relayout(NULL, r(pg(pages=0)), r(pg()), 100, 16, None) == sg.EINVAL
@@ -283,7 +283,7 @@ def test_bimodal_argument_errors(L):
     a, p = _forms(1 << 32)
     assert L.sgdrc_bm_register(h, 3, r(a), r(p), 64, 12, None, r(i)) == sg.EINVAL      # class
     assert L.sgdrc_bm_register(h, 2, r(a), r(p), 0, 12, None, r(i)) == sg.EINVAL       # 0 bytes
-    assert L.sgdrc_bm_register(h, 2, r(a), r(p), 64, 11, None, r(i)) == sg.EINVAL      # shift
+    assert L.sgdrc_bm_register(h, 2, r(a), r(p), 64, 9, None, r(i)) == sg.EINVAL       # shift
     assert L.sgdrc_bm_register(h, 2, None, r(p), 64, 12, None, r(i)) == sg.EINVAL
     assert L.sgdrc_bm_register(h, 0, r(a), r(p), 64, 12, None, r(i)) == sg.ENODEV      # no ctx
     assert L.sgdrc_bm_register(h, 1, r(a), r(p), 64, 12, None, r(i)) == sg.ENODEV

@@ -127,6 +127,8 @@ def test_classify_repeated_launches_reset_histogram(ctx, orc):
     (12, 200003, 6, range(16), 40000, 0),
     (21, 5000, 6, range(48), 3000, 1 << 33),
     (16, 393216, 6, range(8), 3 * 16384, 1 << 36),  # three 1 GiB arrays at 8 of 64 colours
+    (10, 300000, 6, range(16), 60000, 1 << 30),     # 1 KiB sectors
+    (11, 100000, 6, range(24, 56), 40000, 0),       # 2 KiB sectors
 ])
 def test_pagetable_matches_oracle(ctx, orc, shift, pool, K, S, n, origin):
     say(f"pagetable shift={shift} pool={pool} K={K} |S|={len(S)} n={n}")
@@ -180,7 +182,8 @@ def make_tables(orc, shift, n_pages, S, seed, K=6):
 @pytest.mark.parametrize("shift,n_bytes", [(12, 37 * 4096 + 1234), (16, 9 * 65536 + 17),
                                            (21, 2 * 2097152 + 4096 * 3 + 5), (15, 1),
                                            (16, 64 * 65536), (14, 11 * 16384 + 4015),
-                                           (13, 15), (17, 3 * 131072 + 65536 + 32)])
+                                           (13, 15), (17, 3 * 131072 + 65536 + 32),
+                                           (10, 37 * 1024 + 77), (11, 19 * 2048 + 1500)])
 def test_relayout_matches_oracle(ctx, orc, shift, n_bytes):
     say(f"relayout shift={shift} n_bytes={n_bytes}")
     P = 1 << shift
@@ -221,7 +224,8 @@ def test_relayout_round_trip_fp16_is_identity(ctx, orc):
 
 @pytest.mark.parametrize("shift,n", [(12, 5 * 1024 + 77), (16, 3 * 16384 + 5), (16, 40 * 16384),
                                      (21, 524288 + 3), (13, 7), (14, 9 * 4096 + 2),
-                                     (15, 5 * 8192 + 1), (16, 3)])
+                                     (15, 5 * 8192 + 1), (16, 3), (10, 9 * 256 + 3),
+                                     (11, 40 * 512 + 1), (10, 600 * 256)])
 def test_triad_matches_oracle(ctx, orc, shift, n):
     say(f"triad shift={shift} n={n}")
     P = 1 << shift
@@ -449,6 +453,13 @@ def test_gemv_mfma_k_chunks(ctx, orc, M, K, B, dt):
     than a chunk."""
     say(f"gemv mfma {M}x{K} B={B} dtype {dt}, 4 KiB pages")
     run_gemv(ctx, orc, M, K, B, dt, dt, 12, seed=M + K + B)
+
+
+@pytest.mark.parametrize("shift,B", [(10, 1), (10, 8), (11, 2), (11, 5)])
+def test_gemv_sector_pages(ctx, orc, shift, B):
+    """W in 1 KiB and 2 KiB pages (the paper's sector granularities)."""
+    say(f"gemv bf16 300x1024 B={B}, {1 << (shift - 10)} KiB pages")
+    run_gemv(ctx, orc, 300, 1024, B, sg.BF16, sg.BF16, shift, seed=shift + B)
 
 
 @pytest.mark.parametrize("M,K,B", [(4096, 11008, 1), (11008, 4096, 8)])
