@@ -51,6 +51,12 @@ def lib():
         L.oracle_classify.restype = None
         L.oracle_pagetable.argtypes = [vp, u32, u64, u32, u64, vp, u64, vp]
         L.oracle_pagetable.restype = u64
+        L.oracle_lut_colour.argtypes = [u64, vp, u64, u64, u32]
+        L.oracle_lut_colour.restype = u32
+        L.oracle_classify_lut.argtypes = [vp, u64, vp, u64, u64, u32, vp, vp]
+        L.oracle_classify_lut.restype = None
+        L.oracle_pagetable_lut.argtypes = [vp, u64, u64, u32, u64, u32, u64, vp, u64, vp]
+        L.oracle_pagetable_lut.restype = u64
         L.oracle_relayout.argtypes = [vp, vp, vp, vp, u64, u32]
         L.oracle_relayout.restype = None
         L.oracle_triad.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.c_float, u64, u32]
@@ -136,3 +142,33 @@ def gemv(w_pool, pt_w, w_dtype: int, M: int, K: int, x, x_dtype: int, B: int,
                       int(x_dtype), int(B), int(page_shift), _ptr(y),
                       _ptr(ad) if ad is not None else None)
     return y, ad
+
+
+def lut_colour(addr: int, lut: np.ndarray, origin: int, lut_shift: int) -> int:
+    t = np.ascontiguousarray(lut, dtype=np.uint8)
+    return int(lib().oracle_lut_colour(int(addr), _ptr(t), int(origin), t.size, int(lut_shift)))
+
+
+def classify_lut(addrs: np.ndarray, lut: np.ndarray, origin: int, lut_shift: int,
+                 with_hist: bool = True):
+    """Returns (colours uint8[n], hist uint64[256] or None)."""
+    a = np.ascontiguousarray(addrs, dtype=np.uint64)
+    t = np.ascontiguousarray(lut, dtype=np.uint8)
+    colours = np.empty(a.size, dtype=np.uint8)
+    hist = np.empty(256, dtype=np.uint64) if with_hist else None
+    lib().oracle_classify_lut(_ptr(a), a.size, _ptr(t), int(origin), t.size, int(lut_shift),
+                              _ptr(colours), _ptr(hist) if hist is not None else None)
+    return colours, hist
+
+
+def pagetable_lut(lut: np.ndarray, origin: int, lut_shift: int, addr_origin: int,
+                  page_shift: int, pool_pages: int, colour_set_words, n_needed: int):
+    """Returns (pt uint32[min(found, n_needed)], found)."""
+    t = np.ascontiguousarray(lut, dtype=np.uint8)
+    s = np.ascontiguousarray(np.array([int(w) for w in colour_set_words], dtype=np.uint64))
+    assert s.size == 4
+    pt = np.zeros(max(n_needed, 1), dtype=np.uint32)
+    found = int(lib().oracle_pagetable_lut(_ptr(t), int(origin), t.size, int(lut_shift),
+                                           int(addr_origin), int(page_shift), int(pool_pages),
+                                           _ptr(s), int(n_needed), _ptr(pt)))
+    return pt[:min(found, n_needed)].copy(), found

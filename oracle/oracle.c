@@ -86,6 +86,66 @@ uint64_t oracle_pagetable(const uint64_t *masks, uint32_t n_masks, uint64_t orig
     return found;
 }
 
+/* Paper section 5.3: for hashes that are not XOR-linear, a table holds the
+ * channel of every partition (1 KiB there).  Entry i is the colour of the
+ * bytes [origin + i * 2^s, origin + (i + 1) * 2^s); an address outside the
+ * table has no colour, written 255 (as is an entry of 255). */
+uint32_t oracle_lut_colour(uint64_t addr, const uint8_t *lut, uint64_t origin, uint64_t entries,
+                           uint32_t lut_shift)
+{
+    if (addr < origin)
+        return 255u;
+    uint64_t i = (addr - origin) >> lut_shift;
+    if (i >= entries)
+        return 255u;
+    return lut[i];
+}
+
+void oracle_classify_lut(const uint64_t *addrs, uint64_t n, const uint8_t *lut, uint64_t origin,
+                         uint64_t entries, uint32_t lut_shift, uint8_t *colours, uint64_t *hist)
+{
+    if (hist)
+        for (uint32_t c = 0; c < 256u; ++c)
+            hist[c] = 0;
+    for (uint64_t i = 0; i < n; ++i) {
+        uint32_t c = oracle_lut_colour(addrs[i], lut, origin, entries, lut_shift);
+        colours[i] = (uint8_t)c;
+        if (hist)
+            hist[c] += 1;
+    }
+}
+
+/* Page-table build with a colour table (paper section 6 with the table of
+ * section 5.3): pool page i covers the bytes [a, a + 2^page_shift) with
+ * a = addr_origin + i * 2^page_shift; it qualifies when every partition it
+ * touches lies in the table and has a colour (not 255) in the set.
+ * Ascending page order, first n_needed pages; returns all qualifying. */
+uint64_t oracle_pagetable_lut(const uint8_t *lut, uint64_t origin, uint64_t entries,
+                              uint32_t lut_shift, uint64_t addr_origin, uint32_t page_shift,
+                              uint64_t pool_pages, const uint64_t colour_set[4],
+                              uint64_t n_needed, uint32_t *pt)
+{
+    const uint64_t page = 1ull << page_shift;
+    const uint64_t part = 1ull << lut_shift;
+    uint64_t found = 0;
+    for (uint64_t i = 0; i < pool_pages; ++i) {
+        const uint64_t first = addr_origin + i * page;
+        int ok = 1;
+        /* one address per partition the page touches: its first byte, then
+         * the start of every later partition inside the page */
+        for (uint64_t a = first; a < first + page && ok; a = (a | (part - 1u)) + 1u) {
+            uint32_t c = oracle_lut_colour(a, lut, origin, entries, lut_shift);
+            ok = c != 255u && in_set(colour_set, c);
+        }
+        if (ok) {
+            if (found < n_needed)
+                pt[found] = (uint32_t)i;
+            found += 1;
+        }
+    }
+    return found;
+}
+
 /* Paper section 7.2: switching a tensor between the all-channel and the
  * restricted page set is a move of its bytes from one set of pages to the
  * other; logical byte b keeps its place in the tensor. */

@@ -46,6 +46,25 @@ uint64_t oracle_pagetable(const uint64_t *masks, uint32_t n_masks, uint64_t orig
                           const uint64_t colour_set[4], uint64_t n_needed,
                           uint32_t *pt);
 
+/* Colour through a table of one colour per 2^lut_shift-byte partition
+ * (paper section 5.3): entry i covers [origin + i 2^s, origin + (i+1) 2^s).
+ * Outside the table, or an entry of 255: no colour, returned as 255. */
+uint32_t oracle_lut_colour(uint64_t addr, const uint8_t *lut, uint64_t origin, uint64_t entries,
+                           uint32_t lut_shift);
+
+/* colours[i] = oracle_lut_colour(addrs[i]); hist (256 entries, overwritten,
+ * may be NULL) counts every colour value including 255. */
+void oracle_classify_lut(const uint64_t *addrs, uint64_t n, const uint8_t *lut, uint64_t origin,
+                         uint64_t entries, uint32_t lut_shift, uint8_t *colours, uint64_t *hist);
+
+/* Page-table build through a colour table: page i = [addr_origin + i P,
+ * + P) qualifies when every partition it touches is in the table and has a
+ * colour (not 255) in the set.  As oracle_pagetable otherwise. */
+uint64_t oracle_pagetable_lut(const uint8_t *lut, uint64_t origin, uint64_t entries,
+                              uint32_t lut_shift, uint64_t addr_origin, uint32_t page_shift,
+                              uint64_t pool_pages, const uint64_t colour_set[4],
+                              uint64_t n_needed, uint32_t *pt);
+
 /* Bimodal relayout (paper section 7.2): for every logical byte b < n_bytes,
  * dst[pt_dst[b >> s] << s | (b & (2^s - 1))] = src[pt_src[b >> s] << s | ...]. */
 void oracle_relayout(uint8_t *dst_pool, const uint32_t *pt_dst, const uint8_t *src_pool,

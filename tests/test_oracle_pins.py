@@ -405,3 +405,73 @@ def test_gemv_tiny_exact_rational_sum(orc):
         exact = sum(Fraction(float(w[m * K + k])) * Fraction(float(x[b * K + k])) for k in range(K))
         assert abs(Fraction(y[b, m]) - exact) <= Fraction(K * 2 ** -52) * sum(
             abs(Fraction(float(w[m * K + k])) * Fraction(float(x[b * K + k]))) for k in range(K))
+
+
+# ------------------------------------------------ colour table (section 5.3)
+# The table form of the hash: one colour per 2^s-byte partition.
+
+def test_lut_colour_hand_worked(orc):
+    lut = np.array([3, 1, 255, 0], dtype=np.uint8)     # partitions of 1 KiB from 4096
+    assert orc.lut_colour(4096, lut, 4096, 10) == 3
+    assert orc.lut_colour(4096 + 1500, lut, 4096, 10) == 1
+    assert orc.lut_colour(4096 + 2048 + 5, lut, 4096, 10) == 255   # entry 255: no colour
+    assert orc.lut_colour(4096 + 3 * 1024 + 1023, lut, 4096, 10) == 0
+    assert orc.lut_colour(4095, lut, 4096, 10) == 255              # below the table
+    assert orc.lut_colour(4096 + 4 * 1024, lut, 4096, 10) == 255   # past its end
+    addrs = np.array([4096, 4096 + 1500, 4095, 4096 + 3100, 4096 + 1024], dtype=np.uint64)
+    col, hist = orc.classify_lut(addrs, lut, 4096, 10)
+    assert col.tolist() == [3, 1, 255, 0, 1]
+    assert hist[1] == 2 and hist[3] == 1 and hist[0] == 1 and hist[255] == 1 and hist.sum() == 5
+
+
+def test_pagetable_lut_hand_worked(orc):
+    lut = np.array([3, 1, 255, 0], dtype=np.uint8)
+    S = synth.colour_set_bits([0, 1, 3])
+    # 2 KiB pages from 4096: [p0 p1] = (3, 1) ok; [p2 p3] = (255, 0) no; past the table no
+    pt, found = orc.pagetable_lut(lut, 4096, 10, 4096, 11, 3, S, 3)
+    assert found == 1 and pt.tolist() == [0]
+    # 512 B pages from 4608: one partition each -> colours 3, 1, 1, 255, 255, 0, 0, (past)
+    pt, found = orc.pagetable_lut(lut, 4096, 10, 4608, 9, 8, synth.colour_set_bits([1]), 8)
+    assert found == 2 and pt.tolist() == [1, 2]
+    pt, found = orc.pagetable_lut(lut, 4096, 10, 4608, 9, 8, synth.colour_set_bits([0, 3]), 8)
+    assert pt.tolist() == [0, 5, 6] and found == 3
+
+
+def test_lut_from_xor_hash_agrees_with_the_xor_path(orc):
+    """A table filled with the XOR colours of the partition bases gives the
+    XOR results: classify for masks above the partition bits, and the page
+    table for masks above the page bits (colour constant over a page)."""
+    s, origin = 10, 1 << 30
+    entries = 1 << 14
+    masks = [m & ~((1 << 14) - 1) for m in synth.xor_masks(5, seed=4, min_bit=14)]
+    lut = np.array([orc.colour(origin + (i << s), masks) for i in range(entries)], dtype=np.uint8)
+    rng = np.random.default_rng(5)
+    addrs = (origin + rng.integers(0, entries << s, size=5000)).astype(np.uint64)
+    got, gh = orc.classify_lut(addrs, lut, origin, s)
+    ref, rh = orc.classify(addrs, masks)
+    assert (got == ref).all() and (gh[:32] == rh).all() and gh[32:].sum() == 0
+    S = synth.colour_set_bits([1, 4, 9, 30])
+    for shift in (13, 14):
+        pages = (entries << s) >> shift
+        got_pt, gf = orc.pagetable_lut(lut, origin, s, origin, shift, pages, S, pages)
+        ref_pt, rf = orc.pagetable(masks, origin, shift, pages, S, pages)
+        assert gf == rf and (got_pt == ref_pt).all()
+
+
+def test_pagetable_lut_needs_every_partition_of_the_page(orc):
+    """Masks below the page bits make partitions of one page differ; a page
+    then qualifies only if all of them are in the set, so the table form
+    takes a subset of the pages the base-address rule would take."""
+    s, origin = 10, 0
+    entries = 1 << 12
+    masks = [m & ~((1 << 10) - 1) for m in synth.xor_masks(4, seed=6, min_bit=10)]
+    lut = np.array([orc.colour(origin + (i << s), masks) for i in range(entries)], dtype=np.uint8)
+    S = synth.colour_set_bits(range(10))
+    shift = 12
+    pages = (entries << s) >> shift
+    got_pt, gf = orc.pagetable_lut(lut, origin, s, origin, shift, pages, S, pages)
+    base_pt, bf = orc.pagetable(masks, origin, shift, pages, S, pages)
+    assert set(got_pt.tolist()) <= set(base_pt.tolist()) and gf < bf
+    for p in got_pt:
+        cols = [orc.colour((int(p) << shift) + (j << s), masks) for j in range(4)]
+        assert all(c < 10 for c in cols)
