@@ -43,7 +43,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--rows", default="classify,pagetable,relayout,gemv,corun,preempt,bimodal",
+    ap.add_argument("--rows", default="classify,pagetable,relayout,gemv,corun,preempt,bimodal,sectors",
                     help="comma list of extra rows to measure ('' for none)")
     ap.add_argument("--gemv-launches", type=int, default=300)
     ap.add_argument("--corun-launches", type=int, default=2000)
@@ -314,6 +314,9 @@ def main():
     if "bimodal" in want:
         rows["bimodal"] = bench_bimodal(torch, sg, synth, ctx, stream)
         flags["bimodal"] = ctx.device_error()
+    if "sectors" in want:
+        rows["sectors"] = bench_sectors(torch, sg, synth, ctx, stream, timer)
+        flags["sectors"] = ctx.device_error()
     if rows:
         result["rows"] = rows
 
@@ -823,6 +826,90 @@ def bench_bimodal(torch, sg, synth, ctx, stream, reps=20, launches=100):
     bm.close()
     log(f"bimodal: {out}")
     del keep
+    torch.cuda.empty_cache()
+    return out
+
+
+def bench_sectors(torch, sg, synth, ctx, stream, timer, reps=20):
+    """Colouring granularity (paper section 6: 1-2 KiB sectors; section 5.3:
+    a colour table for hashes that are not XOR-linear).  The C2 triad (three
+    1 GiB fp32 arrays, colours 0..15 of 64) with 1, 2, 4 and 64 KiB pages:
+    the cost of finer page-table indirection.  Then classify and the page-
+    table build through a random colour table of 2^26 1 KiB partitions
+    (64 GiB of address space)."""
+    import numpy as np
+    dev = "cuda:0"
+    n = 1 << 28
+    out = {"what": "triad 3x1 GiB fp32 on colours 0..15 of 64 by page size; colour-table "
+                   "classify and page-table build"}
+    g = torch.Generator(device=dev)
+    g.manual_seed(21)
+    b_lin = torch.empty(n, dtype=torch.float32, device=dev).uniform_(-1, 1, generator=g)
+    c_lin = torch.empty(n, dtype=torch.float32, device=dev).uniform_(-1, 1, generator=g)
+    for shift in (10, 11, 12, 16):
+        P = 1 << shift
+        pages = (n * 4) >> shift
+        masks = synth.xor_masks(6, seed=1, min_bit=shift)
+        pool_pages = int(3 * pages * 4 * 1.08) + 64
+        raw, base = aligned_pool(torch, pool_pages, shift)
+        pt = torch.empty(3 * pages, dtype=torch.int32, device=dev)
+        e0 = time.perf_counter()
+        sg.colour_alloc_pagetable(ctx, masks, base, shift, pool_pages, range(16), 3 * pages, pt)
+        pt_ms = (time.perf_counter() - e0) * 1e3
+        A, B, C = (sg.paged(base, pt[i * pages:(i + 1) * pages], pool_pages) for i in range(3))
+        ident = torch.arange(pages, dtype=torch.int32, device=dev)
+        sg.bimodal_relayout(ctx, B, sg.paged(b_lin, ident, pages), n * 4, shift)
+        sg.bimodal_relayout(ctx, C, sg.paged(c_lin, ident, pages), n * 4, shift)
+        tag = ("sectors", shift)
+        with torch.cuda.stream(stream):
+            for _ in range(3):
+                sg.colored_stream(ctx, A, B, C, 3.0, n, shift, stream)
+            for _ in range(reps):
+                e = timer.start()
+                sg.colored_stream(ctx, A, B, C, 3.0, n, shift, stream)
+                timer.stop(e, tag)
+        torch.cuda.synchronize()
+        ms = pctl(timer.durations_ms(tag), 50)
+        out[f"triad_{P >> 10}KiB_GBps"] = round(12 * n / (ms * 1e-3) / 1e9, 1)
+        out[f"triad_{P >> 10}KiB_ms"] = round(ms, 4)
+        out[f"pagetable_{P >> 10}KiB_ms"] = round(pt_ms, 3)
+        log(f"sectors: {P >> 10} KiB pages: triad {ms:.4f} ms "
+            f"({12 * n / (ms * 1e-3) / 1e9:.0f} GB/s), page table {pt_ms:.2f} ms")
+        del raw, pt, A, B, C, ident
+        torch.cuda.empty_cache()
+    del b_lin, c_lin
+    # a random table of 2^26 1 KiB partitions
+    entries, origin = 1 << 26, 1 << 36
+    lut = torch.randint(0, 64, (entries,), dtype=torch.uint8, device=dev, generator=g)
+    t = sg.colour_table(lut, origin, 10)
+    na = 1 << 26
+    addrs = (origin + torch.randint(0, entries << 10, (na,), device=dev, generator=g)).to(torch.int64)
+    cols = torch.empty(na, dtype=torch.uint8, device=dev)
+    hist = torch.empty(256, dtype=torch.int64, device=dev)
+    tag = ("sectors", "classify_table")
+    with torch.cuda.stream(stream):
+        for _ in range(3):
+            sg.colour_classify_table(ctx, t, addrs, cols, hist, stream)
+        for _ in range(reps):
+            e = timer.start()
+            sg.colour_classify_table(ctx, t, addrs, cols, hist, stream)
+            timer.stop(e, tag)
+    torch.cuda.synchronize()
+    ms = pctl(timer.durations_ms(tag), 50)
+    out["classify_table_2e26_us"] = round(ms * 1e3, 2)
+    out["classify_table_addrs_per_s"] = round(na / (ms * 1e-3), 0)
+    pool_pages = entries                          # 1 KiB pages over the whole table
+    pt = torch.empty(1 << 20, dtype=torch.int32, device=dev)
+    times = []
+    for _ in range(5):
+        e0 = time.perf_counter()
+        sg.colour_alloc_pagetable_table(ctx, t, origin, 10, pool_pages, range(16), 1 << 20, pt,
+                                        stream)
+        times.append((time.perf_counter() - e0) * 1e3)
+    out["pagetable_table_1KiB_ms"] = round(float(np.median(times)), 3)
+    out["pagetable_table_pool_pages"] = pool_pages
+    log(f"sectors: {out}")
+    del lut, addrs, cols, pt
     torch.cuda.empty_cache()
     return out
 

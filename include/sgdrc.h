@@ -255,6 +255,41 @@ int colour_alloc_pagetable(sgdrc_ctx *ctx, const sgdrc_hash *hash, uint64_t addr
                            const sgdrc_colour_set *set, uint64_t n_needed, uint32_t *d_pt,
                            uint64_t *n_found, void *stream);
 
+/* A colour table (paper section 5.3: for hashes that are not XOR-linear, a
+ * table made offline holds the channel of every 1 KiB partition): lut[i]
+ * (device memory) is the colour of the bytes [origin + i 2^shift,
+ * origin + (i + 1) 2^shift); 255 means no colour, as does any address
+ * outside the table. */
+typedef struct {
+    const uint8_t *lut;
+    uint64_t origin;
+    uint64_t entries;
+    uint32_t shift;     /* log2 of the partition size, 8..30 */
+    uint32_t reserved;  /* must be 0 */
+} sgdrc_colour_table;
+
+/* colour_classify through a colour table: d_colours[i] = the colour of
+ * d_addrs[i] (255 if none); d_hist (nullable, 256 entries) counts every
+ * colour value, 255 included.  Same launch, gate and alignment rules as
+ * colour_classify.  EINVAL: NULL table, shift outside 8..30, reserved not
+ * 0, entries without a table pointer, a table past 2^48, NULL or
+ * misaligned buffers. */
+int colour_classify_table(sgdrc_ctx *ctx, const sgdrc_colour_table *table,
+                          const uint64_t *d_addrs, uint64_t n, uint8_t *d_colours,
+                          uint64_t *d_hist, void *stream);
+
+/* colour_alloc_pagetable through a colour table: pool page i, the bytes
+ * [a, a + 2^page_shift) with a = addr_origin + i 2^page_shift, qualifies
+ * when every partition it touches lies in the table and has a colour in the
+ * set.  Pages smaller than a partition (page_shift < shift) take the
+ * colour of their partition.  Synchronous, ENOMEM on shortfall, as
+ * colour_alloc_pagetable; EINVAL as there (the set may not name colour
+ * 255) and as colour_classify_table for the table. */
+int colour_alloc_pagetable_table(sgdrc_ctx *ctx, const sgdrc_colour_table *table,
+                                 uint64_t addr_origin, uint32_t page_shift, uint64_t pool_pages,
+                                 const sgdrc_colour_set *set, uint64_t n_needed, uint32_t *d_pt,
+                                 uint64_t *n_found, void *stream);
+
 /* Bimodal relayout (paper section 7.2, moving a tensor between its
  * all-channel and its restricted page set): copies n_bytes logical bytes,
  * logical byte b going from src's page pt[b >> s] to dst's page

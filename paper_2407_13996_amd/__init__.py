@@ -48,6 +48,11 @@ class CuMask(ctypes.Structure):
     _fields_ = [("bits", ctypes.c_uint64 * 4)]
 
 
+class ColourTable(ctypes.Structure):
+    _fields_ = [("lut", ctypes.c_void_p), ("origin", ctypes.c_uint64), ("entries", ctypes.c_uint64),
+                ("shift", ctypes.c_uint32), ("reserved", ctypes.c_uint32)]
+
+
 class Paged(ctypes.Structure):
     _fields_ = [("pool", ctypes.c_void_p), ("pt", ctypes.c_void_p),
                 ("pool_pages", ctypes.c_uint64)]
@@ -100,6 +105,9 @@ def lib() -> ctypes.CDLL:
             "colored_stream": ([vp, P(Paged), P(Paged), P(Paged), ctypes.c_float, u64, u32, vp],
                                i32),
             "colored_gemv": ([vp, P(Paged), i32, u32, u32, vp, i32, u32, vp, u32, vp], i32),
+            "colour_classify_table": ([vp, P(ColourTable), vp, u64, vp, vp, vp], i32),
+            "colour_alloc_pagetable_table": ([vp, P(ColourTable), u64, u32, u64, P(ColourSet), u64,
+                                              vp, P(u64), vp], i32),
         }
         for name, (args, res) in sigs.items():
             fn = getattr(L, name)
@@ -293,6 +301,33 @@ def colour_alloc_pagetable(ctx, masks, addr_origin: int, page_shift: int, pool_p
                                       int(page_shift), int(pool_pages),
                                       ctypes.byref(make_set(words_of(colours))), int(n_needed),
                                       _addr(pt), ctypes.byref(found), _stream(stream))
+    _check(rc, found.value)
+    return found.value
+
+
+def colour_table(lut, origin: int, shift: int) -> ColourTable:
+    """Descriptor of a colour table (uint8 device tensor, one entry per
+    2^shift-byte partition from ``origin``); keeps a reference to ``lut``."""
+    t = ColourTable(_addr(lut), int(origin), int(lut.numel()), int(shift), 0)
+    t._keep = lut
+    return t
+
+
+def colour_classify_table(ctx, table: ColourTable, addrs, colours, hist=None, stream=None) -> None:
+    _check(lib().colour_classify_table(_h(ctx), ctypes.byref(table), _addr(addrs),
+                                       int(addrs.numel()), _addr(colours), _addr(hist),
+                                       _stream(stream)))
+
+
+def colour_alloc_pagetable_table(ctx, table: ColourTable, addr_origin: int, page_shift: int,
+                                 pool_pages: int, colours, n_needed: int, pt, stream=None) -> int:
+    """Returns n_found; raises SgdrcError (code ENOMEM, .n_found) on shortfall."""
+    found = ctypes.c_uint64()
+    rc = lib().colour_alloc_pagetable_table(_h(ctx), ctypes.byref(table), int(addr_origin),
+                                            int(page_shift), int(pool_pages),
+                                            ctypes.byref(make_set(words_of(colours))),
+                                            int(n_needed), _addr(pt), ctypes.byref(found),
+                                            _stream(stream))
     _check(rc, found.value)
     return found.value
 

@@ -61,6 +61,22 @@ __device__ __forceinline__ uint32_t colour_lut(const uint8_t (*lut)[256], uint32
            (uint32_t)lut[4][hi & 0xffu] ^ (uint32_t)lut[5][(hi >> 8) & 0xffu];
 }
 
+// The table form of the hash (paper section 5.3): one colour byte per
+// 2^shift-byte partition from ``origin``; 255 = no colour (also outside).
+struct TableArgs {
+    const uint8_t *lut;
+    uint64_t origin;
+    uint64_t entries;
+    uint32_t shift;
+};
+
+__device__ __forceinline__ uint32_t table_colour(const TableArgs &t, uint64_t a)
+{
+    const uint64_t i = (a - t.origin) >> t.shift;
+    const bool in = a >= t.origin && i < t.entries;
+    return in ? (uint32_t)t.lut[in ? i : 0u] : 255u;
+}
+
 constexpr int kClsThreads = 256;
 constexpr int kClsLoads = 16;                            // 16-byte loads per lane per tile
 constexpr uint32_t kClsWaveTile = 64u * 2u * kClsLoads;  // 2048 addresses per wavefront
@@ -78,12 +94,14 @@ constexpr int kClsHistWgsPerCu = 1;
 // the LDS atomics of one wavefront rarely meet on one address.
 constexpr int kHistCopies = 16;
 
-template <int K, bool HIST>
+// TAB: colours come from a colour table in device memory (one gathered
+// byte per address) instead of the XOR hash; K is then 8 (256 bins).
+template <int K, bool HIST, bool TAB>
 __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__restrict__ addrs,
                                                           uint64_t n, uint8_t *__restrict__ colours,
-                                                          HashArgs h, uint64_t *hist_acc,
-                                                          uint64_t *hist_out, uint32_t n_tiles,
-                                                          Gate g)
+                                                          HashArgs h, TableArgs tab,
+                                                          uint64_t *hist_acc, uint64_t *hist_out,
+                                                          uint32_t n_tiles, Gate g)
 {
     constexpr uint32_t kBins = 1u << K;
     __shared__ uint32_t s_hist[HIST ? kBins * kHistCopies : 1];
@@ -113,8 +131,10 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
         claim();
 #pragma unroll
         for (int j = 0; j < kClsLoads; ++j) {
-            const uint32_t c0 = colour_lut(s_lut, v[j].x, v[j].y);
-            const uint32_t c1 = colour_lut(s_lut, v[j].z, v[j].w);
+            const uint32_t c0 = TAB ? table_colour(tab, ((uint64_t)v[j].y << 32) | v[j].x)
+                                    : colour_lut(s_lut, v[j].x, v[j].y);
+            const uint32_t c1 = TAB ? table_colour(tab, ((uint64_t)v[j].w << 32) | v[j].z)
+                                    : colour_lut(s_lut, v[j].z, v[j].w);
             s_col[wave][j * 64u + lane] = (uint16_t)(c0 | (c1 << 8));
             // both addresses of the load are valid or neither (valid is even)
             if (HIST && 2u * (j * 64u + lane) < valid) {
@@ -157,7 +177,8 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
         const uint64_t i = n16 + threadIdx.x;
         if (i < n) {
             const uint64_t a = addrs[i];
-            const uint32_t c = colour_of<K>((uint32_t)a, (uint32_t)(a >> 32), h);
+            const uint32_t c = TAB ? table_colour(tab, a)
+                                   : colour_of<K>((uint32_t)a, (uint32_t)(a >> 32), h);
             colours[i] = (uint8_t)c;
             if (HIST)
                 __hip_atomic_fetch_add(&hist_acc[c], (uint64_t)1, __ATOMIC_RELAXED,
@@ -178,6 +199,8 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
     // the byte tables, visible to the whole workgroup after the loop's
     // opening barrier
     auto prologue = [&]() {
+        if (TAB)
+            return;
 #pragma unroll
         for (int r = 0; r < kLutBytes * 256 / kClsThreads; ++r) {
             const uint32_t i = (uint32_t)r * kClsThreads + threadIdx.x;
@@ -197,8 +220,41 @@ constexpr uint64_t kPtBlockPages = (uint64_t)kPtThreads * kPtIters;
 // [b*4096, (b+1)*4096) in 16 rounds of 256 consecutive pages.  The counting
 // pass writes the number of qualifying pages per workgroup; the emitting
 // pass writes each qualifying page at its rank among all qualifying pages.
-template <int K, bool EMIT>
-__global__ __launch_bounds__(kPtThreads) void k_pt_pass(HashArgs h, uint64_t origin, uint32_t shift,
+// Page tests.  QXor: the colour of the page's base address (XOR hash).
+// QTable: every partition that the page touches is in the table and has a
+// colour in the set.
+template <int K>
+struct QXor {
+    HashArgs h;
+    __device__ bool operator()(uint64_t a, const uint32_t *s_set) const
+    {
+        const uint32_t c = colour_of<K>((uint32_t)a, (uint32_t)(a >> 32), h);
+        return ((s_set[c >> 5] >> (c & 31u)) & 1u) != 0u;
+    }
+};
+
+struct QTable {
+    TableArgs t;
+    uint32_t page_shift;
+    __device__ bool operator()(uint64_t a, const uint32_t *s_set) const
+    {
+        if (a < t.origin)
+            return false;
+        const uint64_t j0 = (a - t.origin) >> t.shift;
+        const uint64_t j1 = (a + (1ull << page_shift) - 1u - t.origin) >> t.shift;
+        if (j1 >= t.entries)
+            return false;
+        bool ok = true;
+        for (uint64_t j = j0; j <= j1 && ok; ++j) {
+            const uint32_t c = t.lut[j];
+            ok = c != 255u && ((s_set[c >> 5] >> (c & 31u)) & 1u) != 0u;
+        }
+        return ok;
+    }
+};
+
+template <class Q, bool EMIT>
+__global__ __launch_bounds__(kPtThreads) void k_pt_pass(Q qual, uint64_t origin, uint32_t shift,
                                                         uint64_t pool_pages, SetArgs set,
                                                         uint32_t *block_counts,
                                                         const uint64_t *block_offsets,
@@ -215,12 +271,7 @@ __global__ __launch_bounds__(kPtThreads) void k_pt_pass(HashArgs h, uint64_t ori
     uint32_t total = 0;
     for (int it = 0; it < kPtIters; ++it) {
         const uint64_t page = base + (uint64_t)it * kPtThreads + threadIdx.x;
-        bool q = false;
-        if (page < pool_pages) {
-            const uint64_t a = origin + (page << shift);
-            const uint32_t c = colour_of<K>((uint32_t)a, (uint32_t)(a >> 32), h);
-            q = ((s_set[c >> 5] >> (c & 31u)) & 1u) != 0u;
-        }
+        const bool q = page < pool_pages && qual(origin + (page << shift), s_set);
         const uint64_t bal = __ballot(q);
         const uint32_t below = __builtin_amdgcn_mbcnt_hi(
             (uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
@@ -284,9 +335,10 @@ static HashArgs hash_args(const sgdrc_hash *h)
     return a;
 }
 
-template <int K>
-static int launch_classify(Ctx *c, const HashArgs &h, const uint64_t *d_addrs, uint64_t n,
-                           uint8_t *d_colours, uint64_t *d_hist, void *stream)
+template <int K, bool TAB>
+static int launch_classify(Ctx *c, const HashArgs &h, const TableArgs &tab,
+                           const uint64_t *d_addrs, uint64_t n, uint8_t *d_colours,
+                           uint64_t *d_hist, void *stream)
 {
     const uint64_t n_tiles = ((n & ~15ull) + kClsWaveTile - 1) / kClsWaveTile;
     if (n_tiles >= (1ull << 31))
@@ -301,27 +353,34 @@ static int launch_classify(Ctx *c, const HashArgs &h, const uint64_t *d_addrs, u
     uint64_t *acc = c->d_hist_acc + (size_t)(g.q - c->d_queues) * kHistBins;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (d_hist) {
-        static const int occ = occupancy(k_classify<K, true>, kClsThreads);
+        static const int occ = occupancy(k_classify<K, true, TAB>, kClsThreads);
         uint32_t grid = gated_grid(c, std::min(occ, kClsHistWgsPerCu), wg_tiles, li);
-        hipLaunchKernelGGL((k_classify<K, true>), dim3(grid), dim3(kClsThreads), 0, s, d_addrs, n,
-                           d_colours, h, acc, d_hist, (uint32_t)n_tiles, g);
+        hipLaunchKernelGGL((k_classify<K, true, TAB>), dim3(grid), dim3(kClsThreads), 0, s,
+                           d_addrs, n, d_colours, h, tab, acc, d_hist, (uint32_t)n_tiles, g);
     } else {
-        static const int occ = occupancy(k_classify<K, false>, kClsThreads);
+        static const int occ = occupancy(k_classify<K, false, TAB>, kClsThreads);
         uint32_t grid = gated_grid(c, std::min(occ, kClsWgsPerCu), wg_tiles, li);
-        hipLaunchKernelGGL((k_classify<K, false>), dim3(grid), dim3(kClsThreads), 0, s, d_addrs,
-                           n, d_colours, h, acc, d_hist, (uint32_t)n_tiles, g);
+        hipLaunchKernelGGL((k_classify<K, false, TAB>), dim3(grid), dim3(kClsThreads), 0, s,
+                           d_addrs, n, d_colours, h, tab, acc, d_hist, (uint32_t)n_tiles, g);
     }
     SGDRC_HIP(hipGetLastError());
     return SGDRC_OK;
 }
 
 template <int K>
-static int launch_pagetable(Ctx *c, const HashArgs &h, uint64_t origin, uint32_t shift,
+static int launch_classify_xor(Ctx *c, const HashArgs &h, const uint64_t *d_addrs, uint64_t n,
+                               uint8_t *d_colours, uint64_t *d_hist, void *stream)
+{
+    return launch_classify<K, false>(c, h, TableArgs{}, d_addrs, n, d_colours, d_hist, stream);
+}
+
+template <class Q>
+static int launch_pagetable(Ctx *c, const Q &q, uint64_t origin, uint32_t shift,
                             uint64_t pool_pages, const SetArgs &set, uint64_t n_needed,
                             uint32_t *d_pt, uint64_t nblocks, uint32_t *d_counts,
                             uint64_t *d_offsets, uint64_t *d_total, hipStream_t s)
 {
-    hipLaunchKernelGGL((k_pt_pass<K, false>), dim3((uint32_t)nblocks), dim3(kPtThreads), 0, s, h,
+    hipLaunchKernelGGL((k_pt_pass<Q, false>), dim3((uint32_t)nblocks), dim3(kPtThreads), 0, s, q,
                        origin, shift, pool_pages, set, d_counts, (const uint64_t *)nullptr,
                        (uint32_t *)nullptr, (uint64_t)0);
     SGDRC_HIP(hipGetLastError());
@@ -329,15 +388,120 @@ static int launch_pagetable(Ctx *c, const HashArgs &h, uint64_t origin, uint32_t
                        nblocks, d_total);
     SGDRC_HIP(hipGetLastError());
     if (n_needed > 0) {
-        hipLaunchKernelGGL((k_pt_pass<K, true>), dim3((uint32_t)nblocks), dim3(kPtThreads), 0, s,
-                           h, origin, shift, pool_pages, set, d_counts,
+        hipLaunchKernelGGL((k_pt_pass<Q, true>), dim3((uint32_t)nblocks), dim3(kPtThreads), 0, s,
+                           q, origin, shift, pool_pages, set, d_counts,
                            (const uint64_t *)d_offsets, d_pt, n_needed);
         SGDRC_HIP(hipGetLastError());
     }
     return SGDRC_OK;
 }
 
+template <int K>
+static int launch_pagetable_xor(Ctx *c, const HashArgs &h, uint64_t origin, uint32_t shift,
+                                uint64_t pool_pages, const SetArgs &set, uint64_t n_needed,
+                                uint32_t *d_pt, uint64_t nblocks, uint32_t *d_counts,
+                                uint64_t *d_offsets, uint64_t *d_total, hipStream_t s)
+{
+    return launch_pagetable(c, QXor<K>{h}, origin, shift, pool_pages, set, n_needed, d_pt, nblocks,
+                            d_counts, d_offsets, d_total, s);
+}
+
 static std::mutex g_pt_mu;  // page-table scratch is per context; builds are serialised
+
+static int check_pool_args(uint64_t addr_origin, uint32_t page_shift, uint64_t pool_pages,
+                           const sgdrc_colour_set *set, uint64_t n_needed, uint32_t *d_pt,
+                           uint64_t *n_found)
+{
+    int rc = check_shift(page_shift);
+    if (rc)
+        return rc;
+    if (!set || !n_found)
+        return set_error(SGDRC_EINVAL, "NULL colour set or n_found");
+    if (addr_origin & ((1ull << page_shift) - 1ull))
+        return set_error(SGDRC_EINVAL, "addr_origin not aligned to the page size");
+    if (pool_pages == 0 || pool_pages > (1ull << 32))
+        return set_error(SGDRC_EINVAL, "pool_pages must be in 1..2^32");
+    if (addr_origin >= (1ull << 48) || pool_pages > (((1ull << 48) - addr_origin) >> page_shift))
+        return set_error(SGDRC_EINVAL, "pool extends beyond the 48-bit address space");
+    if (n_needed > pool_pages)
+        return set_error(SGDRC_EINVAL, "n_needed exceeds pool_pages");
+    if (n_needed > 0 && (!d_pt || (reinterpret_cast<uintptr_t>(d_pt) & 3u)))
+        return set_error(SGDRC_EINVAL, "page table pointer NULL or not 4-byte aligned");
+    return SGDRC_OK;
+}
+
+// Every colour of the set must be below ``colours``; the set must not be empty.
+static int check_set(const sgdrc_colour_set *set, uint32_t colours)
+{
+    bool any = false;
+    for (uint32_t cc = 0; cc < 256; ++cc) {
+        if ((set->bits[cc >> 6] >> (cc & 63)) & 1ull) {
+            if (cc >= colours)
+                return set_error(SGDRC_EINVAL, "colour %u in set, hash has %u colours", cc, colours);
+            any = true;
+        }
+    }
+    if (!any)
+        return set_error(SGDRC_EINVAL, "empty colour set");
+    return SGDRC_OK;
+}
+
+static int check_table(const sgdrc_colour_table *t)
+{
+    if (!t)
+        return set_error(SGDRC_EINVAL, "colour table is NULL");
+    if (t->reserved != 0)
+        return set_error(SGDRC_EINVAL, "colour table reserved field must be 0");
+    if (t->shift < 8 || t->shift > SGDRC_MAX_PAGE_SHIFT)
+        return set_error(SGDRC_EINVAL, "partition shift %u outside [8, %d]", t->shift,
+                         SGDRC_MAX_PAGE_SHIFT);
+    if (t->entries > 0 && !t->lut)
+        return set_error(SGDRC_EINVAL, "colour table has entries but no device pointer");
+    if (t->origin >= (1ull << 48) || t->entries > (((1ull << 48) - t->origin) >> t->shift))
+        return set_error(SGDRC_EINVAL, "colour table extends beyond the 48-bit address space");
+    return SGDRC_OK;
+}
+
+// The ordered compaction shared by both page tests: scratch, counting pass,
+// scan, emitting pass (``launch``), then the count back to the host.
+template <class Launch>
+static int build_pagetable(Ctx *c, uint64_t pool_pages, const sgdrc_colour_set *set,
+                           uint64_t n_needed, uint64_t *n_found, void *stream, Launch launch)
+{
+    std::lock_guard<std::mutex> lock(g_pt_mu);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const uint64_t nblocks = (pool_pages + kPtBlockPages - 1) / kPtBlockPages;
+    const size_t need = 256 + nblocks * sizeof(uint64_t) + nblocks * sizeof(uint32_t);
+    if (c->scratch_bytes < need) {
+        SGDRC_HIP(hipDeviceSynchronize());
+        if (c->d_scratch)
+            SGDRC_HIP(hipFree(c->d_scratch));
+        c->d_scratch = nullptr;
+        c->scratch_bytes = 0;
+        size_t bytes = need < (1u << 20) ? (1u << 20) : need;
+        SGDRC_HIP(hipMalloc(&c->d_scratch, bytes));
+        c->scratch_bytes = bytes;
+    }
+    uint8_t *base = static_cast<uint8_t *>(c->d_scratch);
+    uint64_t *d_total = reinterpret_cast<uint64_t *>(base);
+    uint64_t *d_offsets = reinterpret_cast<uint64_t *>(base + 256);
+    uint32_t *d_counts = reinterpret_cast<uint32_t *>(base + 256 + nblocks * sizeof(uint64_t));
+    SetArgs sa;
+    for (int i = 0; i < 4; ++i) {
+        sa.w[2 * i] = (uint32_t)set->bits[i];
+        sa.w[2 * i + 1] = (uint32_t)(set->bits[i] >> 32);
+    }
+    int rc = launch(sa, nblocks, d_counts, d_offsets, d_total, s);
+    if (rc)
+        return rc;
+    SGDRC_HIP(hipMemcpyAsync(c->h_pinned, d_total, sizeof(uint64_t), hipMemcpyDeviceToHost, s));
+    SGDRC_HIP(hipStreamSynchronize(s));
+    *n_found = c->h_pinned[0];
+    if (*n_found < n_needed)
+        return set_error(SGDRC_ENOMEM, "pool holds %llu pages of the set, %llu needed",
+                         (unsigned long long)*n_found, (unsigned long long)n_needed);
+    return SGDRC_OK;
+}
 
 }  // namespace sgdrc
 
@@ -375,7 +539,8 @@ int colour_classify(sgdrc_ctx *ctx, const sgdrc_hash *hash, const uint64_t *d_ad
     if (rc)
         return rc;
     HashArgs h = hash_args(hash);
-    SGDRC_DISPATCH_K(hash->n_masks, launch_classify, c, h, d_addrs, n, d_colours, d_hist, stream);
+    SGDRC_DISPATCH_K(hash->n_masks, launch_classify_xor, c, h, d_addrs, n, d_colours, d_hist,
+                     stream);
     return rc;
 }
 
@@ -387,73 +552,70 @@ int colour_alloc_pagetable(sgdrc_ctx *ctx, const sgdrc_hash *hash, uint64_t addr
     int rc = check_hash(hash);
     if (rc)
         return rc;
-    rc = check_shift(page_shift);
-    if (rc)
+    if ((rc = check_pool_args(addr_origin, page_shift, pool_pages, set, n_needed, d_pt, n_found)))
         return rc;
-    if (!set || !n_found)
-        return set_error(SGDRC_EINVAL, "NULL colour set or n_found");
-    if (addr_origin & ((1ull << page_shift) - 1ull))
-        return set_error(SGDRC_EINVAL, "addr_origin not aligned to the page size");
-    if (pool_pages == 0 || pool_pages > (1ull << 32))
-        return set_error(SGDRC_EINVAL, "pool_pages must be in 1..2^32");
-    if (addr_origin >= (1ull << 48) || pool_pages > (((1ull << 48) - addr_origin) >> page_shift))
-        return set_error(SGDRC_EINVAL, "pool extends beyond the 48-bit address space");
-    if (n_needed > pool_pages)
-        return set_error(SGDRC_EINVAL, "n_needed exceeds pool_pages");
-    if (n_needed > 0 && (!d_pt || (reinterpret_cast<uintptr_t>(d_pt) & 3u)))
-        return set_error(SGDRC_EINVAL, "page table pointer NULL or not 4-byte aligned");
-    const uint32_t colours = 1u << hash->n_masks;
-    bool any = false;
-    for (uint32_t cc = 0; cc < 256; ++cc) {
-        if ((set->bits[cc >> 6] >> (cc & 63)) & 1ull) {
-            if (cc >= colours)
-                return set_error(SGDRC_EINVAL, "colour %u in set, hash has %u colours", cc, colours);
-            any = true;
-        }
-    }
-    if (!any)
-        return set_error(SGDRC_EINVAL, "empty colour set");
+    if ((rc = check_set(set, 1u << hash->n_masks)))
+        return rc;
     Ctx *c = nullptr;
-    rc = check_ctx(ctx, &c);
+    if ((rc = check_ctx(ctx, &c)))
+        return rc;
+    const HashArgs h = hash_args(hash);
+    return build_pagetable(c, pool_pages, set, n_needed, n_found, stream,
+                           [&](const SetArgs &sa, uint64_t nblocks, uint32_t *d_counts,
+                               uint64_t *d_offsets, uint64_t *d_total, hipStream_t s) {
+                               int rc = SGDRC_OK;
+                               SGDRC_DISPATCH_K(hash->n_masks, launch_pagetable_xor, c, h,
+                                                addr_origin, page_shift, pool_pages, sa, n_needed,
+                                                d_pt, nblocks, d_counts, d_offsets, d_total, s);
+                               return rc;
+                           });
+}
+
+int colour_classify_table(sgdrc_ctx *ctx, const sgdrc_colour_table *table,
+                          const uint64_t *d_addrs, uint64_t n, uint8_t *d_colours,
+                          uint64_t *d_hist, void *stream)
+{
+    clear_error();
+    int rc = check_table(table);
     if (rc)
         return rc;
+    if (n > 0 && (!d_addrs || !d_colours))
+        return set_error(SGDRC_EINVAL, "NULL address or colour buffer");
+    if ((reinterpret_cast<uintptr_t>(d_addrs) & 15u) || (reinterpret_cast<uintptr_t>(d_colours) & 15u))
+        return set_error(SGDRC_EINVAL, "address and colour buffers must be 16-byte aligned");
+    if (reinterpret_cast<uintptr_t>(d_hist) & 7u)
+        return set_error(SGDRC_EINVAL, "histogram not 8-byte aligned");
+    Ctx *c = nullptr;
+    if ((rc = check_ctx(ctx, &c)))
+        return rc;
+    const TableArgs t{table->lut, table->origin, table->entries, table->shift};
+    return launch_classify<8, true>(c, HashArgs{}, t, d_addrs, n, d_colours, d_hist, stream);
+}
 
-    std::lock_guard<std::mutex> lock(g_pt_mu);
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    const uint64_t nblocks = (pool_pages + kPtBlockPages - 1) / kPtBlockPages;
-    const size_t need = 256 + nblocks * sizeof(uint64_t) + nblocks * sizeof(uint32_t);
-    if (c->scratch_bytes < need) {
-        SGDRC_HIP(hipDeviceSynchronize());
-        if (c->d_scratch)
-            SGDRC_HIP(hipFree(c->d_scratch));
-        c->d_scratch = nullptr;
-        c->scratch_bytes = 0;
-        size_t bytes = need < (1u << 20) ? (1u << 20) : need;
-        SGDRC_HIP(hipMalloc(&c->d_scratch, bytes));
-        c->scratch_bytes = bytes;
-    }
-    uint8_t *base = static_cast<uint8_t *>(c->d_scratch);
-    uint64_t *d_total = reinterpret_cast<uint64_t *>(base);
-    uint64_t *d_offsets = reinterpret_cast<uint64_t *>(base + 256);
-    uint32_t *d_counts = reinterpret_cast<uint32_t *>(base + 256 + nblocks * sizeof(uint64_t));
-
-    SetArgs sa;
-    for (int i = 0; i < 4; ++i) {
-        sa.w[2 * i] = (uint32_t)set->bits[i];
-        sa.w[2 * i + 1] = (uint32_t)(set->bits[i] >> 32);
-    }
-    HashArgs h = hash_args(hash);
-    SGDRC_DISPATCH_K(hash->n_masks, launch_pagetable, c, h, addr_origin, page_shift, pool_pages,
-                     sa, n_needed, d_pt, nblocks, d_counts, d_offsets, d_total, s);
+int colour_alloc_pagetable_table(sgdrc_ctx *ctx, const sgdrc_colour_table *table,
+                                 uint64_t addr_origin, uint32_t page_shift, uint64_t pool_pages,
+                                 const sgdrc_colour_set *set, uint64_t n_needed, uint32_t *d_pt,
+                                 uint64_t *n_found, void *stream)
+{
+    clear_error();
+    int rc = check_table(table);
     if (rc)
         return rc;
-    SGDRC_HIP(hipMemcpyAsync(c->h_pinned, d_total, sizeof(uint64_t), hipMemcpyDeviceToHost, s));
-    SGDRC_HIP(hipStreamSynchronize(s));
-    *n_found = c->h_pinned[0];
-    if (*n_found < n_needed)
-        return set_error(SGDRC_ENOMEM, "pool holds %llu pages of the set, %llu needed",
-                         (unsigned long long)*n_found, (unsigned long long)n_needed);
-    return SGDRC_OK;
+    if ((rc = check_pool_args(addr_origin, page_shift, pool_pages, set, n_needed, d_pt, n_found)))
+        return rc;
+    if ((rc = check_set(set, 255u)))
+        return rc;
+    Ctx *c = nullptr;
+    if ((rc = check_ctx(ctx, &c)))
+        return rc;
+    const QTable q{TableArgs{table->lut, table->origin, table->entries, table->shift}, page_shift};
+    return build_pagetable(c, pool_pages, set, n_needed, n_found, stream,
+                           [&](const SetArgs &sa, uint64_t nblocks, uint32_t *d_counts,
+                               uint64_t *d_offsets, uint64_t *d_total, hipStream_t s) {
+                               return launch_pagetable(c, q, addr_origin, page_shift, pool_pages,
+                                                       sa, n_needed, d_pt, nblocks, d_counts,
+                                                       d_offsets, d_total, s);
+                           });
 }
 
 }  // extern "C"

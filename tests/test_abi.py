@@ -295,3 +295,25 @@ def test_bimodal_argument_errors(L):
     assert L.sgdrc_bm_release(h, 0) == sg.EINVAL                                       # not acquired
     assert L.sgdrc_bm_destroy(h) == sg.OK
     assert L.sgdrc_bm_input(None, 0, r(out), None) == sg.EINVAL
+
+
+def test_colour_table_argument_errors(L):
+    r = ctypes.byref
+    t = sg.ColourTable(4096, 0, 100, 10, 0)
+    s = sg.make_set(sg.words_of([1, 2]))
+    f = ctypes.c_uint64()
+    assert L.colour_classify_table(NULL, r(t), 16, 1, 32, None, None) == sg.ENODEV
+    assert L.colour_classify_table(NULL, None, 16, 1, 32, None, None) == sg.EINVAL
+    for bad in (sg.ColourTable(4096, 0, 100, 7, 0), sg.ColourTable(4096, 0, 100, 31, 0),
+                sg.ColourTable(4096, 0, 100, 10, 1), sg.ColourTable(None, 0, 100, 10, 0),
+                sg.ColourTable(4096, (1 << 48) - 1024, 2, 10, 0)):
+        assert L.colour_classify_table(NULL, r(bad), 16, 1, 32, None, None) == sg.EINVAL
+    assert L.colour_classify_table(NULL, r(sg.ColourTable(None, 0, 0, 10, 0)), 16, 1, 32, None,
+                                   None) == sg.ENODEV                       # empty table is fine
+    assert L.colour_classify_table(NULL, r(t), 8, 1, 32, None, None) == sg.EINVAL   # misaligned
+    assert L.colour_alloc_pagetable_table(NULL, r(t), 0, 12, 64, r(s), 8, 256, r(f), None) == sg.ENODEV
+    assert L.colour_alloc_pagetable_table(NULL, r(t), 0, 9, 64, r(s), 8, 256, r(f), None) == sg.EINVAL
+    s255 = sg.make_set(sg.words_of([255]))
+    assert L.colour_alloc_pagetable_table(NULL, r(t), 0, 12, 64, r(s255), 8, 256, r(f), None) == sg.EINVAL
+    assert L.colour_alloc_pagetable_table(NULL, r(t), 100, 12, 64, r(s), 8, 256, r(f), None) == sg.EINVAL
+    assert L.colour_alloc_pagetable_table(NULL, r(t), 0, 12, 64, r(s), 80, 256, r(f), None) == sg.EINVAL

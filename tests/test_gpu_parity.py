@@ -120,6 +120,64 @@ def test_classify_repeated_launches_reset_histogram(ctx, orc):
         assert (to_host(d_hist).astype(np.uint64) == ref_hist).all(), i
 
 
+# ----------------------------------------------------- colour table (5.3)
+
+def random_table(entries, seed, colours=64, holes=0.02):
+    """A non-linear colour table: random colours, a few partitions with none."""
+    rng = np.random.default_rng(seed)
+    lut = rng.integers(0, colours, size=entries).astype(np.uint8)
+    lut[rng.random(entries) < holes] = 255
+    return lut
+
+
+@pytest.mark.parametrize("n,shift,hist", [(65536, 10, True), (100003, 10, False),
+                                          (3 * 2048 + 31, 11, True), (7, 10, True), (0, 10, True)])
+def test_classify_table_matches_oracle(ctx, orc, n, shift, hist):
+    say(f"classify through a colour table n={n} shift={shift} hist={hist}")
+    entries, origin = 1 << 16, 1 << 34
+    lut = random_table(entries, seed=n + shift)
+    rng = np.random.default_rng(3)
+    # most addresses inside the table, some below it and past its end
+    addrs = (origin + rng.integers(-(1 << 20), (entries << shift) + (1 << 20), size=max(n, 1)))
+    addrs = addrs.astype(np.uint64)[:n]
+    d_lut = to_dev(lut)
+    t = sg.colour_table(d_lut, origin, shift)
+    d_addrs = to_dev(addrs) if n else torch.empty(0, dtype=torch.int64, device=DEV)
+    d_col = torch.full((max(n, 16) + 16,), 0xEE, dtype=torch.uint8, device=DEV)
+    d_hist = torch.full((256,), 777, dtype=torch.int64, device=DEV) if hist else None
+    sg.colour_classify_table(ctx, t, d_addrs, d_col, d_hist)
+    ref, ref_hist = orc.classify_lut(addrs, lut, origin, shift)
+    got = to_host(d_col)
+    assert (got[:n] == ref).all() and (got[n:] == 0xEE).all()
+    if hist:
+        assert (to_host(d_hist).astype(np.uint64) == ref_hist).all()
+
+
+@pytest.mark.parametrize("lut_shift,page_shift,S", [(10, 10, range(32)), (10, 11, range(48)),
+                                                    (10, 12, range(60)), (11, 10, [3, 7, 9, 40]),
+                                                    (10, 16, range(64))])
+def test_pagetable_table_matches_oracle(ctx, orc, lut_shift, page_shift, S):
+    say(f"pagetable through a colour table: partitions 2^{lut_shift}, pages 2^{page_shift}")
+    entries, origin = 1 << 18, 1 << 30
+    lut = random_table(entries, seed=lut_shift * 31 + page_shift, holes=0.002)
+    addr_origin = origin - (1 << 16)           # the pool starts before the table
+    pool = ((entries << lut_shift) + (1 << 17)) >> page_shift
+    words = synth.colour_set_bits(S)
+    ref, ref_found = orc.pagetable_lut(lut, origin, lut_shift, addr_origin, page_shift, pool,
+                                       words, pool)
+    n = max(1, min(ref_found, 5000))
+    d_pt = torch.full((n + 8,), -1, dtype=torch.int32, device=DEV)
+    t = sg.colour_table(to_dev(lut), origin, lut_shift)
+    if ref_found == 0:
+        with pytest.raises(sg.SgdrcError):
+            sg.colour_alloc_pagetable_table(ctx, t, addr_origin, page_shift, pool, S, n, d_pt)
+        return
+    found = sg.colour_alloc_pagetable_table(ctx, t, addr_origin, page_shift, pool, S, n, d_pt)
+    assert found == ref_found
+    got = to_host(d_pt).view(np.uint32)
+    assert (got[:n] == ref[:n]).all() and (got[n:] == 0xFFFFFFFF).all()
+
+
 # --------------------------------------------------------------- page table
 
 @pytest.mark.parametrize("shift,pool,K,S,n,origin", [
