@@ -204,6 +204,13 @@ __global__ __launch_bounds__(64) void k_signal_flag(uint32_t *flag, uint32_t val
                            __HIP_MEMORY_SCOPE_AGENT);
 }
 
+int stream_allowed_cus(Ctx *c, void *stream)
+{
+    std::lock_guard<std::mutex> lock(c->mu);
+    auto it = c->streams.find(stream);
+    return popcount_mask(it != c->streams.end() ? it->second.mask : c->all_cus);
+}
+
 bool stream_preemptible(Ctx *c, void *stream)
 {
     std::lock_guard<std::mutex> lock(c->mu);

@@ -111,6 +111,9 @@ int stream_state(Ctx *c, void *stream, StreamState **out);
 int make_gate(Ctx *c, void *stream, uint64_t n_tiles, int group_cus, Gate *g, LaunchInfo *li,
               bool preemptible = false);
 
+// CUs that the stream's mask allows (all CUs for a stream not seen yet).
+int stream_allowed_cus(Ctx *c, void *stream);
+
 // Whether launches on ``stream`` are to be preemptible (eviction flag set).
 bool stream_preemptible(Ctx *c, void *stream);
 

@@ -513,6 +513,16 @@ def test_gemv_mfma_k_chunks(ctx, orc, M, K, B, dt):
     run_gemv(ctx, orc, M, K, B, dt, dt, 12, seed=M + K + B)
 
 
+@pytest.mark.parametrize("M,K,cus", [(37, 11008, None), (4097, 11008, None), (2000, 9000, 64),
+                                      (3, 8200, [7])])
+def test_gemv_long_rows_batch1(ctx, orc, M, K, cus):
+    """Batch 1 with rows above 8 KiB: two-row tiles when each allowed CU has
+    few tiles, four-row tiles otherwise (the mask decides too)."""
+    say(f"gemv bf16 {M}x{K} B=1 on {'all' if cus is None else cus if isinstance(cus, list) else cus} CUs")
+    cu_set = None if cus is None else (cus if isinstance(cus, list) else range(cus))
+    run_gemv(ctx, orc, M, K, 1, sg.BF16, sg.BF16, 16, seed=M + K, cus=cu_set)
+
+
 @pytest.mark.parametrize("shift,B", [(10, 1), (10, 8), (11, 2), (11, 5)])
 def test_gemv_sector_pages(ctx, orc, shift, B):
     """W in 1 KiB and 2 KiB pages (the paper's sector granularities)."""
