@@ -624,6 +624,10 @@ __device__ __forceinline__ uint32_t checked_page(const uint32_t *pt, uint64_t j,
 typedef __amdgpu_buffer_rsrc_t Rsrc;
 constexpr int kRsrcWord3 = 0x00020000;
 constexpr int kAuxNt = 2;  // cache policy: non-temporal
+// Streaming stores: non-temporal and SC1 (written through past the L2 rather
+// than left dirty in it); measured 1.5-2.5 percent faster than non-temporal
+// alone for the triad and the relayout on MI355X, SC1 alone no faster.
+constexpr int kAuxStore = 16 | kAuxNt;
 
 __device__ __forceinline__ Rsrc make_rsrc(const void *base, uint32_t bytes)
 {
@@ -638,7 +642,7 @@ __device__ __forceinline__ u32x4 buf_load_nt(Rsrc r, uint32_t off)
 
 __device__ __forceinline__ void buf_store_nt(Rsrc r, uint32_t off, u32x4 v)
 {
-    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, v), r, off, 0, kAuxNt);
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, v), r, off, 0, kAuxStore);
 }
 
 __device__ __forceinline__ u32x4 load_nt(const void *p)
