@@ -317,6 +317,9 @@ def main():
     if "sectors" in want:
         rows["sectors"] = bench_sectors(torch, sg, synth, ctx, stream, timer)
         flags["sectors"] = ctx.device_error()
+    if "probe" in want:
+        rows["probe"] = bench_probe(torch, sg, synth, ctx, stream, timer)
+        flags["probe"] = ctx.device_error()
     if rows:
         result["rows"] = rows
 
@@ -910,6 +913,54 @@ def bench_sectors(torch, sg, synth, ctx, stream, timer, reps=20):
     out["pagetable_table_pool_pages"] = pool_pages
     log(f"sectors: {out}")
     del lut, addrs, cols, pt
+    torch.cuda.empty_cache()
+    return out
+
+
+def bench_probe(torch, sg, synth, ctx, stream, timer, reps=10, masks=None):
+    """Channel probing by bandwidth (in the spirit of the paper's section 5,
+    measured through this library).  A triad over three 256 MiB fp32 arrays
+    in 1 KiB pages runs on the pages of a 2 GiB pool where parity(address &
+    M) = 0 (a one-mask hash, colour 0).  If the bits of M feed the channel
+    hash, those pages use half of the channels and the triad slows towards
+    half speed; otherwise it keeps the speed of the unrestricted control
+    (M = bit 8, below the page size, keeps every page).  Only address bits
+    below 21 are probed: user space sees virtual addresses, which agree with
+    physical ones inside 2 MiB fragments."""
+    import numpy as np
+    dev = "cuda:0"
+    shift = 10
+    n = 1 << 26                       # floats per array (256 MiB)
+    pages = (n * 4) >> shift
+    pool_pages = (2 << 30) >> shift
+    raw, base = aligned_pool(torch, pool_pages >> 11, 21)     # 2 GiB at a 2 MiB boundary
+    pt = torch.empty(3 * pages, dtype=torch.int32, device=dev)
+    if masks is None:
+        masks = [1 << 8] + [1 << b for b in range(10, 21)] + \
+                [(1 << a) | (1 << b) for a in range(10, 16) for b in range(a + 1, 17)]
+    out = {"what": "triad 3x256 MiB fp32, 1 KiB pages restricted to parity(addr & M) = 0 "
+                   "in a 2 GiB pool (2 MiB aligned); GB/s and ratio to the control M = bit 8",
+           "points": []}
+    ref = None
+    for m in masks:
+        sg.colour_alloc_pagetable(ctx, [m], base, shift, pool_pages, [0], 3 * pages, pt)
+        A, B, C = (sg.paged(base, pt[i * pages:(i + 1) * pages], pool_pages) for i in range(3))
+        tag = ("probe", m)
+        with torch.cuda.stream(stream):
+            for _ in range(2):
+                sg.colored_stream(ctx, A, B, C, 3.0, n, shift, stream)
+            for _ in range(reps):
+                e = timer.start()
+                sg.colored_stream(ctx, A, B, C, 3.0, n, shift, stream)
+                timer.stop(e, tag)
+        torch.cuda.synchronize()
+        gbs = 12 * n / (pctl(timer.durations_ms(tag), 50) * 1e-3) / 1e9
+        if ref is None:
+            ref = gbs
+        bits = [b for b in range(48) if (m >> b) & 1]
+        out["points"].append({"bits": bits, "GBps": round(gbs, 1), "ratio": round(gbs / ref, 3)})
+        log(f"probe: bits {bits}: {gbs:.0f} GB/s ({gbs / ref:.2f} of control)")
+    del raw, pt
     torch.cuda.empty_cache()
     return out
 
