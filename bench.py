@@ -43,7 +43,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--rows", default="classify,pagetable,relayout,gemv,corun,preempt,bimodal,sectors",
+    ap.add_argument("--rows", default="classify,pagetable,relayout,gemv,xcd,corun,preempt,bimodal,sectors",
                     help="comma list of extra rows to measure ('' for none)")
     ap.add_argument("--gemv-launches", type=int, default=300)
     ap.add_argument("--corun-launches", type=int, default=2000)
@@ -317,6 +317,9 @@ def main():
     if "sectors" in want:
         rows["sectors"] = bench_sectors(torch, sg, synth, ctx, stream, timer)
         flags["sectors"] = ctx.device_error()
+    if "xcd" in want:
+        rows["xcd"] = bench_xcd(torch, sg, ctx, stream)
+        flags["xcd"] = ctx.device_error()
     if "probe" in want:
         rows["probe"] = bench_probe(torch, sg, synth, ctx, stream, timer)
         flags["probe"] = ctx.device_error()
@@ -451,12 +454,14 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
         setup_flags = ctx.device_error()
         log(f"gemv {M}x{K}: {copies} weight copies rotated (setup flags {setup_flags})")
         for B in (1, 2, 4, 8):
-            for ncu in (64, 128, 192, 256):
+            for ncu, place in [(c, p) for c in (64, 128, 192, 256)
+                               for p in ("xcds", "spread") if p == "xcds" or (c < n_cus and B in (1, 8))]:
                 if ncu > n_cus:
                     continue
-                tag = ("gemv", M, B, ncu)
+                tag = ("gemv", M, B, ncu, place)
+                cus = range(ncu) if place == "xcds" else spread_cus(n_cus, ncu)
                 with torch.cuda.stream(stream):
-                    sg.set_cu_mask(ctx, stream, range(ncu))
+                    sg.set_cu_mask(ctx, stream, cus)
                     for i in range(20):
                         sg.colored_gemv(ctx, W[i % copies], sg.BF16, M, K, x, sg.BF16, B, y,
                                         shift, stream)
@@ -474,7 +479,8 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
                 nbytes = M * K * 2 + B * K * 2 + B * M * 4
                 med, p99 = pctl(list(spans), 50), pctl(list(spans), 99)
                 gbs = nbytes / (med * 1e-6) / 1e9
-                out.append({"M": M, "K": K, "batch": B, "cus": ncu, "device_flags": flag,
+                out.append({"M": M, "K": K, "batch": B, "cus": ncu, "placement": place,
+                            "device_flags": flag,
                             "path": "mfma" if B >= 3 else "valu",
                             "p50_us": round(med, 2), "p99_us": round(p99, 2),
                             "GBps": round(gbs, 1),
@@ -482,16 +488,72 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
                             "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1),
                             "launch_p50_us": round(pctl(d, 50) * 1e3, 2),
                             "launch_p99_us": round(pctl(d, 99) * 1e3, 2)})
-                log(f"gemv {M}x{K} B={B} cus={ncu}: kernel p50 {med:.1f} us p99 {p99:.1f} us "
+                log(f"gemv {M}x{K} B={B} cus={ncu} ({place}): kernel p50 {med:.1f} us p99 {p99:.1f} us "
                     f"{gbs:.0f} GB/s; with launch p50 {pctl(d, 50) * 1e3:.1f} us")
         del raw, W
         torch.cuda.empty_cache()
     return {"what": "bf16 W on 48/64 colours in 2 MiB pages, bf16 x, fp32 y; "
                     f"{copies} rotated weight copies; {launches} launches per point",
+            "placement": "xcds: the first n logical CUs (whole XCDs, n/32 of them); spread: n/8 "
+                         "CUs in each of the 8 XCDs",
             "bytes": "M*K*2 + B*K*2 + B*M*4",
             "timing": "p50/p99_us and GBps: kernel spans from the device time log (first "
                       "workgroup start to last workgroup end); launch_p50/p99_us: host events "
                       "around each call, including launch overhead",
+            "points": out}
+
+
+def spread_cus(n_cus, ncu, n_xcds=8):
+    """ncu logical CUs spread evenly over all XCDs (logical CUs are numbered
+    XCD by XCD, n_cus / n_xcds in each)."""
+    per = n_cus // n_xcds
+    return [x * per + i for x in range(n_xcds) for i in range(ncu // n_xcds)]
+
+
+def bench_xcd(torch, sg, ctx, stream, reps=20):
+    """Streaming bandwidth against the XCDs a CU mask reaches: the triad over
+    three contiguous 1 GiB fp32 arrays (identity page tables, 64 KiB pages)
+    on whole XCDs (the first 32k logical CUs) and on the same CU count
+    spread over all eight XCDs."""
+    shift = 16
+    n = 1 << 28
+    pages = (n * 4) >> shift
+    n_cus = ctx.num_cus
+    per_xcd = n_cus // 8
+    g = torch.Generator(device="cuda:0")
+    g.manual_seed(11)
+    a = torch.empty(n, dtype=torch.float32, device="cuda:0")
+    b = torch.rand(n, generator=g, device="cuda:0") * 2 - 1
+    c = torch.rand(n, generator=g, device="cuda:0") * 2 - 1
+    ident = torch.arange(pages, dtype=torch.int32, device="cuda:0")
+    A, B, C = (sg.paged(t, ident, pages) for t in (a, b, c))
+    torch.cuda.synchronize()
+    out = []
+    for k in range(1, 9):
+        for place in ("xcds", "spread") if k < 8 else ("xcds",):
+            ncu = k * per_xcd
+            cus = range(ncu) if place == "xcds" else spread_cus(n_cus, ncu)
+            with torch.cuda.stream(stream):
+                sg.set_cu_mask(ctx, stream, cus)
+                for _ in range(3):
+                    sg.colored_stream(ctx, A, B, C, 3.0, n, shift, stream)
+                dev = DevTimes(torch, ctx, stream, reps)
+                for _ in range(reps):
+                    sg.colored_stream(ctx, A, B, C, 3.0, n, shift, stream)
+                spans = dev.close_us()
+                sg.set_cu_mask(ctx, stream, None)
+            med = pctl(list(spans), 50)
+            gbs = 12 * n / (med * 1e-6) / 1e9
+            xcds = k if place == "xcds" else 8
+            out.append({"cus": ncu, "xcds": xcds, "placement": place,
+                        "p50_ms": round(med / 1e3, 4), "GBps": round(gbs, 1),
+                        "GBps_per_xcd": round(gbs / xcds, 1),
+                        "device_flags": ctx.device_error()})
+            log(f"xcd triad {ncu} CUs on {xcds} XCDs: {med / 1e3:.3f} ms, {gbs:.0f} GB/s")
+    del a, b, c
+    torch.cuda.empty_cache()
+    return {"what": "triad a=b+3c, three contiguous 1 GiB fp32 arrays, 64 KiB pages, by CU mask; "
+                    f"{reps} launches per point, kernel spans from the device time log",
             "points": out}
 
 

@@ -279,9 +279,9 @@ constexpr uint32_t kMfmaChunk = 2048;                  // bytes per row per chun
 constexpr uint32_t kMfmaChunkSlices = kMfmaChunk / 16u;  // 128
 constexpr uint32_t kMfmaLdsRow = kMfmaChunk + 16u;     // padded LDS row
 constexpr int kMfmaBatchRows = 8;                      // x rows staged (batch <= 8)
-constexpr int kMfmaWLoads = kMfmaRows * (int)kMfmaChunkSlices / kMfmaThreads;       // 4
 constexpr int kMfmaXLoads = kMfmaBatchRows * (int)kMfmaChunkSlices / kMfmaThreads;  // 2
 constexpr int kMfmaStepsPerWave = (int)(kMfmaChunk / 64u) / kMfmaWaves;             // 4
+constexpr int kMfmaSets = 2;  // register sets of chunk loads in flight
 
 // x through a buffer resource, cached (every workgroup reads all of x).
 constexpr uint32_t kXOutside = 0xFFFFFFF0u;  // offset past any x resource
@@ -290,15 +290,21 @@ __device__ __forceinline__ u32x4 buf_load(Rsrc r, uint32_t off)
     return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
 
-template <int DT>
-__global__ __launch_bounds__(kMfmaThreads) void k_gemm_mfma(
+template <int DT, int ROWS>
+__global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_gemm_mfma(
     const uint8_t *__restrict__ w_pool, const uint32_t *__restrict__ pt, uint64_t pool_pages,
     uint32_t M, uint32_t K, const uint8_t *__restrict__ x, uint32_t nb, float *__restrict__ y,
     uint32_t shift, uint32_t n_tiles, Gate g)
 {
     __shared__ uint32_t s_pt[kPtCap];
     __shared__ f32x4 s_red[kMfmaWaves][64];
-    __shared__ __attribute__((aligned(16))) uint8_t s_w[kMfmaRows][kMfmaLdsRow];
+    // ROWS = 16 fills the MFMA's A operand; ROWS = 8 leaves its upper half
+    // zero (twice the tiles, for masks with few tiles per CU).  An output's
+    // sum does not depend on the other rows of its tile, so both give the
+    // same bits.
+    static_assert(ROWS == 16 || ROWS == 8, "tiles of 16 or 8 rows");
+    constexpr int WL = ROWS * (int)kMfmaChunkSlices / kMfmaThreads;  // W loads per lane
+    __shared__ __attribute__((aligned(16))) uint8_t s_w[ROWS][kMfmaLdsRow];
     __shared__ __attribute__((aligned(16))) uint8_t s_x[kMfmaBatchRows][kMfmaLdsRow];
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const uint32_t lane = threadIdx.x & 63u;
@@ -316,24 +322,24 @@ __global__ __launch_bounds__(kMfmaThreads) void k_gemm_mfma(
     auto prologue = [&]() { stage_whole_table(pt, pool_pages, w_pages, s_pt, pro_err); };
 
     auto body = [&](uint32_t t, uint32_t, uint32_t &err, auto &&) {
-        const uint32_t m0 = t * kMfmaRows;
-        const uint32_t m_end = min(m0 + (uint32_t)kMfmaRows, M);
+        const uint32_t m0 = t * (uint32_t)ROWS;
+        const uint32_t m_end = min(m0 + (uint32_t)ROWS, M);
         const TilePages tp = tile_pages(whole, pt, pool_pages, (uint64_t)m0 * row_bytes,
                                         (uint64_t)m_end * row_bytes, shift, s_pt, err);
-        // Two register sets of chunk loads, so that two chunks are in flight
-        // while a third feeds the MFMAs.  Loads are always issued and are zero
-        // where out of range (rows beyond M, slices beyond K, batch rows
-        // beyond nb), so chunks are taken in pairs without a branch; the pad
-        // chunk of an odd count adds zeros.
+        // kMfmaSets register sets of chunk loads, so that that many chunks are
+        // in flight while another feeds the MFMAs.  Loads are always issued
+        // and are zero where out of range (rows beyond M, slices beyond K,
+        // batch rows beyond nb), so chunks are taken kMfmaSets at a time
+        // without a branch; pad chunks past the end add zeros.
         // The in-range test of each load travels beside its data as a bit of
         // ``okv`` and is applied where the data goes to LDS: a select right
         // after the load would make the loop wait for the data there.
-        u32x4 wa[kMfmaWLoads], xa[kMfmaXLoads], wb[kMfmaWLoads], xb[kMfmaXLoads];
-        uint32_t oka = 0u, okb = 0u;
+        u32x4 ws[kMfmaSets][WL], xs[kMfmaSets][kMfmaXLoads];
+        uint32_t oks[kMfmaSets];
         auto load_chunk = [&](uint32_t c, u32x4 *wv, u32x4 *xv, uint32_t &okv) __attribute__((always_inline)) {
             okv = 0u;
 #pragma unroll
-            for (int q = 0; q < kMfmaWLoads; ++q) {
+            for (int q = 0; q < WL; ++q) {
                 const uint32_t L = (uint32_t)q * kMfmaThreads + threadIdx.x;
                 const uint32_t r = L / kMfmaChunkSlices, sl = L % kMfmaChunkSlices;
                 const uint32_t kv = c * kMfmaChunkSlices + sl;
@@ -357,7 +363,7 @@ __global__ __launch_bounds__(kMfmaThreads) void k_gemm_mfma(
         auto store_chunk = [&](const u32x4 *wv, const u32x4 *xv, uint32_t okv) __attribute__((always_inline)) {
             const u32x4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
-            for (int q = 0; q < kMfmaWLoads; ++q) {
+            for (int q = 0; q < WL; ++q) {
                 const uint32_t L = (uint32_t)q * kMfmaThreads + threadIdx.x;
                 *reinterpret_cast<u32x4 *>(&s_w[L / kMfmaChunkSlices][(L % kMfmaChunkSlices) * 16u]) =
                     (okv >> q) & 1u ? wv[q] : z;
@@ -373,24 +379,26 @@ __global__ __launch_bounds__(kMfmaThreads) void k_gemm_mfma(
 #pragma unroll
             for (int i = 0; i < kMfmaStepsPerWave; ++i) {
                 const uint32_t j = wave * (uint32_t)kMfmaStepsPerWave + (uint32_t)i;
-                const u32x4 a = *reinterpret_cast<const u32x4 *>(&s_w[rl][j * 64u + grp * 16u]);
+                const u32x4 a = *reinterpret_cast<const u32x4 *>(
+                    &s_w[rl & (uint32_t)(ROWS - 1)][j * 64u + grp * 16u]);
                 const u32x4 bx = *reinterpret_cast<const u32x4 *>(&s_x[rl & 7u][j * 64u + grp * 16u]);
-                acc = mfma16x16x32<DT>(a, rl < (uint32_t)kMfmaBatchRows ? bx : u32x4{0u, 0u, 0u, 0u}, acc);
+                const u32x4 z = {0u, 0u, 0u, 0u};
+                acc = mfma16x16x32<DT>(rl < (uint32_t)ROWS ? a : z,
+                                       rl < (uint32_t)kMfmaBatchRows ? bx : z, acc);
             }
         };
-        load_chunk(0u, wa, xa, oka);
-        load_chunk(1u, wb, xb, okb);
-        for (uint32_t c = 0; c < n_chunks; c += 2u) {
-            __syncthreads();  // the previous chunk's MFMAs have read the LDS
-            store_chunk(wa, xa, oka);
-            __syncthreads();
-            load_chunk(c + 2u, wa, xa, oka);
-            mfma_chunk();
-            __syncthreads();
-            store_chunk(wb, xb, okb);
-            __syncthreads();
-            load_chunk(c + 3u, wb, xb, okb);
-            mfma_chunk();
+#pragma unroll
+        for (int s = 0; s < kMfmaSets; ++s)
+            load_chunk((uint32_t)s, ws[s], xs[s], oks[s]);
+        for (uint32_t c = 0; c < n_chunks; c += (uint32_t)kMfmaSets) {
+#pragma unroll
+            for (int s = 0; s < kMfmaSets; ++s) {
+                __syncthreads();  // the previous chunk's MFMAs have read the LDS
+                store_chunk(ws[s], xs[s], oks[s]);
+                __syncthreads();
+                load_chunk(c + (uint32_t)(kMfmaSets + s), ws[s], xs[s], oks[s]);
+                mfma_chunk();
+            }
         }
         s_red[wave][lane] = acc;
         __syncthreads();
@@ -409,7 +417,7 @@ __global__ __launch_bounds__(kMfmaThreads) void k_gemm_mfma(
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const uint32_t m = m0 + grp * 4u + (uint32_t)i;
-                    if (m < M)
+                    if (m < m_end)
                         y[(uint64_t)rl * M + m] = vals[i];
                 }
             }
@@ -531,8 +539,16 @@ int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, 
     GemvKernel k;
     uint64_t n_tiles;
     if (mfma) {
-        k = w_dtype == SGDRC_BF16 ? k_gemm_mfma<SGDRC_BF16> : k_gemm_mfma<SGDRC_F16>;
-        n_tiles = (M + kMfmaRows - 1) / kMfmaRows;
+        // Between one and two 16-row tiles per allowed CU, some CUs would
+        // take two tiles and the rest one; 8-row tiles halve that imbalance
+        // (and give the same bits).
+        const uint64_t t16 = (M + 15u) / 16u, allowed = (uint64_t)stream_allowed_cus(c, stream);
+        const int rows = t16 > allowed && t16 < 2u * allowed ? 8 : 16;
+        if (rows == 16)
+            k = w_dtype == SGDRC_BF16 ? k_gemm_mfma<SGDRC_BF16, 16> : k_gemm_mfma<SGDRC_F16, 16>;
+        else
+            k = w_dtype == SGDRC_BF16 ? k_gemm_mfma<SGDRC_BF16, 8> : k_gemm_mfma<SGDRC_F16, 8>;
+        n_tiles = (M + rows - 1) / rows;
     } else {
         // rows of more than 512 slices of 16 bytes take two rounds of loads
         const bool long_rows = (uint64_t)K * dtype_size(w_dtype) > 512u * 16u;

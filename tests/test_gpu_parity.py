@@ -506,11 +506,26 @@ def test_gemv_page_table_staging_boundary(ctx, orc, M, B):
 @pytest.mark.parametrize("M,K,B,dt", [(300, 11008, 8, sg.BF16), (37, 3000, 3, sg.F16),
                                       (64, 1024, 4, sg.BF16), (17, 8, 8, sg.F16)])
 def test_gemv_mfma_k_chunks(ctx, orc, M, K, B, dt):
-    """The MFMA path takes rows in chunks of 2 KiB, two chunks per loop trip:
+    """The MFMA path takes rows in chunks of 2 KiB, two chunks (one per
+    register set) per loop trip:
     an odd chunk count (11, 3, 1), a ragged last chunk and a row far shorter
     than a chunk."""
     say(f"gemv mfma {M}x{K} B={B} dtype {dt}, 4 KiB pages")
     run_gemv(ctx, orc, M, K, B, dt, dt, 12, seed=M + K + B)
+
+
+@pytest.mark.parametrize("M,K,B,cus", [(203, 3000, 8, 10), (4096, 11008, 4, 192),
+                                      (37, 11008, 3, [1, 2])])
+def test_gemv_mfma_half_tiles(ctx, orc, M, K, B, cus):
+    """Between one and two 16-row tiles per allowed CU the MFMA path takes
+    8-row tiles (upper half of the A operand zero): a ragged last tile, the
+    4096 x 11008 layer on 192 CUs, two CUs.  The 16-row tiles of the
+    unmasked run give the same bits."""
+    say(f"gemv mfma {M}x{K} B={B} on {cus if isinstance(cus, list) else cus} CUs (8-row tiles)")
+    cu_set = cus if isinstance(cus, list) else range(cus)
+    y8 = run_gemv(ctx, orc, M, K, B, sg.BF16, sg.BF16, 16, seed=M + B, cus=cu_set)
+    y16 = run_gemv(ctx, orc, M, K, B, sg.BF16, sg.BF16, 16, seed=M + B, check=False)
+    assert (y8.view(np.uint32) == y16.view(np.uint32)).all()
 
 
 @pytest.mark.parametrize("M,K,cus", [(37, 11008, None), (4097, 11008, None), (2000, 9000, 64),
