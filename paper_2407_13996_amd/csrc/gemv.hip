@@ -264,8 +264,8 @@ __device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c)
                                                       __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
 }
 
-// Batch 3..8 on MFMA.  A tile (16 rows x K) is consumed in chunks of
-// kMfmaChunk bytes per row.  Each chunk of W (16 rows) and of x (8 batch
+// Batch 3..8 on MFMA.  A tile (16 or 8 rows x K) is consumed in chunks of
+// kMfmaChunk bytes per row.  Each chunk of W (the tile's rows) and of x (8 batch
 // rows) is read with row-contiguous 16-byte loads (each wavefront
 // instruction covers 1 KiB of one row) and staged in LDS; the MFMAs then
 // read their operands from LDS: lane l supplies row (l % 16) of the W block
@@ -273,8 +273,10 @@ __device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c)
 // group g = l / 16, so the k order inside the instruction matches between
 // the operands, and the accumulator holds rows 4g..4g+3 of batch column
 // l % 16.  The eight waves take the chunk's 32 k-steps four each.  The
-// two chunks that follow are in flight during the current chunk's MFMAs;
-// beyond the last chunk the loads read a valid address and are discarded.
+// kMfmaSets chunks that follow are in flight during the current chunk's
+// MFMAs; beyond the last chunk the loads read a valid address and are
+// discarded.  Two sets keep two workgroups per CU (three or more need
+// more than 128 VGPRs and measured slower).
 constexpr uint32_t kMfmaChunk = 2048;                  // bytes per row per chunk
 constexpr uint32_t kMfmaChunkSlices = kMfmaChunk / 16u;  // 128
 constexpr uint32_t kMfmaLdsRow = kMfmaChunk + 16u;     // padded LDS row
