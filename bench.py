@@ -376,50 +376,68 @@ def bench_classify_one(torch, sg, synth, ctx, stream, timer, n, reps, hist):
 
 
 def bench_relayout(torch, sg, synth, ctx, stream, timer, reps=10):
-    shift = 16
-    P = 1 << shift
+    """The 4 GiB fp16 tensor moved between the all-colour form and colours
+    0..15 of 64, both directions, in 64 KiB pages and in 2 MiB pages; and
+    the same bytes copied between two contiguous buffers (identity tables)
+    as the ceiling the indirection is measured against."""
     n_bytes = 4 << 30
-    pages = n_bytes >> shift
-    masks = synth.xor_masks(6, seed=1, min_bit=shift)
-    pool_pages = int(pages * 64 / 16 * 1.04) + 64
-    log(f"relayout 4 GiB fp16, restricted pool {pool_pages} pages")
     g = torch.Generator(device="cuda:0")
     g.manual_seed(5)
     all_form = torch.randint(-32768, 32767, (n_bytes // 2,), dtype=torch.int16, device="cuda:0",
                              generator=g)
-    ident = torch.arange(pages, dtype=torch.int32, device="cuda:0")
-    raw, base = aligned_pool(torch, pool_pages, shift)
-    pt = torch.empty(pages, dtype=torch.int32, device="cuda:0")
-    sg.colour_alloc_pagetable(ctx, masks, base, shift, pool_pages, range(16), pages, pt, stream)
     back = torch.empty_like(all_form)
-    torch.cuda.synchronize()   # operands made on torch's stream, used on ``stream``
-    A = sg.paged(all_form, ident, pages)
-    S = sg.paged(base, pt, pool_pages)
-    B = sg.paged(back, ident, pages)
-    with torch.cuda.stream(stream):
-        for _ in range(2):
-            sg.bimodal_relayout(ctx, S, A, n_bytes, shift, stream)
-            sg.bimodal_relayout(ctx, B, S, n_bytes, shift, stream)
-        for _ in range(reps):
-            e0 = timer.start()
-            sg.bimodal_relayout(ctx, S, A, n_bytes, shift, stream)
-            timer.stop(e0, "to_restricted")
-            e0 = timer.start()
-            sg.bimodal_relayout(ctx, B, S, n_bytes, shift, stream)
-            timer.stop(e0, "to_all")
-        torch.cuda.synchronize()
-    same = bool(torch.equal(back, all_form))
-    out = {"what": "4 GiB fp16 (65,536 pages of 64 KiB), all colours <-> 16 of 64 colours",
-           "round_trip_identity": same}
-    for tag in ("to_restricted", "to_all"):
-        d = timer.durations_ms(tag)
-        med = pctl(d, 50)
+    out = {"what": "4 GiB fp16, all colours <-> 16 of 64 colours; 64 KiB pages (65,536) and "
+                   "2 MiB pages (2,048); contiguous copy with identity tables as the ceiling"}
+
+    def timed(tag, dst, src, shift):
+        with torch.cuda.stream(stream):
+            for _ in range(2):
+                sg.bimodal_relayout(ctx, dst, src, n_bytes, shift, stream)
+            for _ in range(reps):
+                e0 = timer.start()
+                sg.bimodal_relayout(ctx, dst, src, n_bytes, shift, stream)
+                timer.stop(e0, tag)
+            torch.cuda.synchronize()
+        med = pctl(timer.durations_ms(tag), 50)
         gbs = 2 * n_bytes / (med * 1e-3) / 1e9
-        out[tag] = {"median_ms": round(med, 4), "GBps": round(gbs, 1),
-                    "pages_per_s": round(pages / (med * 1e-3), 0),
-                    "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1)}
+        pages = n_bytes >> shift
         log(f"relayout {tag}: {med:.3f} ms  {gbs:.0f} GB/s")
-    del raw
+        return {"median_ms": round(med, 4), "GBps": round(gbs, 1),
+                "pages_per_s": round(pages / (med * 1e-3), 0),
+                "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1)}
+
+    for shift in (16, 21):
+        pages = n_bytes >> shift
+        masks = synth.xor_masks(6, seed=1, min_bit=shift)
+        ident = torch.arange(pages, dtype=torch.int32, device="cuda:0")
+        pt = torch.empty(pages, dtype=torch.int32, device="cuda:0")
+        for margin in (1.04, 1.25, 1.6):
+            # a short pool of 2 MiB pages can hold slightly fewer of the colours than
+            # a quarter of its pages: grow it until the table fills
+            pool_pages = int(pages * 64 / 16 * margin) + 64
+            raw, base = aligned_pool(torch, pool_pages, shift)
+            try:
+                sg.colour_alloc_pagetable(ctx, masks, base, shift, pool_pages, range(16), pages,
+                                          pt, stream)
+                break
+            except sg.SgdrcError as e:
+                if e.code != sg.ENOMEM or margin == 1.6:
+                    raise
+                del raw
+                torch.cuda.empty_cache()
+        log(f"relayout 4 GiB fp16, {1 << (shift - 10)} KiB pages, restricted pool {pool_pages} pages")
+        torch.cuda.synchronize()   # operands made on torch's stream, used on ``stream``
+        A = sg.paged(all_form, ident, pages)
+        S = sg.paged(base, pt, pool_pages)
+        B = sg.paged(back, ident, pages)
+        key = "" if shift == 16 else "_2MiB"
+        out["to_restricted" + key] = timed(("to_restricted", shift), S, A, shift)
+        out["to_all" + key] = timed(("to_all", shift), B, S, shift)
+        out["round_trip_identity" + key] = bool(torch.equal(back, all_form))
+        if shift == 16:
+            out["contiguous_copy"] = timed(("contiguous", shift), B, A, shift)
+        del raw, pt, S
+        torch.cuda.empty_cache()
     return out
 
 
@@ -453,47 +471,65 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
         y = torch.empty(8 * M, dtype=torch.float32, device="cuda:0")
         setup_flags = ctx.device_error()
         log(f"gemv {M}x{K}: {copies} weight copies rotated (setup flags {setup_flags})")
+
+        def point(Ws, B, ncu, place, layout):
+            tag = ("gemv", M, B, ncu, place, layout)
+            cus = range(ncu) if place == "xcds" else spread_cus(n_cus, ncu)
+            with torch.cuda.stream(stream):
+                sg.set_cu_mask(ctx, stream, cus)
+                for i in range(20):
+                    sg.colored_gemv(ctx, Ws[i % copies], sg.BF16, M, K, x, sg.BF16, B, y,
+                                    shift, stream)
+                dev = DevTimes(torch, ctx, stream, launches)
+                for i in range(launches):
+                    e0 = timer.start()
+                    sg.colored_gemv(ctx, Ws[i % copies], sg.BF16, M, K, x, sg.BF16, B, y,
+                                    shift, stream)
+                    timer.stop(e0, tag)
+                spans = dev.close_us()
+                sg.set_cu_mask(ctx, stream, None)
+                torch.cuda.synchronize()
+            d = timer.durations_ms(tag)
+            flag = ctx.device_error()
+            nbytes = M * K * 2 + B * K * 2 + B * M * 4
+            med, p99 = pctl(list(spans), 50), pctl(list(spans), 99)
+            gbs = nbytes / (med * 1e-6) / 1e9
+            out.append({"M": M, "K": K, "batch": B, "cus": ncu, "placement": place,
+                        "layout": layout, "device_flags": flag,
+                        "path": "mfma" if B >= 3 else "valu",
+                        "p50_us": round(med, 2), "p99_us": round(p99, 2),
+                        "GBps": round(gbs, 1),
+                        "pct_of_colour_scaled_peak": round(100 * gbs / (0.75 * HBM_PEAK_GBS), 1),
+                        "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1),
+                        "launch_p50_us": round(pctl(d, 50) * 1e3, 2),
+                        "launch_p99_us": round(pctl(d, 99) * 1e3, 2)})
+            log(f"gemv {M}x{K} B={B} cus={ncu} ({place}, {layout}): kernel p50 {med:.1f} us "
+                f"p99 {p99:.1f} us {gbs:.0f} GB/s; with launch p50 {pctl(d, 50) * 1e3:.1f} us")
+
         for B in (1, 2, 4, 8):
-            for ncu, place in [(c, p) for c in (64, 128, 192, 256)
-                               for p in ("xcds", "spread") if p == "xcds" or (c < n_cus and B in (1, 8))]:
+            for ncu in (64, 128, 192, 256):
                 if ncu > n_cus:
                     continue
-                tag = ("gemv", M, B, ncu, place)
-                cus = range(ncu) if place == "xcds" else spread_cus(n_cus, ncu)
-                with torch.cuda.stream(stream):
-                    sg.set_cu_mask(ctx, stream, cus)
-                    for i in range(20):
-                        sg.colored_gemv(ctx, W[i % copies], sg.BF16, M, K, x, sg.BF16, B, y,
-                                        shift, stream)
-                    dev = DevTimes(torch, ctx, stream, launches)
-                    for i in range(launches):
-                        e0 = timer.start()
-                        sg.colored_gemv(ctx, W[i % copies], sg.BF16, M, K, x, sg.BF16, B, y,
-                                        shift, stream)
-                        timer.stop(e0, tag)
-                    spans = dev.close_us()
-                    sg.set_cu_mask(ctx, stream, None)
-                    torch.cuda.synchronize()
-                d = timer.durations_ms(tag)
-                flag = ctx.device_error()
-                nbytes = M * K * 2 + B * K * 2 + B * M * 4
-                med, p99 = pctl(list(spans), 50), pctl(list(spans), 99)
-                gbs = nbytes / (med * 1e-6) / 1e9
-                out.append({"M": M, "K": K, "batch": B, "cus": ncu, "placement": place,
-                            "device_flags": flag,
-                            "path": "mfma" if B >= 3 else "valu",
-                            "p50_us": round(med, 2), "p99_us": round(p99, 2),
-                            "GBps": round(gbs, 1),
-                            "pct_of_colour_scaled_peak": round(100 * gbs / (0.75 * HBM_PEAK_GBS), 1),
-                            "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1),
-                            "launch_p50_us": round(pctl(d, 50) * 1e3, 2),
-                            "launch_p99_us": round(pctl(d, 99) * 1e3, 2)})
-                log(f"gemv {M}x{K} B={B} cus={ncu} ({place}): kernel p50 {med:.1f} us p99 {p99:.1f} us "
-                    f"{gbs:.0f} GB/s; with launch p50 {pctl(d, 50) * 1e3:.1f} us")
+                point(W, B, ncu, "xcds", "coloured")
+                if ncu < n_cus and B in (1, 8):
+                    point(W, B, ncu, "spread", "coloured")
+        if M == 4096:
+            # the same weights in contiguous buffers (identity tables): the
+            # cost of the page-table indirection
+            Wc = [torch.empty(pages * P, dtype=torch.uint8, device="cuda:0") for _ in range(copies)]
+            WC = [sg.paged(t, ident, pages) for t in Wc]
+            torch.cuda.synchronize()
+            for Wi in WC:
+                sg.bimodal_relayout(ctx, Wi, sg.paged(w, ident, pages), w_bytes, shift, stream)
+            torch.cuda.synchronize()
+            for B in (1, 8):
+                point(WC, B, n_cus, "xcds", "contiguous")
+            del Wc, WC
         del raw, W
         torch.cuda.empty_cache()
     return {"what": "bf16 W on 48/64 colours in 2 MiB pages, bf16 x, fp32 y; "
-                    f"{copies} rotated weight copies; {launches} launches per point",
+                    f"{copies} rotated weight copies; {launches} launches per point; layout "
+                    "contiguous: the same weights in plain buffers with identity tables",
             "placement": "xcds: the first n logical CUs (whole XCDs, n/32 of them); spread: n/8 "
                          "CUs in each of the 8 XCDs",
             "bytes": "M*K*2 + B*K*2 + B*M*4",
@@ -905,13 +941,13 @@ def bench_sectors(torch, sg, synth, ctx, stream, timer, reps=20):
     import numpy as np
     dev = "cuda:0"
     n = 1 << 28
-    out = {"what": "triad 3x1 GiB fp32 on colours 0..15 of 64 by page size; colour-table "
-                   "classify and page-table build"}
+    out = {"what": "triad 3x1 GiB fp32 on colours 0..15 of 64 by page size (1, 2, 4, 64 KiB "
+                   "and 2 MiB); colour-table classify and page-table build"}
     g = torch.Generator(device=dev)
     g.manual_seed(21)
     b_lin = torch.empty(n, dtype=torch.float32, device=dev).uniform_(-1, 1, generator=g)
     c_lin = torch.empty(n, dtype=torch.float32, device=dev).uniform_(-1, 1, generator=g)
-    for shift in (10, 11, 12, 16):
+    for shift in (10, 11, 12, 16, 21):
         P = 1 << shift
         pages = (n * 4) >> shift
         masks = synth.xor_masks(6, seed=1, min_bit=shift)
@@ -982,32 +1018,26 @@ def bench_sectors(torch, sg, synth, ctx, stream, timer, reps=20):
 def bench_probe(torch, sg, synth, ctx, stream, timer, reps=10, masks=None):
     """Channel probing by bandwidth (in the spirit of the paper's section 5,
     measured through this library).  A triad over three 256 MiB fp32 arrays
-    in 1 KiB pages runs on the pages of a 2 GiB pool where parity(address &
-    M) = 0 (a one-mask hash, colour 0).  If the bits of M feed the channel
-    hash, those pages use half of the channels and the triad slows towards
-    half speed; otherwise it keeps the speed of the unrestricted control
-    (M = bit 8, below the page size, keeps every page).  Only address bits
-    below 21 are probed: user space sees virtual addresses, which agree with
-    physical ones inside 2 MiB fragments."""
-    import numpy as np
+    runs on the pages of a pool where parity(address & M) = 0 (a one-mask
+    hash, colour 0).  If the bits of M feed the channel hash, those pages
+    use half of the channels and the triad slows towards half speed;
+    otherwise it keeps the speed of the unrestricted control (M = bit 8,
+    below the page size, keeps every page).  Bits below 21 are probed with
+    1 KiB pages in a 2 GiB pool: user space sees virtual addresses, which
+    agree with physical ones inside 2 MiB fragments.  Bits 16..32 are then
+    probed with 64 KiB pages in an 8 GiB pool; above bit 20 the result
+    describes where this allocation's fragments landed.  Last, placement at
+    64 KiB and 2 MiB granularity: three 1 GiB arrays on the first pages of a
+    pool four times their size, on a random quarter of its pages, and on
+    colours 0..15 of 64."""
     dev = "cuda:0"
-    shift = 10
-    n = 1 << 26                       # floats per array (256 MiB)
-    pages = (n * 4) >> shift
-    pool_pages = (2 << 30) >> shift
-    raw, base = aligned_pool(torch, pool_pages >> 11, 21)     # 2 GiB at a 2 MiB boundary
-    pt = torch.empty(3 * pages, dtype=torch.int32, device=dev)
-    if masks is None:
-        masks = [1 << 8] + [1 << b for b in range(10, 21)] + \
-                [(1 << a) | (1 << b) for a in range(10, 16) for b in range(a + 1, 17)]
-    out = {"what": "triad 3x256 MiB fp32, 1 KiB pages restricted to parity(addr & M) = 0 "
-                   "in a 2 GiB pool (2 MiB aligned); GB/s and ratio to the control M = bit 8",
-           "points": []}
-    ref = None
-    for m in masks:
-        sg.colour_alloc_pagetable(ctx, [m], base, shift, pool_pages, [0], 3 * pages, pt)
+    out = {"what": "triad 3x256 MiB fp32 restricted to parity(addr & M) = 0; GB/s and ratio to "
+                   "the control M = bit 8. low_bits: 1 KiB pages, 2 GiB pool; high_bits: 64 KiB "
+                   "pages, 8 GiB pool. placement: triad 3x1 GiB on a quarter of a pool",
+           "points": [], "high_bits": [], "placement": []}
+
+    def triad_gbs(tag, pt, base, pool_pages, shift, n, pages):
         A, B, C = (sg.paged(base, pt[i * pages:(i + 1) * pages], pool_pages) for i in range(3))
-        tag = ("probe", m)
         with torch.cuda.stream(stream):
             for _ in range(2):
                 sg.colored_stream(ctx, A, B, C, 3.0, n, shift, stream)
@@ -1016,14 +1046,52 @@ def bench_probe(torch, sg, synth, ctx, stream, timer, reps=10, masks=None):
                 sg.colored_stream(ctx, A, B, C, 3.0, n, shift, stream)
                 timer.stop(e, tag)
         torch.cuda.synchronize()
-        gbs = 12 * n / (pctl(timer.durations_ms(tag), 50) * 1e-3) / 1e9
-        if ref is None:
-            ref = gbs
-        bits = [b for b in range(48) if (m >> b) & 1]
-        out["points"].append({"bits": bits, "GBps": round(gbs, 1), "ratio": round(gbs / ref, 3)})
-        log(f"probe: bits {bits}: {gbs:.0f} GB/s ({gbs / ref:.2f} of control)")
-    del raw, pt
-    torch.cuda.empty_cache()
+        return 12 * n / (pctl(timer.durations_ms(tag), 50) * 1e-3) / 1e9
+
+    def probe(key, shift, pool_bytes, mask_list):
+        n = 1 << 26                       # floats per array (256 MiB)
+        pages = (n * 4) >> shift
+        pool_pages = pool_bytes >> shift
+        raw, base = aligned_pool(torch, pool_bytes >> 21, 21)     # 2 MiB aligned
+        pt = torch.empty(3 * pages, dtype=torch.int32, device=dev)
+        ref = None
+        for m in mask_list:
+            sg.colour_alloc_pagetable(ctx, [m], base, shift, pool_pages, [0], 3 * pages, pt)
+            gbs = triad_gbs(("probe", key, m), pt, base, pool_pages, shift, n, pages)
+            if ref is None:
+                ref = gbs
+            bits = [b for b in range(48) if (m >> b) & 1]
+            out[key].append({"bits": bits, "GBps": round(gbs, 1), "ratio": round(gbs / ref, 3)})
+            log(f"probe ({key}): bits {bits}: {gbs:.0f} GB/s ({gbs / ref:.2f} of control)")
+        del raw, pt
+        torch.cuda.empty_cache()
+
+    if masks is None:
+        masks = [1 << 8] + [1 << b for b in range(10, 21)] + \
+                [(1 << a) | (1 << b) for a in range(10, 16) for b in range(a + 1, 17)]
+    probe("points", 10, 2 << 30, masks)
+    probe("high_bits", 16, 8 << 30, [1 << 8] + [1 << b for b in range(16, 33)] +
+          [(1 << 21) | (1 << 22), (1 << 21) | (1 << 23), (1 << 22) | (1 << 23)])
+
+    n = 1 << 28
+    g = torch.Generator(device=dev)
+    g.manual_seed(13)
+    for shift in (16, 21):
+        pages = (n * 4) >> shift
+        pool_pages = 4 * 3 * pages + 64
+        raw, base = aligned_pool(torch, pool_pages, shift)
+        perm = torch.randperm(pool_pages, device=dev, generator=g)[:3 * pages].to(torch.int32)
+        pt = torch.empty(3 * pages, dtype=torch.int32, device=dev)
+        sg.colour_alloc_pagetable(ctx, synth.xor_masks(6, seed=1, min_bit=shift), base, shift,
+                                  pool_pages, range(16), 3 * pages, pt, stream)
+        for name, table in (("first pages", torch.arange(3 * pages, dtype=torch.int32, device=dev)),
+                            ("random quarter", perm), ("colours 0..15 of 64", pt)):
+            gbs = triad_gbs(("placement", shift, name), table, base, pool_pages, shift, n, pages)
+            out["placement"].append({"page_KiB": 1 << (shift - 10), "pages": name,
+                                     "GBps": round(gbs, 1)})
+            log(f"probe (placement): {1 << (shift - 10)} KiB pages, {name}: {gbs:.0f} GB/s")
+        del raw, perm, pt
+        torch.cuda.empty_cache()
     return out
 
 
