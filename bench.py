@@ -238,6 +238,9 @@ def main():
         gbs = bytes_per_pass / (med * 1e-3) / 1e9
         per_frac[nc] = {
             "colours": f"{nc}/64", "median_ms": round(med, 4), "p99_ms": round(pctl(d, 99), 4),
+            "mean_ms": round(float(np.mean(d)), 4), "max_ms": round(max(d), 4),
+            "slowest_launch": int(np.argmax(d)),
+            "launches_over_1.2x_median": int(sum(1 for v in d if v > 1.2 * med)),
             "GBps": round(gbs, 1), "colour_scaled_peak_GBps": f * HBM_PEAK_GBS,
             "pct_of_colour_scaled_peak": round(100 * gbs / (f * HBM_PEAK_GBS), 1),
             "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1),
