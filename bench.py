@@ -945,7 +945,8 @@ def bench_sectors(torch, sg, synth, ctx, stream, timer, reps=20):
     dev = "cuda:0"
     n = 1 << 28
     out = {"what": "triad 3x1 GiB fp32 on colours 0..15 of 64 by page size (1, 2, 4, 64 KiB "
-                   "and 2 MiB); colour-table classify and page-table build"}
+                   "and 2 MiB), and on contiguous arrays through identity and randomly permuted "
+                   "tables of the same page size; colour-table classify and page-table build"}
     g = torch.Generator(device=dev)
     g.manual_seed(21)
     b_lin = torch.empty(n, dtype=torch.float32, device=dev).uniform_(-1, 1, generator=g)
@@ -979,7 +980,28 @@ def bench_sectors(torch, sg, synth, ctx, stream, timer, reps=20):
         out[f"pagetable_{P >> 10}KiB_ms"] = round(pt_ms, 3)
         log(f"sectors: {P >> 10} KiB pages: triad {ms:.4f} ms "
             f"({12 * n / (ms * 1e-3) / 1e9:.0f} GB/s), page table {pt_ms:.2f} ms")
-        del raw, pt, A, B, C, ident
+        # the same page size over contiguous arrays: identity tables (the
+        # kernel's own cost of the indirection) and the pages of each array in
+        # a random order (the cost of scattered placement)
+        perm = torch.randperm(pages, device=dev, generator=g).to(torch.int32)
+        a_lin = torch.empty(n, dtype=torch.float32, device=dev)
+        torch.cuda.synchronize()
+        for name, table in (("identity", ident), ("permuted", perm)):
+            X = [sg.paged(t, table, pages) for t in (a_lin, b_lin, c_lin)]
+            tag = ("sectors", shift, name)
+            with torch.cuda.stream(stream):
+                for _ in range(3):
+                    sg.colored_stream(ctx, *X, 3.0, n, shift, stream)
+                for _ in range(reps):
+                    e = timer.start()
+                    sg.colored_stream(ctx, *X, 3.0, n, shift, stream)
+                    timer.stop(e, tag)
+            torch.cuda.synchronize()
+            m2 = pctl(timer.durations_ms(tag), 50)
+            out[f"triad_{P >> 10}KiB_{name}_GBps"] = round(12 * n / (m2 * 1e-3) / 1e9, 1)
+            log(f"sectors: {P >> 10} KiB pages, contiguous arrays, {name} tables: "
+                f"{12 * n / (m2 * 1e-3) / 1e9:.0f} GB/s")
+        del raw, pt, A, B, C, ident, perm, a_lin
         torch.cuda.empty_cache()
     del b_lin, c_lin
     # a random table of 2^26 1 KiB partitions
