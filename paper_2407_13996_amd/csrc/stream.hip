@@ -47,6 +47,9 @@ struct Geo {
 // the copy alike; a second workgroup per CU, or 8 loads per lane, costs 5
 // to 20 percent.
 constexpr int kTriadUnroll = 16;
+// Preemptible triad launches: a workgroup stops after the tile it is on and
+// the one it has already claimed, so the tile size bounds the eviction delay.
+constexpr int kTriadUnrollEv = 16;
 constexpr int kRelayoutUnroll = 16;
 constexpr int kStreamWgsPerCu = 1;
 
@@ -309,12 +312,12 @@ int colored_stream(sgdrc_ctx *ctx, const sgdrc_paged *a, const sgdrc_paged *b,
     if (rc)
         return rc;
     const uint64_t n_bytes = n_elems * 4u;
-    constexpr int U = kTriadUnroll;
-    constexpr uint32_t tile = Geo<U>::kTile;
+    constexpr int U = kTriadUnroll, UE = kTriadUnrollEv;
+    const bool ev = stream_preemptible(c, stream);
+    const uint32_t tile = ev ? Geo<UE>::kTile : Geo<U>::kTile;
     const uint64_t n_tiles = ((n_bytes & ~15ull) + tile - 1) / tile;
     if (n_tiles >= (1ull << 31))
         return set_error(SGDRC_EINVAL, "n_elems too large");
-    const bool ev = stream_preemptible(c, stream);
     if (ev && (rc = discard_suspended(c, stream)))
         return rc;
     Gate g;
@@ -333,7 +336,7 @@ int colored_stream(sgdrc_ctx *ctx, const sgdrc_paged *a, const sgdrc_paged *b,
     const uint64_t an = a->pool_pages, bn = b->pool_pages, cn = c_arr->pool_pages;
     auto launch = [=](const Gate &gg, uint32_t gr, bool preempt) {
         if (preempt)
-            hipLaunchKernelGGL((k_triad<U, true>), dim3(gr), dim3(kStreamThreads), 0, hs, ap, apt,
+            hipLaunchKernelGGL((k_triad<UE, true>), dim3(gr), dim3(kStreamThreads), 0, hs, ap, apt,
                                an, bp, bpt, bn, cp, cpt, cn, s, n_bytes, page_shift,
                                (uint32_t)n_tiles, gg);
         else
