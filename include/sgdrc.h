@@ -61,6 +61,8 @@ extern "C" {
 #define SGDRC_DEVERR_PT_RANGE 1u
 #define SGDRC_DEVFLAG_GATE_FALLBACK 2u     /* no workgroup reached an allowed CU; the last did the tiles */
 #define SGDRC_DEVERR_SUSPENDED_DROPPED 4u  /* a suspended launch was discarded unresumed */
+#define SGDRC_DEVERR_HANDBACK 8u           /* a handed-back tile index out of range (skipped;
+                                            * a library fault, never expected) */
 
 /* element encodings */
 enum { SGDRC_F32 = 0, SGDRC_BF16 = 1, SGDRC_F16 = 2 };
@@ -173,10 +175,12 @@ int set_cu_mask(sgdrc_ctx *ctx, void *stream, const sgdrc_cu_mask *mask);
  * eviction flag that the persistent kernel polls; the kernel then restarts
  * on fewer units).  With a flag set, later colored_stream and
  * bimodal_relayout launches on ``stream`` are preemptible: each workgroup
- * reads *d_flag at the start of every tile and, once it reads non-zero,
- * finishes that tile and leaves.  If tiles remain unclaimed, the
- * launch ends "suspended": the rest of the work, including the last n mod
- * 16 bytes, waits for sgdrc_resume.  Every tile is processed exactly once
+ * reads *d_flag at the start of every tile and after claiming the next one
+ * and, once it reads non-zero, finishes the tile it is on, hands back a
+ * tile it has claimed but not begun, and leaves.  If tiles remain
+ * (unclaimed or handed back), the launch ends "suspended": the rest of the
+ * work, including the last n mod 16 bytes, waits for sgdrc_resume, whose
+ * workgroups take the handed-back tiles first.  Every tile is processed exactly once
  * over a launch and its resumptions, so the result equals an uninterrupted
  * launch.  d_flag: device memory, 4-byte aligned, owned by the caller, who
  * writes it (from the host or from a kernel on another stream) and keeps it

@@ -22,6 +22,7 @@ F32, BF16, F16 = 0, 1, 2
 DEVERR_PT_RANGE = 1
 DEVFLAG_GATE_FALLBACK = 2
 DEVERR_SUSPENDED_DROPPED = 4
+DEVERR_HANDBACK = 8
 MAX_MASKS = 8
 BM_BE_WEIGHT, BM_LS_TENSOR, BM_ACTIVATION = 0, 1, 2
 BM_MONOPOLY, BM_COLOCATED = 0, 1

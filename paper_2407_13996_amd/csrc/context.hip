@@ -171,6 +171,9 @@ __global__ __launch_bounds__(64) void k_slot_discard(QueueSlot *q, uint32_t *err
                        __HIP_MEMORY_SCOPE_AGENT);
     if (threadIdx.x == 0) {
         __hip_atomic_store(&q->stopped[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&q->hb_count[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&q->hb_take[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&q->hb_limit[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(&q->state[0], kSlotIdle, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         raise_flag(err, kDevErrSuspendedDropped);
     }
@@ -688,6 +691,9 @@ int sgdrc_suspended(sgdrc_ctx *ctx, void *stream, uint64_t *tiles_left)
             const uint32_t taken = q.grp_next[i * kCounterStride];
             left += taken < size ? size - taken : 0u;
         }
+        // tiles handed back by stopped workgroups (the suspension set the
+        // ring's claim counter to the first of them)
+        left += q.hb_count[0] - q.hb_take[0];
     }
     *tiles_left = left;
     return SGDRC_OK;

@@ -16,11 +16,13 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kLutSize = 4096;          // (XCC_ID[3:0] << 8) | HW_ID[15:8]
 constexpr uint32_t kLutNone = 0xFFFFFFFFu;  // key never seen by the probe
+constexpr uint32_t kSkipTile = 0xFFFFFFFEu;  // a hand-back entry passed over
 constexpr uint32_t kBadPage = 0xFFFFFFFFu;
 
 constexpr uint32_t kDevErrPtRange = 1u;
 constexpr uint32_t kDevFlagGateFallback = 2u;
 constexpr uint32_t kDevErrSuspendedDropped = 4u;  // a suspended launch was discarded unresumed
+constexpr uint32_t kDevErrHandBack = 8u;          // a handed-back tile index out of range
 
 // Queue slot states (QueueSlot::state).
 constexpr uint32_t kSlotIdle = 0u;
@@ -31,6 +33,10 @@ constexpr int kMaxXcds = 16;        // XCC_ID has 4 bits
 constexpr int kMaxGroups = 64;      // queue groups: runs of CUs inside one XCD
 constexpr int kArrivalClasses = 8;
 constexpr int kCounterStride = 32;  // 32-bit words between counters (128 bytes)
+// Tiles a preemptible launch's workgroups can hand back to the resuming
+// launch: at most one per workgroup per launch, so at most twice the grid
+// of one launch is ever live in the ring.
+constexpr uint32_t kHandBackCap = 2048;
 
 // Work distribution state of one stream.  The CUs of each XCD are cut into
 // runs of 2^grp_shift CUs ("queue groups"; a launch picks the run length:
@@ -46,12 +52,14 @@ constexpr int kCounterStride = 32;  // 32-bit words between counters (128 bytes)
 // range that no workgroup took and zeroes the slot for the next launch on
 // the stream.
 //
-// Preemptible launches (see gated_tile_loop) use three more words: the
-// slot's state (kSlotIdle, or kSlotSuspended while an evicted launch still
-// has unclaimed tiles, whose group counters are then kept for the resuming
-// launch), a mark set by every workgroup that stopped on the eviction flag,
-// and a word that stays zero (the flag of a preemptible launch that has
-// none).
+// Preemptible launches (see gated_tile_loop) use more words: the slot's
+// state (kSlotIdle, or kSlotSuspended while an evicted launch still has
+// tiles to do, whose group counters are then kept for the resuming launch),
+// a mark set by every workgroup that stopped on the eviction flag, a word
+// that stays zero (the flag of a preemptible launch that has none), and a
+// ring of tiles handed back: entries [hb_take, hb_count) (indices modulo
+// kHandBackCap) wait for a resuming launch, which may claim those below
+// hb_limit.
 struct QueueSlot {
     uint32_t grp_next[kMaxGroups * kCounterStride];
     uint32_t done[kArrivalClasses * kCounterStride];
@@ -59,6 +67,10 @@ struct QueueSlot {
     uint32_t state[kCounterStride];
     uint32_t stopped[kCounterStride];
     uint32_t zero[kCounterStride];
+    uint32_t hb_count[kCounterStride];
+    uint32_t hb_take[kCounterStride];
+    uint32_t hb_limit[kCounterStride];
+    uint32_t hb[kHandBackCap];
 };
 
 // Per-launch gate arguments (passed by value in the kernel arguments).
@@ -120,6 +132,15 @@ __device__ __forceinline__ uint32_t claim_ticket(uint32_t *ctr, uint32_t *s_tick
     const uint32_t t = __builtin_amdgcn_readfirstlane(*s_ticket);
     __syncthreads();
     return t;
+}
+
+// Preemptible launches, one thread: hands tile ``tile`` (claimed, not
+// processed) back to the resuming launch.
+__device__ __forceinline__ void hand_back(QueueSlot *q, uint32_t tile)
+{
+    const uint32_t i = __hip_atomic_fetch_add(&q->hb_count[0], 1u, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&q->hb[i % kHandBackCap], tile, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ __forceinline__ void log_tile(const Gate &g, uint32_t cu, uint32_t tile)
@@ -218,18 +239,22 @@ enum class Claim { Ahead, Mid, After };
 // effect.
 //
 // Preemptible launches (EV, Claim::Mid only): a workgroup reads the
-// eviction flag ``*g.evict`` at its start and at the start of each tile.
-// Once it has seen the flag set it takes no more tickets: it finishes the
-// tile it is working on and leaves, and marks the slot.
-// If tiles are left unclaimed when the last workgroup arrives and some
-// workgroup stopped on the flag, the launch is suspended instead of
-// completed: the last workgroup leaves the remaining tiles and the
-// epilogue alone, keeps the group counters and sets the slot's state to
-// kSlotSuspended.  A resuming launch (``g.resume``, same kernel arguments
-// and tile ranges, any mask) continues from those counters, stealing
-// across groups as usual, and does nothing if the slot is idle (the
-// launch it resumes had completed).  Fresh launches start on an idle slot
-// (the host discards a suspended launch first, see k_slot_discard).
+// eviction flag ``*g.evict`` at its start, at the start of each tile and
+// right after each claim.  Once it has seen the flag set it takes no more
+// tickets: it finishes the tile it is working on and leaves, and marks the
+// slot; a ticket it claimed before the flag rose is handed back (its tile
+// goes to the slot's hand-back ring) rather than worked on, so that the
+// workgroup leaves after one tile, not two.
+// If tiles are left (unclaimed or handed back) when the last workgroup
+// arrives and some workgroup stopped on the flag, the launch is suspended
+// instead of completed: the last workgroup leaves the remaining tiles and
+// the epilogue alone, keeps the group counters and the ring, and sets the
+// slot's state to kSlotSuspended.  A resuming launch (``g.resume``, same
+// kernel arguments and tile ranges, any mask) first works through the
+// handed-back tiles, then continues from the group counters, stealing
+// across groups as usual, and does nothing if the slot is idle (the launch
+// it resumes had completed).  Fresh launches start on an idle slot (the
+// host discards a suspended launch first, see k_slot_discard).
 //
 // Bodies must not return early or branch around the rest of the tile on a
 // per-lane condition: the loop contains barriers, and a lane-dependent exit
@@ -247,6 +272,7 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
     __shared__ uint32_t s_flag;
     __shared__ uint32_t s_left_lo[kMaxGroups], s_left_hi[kMaxGroups];
     __shared__ uint32_t s_grp_tile[kMaxGroups + 1];
+    __shared__ uint32_t s_hb_lo, s_hb_hi;
     // Prologue: every memory read it needs is issued before any branch on
     // a value read, so that the round trips overlap (the CU-table entry is
     // read even on an XCD without allowed CUs, and then ignored).
@@ -294,6 +320,50 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
         // preemptible: a workgroup that sees the flag at its start takes no
         // ticket at all
         bool stop = stop0;
+        if (EV && g.resume) {
+            // a resuming launch first works through the tiles handed back by
+            // the launch it resumes, claiming them one at a time; a claimed
+            // one goes back to the ring if the flag is up again.  (The
+            // barrier: every wave has read s_stop before it is reused.)
+            __syncthreads();
+            for (;;) {
+                if (threadIdx.x == 0) {
+                    uint32_t tile = kLutNone, fl = 0u;
+                    if (!stop) {
+                        const uint32_t lim = __hip_atomic_load(&g.q->hb_limit[0], __ATOMIC_RELAXED,
+                                                               __HIP_MEMORY_SCOPE_AGENT);
+                        const uint32_t i = __hip_atomic_fetch_add(&g.q->hb_take[0], 1u,
+                                                                  __ATOMIC_RELAXED,
+                                                                  __HIP_MEMORY_SCOPE_AGENT);
+                        fl = __hip_atomic_load(g.evict, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        if (i < lim) {
+                            tile = __hip_atomic_load(&g.q->hb[i % kHandBackCap], __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+                            if (tile >= n_tiles) {
+                                // never expected: skip the entry, keep draining
+                                err |= kDevErrHandBack;
+                                tile = kSkipTile;
+                            } else if (fl != 0u) {
+                                hand_back(g.q, tile);
+                                tile = kLutNone;
+                            }
+                        }
+                    }
+                    s_ticket = tile;
+                    s_stop = (stop || fl != 0u) ? 1u : 0u;
+                }
+                __syncthreads();
+                const uint32_t tile = __builtin_amdgcn_readfirstlane(s_ticket);
+                stop = __builtin_amdgcn_readfirstlane(s_stop) != 0u;
+                __syncthreads();
+                if (tile == kLutNone)
+                    break;
+                if (tile != kSkipTile) {
+                    log_tile(g, cu, tile);
+                    body(tile, cu, err, NoOp());
+                }
+            }
+        }
         uint32_t k = stop ? kLutNone : claim_ticket(&g.q->grp_next[grp * kCounterStride], &s_ticket);
         // One flat loop: work through the own group's range, then steal from
         // the next group in ring order that still has tiles, found by wave 0
@@ -304,7 +374,7 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
         // to the atomic's destination register, for which the compiler waits
         // on the memory counter, stalling the tile's loads behind the
         // previous tile's stores.
-        uint32_t next = 0u;
+        uint32_t next = 0u, fl2 = 0u;
         for (;;) {
             if (k < hi - lo) {
                 uint32_t *const ctr = &g.q->grp_next[grp * kCounterStride];
@@ -318,19 +388,31 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
                 if (CL == Claim::Ahead && threadIdx.x == 0)
                     next = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 auto claim = [&]() {
-                    if (CL == Claim::Mid && threadIdx.x == 0)
+                    if (CL == Claim::Mid && threadIdx.x == 0) {
                         next = __hip_atomic_fetch_add(ctr, (EV && fl != 0u) ? 0u : 1u,
                                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        // preemptible: the flag again, issued before the
+                        // stores, so its value is back with the ticket
+                        if (EV)
+                            fl2 = __hip_atomic_load(g.evict, __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
+                    }
                 };
                 log_tile(g, cu, lo + k);
                 body(lo + k, cu, err, claim);
                 if (CL == Claim::After && threadIdx.x == 0)
                     next = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 if (threadIdx.x == 0) {
+                    // halt: the claim added nothing (flag seen at the tile's
+                    // start); late: the flag rose after that, so the ticket
+                    // just claimed is handed back instead of worked on
                     const bool halt = EV && fl != 0u;
-                    s_ticket = halt ? kLutNone : next;
+                    const bool late = EV && !halt && fl2 != 0u;
+                    if (late && next < hi - lo)
+                        hand_back(g.q, lo + next);
+                    s_ticket = (halt || late) ? kLutNone : next;
                     if (EV)
-                        s_stop = halt ? 1u : 0u;
+                        s_stop = (halt || late) ? 1u : 0u;
                 }
                 __syncthreads();
                 k = __builtin_amdgcn_readfirstlane(s_ticket);
@@ -400,25 +482,61 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
             s_left_hi[threadIdx.x] = b;
             left = a < b;
         }
-        if (threadIdx.x == 0)
+        if (threadIdx.x == 0) {
             s_stop = EV ? __hip_atomic_load(&g.q->stopped[0], __ATOMIC_RELAXED,
                                             __HIP_MEMORY_SCOPE_AGENT)
                         : 0u;
+            if (EV) {
+                // handed-back tiles not yet worked on: [min(take, limit), count)
+                const uint32_t cnt = __hip_atomic_load(&g.q->hb_count[0], __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT);
+                const uint32_t take = __hip_atomic_load(&g.q->hb_take[0], __ATOMIC_RELAXED,
+                                                        __HIP_MEMORY_SCOPE_AGENT);
+                const uint32_t lim = __hip_atomic_load(&g.q->hb_limit[0], __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT);
+                const uint32_t from = take < lim ? take : lim;
+                s_hb_lo = from;
+                s_hb_hi = cnt;
+                left = left || from < cnt;
+            }
+        }
         const bool any_left = __syncthreads_or(left ? 1 : 0) != 0;
         const bool stopped = EV && __builtin_amdgcn_readfirstlane(s_stop) != 0u;
         if (EV && dead) {
             // nothing ran: only the arrival counters are reset
             reset_slot(g.q, true);
         } else if (EV && any_left && stopped) {
-            // suspended: the unclaimed tiles wait for a resuming launch
+            // suspended: the unclaimed and handed-back tiles wait for a
+            // resuming launch, which may claim the ring up to its end now
             reset_slot(g.q, true);
             if (threadIdx.x == 0) {
+                __hip_atomic_store(&g.q->hb_take[0], s_hb_lo, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&g.q->hb_limit[0], s_hb_hi, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
                 __hip_atomic_store(&g.q->stopped[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 __hip_atomic_store(&g.q->state[0], kSlotSuspended, __ATOMIC_RELAXED,
                                    __HIP_MEMORY_SCOPE_AGENT);
             }
         } else {
             if (any_left) {
+                if (EV) {
+                    // handed-back tiles that no workgroup took (none reached
+                    // an allowed CU)
+                    uint32_t i = __builtin_amdgcn_readfirstlane(s_hb_lo);
+                    const uint32_t e = __builtin_amdgcn_readfirstlane(s_hb_hi);
+                    while (i < e) {
+                        const uint32_t t = __builtin_amdgcn_readfirstlane(__hip_atomic_load(
+                            &g.q->hb[i % kHandBackCap], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                        if (t < n_tiles) {
+                            log_tile(g, cu, t);
+                            body(t, cu, err, NoOp());
+                        } else {
+                            err |= threadIdx.x == 0 ? kDevErrHandBack : 0u;
+                        }
+                        i += 1u;
+                    }
+                }
                 // worked through in one flat loop so that no barrier of the
                 // body ends up in a nested loop
                 uint32_t c = 0u;
@@ -445,6 +563,9 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
             reset_slot(g.q);
             if (EV && threadIdx.x == 0) {
                 __hip_atomic_store(&g.q->stopped[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&g.q->hb_count[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&g.q->hb_take[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&g.q->hb_limit[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 __hip_atomic_store(&g.q->state[0], kSlotIdle, __ATOMIC_RELAXED,
                                    __HIP_MEMORY_SCOPE_AGENT);
             }

@@ -52,6 +52,8 @@ constexpr int kTriadUnroll = 16;
 constexpr int kTriadUnrollEv = 16;
 constexpr int kRelayoutUnroll = 16;
 constexpr int kStreamWgsPerCu = 1;
+// each workgroup of a preemptible launch hands back at most one tile
+static_assert(2 * kStreamWgsPerCu * kMaxCus <= (int)kHandBackCap, "hand-back ring too small");
 
 // Bytes of the span [from, from + span) that lie below n16.
 __device__ __forceinline__ uint32_t span_valid(uint64_t from, uint64_t n16, uint32_t span)

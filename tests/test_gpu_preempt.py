@@ -187,6 +187,59 @@ def test_triad_evicted_mid_run_every_tile_once(ctx, orc):
     assert mid >= 1, "no attempt was evicted mid-run"
 
 
+def test_triad_resumption_evicted_mid_run_again(ctx, orc):
+    """Evicted mid-run, resumed on 16 CUs and evicted mid-run again (tiles
+    handed back by the first eviction are worked through first, and may be
+    handed back again), then finished on all CUs: every tile once."""
+    n_cu = ctx.num_cus
+    tr = Triad(orc, 16, 64 * 1024 * 1024 + 3, seed=55)    # 256 MiB arrays, 4097 tiles
+    st, st2 = torch.cuda.Stream(), torch.cuda.Stream()
+    flag = torch.zeros(1, dtype=torch.int32, device=DEV)
+    twice = 0
+    for d1, d2 in ((20, 100), (40, 300), (80, 600)):
+        tr.reset()
+        flag.zero_()
+        torch.cuda.synchronize()
+        logs = Logs(ctx, tr.tiles)
+        try:
+            sg.set_eviction_flag(ctx, st, flag)
+            tr.launch(ctx, st)
+            _delay(st2, d1)
+            with torch.cuda.stream(st2):
+                flag.fill_(1)
+            left1 = sg.suspended(ctx, st)
+            torch.cuda.synchronize()
+            flag.zero_()
+            torch.cuda.synchronize()
+            sg.set_cu_mask(ctx, st, range(16))
+            sg.resume(ctx, st)
+            _delay(st2, d2)
+            with torch.cuda.stream(st2):
+                flag.fill_(1)
+            left2 = sg.suspended(ctx, st)
+            torch.cuda.synchronize()
+            say(f"evicted after ~{d1} us: {left1} left; resumed on 16 CUs, evicted after ~{d2} us: "
+                f"{left2} left of {tr.tiles}")
+            twice += 0 < left2 < left1
+            flag.zero_()
+            torch.cuda.synchronize()
+            sg.set_cu_mask(ctx, st, None)
+            rounds = 0
+            while sg.suspended(ctx, st) and rounds < 4:
+                sg.resume(ctx, st)
+                rounds += 1
+            assert sg.suspended(ctx, st) == 0
+            cl, tl = logs.snapshot()
+        finally:
+            logs.close()
+            sg.set_cu_mask(ctx, st, None)
+            sg.set_eviction_flag(ctx, st, None)
+        tr.check()
+        assert (tl == 1).all(), np.unique(tl, return_counts=True)
+        assert cl.sum() == tr.tiles
+    assert twice >= 1, "no resumption was evicted mid-run"
+
+
 def test_resume_after_completion_does_nothing(ctx, orc):
     tr = Triad(orc, 12, 5 * 1024 + 77, seed=60)
     st = torch.cuda.Stream()
