@@ -62,15 +62,29 @@ class Timer:
     """Per-launch HIP event pairs on one stream."""
 
     def __init__(self, torch, stream):
-        self.torch, self.stream, self.pairs = torch, stream, []
+        self.torch, self.stream, self.pairs, self.pool = torch, stream, [], []
+
+    def reserve(self, n):
+        """Creates n events ahead of a timed region (recording each once, so
+        that the runtime allocates it now): creating events inside the region
+        once stalled the host long enough to leave the GPU idle for tens of
+        milliseconds between two launches."""
+        for _ in range(n):
+            e = self.torch.cuda.Event(enable_timing=True)
+            e.record(self.stream)
+            self.pool.append(e)
+        self.torch.cuda.synchronize()
+
+    def _event(self):
+        return self.pool.pop() if self.pool else self.torch.cuda.Event(enable_timing=True)
 
     def start(self):
-        e = self.torch.cuda.Event(enable_timing=True)
+        e = self._event()
         e.record(self.stream)
         return e
 
     def stop(self, e0, tag=None):
-        e1 = self.torch.cuda.Event(enable_timing=True)
+        e1 = self._event()
         e1.record(self.stream)
         self.pairs.append((tag, e0, e1))
 
@@ -218,7 +232,7 @@ def main():
             for nc in fractions:
                 a, b, c = arrays[nc]
                 sg.colored_stream(ctx, a, b, c, 3.0, n, shift, stream)
-        torch.cuda.synchronize()
+        timer.reserve(2 * args.steps * len(fractions))
         log(f"timing {args.steps} steps x {len(fractions)} triad passes")
         t0 = time.perf_counter()
         for _ in range(args.steps):
