@@ -66,9 +66,9 @@ class Timer:
 
     def reserve(self, n):
         """Creates n events ahead of a timed region (recording each once, so
-        that the runtime allocates it now): creating events inside the region
-        once stalled the host long enough to leave the GPU idle for tens of
-        milliseconds between two launches."""
+        that the runtime allocates it now) and keeps host-side allocation out
+        of the region: an event pair there once spanned 21 ms around a
+        0.5 ms launch, which a host stall that let the GPU run dry explains."""
         for _ in range(n):
             e = self.torch.cuda.Event(enable_timing=True)
             e.record(self.stream)
