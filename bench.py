@@ -157,7 +157,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: the colour-restricted path is per device and "
-              "this build runs no collectives; use --gpus 1", file=sys.stderr)
+              "runs no collectives; use --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
