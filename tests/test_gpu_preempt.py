@@ -333,6 +333,64 @@ def test_relayout_evicted_then_resumed(ctx, orc, shift, n_bytes):
     assert (to_host(d_dst).view(np.uint8) == ref).all()
 
 
+def test_relayout_evicted_mid_run_every_tile_once(ctx, orc):
+    """A 128 MiB relayout on 16 CUs, evicted from another stream while it
+    runs (tiles claimed just before the flag rose are handed back), then
+    finished on all CUs: byte-exact, every 64 KiB tile once."""
+    shift, n_bytes = 16, 128 * 1024 * 1024 + 9
+    P = 1 << shift
+    n_pages = -(-n_bytes // P)
+    tiles = -(-(n_bytes & ~15) // 65536)
+    pool = int(n_pages * 4 * 1.5) + 64
+    masks = synth.xor_masks(6, seed=5, min_bit=shift)
+    pt_s, f1 = orc.pagetable(masks, 0, shift, pool, synth.colour_set_bits(range(16)), n_pages)
+    pt_d, f2 = orc.pagetable(masks, 0, shift, pool, synth.colour_set_bits(range(16, 32)), n_pages)
+    assert min(f1, f2) >= n_pages
+    src = synth.random_u16(pool * P // 2, seed=6)
+    d_src = to_dev(src)
+    d_dst = torch.zeros(pool * P // 2, dtype=torch.int16, device=DEV)
+    ref = np.zeros(pool * P, dtype=np.uint8)
+    orc.relayout(ref, pt_d, src.view(np.uint8), pt_s, n_bytes, shift)
+    st, st2 = torch.cuda.Stream(), torch.cuda.Stream()
+    flag = torch.zeros(1, dtype=torch.int32, device=DEV)
+    dpt_s, dpt_d = to_dev(pt_s), to_dev(pt_d)
+    mid = 0
+    for delay_us in (30, 100, 250):
+        d_dst.zero_()
+        flag.zero_()
+        torch.cuda.synchronize()
+        logs = Logs(ctx, tiles)
+        try:
+            sg.set_eviction_flag(ctx, st, flag)
+            sg.set_cu_mask(ctx, st, range(16))
+            sg.bimodal_relayout(ctx, sg.paged(d_dst, dpt_d, pool), sg.paged(d_src, dpt_s, pool),
+                                n_bytes, shift, st)
+            _delay(st2, delay_us)
+            with torch.cuda.stream(st2):
+                flag.fill_(1)
+            left = sg.suspended(ctx, st)
+            torch.cuda.synchronize()
+            say(f"relayout flag after ~{delay_us} us: {left} of {tiles} tiles left")
+            mid += 0 < left < tiles
+            flag.zero_()
+            torch.cuda.synchronize()
+            sg.set_cu_mask(ctx, st, None)
+            rounds = 0
+            while sg.suspended(ctx, st) and rounds < 4:
+                sg.resume(ctx, st)
+                rounds += 1
+            assert sg.suspended(ctx, st) == 0
+            cl, tl = logs.snapshot()
+        finally:
+            logs.close()
+            sg.set_cu_mask(ctx, st, None)
+            sg.set_eviction_flag(ctx, st, None)
+        assert (to_host(d_dst).view(np.uint8) == ref).all()
+        assert (tl == 1).all(), np.unique(tl, return_counts=True)
+        assert cl.sum() == tiles
+    assert mid >= 1, "no attempt was evicted mid-run"
+
+
 def test_tidal_handover_ls_gemv_and_evicted_triad(ctx, orc):
     """The section 7.1 sequence on one GPU: a best-effort triad runs on all
     CUs; a latency-sensitive GEMV arrives, the triad is evicted, the
