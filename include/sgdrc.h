@@ -304,6 +304,28 @@ int colour_alloc_pagetable_table(sgdrc_ctx *ctx, const sgdrc_colour_table *table
 int bimodal_relayout(sgdrc_ctx *ctx, const sgdrc_paged *dst, const sgdrc_paged *src,
                      uint64_t n_bytes, uint32_t page_shift, void *stream);
 
+/* One copy of a batched relayout. */
+typedef struct {
+    sgdrc_paged dst;
+    sgdrc_paged src;
+    uint64_t n_bytes;
+    uint32_t page_shift;
+    uint32_t reserved; /* 0 */
+} sgdrc_relayout_item;
+
+/* Batched bimodal relayout (paper section 7.2: on a change of co-location
+ * state every latency-sensitive tensor moves): the n_items copies of
+ * ``items``, each exactly as bimodal_relayout would make it, in one launch
+ * per 32 items instead of one per tensor.  Items may differ in page size;
+ * no item's destination may overlap another item's source or destination.
+ * Always a plain launch (not preemptible, even on a stream with an
+ * eviction flag).  n_items == 0 does nothing.  Asynchronous; ``items`` is
+ * read before the call returns.  EINVAL: items NULL with n_items > 0, an
+ * item invalid as for bimodal_relayout, reserved not 0, more than 2^31
+ * 64 KiB tiles in one launch. */
+int bimodal_relayout_batch(sgdrc_ctx *ctx, const sgdrc_relayout_item *items, uint32_t n_items,
+                           void *stream);
+
 /* Colour-restricted streaming triad (paper section 6, SPT step 4, the
  * re-indexed vector kernel): a[i] = fmaf(s, c[i], b[i]) for i < n_elems,
  * one rounding, every fp32 element reached through its array's page table
@@ -354,7 +376,8 @@ int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, 
  *                       and read from where it was last written; reused
  *                       through sgdrc_bm_acquire / sgdrc_bm_release.
  *
- * Moves are bimodal_relayout launches on the given stream; the caller
+ * Moves are relayout launches on the given stream (a state change moves
+ * every latency-sensitive tensor with one bimodal_relayout_batch); the caller
  * orders them against the kernels that use the tensors and keeps all
  * buffers alive.  Thread-safe.  Errors as elsewhere; a NULL or destroyed
  * runtime gives EINVAL. */

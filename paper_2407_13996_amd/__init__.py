@@ -59,6 +59,11 @@ class Paged(ctypes.Structure):
                 ("pool_pages", ctypes.c_uint64)]
 
 
+class RelayoutItem(ctypes.Structure):
+    _fields_ = [("dst", Paged), ("src", Paged), ("n_bytes", ctypes.c_uint64),
+                ("page_shift", ctypes.c_uint32), ("reserved", ctypes.c_uint32)]
+
+
 _lib = None
 
 
@@ -103,6 +108,7 @@ def lib() -> ctypes.CDLL:
             "colour_alloc_pagetable": ([vp, P(Hash), u64, u32, u64, P(ColourSet), u64, vp,
                                         P(u64), vp], i32),
             "bimodal_relayout": ([vp, P(Paged), P(Paged), u64, u32, vp], i32),
+            "bimodal_relayout_batch": ([vp, P(RelayoutItem), u32, vp], i32),
             "colored_stream": ([vp, P(Paged), P(Paged), P(Paged), ctypes.c_float, u64, u32, vp],
                                i32),
             "colored_gemv": ([vp, P(Paged), i32, u32, u32, vp, i32, u32, vp, u32, vp], i32),
@@ -337,6 +343,15 @@ def bimodal_relayout(ctx, dst: Paged, src: Paged, n_bytes: int, page_shift: int,
                      stream=None) -> None:
     _check(lib().bimodal_relayout(_h(ctx), ctypes.byref(dst), ctypes.byref(src), int(n_bytes),
                                   int(page_shift), _stream(stream)))
+
+
+def bimodal_relayout_batch(ctx, items, stream=None) -> None:
+    """``items``: (dst Paged, src Paged, n_bytes, page_shift) tuples, copied
+    as bimodal_relayout would, in one launch per 32 items."""
+    arr = (RelayoutItem * max(len(items), 1))()
+    for i, (dst, src, n_bytes, shift) in enumerate(items):
+        arr[i] = RelayoutItem(dst, src, int(n_bytes), int(shift), 0)
+    _check(lib().bimodal_relayout_batch(_h(ctx), arr, len(items), _stream(stream)))
 
 
 def colored_stream(ctx, a: Paged, b: Paged, c: Paged, s: float, n_elems: int, page_shift: int,

@@ -13,7 +13,8 @@
 //    kernel's state and read from where they were last written; their
 //    buffers are reused through a free list.
 //
-// Host-only bookkeeping; every move is a bimodal_relayout launch.
+// Host-only bookkeeping; moves are bimodal_relayout launches (a state
+// change moves all latency-sensitive tensors in one batched relayout).
 #include <algorithm>
 #include <cstring>
 #include <mutex>
@@ -166,10 +167,25 @@ int sgdrc_bm_set_state(sgdrc_bimodal *bm, int state, void *stream)
     std::lock_guard<std::mutex> lock(b->mu);
     if (state == b->state)
         return SGDRC_OK;
+    // every latency-sensitive tensor moves to the new state's page set, all
+    // in one batched relayout (one launch per 32 tensors)
     const int home = state == SGDRC_BM_COLOCATED ? SGDRC_BM_PART : SGDRC_BM_ALL;
+    std::vector<sgdrc_relayout_item> moves;
+    std::vector<BmTensor *> moved;
     for (BmTensor &x : b->t)
-        if (x.cls == SGDRC_BM_LS_TENSOR && (rc = move_to(b, x, home, stream)))
-            return rc;
+        if (x.cls == SGDRC_BM_LS_TENSOR && x.where != home) {
+            sgdrc_relayout_item it{};
+            it.dst = home == SGDRC_BM_ALL ? x.all : x.part;
+            it.src = home == SGDRC_BM_ALL ? x.part : x.all;
+            it.n_bytes = x.bytes;
+            it.page_shift = x.shift;
+            moves.push_back(it);
+            moved.push_back(&x);
+        }
+    if ((rc = bimodal_relayout_batch(b->ctx, moves.data(), (uint32_t)moves.size(), stream)))
+        return rc;
+    for (BmTensor *x : moved)
+        x->where = home;
     b->state = state;
     return SGDRC_OK;
 }

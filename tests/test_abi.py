@@ -102,6 +102,29 @@ def test_relayout_and_stream_argument_errors(L):
     assert L.colored_stream(NULL, r(pg()), r(pg(pt=2)), r(pg()), 3.0, 100, 16, None) == sg.EINVAL
 
 
+def test_relayout_batch_argument_errors(L):
+    def items(*its):
+        arr = (sg.RelayoutItem * max(len(its), 1))()
+        for i, it in enumerate(its):
+            arr[i] = it
+        return arr, len(its)
+
+    ok = sg.RelayoutItem(pg(), pg(), 100, 16, 0)
+    a, n = items(ok, ok)
+    assert L.bimodal_relayout_batch(NULL, a, n, None) == sg.ENODEV
+    assert L.bimodal_relayout_batch(NULL, None, 0, None) == sg.ENODEV      # nothing to check
+    assert L.bimodal_relayout_batch(NULL, None, 3, None) == sg.EINVAL
+    for bad in (sg.RelayoutItem(pg(), pg(), 100, 9, 0), sg.RelayoutItem(pg(), pg(), 100, 31, 0),
+                sg.RelayoutItem(pg(pool=128), pg(), 100, 16, 0),
+                sg.RelayoutItem(pg(), pg(pt=0), 100, 16, 0),
+                sg.RelayoutItem(pg(), pg(pages=0), 100, 16, 0),
+                sg.RelayoutItem(pg(), pg(), 100, 16, 1),                   # reserved
+                sg.RelayoutItem(pg(), pg(), 1 << 62, 16, 0)):             # too many tiles
+        a, n = items(ok, bad)
+        assert L.bimodal_relayout_batch(NULL, a, n, None) == sg.EINVAL
+        assert "item 1" in L.sgdrc_last_error().decode()
+
+
 def test_gemv_argument_errors(L):
     r = ctypes.byref
     w = pg()

@@ -258,6 +258,46 @@ def test_relayout_matches_oracle(ctx, orc, shift, n_bytes):
     assert (to_host(d_dst) == ref).all()
 
 
+@pytest.mark.parametrize("n_items,cus", [(40, None), (7, 37)])
+def test_relayout_batch_matches_oracle(ctx, orc, n_items, cus):
+    """Batched relayout: items of mixed page sizes and ragged lengths (one
+    empty, some shorter than 16 bytes, some spanning several tiles), more
+    than one launch's worth of items, and under a random CU subset; each item
+    equals the oracle's relayout, dst bytes past n_bytes untouched."""
+    rng = np.random.default_rng(n_items)
+    shifts = [10, 12, 16, 10, 12, 16, 21, 16]
+    items, refs, devs, keep = [], [], [], []
+    for i in range(n_items):
+        shift = shifts[i % len(shifts)]
+        P = 1 << shift
+        kind = i % 5
+        n_bytes = (0 if i == 3 else int(rng.integers(1, 16)) if kind == 1
+                   else int(rng.integers(1, 3 * 65536 + 100)) if kind != 4
+                   else int(rng.integers(3 * 65536, 9 * 65536)))
+        n_pages = max(1, -(-n_bytes // P))
+        pt_s, src_pages = make_tables(orc, shift, n_pages, range(16), 10 + i)
+        pt_d, dst_pages = make_tables(orc, shift, n_pages, range(32, 48), 60 + i)
+        src = synth.random_bytes(src_pages * P, seed=100 + i)
+        dst0 = synth.random_bytes(dst_pages * P, seed=200 + i)
+        d_src, d_dst, d_ps, d_pd = to_dev(src), to_dev(dst0), to_dev(pt_s), to_dev(pt_d)
+        keep += [d_src, d_ps, d_pd]
+        items.append((sg.paged(d_dst, d_pd, dst_pages), sg.paged(d_src, d_ps, src_pages),
+                      n_bytes, shift))
+        ref = dst0.copy()
+        orc.relayout(ref, pt_d, src, pt_s, n_bytes, shift)
+        refs.append(ref)
+        devs.append(d_dst)
+    say(f"relayout batch of {n_items} items on {'all' if cus is None else cus} CUs")
+    if cus is not None:
+        sg.set_cu_mask(ctx, None, synth.random_cu_subset(ctx.num_cus, cus, seed=9))
+    try:
+        sg.bimodal_relayout_batch(ctx, items)
+    finally:
+        sg.set_cu_mask(ctx, None, None)
+    for i, (d, ref) in enumerate(zip(devs, refs)):
+        assert (to_host(d) == ref).all(), i
+
+
 def test_relayout_round_trip_fp16_is_identity(ctx, orc):
     shift = 16
     n_pages = 300
