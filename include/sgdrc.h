@@ -319,7 +319,7 @@ typedef struct {
  * per 32 items instead of one per tensor.  Items may differ in page size;
  * no item's destination may overlap another item's source or destination.
  * Always a plain launch (not preemptible, even on a stream with an
- * eviction flag).  n_items == 0 does nothing.  Asynchronous; ``items`` is
+ * eviction flag).  n_items == 0 launches nothing.  Asynchronous; ``items`` is
  * read before the call returns.  EINVAL: items NULL with n_items > 0, an
  * item invalid as for bimodal_relayout, reserved not 0, more than 2^31
  * 64 KiB tiles in one launch. */

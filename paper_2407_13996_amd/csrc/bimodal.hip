@@ -182,7 +182,8 @@ int sgdrc_bm_set_state(sgdrc_bimodal *bm, int state, void *stream)
             moves.push_back(it);
             moved.push_back(&x);
         }
-    if ((rc = bimodal_relayout_batch(b->ctx, moves.data(), (uint32_t)moves.size(), stream)))
+    if (!moves.empty() &&
+        (rc = bimodal_relayout_batch(b->ctx, moves.data(), (uint32_t)moves.size(), stream)))
         return rc;
     for (BmTensor *x : moved)
         x->where = home;
