@@ -541,11 +541,18 @@ int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, 
     GemvKernel k;
     uint64_t n_tiles;
     if (mfma) {
-        // Between one and two 16-row tiles per allowed CU, some CUs would
-        // take two tiles and the rest one; 8-row tiles halve that imbalance
-        // (and give the same bits).
-        const uint64_t t16 = (M + 15u) / 16u, allowed = (uint64_t)stream_allowed_cus(c, stream);
-        const int rows = t16 > allowed && t16 < 2u * allowed ? 8 : 16;
+        // Tile height by the rows of the busiest CU: 8-row tiles when they
+        // cut its rows by a fifth or more (fewer tiles than CUs, or a last
+        // round that 16-row tiles fill unevenly), since a row costs more in
+        // an 8-row tile (x is read twice as often per W byte); the same bits
+        // either way.  Over M = 1536..8192 rows of 4096 and 11008, batch 4
+        // and 8, on 64..256 CUs this is never more than 5 percent slower
+        // than the better height (a rule of one to two 16-row tiles per CU
+        // was up to 26 percent slower).
+        const uint64_t allowed = (uint64_t)std::max(1, stream_allowed_cus(c, stream));
+        const uint64_t r16 = (((M + 15u) / 16u + allowed - 1u) / allowed) * 16u;
+        const uint64_t r8 = (((M + 7u) / 8u + allowed - 1u) / allowed) * 8u;
+        const int rows = 5u * r8 <= 4u * r16 ? 8 : 16;
         if (rows == 16)
             k = w_dtype == SGDRC_BF16 ? k_gemm_mfma<SGDRC_BF16, 16> : k_gemm_mfma<SGDRC_F16, 16>;
         else
