@@ -587,6 +587,28 @@ def test_gemv_sector_pages(ctx, orc, shift, B):
     run_gemv(ctx, orc, 300, 1024, B, sg.BF16, sg.BF16, shift, seed=shift + B)
 
 
+@pytest.mark.parametrize("M,K,B", [(1, 11008, 1), (1, 11008, 8), (1, 8, 1), (1, 8, 4), (2, 4096, 3)])
+def test_gemv_single_rows(ctx, orc, M, K, B):
+    """One or two output rows: a single tile with most of its rows outside M
+    (vector path, and MFMA from batch 3)."""
+    say(f"gemv bf16 {M}x{K} B={B}")
+    run_gemv(ctx, orc, M, K, B, sg.BF16, sg.BF16, 16, seed=M * 7 + K + B)
+
+
+def test_zero_length_triad_and_relayout_touch_nothing(ctx):
+    shift, P = 16, 65536
+    pt = torch.zeros(1, dtype=torch.int32, device=DEV)
+    a = torch.full((P // 4,), 7.0, dtype=torch.float32, device=DEV)
+    b = torch.ones(P // 4, dtype=torch.float32, device=DEV)
+    sg.colored_stream(ctx, sg.paged(a, pt, 1), sg.paged(b, pt, 1), sg.paged(b, pt, 1), 3.0, 0, shift)
+    dst = torch.full((P,), 5, dtype=torch.uint8, device=DEV)
+    src = torch.zeros(P, dtype=torch.uint8, device=DEV)
+    sg.bimodal_relayout(ctx, sg.paged(dst, pt, 1), sg.paged(src, pt, 1), 0, shift)
+    sg.bimodal_relayout_batch(ctx, [])
+    assert (to_host(a) == 7.0).all()
+    assert (to_host(dst) == 5).all()
+
+
 @pytest.mark.parametrize("M,K,B", [(4096, 11008, 1), (11008, 4096, 8)])
 def test_gemv_config3_full_size(ctx, orc, M, K, B):
     say(f"gemv bf16 {M}x{K} B={B}, 2 MiB pages, colours 0..47 of 64")
