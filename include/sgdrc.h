@@ -244,9 +244,12 @@ int colour_classify(sgdrc_ctx *ctx, const sgdrc_hash *hash, const uint64_t *d_ad
                     uint64_t n, uint8_t *d_colours, uint64_t *d_hist, void *stream);
 
 /* Page-table build (paper section 6, SPT steps 2-3, per-colour page lists
- * of a reserved pool).  Pool page i (0 <= i < pool_pages) has the address
- * addr_origin + i * 2^page_shift and qualifies when its colour is in
- * ``set``.  Writes to d_pt the first min(found, n_needed) qualifying page
+ * of a reserved pool).  Pool page i (0 <= i < pool_pages) covers the bytes
+ * [a, a + 2^page_shift), a = addr_origin + i * 2^page_shift, and qualifies
+ * when every one of those bytes has a colour in ``set`` (section 6 colours
+ * whole sectors).  With no mask bit below page_shift that is the colour of
+ * a; a mask bit inside the page gives the page's bytes several colours,
+ * all of which must be in the set.  Writes to d_pt the first min(found, n_needed) qualifying page
  * indices in ascending order, and sets *n_found = found, the number of
  * qualifying pages in the whole pool.  Returns SGDRC_ENOMEM when
  * found < n_needed (d_pt then holds all ``found`` pages).  Synchronous:
@@ -351,6 +354,32 @@ int colored_stream(sgdrc_ctx *ctx, const sgdrc_paged *a, const sgdrc_paged *b,
 int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, uint32_t K,
                  const void *d_x, int x_dtype, uint32_t batch, float *d_y,
                  uint32_t page_shift, void *stream);
+
+/* The launch plan colored_gemv uses for a shape, given the number of CUs
+ * the stream's mask allows (host-only, no context, no device): the kernel
+ * path (vector ALUs or MFMA), rows of W per tile, loads in flight (vector
+ * path: 16-byte loads per lane and row; MFMA: register sets of 2 KiB row
+ * chunks), the batch columns the kernel is compiled for, the tile count,
+ * and sum_depth: the most roundings any product W[m][k] x[b][k] meets on its
+ * way into y (the fp32 additions and FMAs of the kernel's fixed summation
+ * tree, each MFMA counted as up to 32 additions), so that
+ * |y - exact| <= sum_depth * 2^-24 * sum_k |W[m][k] x[b][k]| to first order
+ * (products of bf16 or f16 operands are exact in fp32).  Lets tests and
+ * tools see which kernel a configuration runs.  EINVAL: allowed_cus outside
+ * 1..256, NULL out, or a shape colored_gemv rejects. */
+enum { SGDRC_GEMV_VALU = 0, SGDRC_GEMV_MFMA = 1 };
+typedef struct {
+    uint32_t path;
+    uint32_t rows;
+    uint32_t loads;
+    uint32_t batch_cols;
+    uint64_t tiles;
+    uint32_t sum_depth;
+    uint32_t reserved;
+} sgdrc_gemv_plan;
+
+int colored_gemv_plan(uint32_t allowed_cus, int w_dtype, uint32_t M, uint32_t K, int x_dtype,
+                    uint32_t batch, sgdrc_gemv_plan *out);
 
 /* ---------------------------------------------------- bimodal tensors
  *

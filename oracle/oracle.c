@@ -65,6 +65,33 @@ static int in_set(const uint64_t set[4], uint32_t colour)
     return (int)((set[colour >> 6] >> (colour & 63u)) & 1u);
 }
 
+/* Paper section 6 colours whole sectors: all bytes of a sector lie on the
+ * channels of its colour.  A pool page therefore belongs to a colour set
+ * only if every byte of it has a colour in the set.  The colour of an
+ * address depends only on the address bits that some mask selects, so the
+ * colours of the bytes of the page at ``base`` are exactly the colours of
+ * base + o for every offset o made of in-page bits that some mask selects
+ * (o = 0 among them).  With no mask bit below the page size that is the
+ * colour of the page's base alone. */
+static int page_in_set(uint64_t base, uint32_t page_shift, const uint64_t *masks,
+                       uint32_t n_masks, const uint64_t set[4])
+{
+    uint64_t selected = 0;
+    for (uint32_t k = 0; k < n_masks; ++k)
+        selected |= masks[k];
+    const uint64_t in_page = selected & ((1ull << page_shift) - 1ull);
+    /* o runs over every subset of the bits of in_page, in increasing order:
+     * 0, then (o - in_page) & in_page until o == in_page */
+    uint64_t o = 0;
+    for (;;) {
+        if (!in_set(set, oracle_colour(base + o, masks, n_masks)))
+            return 0;
+        if (o == in_page)
+            return 1;
+        o = (o - in_page) & in_page;
+    }
+}
+
 /* Paper section 6, SPT steps 1-3: pages of the reserved pool are sorted
  * into per-colour lists; a tensor takes its pages from the lists of its
  * colours.  Reading used here: ascending pool index, first n pages. */
@@ -76,8 +103,7 @@ uint64_t oracle_pagetable(const uint64_t *masks, uint32_t n_masks, uint64_t orig
     uint64_t found = 0;
     for (uint64_t i = 0; i < pool_pages; ++i) {
         uint64_t page_addr = origin + (i << page_shift);
-        uint32_t c = oracle_colour(page_addr, masks, n_masks);
-        if (in_set(colour_set, c)) {
+        if (page_in_set(page_addr, page_shift, masks, n_masks, colour_set)) {
             if (found < n_needed)
                 pt[found] = (uint32_t)i;
             found += 1;

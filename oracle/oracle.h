@@ -36,9 +36,10 @@ uint32_t oracle_colour_popcount(uint64_t addr, const uint64_t *masks, uint32_t n
 void oracle_classify(const uint64_t *addrs, uint64_t n, const uint64_t *masks,
                      uint32_t n_masks, uint8_t *colours, uint64_t *hist);
 
-/* Page-table build (paper section 6, SPT steps 1-3): pool page i has the
- * address origin + i * 2^page_shift; it qualifies when its colour is in the
- * 256-bit set ``colour_set``.  Writes the first min(found, n_needed)
+/* Page-table build (paper section 6, SPT steps 1-3): pool page i covers the
+ * bytes [a, a + 2^page_shift) with a = origin + i * 2^page_shift; it
+ * qualifies when the colour of every one of those bytes is in the 256-bit
+ * set ``colour_set``.  Writes the first min(found, n_needed)
  * qualifying page indices in ascending order and returns ``found``, the
  * number of qualifying pages in the whole pool. */
 uint64_t oracle_pagetable(const uint64_t *masks, uint32_t n_masks, uint64_t origin,

@@ -59,6 +59,15 @@ class Paged(ctypes.Structure):
                 ("pool_pages", ctypes.c_uint64)]
 
 
+class GemvPlan(ctypes.Structure):
+    _fields_ = [("path", ctypes.c_uint32), ("rows", ctypes.c_uint32), ("loads", ctypes.c_uint32),
+                ("batch_cols", ctypes.c_uint32), ("tiles", ctypes.c_uint64),
+                ("sum_depth", ctypes.c_uint32), ("reserved", ctypes.c_uint32)]
+
+
+GEMV_VALU, GEMV_MFMA = 0, 1
+
+
 class RelayoutItem(ctypes.Structure):
     _fields_ = [("dst", Paged), ("src", Paged), ("n_bytes", ctypes.c_uint64),
                 ("page_shift", ctypes.c_uint32), ("reserved", ctypes.c_uint32)]
@@ -112,6 +121,7 @@ def lib() -> ctypes.CDLL:
             "colored_stream": ([vp, P(Paged), P(Paged), P(Paged), ctypes.c_float, u64, u32, vp],
                                i32),
             "colored_gemv": ([vp, P(Paged), i32, u32, u32, vp, i32, u32, vp, u32, vp], i32),
+            "colored_gemv_plan": ([u32, i32, u32, u32, i32, u32, P(GemvPlan)], i32),
             "colour_classify_table": ([vp, P(ColourTable), vp, u64, vp, vp, vp], i32),
             "colour_alloc_pagetable_table": ([vp, P(ColourTable), u64, u32, u64, P(ColourSet), u64,
                                               vp, P(u64), vp], i32),
@@ -365,6 +375,16 @@ def colored_gemv(ctx, w: Paged, w_dtype: int, M: int, K: int, x, x_dtype: int, b
     _check(lib().colored_gemv(_h(ctx), ctypes.byref(w), int(w_dtype), int(M), int(K), _addr(x),
                               int(x_dtype), int(batch), _addr(y), int(page_shift),
                               _stream(stream)))
+
+
+def gemv_plan(allowed_cus: int, w_dtype: int, M: int, K: int, x_dtype: int, batch: int) -> dict:
+    """The launch plan colored_gemv takes for this shape on ``allowed_cus``
+    CUs (host-only; no device needed)."""
+    p = GemvPlan()
+    _check(lib().colored_gemv_plan(int(allowed_cus), int(w_dtype), int(M), int(K), int(x_dtype),
+                                 int(batch), ctypes.byref(p)))
+    return {"path": "mfma" if p.path == GEMV_MFMA else "valu", "rows": p.rows, "loads": p.loads,
+            "batch_cols": p.batch_cols, "tiles": p.tiles, "sum_depth": p.sum_depth}
 
 
 class Bimodal:

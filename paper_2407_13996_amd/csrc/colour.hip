@@ -224,9 +224,11 @@ constexpr uint64_t kPtBlockPages = (uint64_t)kPtThreads * kPtIters;
 // [b*4096, (b+1)*4096) in 16 rounds of 256 consecutive pages.  The counting
 // pass writes the number of qualifying pages per workgroup; the emitting
 // pass writes each qualifying page at its rank among all qualifying pages.
-// Page tests.  QXor: the colour of the page's base address (XOR hash).
-// QTable: every partition that the page touches is in the table and has a
-// colour in the set.
+// Page tests.  QXor: the colour of the page's base address is in the
+// set given to the kernel, which the host has narrowed to the colours whose
+// whole page lies in the caller's set (see page_colour_set).  QTable: every
+// partition that the page touches is in the table and has a colour in the
+// set.
 template <int K>
 struct QXor {
     HashArgs h;
@@ -410,6 +412,44 @@ static int launch_pagetable_xor(Ctx *c, const HashArgs &h, uint64_t origin, uint
                             d_counts, d_offsets, d_total, s);
 }
 
+// The set of base-address colours whose pages lie wholly in ``set``.  A
+// page holds every address base + o, o < 2^page_shift, and the hash is
+// linear over GF(2), so its bytes have exactly the colours c ^ l, with c the
+// colour of its base and l running over L, the colours of the in-page
+// offsets: the span of colour(1 << b) for b < page_shift.  (Paper section 6
+// colours whole sectors, whose bytes share their channels.)  The page
+// qualifies when that coset lies in the set.  With no mask bit below
+// page_shift, L = {0} and the set is unchanged.
+static sgdrc_colour_set page_colour_set(const sgdrc_hash *h, uint32_t page_shift,
+                                        const sgdrc_colour_set &set)
+{
+    const uint32_t n = 1u << h->n_masks;
+    bool in_l[256] = {};
+    in_l[0] = true;
+    for (uint32_t b = 0; b < page_shift && b < 48u; ++b) {
+        uint32_t v = 0;
+        for (uint32_t k = 0; k < h->n_masks; ++k)
+            v |= (uint32_t)((h->masks[k] >> b) & 1ull) << k;
+        if (in_l[v])
+            continue;
+        bool grown[256];
+        for (uint32_t c = 0; c < n; ++c)
+            grown[c] = in_l[c] || in_l[c ^ v];
+        for (uint32_t c = 0; c < n; ++c)
+            in_l[c] = grown[c];
+    }
+    auto member = [&](uint32_t c) { return ((set.bits[c >> 6] >> (c & 63u)) & 1ull) != 0ull; };
+    sgdrc_colour_set out{};
+    for (uint32_t c = 0; c < n; ++c) {
+        bool all = true;
+        for (uint32_t l = 0; l < n && all; ++l)
+            all = !in_l[l] || member(c ^ l);
+        if (all)
+            out.bits[c >> 6] |= 1ull << (c & 63u);
+    }
+    return out;
+}
+
 static std::mutex g_pt_mu;  // page-table scratch is per context; builds are serialised
 
 static int check_pool_args(uint64_t addr_origin, uint32_t page_shift, uint64_t pool_pages,
@@ -564,7 +604,8 @@ int colour_alloc_pagetable(sgdrc_ctx *ctx, const sgdrc_hash *hash, uint64_t addr
     if ((rc = check_ctx(ctx, &c)))
         return rc;
     const HashArgs h = hash_args(hash);
-    return build_pagetable(c, pool_pages, set, n_needed, n_found, stream,
+    const sgdrc_colour_set whole = page_colour_set(hash, page_shift, *set);
+    return build_pagetable(c, pool_pages, &whole, n_needed, n_found, stream,
                            [&](const SetArgs &sa, uint64_t nblocks, uint32_t *d_counts,
                                uint64_t *d_offsets, uint64_t *d_total, hipStream_t s) {
                                int rc = SGDRC_OK;

@@ -434,11 +434,10 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(4)
 typedef void (*GemvKernel)(const uint8_t *, const uint32_t *, uint64_t, uint32_t, uint32_t,
                            const uint8_t *, uint32_t, float *, uint32_t, uint32_t, Gate);
 
-struct ValuCfg {
-    GemvKernel kernel;
-    uint32_t rows;
-};
+static int dtype_size(int dt) { return dt == SGDRC_F32 ? 4 : 2; }
 
+// The launch plan of colored_gemv: which kernel, tile height and loads in
+// flight, decided from the shape and the number of CUs the mask allows.
 // Rows per tile and slices in flight for the vector-ALU path, by batch and
 // row length (measured on MI355X over the 4096x11008 and 11008x4096 bf16
 // layers): the choice keeps every lane busy in as few rounds as possible
@@ -449,30 +448,103 @@ struct ValuCfg {
 // finish sooner (one-tile launches 4.9 against 6.7 us, 4096 x 11008 on 192
 // CUs 23.4 against 24.2 us); with many tiles per CU, four-row tiles with
 // two rounds amortise the per-tile costs better (64 CUs: 45.2 against 47.1).
-template <int WT, int XT>
-static ValuCfg pick_valu(uint32_t batch, bool long_rows, bool few)
+//
+// MFMA tile height by the rows of the busiest CU: 8-row tiles when they cut
+// its rows by a fifth or more (fewer tiles than CUs, or a last round that
+// 16-row tiles fill unevenly), since a row costs more in an 8-row tile (x is
+// read twice as often per W byte); the same bits either way.  Over M =
+// 1536..8192 rows of 4096 and 11008, batch 4 and 8, on 64..256 CUs this is
+// never more than 5 percent slower than the better height (a rule of one to
+// two 16-row tiles per CU was up to 26 percent slower).
+static sgdrc_gemv_plan make_plan(uint32_t allowed, int w_dtype, uint32_t M, uint32_t K,
+                                 int x_dtype, uint32_t batch)
 {
-    if (batch <= 1) {
-        if (long_rows)
-            return few ? ValuCfg{k_gemv_valu<WT, XT, 1, 2, 6>, 2}
-                       : ValuCfg{k_gemv_valu<WT, XT, 1, 4, 4>, 4};
-        return ValuCfg{k_gemv_valu<WT, XT, 1, 8, 2>, 8};
+    sgdrc_gemv_plan p{};
+    const uint64_t a = allowed ? allowed : 1u;
+    const bool mfma = batch >= 3 && w_dtype == x_dtype && w_dtype != SGDRC_F32;
+    const uint64_t row_bytes = (uint64_t)K * dtype_size(w_dtype);
+    const uint64_t kv = row_bytes / 16u;  // 16-byte slices per row
+    if (mfma) {
+        const uint64_t r16 = (((M + 15u) / 16u + a - 1u) / a) * 16u;
+        const uint64_t r8 = (((M + 7u) / 8u + a - 1u) / a) * 8u;
+        p.path = SGDRC_GEMV_MFMA;
+        p.rows = 5u * r8 <= 4u * r16 ? 8u : 16u;
+        p.loads = (uint32_t)kMfmaSets;
+        p.batch_cols = (uint32_t)kMfmaBatchRows;
+        // per output: the MFMAs of one wave in sequence (4 k-steps per
+        // 2 KiB chunk, each adding 32 products), then the 8 waves' partials
+        const uint64_t chunks = (kv + kMfmaChunkSlices - 1u) / kMfmaChunkSlices;
+        p.sum_depth = (uint32_t)(chunks * (uint64_t)kMfmaStepsPerWave + 32u + (kMfmaWaves - 1));
+    } else {
+        // rows of more than 512 slices of 16 bytes take two rounds of loads
+        const bool long_rows = row_bytes > 512u * 16u;
+        // at most six four-row tiles per allowed CU
+        const bool few = (M + 3u) / 4u <= 6u * a;
+        p.path = SGDRC_GEMV_VALU;
+        p.batch_cols = batch <= 1 ? 1u : batch <= 2 ? 2u : batch <= 4 ? 4u : 8u;
+        if (batch <= 1) {
+            if (long_rows) {
+                p.rows = few ? 2u : 4u;
+                p.loads = few ? 6u : 4u;
+            } else {
+                p.rows = 8u;
+                p.loads = 2u;
+            }
+        } else if (batch <= 2) {
+            p.rows = 8u;
+            p.loads = long_rows ? 3u : 2u;
+        } else {
+            p.rows = 4u;
+            p.loads = 2u;
+        }
+        // per output: each lane's FMA chain over its slices, the butterfly
+        // over 64 lanes, then the 4 waves' partials
+        const uint64_t epv = 16u / (uint64_t)dtype_size(w_dtype);
+        p.sum_depth = (uint32_t)(((kv + kGemvThreads - 1u) / kGemvThreads) * epv + 6u +
+                                 (kGemvWaves - 1));
     }
-    if (batch <= 2)
-        return long_rows ? ValuCfg{k_gemv_valu<WT, XT, 2, 8, 3>, 8}
-                         : ValuCfg{k_gemv_valu<WT, XT, 2, 8, 2>, 8};
-    if (batch <= 4)
-        return ValuCfg{k_gemv_valu<WT, XT, 4, 4, 2>, 4};
-    return ValuCfg{k_gemv_valu<WT, XT, 8, 4, 2>, 4};
+    p.tiles = (M + p.rows - 1u) / p.rows;
+    return p;
+}
+
+template <int WT, int XT>
+static GemvKernel valu_kernel(const sgdrc_gemv_plan &p)
+{
+#define SGDRC_VALU(NB, R, U)                                              \
+    if (p.batch_cols == NB && p.rows == R && p.loads == U)                \
+        return k_gemv_valu<WT, XT, NB, R, U>;
+    SGDRC_VALU(1, 2, 6)
+    SGDRC_VALU(1, 4, 4)
+    SGDRC_VALU(1, 8, 2)
+    SGDRC_VALU(2, 8, 3)
+    SGDRC_VALU(2, 8, 2)
+    SGDRC_VALU(4, 4, 2)
+    SGDRC_VALU(8, 4, 2)
+#undef SGDRC_VALU
+    return nullptr;
 }
 
 template <int WT>
-static ValuCfg pick_valu_x(int x_dtype, uint32_t batch, bool long_rows, bool few)
+static GemvKernel valu_kernel_x(int x_dtype, const sgdrc_gemv_plan &p)
 {
     switch (x_dtype) {
-    case SGDRC_F32: return pick_valu<WT, SGDRC_F32>(batch, long_rows, few);
-    case SGDRC_BF16: return pick_valu<WT, SGDRC_BF16>(batch, long_rows, few);
-    default: return pick_valu<WT, SGDRC_F16>(batch, long_rows, few);
+    case SGDRC_F32: return valu_kernel<WT, SGDRC_F32>(p);
+    case SGDRC_BF16: return valu_kernel<WT, SGDRC_BF16>(p);
+    default: return valu_kernel<WT, SGDRC_F16>(p);
+    }
+}
+
+static GemvKernel plan_kernel(const sgdrc_gemv_plan &p, int w_dtype, int x_dtype)
+{
+    if (p.path == SGDRC_GEMV_MFMA) {
+        if (p.rows == 16)
+            return w_dtype == SGDRC_BF16 ? k_gemm_mfma<SGDRC_BF16, 16> : k_gemm_mfma<SGDRC_F16, 16>;
+        return w_dtype == SGDRC_BF16 ? k_gemm_mfma<SGDRC_BF16, 8> : k_gemm_mfma<SGDRC_F16, 8>;
+    }
+    switch (w_dtype) {
+    case SGDRC_F32: return valu_kernel_x<SGDRC_F32>(x_dtype, p);
+    case SGDRC_BF16: return valu_kernel_x<SGDRC_BF16>(x_dtype, p);
+    default: return valu_kernel_x<SGDRC_F16>(x_dtype, p);
     }
 }
 
@@ -489,24 +561,9 @@ static int kernel_occupancy(GemvKernel k, int threads)
     return n;
 }
 
-static int dtype_size(int dt) { return dt == SGDRC_F32 ? 4 : 2; }
-
-}  // namespace sgdrc
-
-using namespace sgdrc;
-
-extern "C" {
-
-int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, uint32_t K,
-                 const void *d_x, int x_dtype, uint32_t batch, float *d_y, uint32_t page_shift,
-                 void *stream)
+// Argument checks shared by colored_gemv and colored_gemv_plan.
+static int check_gemv_shape(int w_dtype, uint32_t M, uint32_t K, int x_dtype, uint32_t batch)
 {
-    clear_error();
-    int rc = check_shift(page_shift);
-    if (rc)
-        return rc;
-    if ((rc = check_paged(w, "w")))
-        return rc;
     if (w_dtype < SGDRC_F32 || w_dtype > SGDRC_F16 || x_dtype < SGDRC_F32 || x_dtype > SGDRC_F16)
         return set_error(SGDRC_EINVAL, "unknown dtype (w %d, x %d)", w_dtype, x_dtype);
     if (batch < 1 || batch > SGDRC_MAX_BATCH)
@@ -519,18 +576,49 @@ int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, 
         return set_error(SGDRC_EINVAL, "K too large");
     if ((uint64_t)batch * K * dtype_size(x_dtype) > 0xFFFFFFF0ull)
         return set_error(SGDRC_EINVAL, "x must be smaller than 4 GiB");
+    return SGDRC_OK;
+}
+
+}  // namespace sgdrc
+
+using namespace sgdrc;
+
+extern "C" {
+
+int colored_gemv_plan(uint32_t allowed_cus, int w_dtype, uint32_t M, uint32_t K, int x_dtype,
+                    uint32_t batch, sgdrc_gemv_plan *out)
+{
+    clear_error();
+    if (!out)
+        return set_error(SGDRC_EINVAL, "out is NULL");
+    if (allowed_cus < 1 || allowed_cus > SGDRC_MAX_CUS)
+        return set_error(SGDRC_EINVAL, "allowed_cus %u outside 1..%d", allowed_cus, SGDRC_MAX_CUS);
+    int rc = check_gemv_shape(w_dtype, M, K, x_dtype, batch);
+    if (rc)
+        return rc;
+    *out = make_plan(allowed_cus, w_dtype, M, K, x_dtype, batch);
+    return SGDRC_OK;
+}
+
+int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, uint32_t K,
+                 const void *d_x, int x_dtype, uint32_t batch, float *d_y, uint32_t page_shift,
+                 void *stream)
+{
+    clear_error();
+    int rc = check_shift(page_shift);
+    if (rc)
+        return rc;
+    if ((rc = check_paged(w, "w")))
+        return rc;
+    if ((rc = check_gemv_shape(w_dtype, M, K, x_dtype, batch)))
+        return rc;
     if (!d_x || !d_y)
         return set_error(SGDRC_EINVAL, "NULL x or y");
     if ((reinterpret_cast<uintptr_t>(d_x) & 15u) || (reinterpret_cast<uintptr_t>(d_y) & 3u))
         return set_error(SGDRC_EINVAL, "x must be 16-byte and y 4-byte aligned");
-    Ctx *c = nullptr;
-    rc = check_ctx(ctx, &c);
-    if (rc)
-        return rc;
-
-    const bool mfma = batch >= 3 && w_dtype == x_dtype && w_dtype != SGDRC_F32;
     {
         // a tile's rows must span at most kPtCap pages (they are staged in LDS)
+        const bool mfma = batch >= 3 && w_dtype == x_dtype && w_dtype != SGDRC_F32;
         const uint64_t rows = mfma ? kMfmaRows : kGemvRowsMax;
         const uint64_t span = rows * (uint64_t)K * dtype_size(w_dtype);
         if ((span >> page_shift) + 2 > (uint64_t)kPtCap)
@@ -538,51 +626,28 @@ int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, 
                              (unsigned long long)((uint64_t)K * dtype_size(w_dtype)),
                              1u << page_shift);
     }
-    GemvKernel k;
-    uint64_t n_tiles;
-    if (mfma) {
-        // Tile height by the rows of the busiest CU: 8-row tiles when they
-        // cut its rows by a fifth or more (fewer tiles than CUs, or a last
-        // round that 16-row tiles fill unevenly), since a row costs more in
-        // an 8-row tile (x is read twice as often per W byte); the same bits
-        // either way.  Over M = 1536..8192 rows of 4096 and 11008, batch 4
-        // and 8, on 64..256 CUs this is never more than 5 percent slower
-        // than the better height (a rule of one to two 16-row tiles per CU
-        // was up to 26 percent slower).
-        const uint64_t allowed = (uint64_t)std::max(1, stream_allowed_cus(c, stream));
-        const uint64_t r16 = (((M + 15u) / 16u + allowed - 1u) / allowed) * 16u;
-        const uint64_t r8 = (((M + 7u) / 8u + allowed - 1u) / allowed) * 8u;
-        const int rows = 5u * r8 <= 4u * r16 ? 8 : 16;
-        if (rows == 16)
-            k = w_dtype == SGDRC_BF16 ? k_gemm_mfma<SGDRC_BF16, 16> : k_gemm_mfma<SGDRC_F16, 16>;
-        else
-            k = w_dtype == SGDRC_BF16 ? k_gemm_mfma<SGDRC_BF16, 8> : k_gemm_mfma<SGDRC_F16, 8>;
-        n_tiles = (M + rows - 1) / rows;
-    } else {
-        // rows of more than 512 slices of 16 bytes take two rounds of loads
-        const bool long_rows = (uint64_t)K * dtype_size(w_dtype) > 512u * 16u;
-        // at most six four-row tiles per allowed CU
-        const bool few = (M + 3u) / 4u <= 6u * (uint64_t)stream_allowed_cus(c, stream);
-        ValuCfg cfg;
-        switch (w_dtype) {
-        case SGDRC_F32: cfg = pick_valu_x<SGDRC_F32>(x_dtype, batch, long_rows, few); break;
-        case SGDRC_BF16: cfg = pick_valu_x<SGDRC_BF16>(x_dtype, batch, long_rows, few); break;
-        default: cfg = pick_valu_x<SGDRC_F16>(x_dtype, batch, long_rows, few); break;
-        }
-        k = cfg.kernel;
-        n_tiles = (M + cfg.rows - 1) / cfg.rows;
-    }
-    Gate g;
-    LaunchInfo li;
-    rc = make_gate(c, stream, n_tiles, kGemvGroupCus, &g, &li);
+    Ctx *c = nullptr;
+    rc = check_ctx(ctx, &c);
     if (rc)
         return rc;
-    const int threads = mfma ? kMfmaThreads : kGemvThreads;
-    const uint32_t grid = gated_grid(c, kernel_occupancy(k, threads), n_tiles, li);
+
+    const sgdrc_gemv_plan plan =
+        make_plan((uint32_t)std::max(1, stream_allowed_cus(c, stream)), w_dtype, M, K, x_dtype,
+                  batch);
+    const GemvKernel k = plan_kernel(plan, w_dtype, x_dtype);
+    if (!k)
+        return set_error(SGDRC_EINVAL, "no kernel for the plan (library fault)");
+    Gate g;
+    LaunchInfo li;
+    rc = make_gate(c, stream, plan.tiles, kGemvGroupCus, &g, &li);
+    if (rc)
+        return rc;
+    const int threads = plan.path == SGDRC_GEMV_MFMA ? kMfmaThreads : kGemvThreads;
+    const uint32_t grid = gated_grid(c, kernel_occupancy(k, threads), plan.tiles, li);
     hipLaunchKernelGGL(k, dim3(grid), dim3(threads), 0, reinterpret_cast<hipStream_t>(stream),
                        static_cast<const uint8_t *>(w->pool), w->pt, w->pool_pages, M, K,
                        static_cast<const uint8_t *>(d_x), batch, d_y, page_shift,
-                       (uint32_t)n_tiles, g);
+                       (uint32_t)plan.tiles, g);
     SGDRC_HIP(hipGetLastError());
     return SGDRC_OK;
 }

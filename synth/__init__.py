@@ -12,11 +12,13 @@ kernels, paper section 7.2 and section 9.1.1):
 
 * page addresses: ``integers(0, 2**36) << 12`` (uniform 4 KiB-aligned
   48-bit addresses), ``default_rng(seed)``;
-* XOR masks: each mask ``integers(0, 2**33) << 8`` (every bit of 8..40 set
-  with probability 1/2), drawn from ``default_rng(mask_seed)``; the whole set
-  of K masks is redrawn from the same stream until the masks restricted to
-  address bits >= ``min_bit`` are linearly independent over GF(2), so that
-  all 2**K colours exist at that page size;
+* XOR masks: each mask ``integers(0, 2**(41 - b)) << b`` with
+  b = max(8, ``min_bit``) (every bit of b..40 set with probability 1/2),
+  drawn from ``default_rng(mask_seed)``; ``min_bit`` is the largest page
+  shift of the configuration, so that no mask bit falls inside a page and
+  every page has one colour (the paper colours whole sectors); the whole set
+  of K masks is redrawn from the same stream until the masks are linearly
+  independent over GF(2), so that all 2**K colours exist;
 * fp32 data: N(0,1), or U[-1,1) built as ``2*u - 1`` from numpy's 24-bit
   float32 uniforms (every value is a multiple of 2**-23);
 * bf16 data: float32 N(0, sigma) rounded to nearest-even to bf16 bits;
@@ -46,21 +48,22 @@ def gf2_rank(vectors) -> int:
 
 def xor_masks(n_masks: int, seed: int = 1, min_bit: int = 12,
               lo_bit: int = MASK_LO_BIT, hi_bit: int = MASK_HI_BIT):
-    """K random masks on address bits lo_bit..hi_bit, full rank above min_bit.
+    """K random masks on address bits max(lo_bit, min_bit)..hi_bit, full rank.
 
-    Returns a list of python ints. Redraws the whole set from one stream until
-    the masks, with bits below ``min_bit`` cleared, have GF(2) rank K.
+    Returns a list of python ints.  Bits below ``min_bit`` (the page shift)
+    stay clear, so a page of 2**min_bit bytes hashes to one colour.  Redraws
+    the whole set from one stream until the masks have GF(2) rank K.
     """
     if not 1 <= n_masks <= 8:
         raise ValueError("1 <= n_masks <= 8")
-    if hi_bit - max(lo_bit, min_bit) + 1 < n_masks:
+    lo = max(lo_bit, min_bit)
+    if hi_bit - lo + 1 < n_masks:
         raise ValueError("not enough mask bits above min_bit for full rank")
     rng = np.random.default_rng(seed)
-    width = hi_bit - lo_bit + 1
+    width = hi_bit - lo + 1
     while True:
-        masks = [int(rng.integers(0, 2 ** width)) << lo_bit for _ in range(n_masks)]
-        hi_part = [m & ~((1 << min_bit) - 1) for m in masks]
-        if gf2_rank(hi_part) == n_masks:
+        masks = [int(rng.integers(0, 2 ** width)) << lo for _ in range(n_masks)]
+        if gf2_rank(masks) == n_masks:
             return masks
 
 

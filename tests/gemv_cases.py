@@ -1,0 +1,61 @@
+"""GEMV shapes that the GPU tests run, and the shapes the benchmark runs.
+
+Shared by ``test_gpu_parity.py`` (which runs the GPU cases against the
+oracle) and ``test_gemv_coverage.py`` (a CPU check, through the library's
+host-only plan query, that every kernel variant a benchmark configuration
+launches is also launched by some GPU test).  A case is
+(M, K, batch, w_dtype, x_dtype, page_shift, allowed CUs or None for all).
+"""
+BF16, F32, F16 = 1, 0, 2
+NUM_CUS = 256          # MI355X
+
+# the memory-bound layers of the LS configuration (bf16, 2 MiB pages)
+C3_LAYERS = [(4096, 11008), (11008, 4096)]
+C3_BATCHES = [1, 2, 4, 8]
+C3_CUS = [64, 128, 192, 256]
+
+# every GPU GEMV case besides the C3 sweep (which covers C3_LAYERS x
+# C3_BATCHES x C3_CUS in full)
+RAGGED = [(1003, 1000, B, BF16, BF16, 12, None) for B in (1, 2, 3, 4, 5, 8)]
+DTYPE_MIX = [(517, 264, B, wd, xd, 12, None) for wd, xd, B in
+             [(F32, BF16, 2), (BF16, F32, 8), (F16, F16, 6), (F16, F32, 1), (F32, F16, 7),
+              (BF16, F16, 4)]]
+STAGING = [(M, 1024, B, BF16, BF16, 12, None) for M, B in
+           [(512, 1), (512, 8), (513, 1), (513, 8), (511, 3)]]
+MFMA_CHUNKS = [(M, K, B, dt, dt, 12, None) for M, K, B, dt in
+               [(300, 11008, 8, BF16), (37, 3000, 3, F16), (64, 1024, 4, BF16), (17, 8, 8, F16)]]
+LONG_ROWS = [(M, K, 1, BF16, BF16, 16, cus) for M, K, cus in
+             [(37, 11008, None), (4097, 11008, None), (2000, 9000, 64), (3, 8200, 1)]]
+SECTORS = [(300, 1024, B, BF16, BF16, shift, None) for shift, B in
+           [(10, 1), (10, 8), (11, 2), (11, 5)]]
+SINGLE_ROWS = [(M, K, B, BF16, BF16, 16, None) for M, K, B in
+               [(1, 11008, 1), (1, 11008, 8), (1, 8, 1), (1, 8, 4), (2, 4096, 3)]]
+CONFIG1 = [(1024, 1024, 1, F32, F32, 16, None)]
+# MFMA 8-row tiles: (M, K, batch, allowed CUs, dtype); each also runs with
+# one CU per 16-row tile
+HALF_TILES = [(203, 3000, 8, 10, BF16), (4096, 11008, 4, 192, BF16), (37, 11008, 3, [1, 2], BF16),
+              (203, 3000, 5, 10, F16)]
+MASKS_777 = [(777, 2048, B, BF16, BF16, 16, cus) for B in (1, 8) for cus in (None, 64, 128, 37)]
+C4_LS = [(4096, 11008, 1, BF16, BF16, 21, 192)]
+
+
+def gpu_cases():
+    """Every (shape, mask size) a GPU test launches the GEMV with."""
+    cases = RAGGED + DTYPE_MIX + STAGING + MFMA_CHUNKS + LONG_ROWS + SECTORS + SINGLE_ROWS
+    cases += CONFIG1 + C4_LS + MASKS_777
+    for M, K, B, cus, dt in HALF_TILES:
+        n = cus if isinstance(cus, int) else len(cus)
+        cases += [(M, K, B, dt, dt, 16, n), (M, K, B, dt, dt, 16, -(-M // 16))]
+    cases += [(M, K, B, BF16, BF16, 21, cus) for M, K in C3_LAYERS for B in C3_BATCHES
+              for cus in C3_CUS]
+    return cases
+
+
+def bench_cases():
+    """Every (shape, mask size) the benchmark times."""
+    cases = [(1024, 1024, 1, F32, F32, 16, None)]                   # C1
+    cases += [(M, K, B, BF16, BF16, 21, cus) for M, K in C3_LAYERS  # C3, whole and spread XCDs
+              for B in C3_BATCHES for cus in C3_CUS]
+    cases += C4_LS                                                   # C4 LS layer
+    cases += [(M, K, 1, BF16, BF16, 21, None) for M, K in C3_LAYERS]  # bimodal LS tensors
+    return cases

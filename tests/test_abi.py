@@ -147,7 +147,8 @@ def test_gemv_argument_errors(L):
     assert call(x=264) == sg.EINVAL         # x not 16-byte aligned
     assert call(shift=40) == sg.EINVAL
     assert call(K=1 << 28, b=8) == sg.EINVAL  # x of 4 GiB
-    assert call(K=1 << 28, b=7) == sg.ENODEV
+    assert call(K=1 << 28, b=7) == sg.EINVAL  # a 16-row tile spans 4096 pages of 2 MiB
+    assert call(K=1 << 20, b=7) == sg.ENODEV  # 16 pages per tile: fine
 
 
 def test_context_calls_reject_null(L):

@@ -14,6 +14,7 @@ import pytest
 
 import synth
 import paper_2407_13996_amd as sg
+import gemv_cases as gc
 
 pytestmark = pytest.mark.gpu
 
@@ -223,6 +224,65 @@ def test_pagetable_singletons_partition_the_pool(ctx):
             assert e.code == sg.ENOMEM
             seen[d_pt[:e.n_found].long()] += 1
     assert bool((seen == 1).all())
+
+
+@pytest.mark.parametrize("shift,lo,hi,K,S,seed", [
+    (10, 8, 20, 3, [0, 1, 2, 3], 4),           # 1 KiB pages, mask bits 8..9 inside them
+    (12, 10, 22, 3, [0, 1, 4, 5, 6, 7], 1),
+    (16, 12, 30, 4, range(12), 6),
+    (21, 16, 34, 6, range(48), 1),             # 2 MiB pages, bits 16..20 inside them
+    (21, 16, 34, 6, range(48), 37),            # ... a seed where no page qualifies
+    (16, 8, 40, 6, range(48), 24),             # masks on bits 8..40: no page is one colour
+])
+def test_pagetable_whole_pages_match_oracle(ctx, orc, shift, lo, hi, K, S, seed):
+    """Masks with bits inside the page give a page's bytes several colours;
+    the page qualifies only if all of them are in the set (paper section 6
+    colours whole sectors).  Table and count equal the oracle's, which
+    enumerates the in-page mask bits; one page more than the pool holds is
+    ENOMEM with the same count."""
+    masks = synth.xor_masks(K, seed=seed, min_bit=lo, hi_bit=hi)
+    origin, pool = 5 << 32, 3000
+    words = synth.colour_set_bits(S)
+    ref, found = orc.pagetable(masks, origin, shift, pool, words, pool)
+    say(f"pagetable whole pages shift={shift} mask bits {lo}..{hi} K={K}: {found} of {pool}")
+    d_pt = torch.full((pool + 8,), -1, dtype=torch.int32, device=DEV)
+    got_found = sg.colour_alloc_pagetable(ctx, masks, origin, shift, pool, S, found, d_pt)
+    assert got_found == found
+    got = to_host(d_pt).view(np.uint32)
+    assert (got[:found] == ref).all() and (got[found:] == 0xFFFFFFFF).all()
+    if found < pool:
+        with pytest.raises(sg.SgdrcError) as e:
+            sg.colour_alloc_pagetable(ctx, masks, origin, shift, pool, S, found + 1, d_pt)
+        assert e.value.code == sg.ENOMEM and e.value.n_found == found
+
+
+def test_pagetable_pages_hold_only_set_colours(ctx, orc):
+    """Every 256-byte sub-address of every page of a GPU-built table,
+    coloured by the GPU, lies in the colour set.  Mask bits 14 and 15 fall
+    inside the 64 KiB pages and span colour bits 0-1, so colours 0..3 are
+    whole pages: those whose address bits 17^25 and 19^30 are even, a
+    quarter of the pool (closed form)."""
+    masks = [(1 << 14) | (1 << 20), (1 << 15) | (1 << 22), (1 << 17) | (1 << 25),
+             (1 << 19) | (1 << 30)]
+    shift, pool, origin = 16, 4096, 1 << 40
+    S = range(4)
+    d_pt = torch.empty(pool, dtype=torch.int32, device=DEV)
+    want = [i for i in range(pool) if ((i >> 1) & 1) == ((i >> 9) & 1) and ((i >> 3) & 1) == 0]
+    say("pagetable colours 0..3 with in-page mask bits, then classify every 256 B")
+    found = sg.colour_alloc_pagetable(ctx, masks, origin, shift, pool, S, len(want), d_pt)
+    assert found == len(want) == pool // 4
+    pt = to_host(d_pt).view(np.uint32)
+    assert pt.tolist() == want
+    sub = (np.uint64(origin) + (pt.astype(np.uint64)[:, None] << np.uint64(shift))
+           + (np.arange(256, dtype=np.uint64) << np.uint64(8))[None, :]).reshape(-1)
+    d_col = torch.empty(sub.size, dtype=torch.uint8, device=DEV)
+    sg.colour_classify(ctx, masks, to_dev(sub), d_col)
+    assert int(to_host(d_col).max()) <= 3
+    # the same masks with the base-address rule would also take pages whose
+    # other sub-addresses leave the set: colours 0..2 hold no whole page
+    with pytest.raises(sg.SgdrcError) as e:
+        sg.colour_alloc_pagetable(ctx, masks, origin, shift, pool, range(3), 1, d_pt)
+    assert e.value.code == sg.ENOMEM and e.value.n_found == 0
 
 
 # ---------------------------------------------------------------- relayout
@@ -491,11 +551,37 @@ def x_bits(dt, n, seed):
     return synth.normal_f32(n, seed=seed).astype(np.float16).view(np.uint16)
 
 
-def run_gemv(ctx, orc, M, K, B, wd, xd, shift, S=range(48), seed=0, masks_seed=1, cus=None,
-             check=True, n_masks=6):
+def cu_list(cus):
+    """None (all CUs), a count n (the first n logical CUs) or a list."""
+    if cus is None or isinstance(cus, (list, range)):
+        return cus
+    return range(cus)
+
+
+ERR_LOG = {}
+
+
+def gemv_check(ctx, y, ref, absdot, M, K, B, wd, xd, cus, tag=""):
+    """The 1e-3 criterion, and the tighter bound of the kernel's own
+    summation tree: |y - ref| <= 2 * depth * 2^-24 * sum|W x| with depth the
+    plan's sum_depth (each of at most depth fp32 roundings errs by at most
+    one unit, or two if a step rounds towards zero)."""
+    gemv_ok(y, ref, absdot)
+    n = ctx.num_cus if cus is None else len(list(cus))
+    depth = sg.gemv_plan(n, wd, M, K, xd, B)["sum_depth"]
+    err = np.abs(y.astype(np.float64) - ref)
+    ratio = err / (absdot + 1e-30)
+    ERR_LOG[(M, K, B, wd, xd, n, tag)] = (float(ratio.max()), depth)
+    say(f"  max |err| / sum|Wx| = {ratio.max():.3g} (bound {2 * depth * 2.0 ** -24:.3g}, "
+        f"depth {depth})")
+    assert np.all(err <= 2 * depth * 2.0 ** -24 * absdot + 1e-30), float(ratio.max())
+
+
+def upload_w(orc, M, K, wd, shift, S, seed, masks_seed, n_masks):
+    """W [M x K] of dtype wd placed on an oracle page table of colours S;
+    returns host pool and table, device pool and table, and the pool size."""
     P = 1 << shift
     wb = w_bits(wd, M * K, seed + 1)
-    xb = x_bits(xd, B * K, seed + 2)
     wbytes = wb.view(np.uint8)
     n_pages = -(-wbytes.size // P)
     pt, pool_pages = make_tables(orc, shift, n_pages, S, masks_seed, K=n_masks)
@@ -503,18 +589,37 @@ def run_gemv(ctx, orc, M, K, B, wd, xd, shift, S=range(48), seed=0, masks_seed=1
     padded = np.zeros(n_pages * P, dtype=np.uint8)
     padded[:wbytes.size] = wbytes
     pool.reshape(pool_pages, P)[pt.astype(np.int64)] = padded.reshape(n_pages, P)
-    d_pool, d_pt, d_x = to_dev(pool), to_dev(pt), to_dev(xb)
+    return pool, pt, to_dev(pool), to_dev(pt), pool_pages
+
+
+def launch_gemv(ctx, d_pool, d_pt, pool_pages, M, K, B, wd, xd, d_x, shift, cus):
     d_y = torch.full((B * M,), float("nan"), dtype=torch.float32, device=DEV)
     if cus is not None:
         sg.set_cu_mask(ctx, None, cus)
-    sg.colored_gemv(ctx, sg.paged(d_pool, d_pt, pool_pages), wd, M, K, d_x, xd, B, d_y, shift)
-    if cus is not None:
-        sg.set_cu_mask(ctx, None, None)
-    y = to_host(d_y).reshape(B, M)
+    try:
+        sg.colored_gemv(ctx, sg.paged(d_pool, d_pt, pool_pages), wd, M, K, d_x, xd, B, d_y, shift)
+    finally:
+        if cus is not None:
+            sg.set_cu_mask(ctx, None, None)
+    return to_host(d_y).reshape(B, M)
+
+
+def run_gemv(ctx, orc, M, K, B, wd, xd, shift, S=range(48), seed=0, masks_seed=1, cus=None,
+             check=True, n_masks=6):
+    cus = cu_list(cus)
+    pool, pt, d_pool, d_pt, pool_pages = upload_w(orc, M, K, wd, shift, S, seed, masks_seed,
+                                                  n_masks)
+    xb = x_bits(xd, B * K, seed + 2)
+    y = launch_gemv(ctx, d_pool, d_pt, pool_pages, M, K, B, wd, xd, to_dev(xb), shift, cus)
     if check:
         ref, absdot = orc.gemv(pool, pt, wd, M, K, xb, xd, B, shift)
-        gemv_ok(y, ref, absdot)
+        gemv_check(ctx, y, ref, absdot, M, K, B, wd, xd, cus)
     return y
+
+
+def _case_id(c):
+    M, K, B, wd, xd, shift, cus = c
+    return f"{M}x{K}-B{B}-w{wd}x{xd}-p{1 << (shift - 10)}K-cus{cus}"
 
 
 def test_gemv_config1_fp32_1024(ctx, orc):
@@ -522,77 +627,31 @@ def test_gemv_config1_fp32_1024(ctx, orc):
     run_gemv(ctx, orc, 1024, 1024, 1, sg.F32, sg.F32, 16, S=range(4), n_masks=4)
 
 
-@pytest.mark.parametrize("B", [1, 2, 3, 4, 5, 8])
-def test_gemv_bf16_ragged(ctx, orc, B):
-    say(f"gemv bf16 1003x1000 B={B}")
-    run_gemv(ctx, orc, 1003, 1000, B, sg.BF16, sg.BF16, 12, seed=B)
+@pytest.mark.parametrize("case", gc.RAGGED + gc.DTYPE_MIX + gc.STAGING + gc.MFMA_CHUNKS
+                         + gc.LONG_ROWS + gc.SECTORS + gc.SINGLE_ROWS, ids=_case_id)
+def test_gemv_matches_oracle(ctx, orc, case):
+    """Ragged shapes (1003 x 1000, batches 1..8), mixed dtypes, W tables of
+    256 pages (staged once per workgroup) and 257 (staged per tile), MFMA
+    chunk counts (odd, ragged last chunk, rows far shorter than a chunk),
+    long rows at batch 1 on few and many CUs, 1-2 KiB sector pages, and
+    single-row matrices (most of the tile outside M)."""
+    M, K, B, wd, xd, shift, cus = case
+    say(f"gemv {_case_id(case)}")
+    run_gemv(ctx, orc, M, K, B, wd, xd, shift, seed=M + K + B + shift, cus=cus)
 
 
-@pytest.mark.parametrize("wd,xd,B", [(sg.F32, sg.BF16, 2), (sg.BF16, sg.F32, 8), (sg.F16, sg.F16, 6),
-                                     (sg.F16, sg.F32, 1), (sg.F32, sg.F16, 7), (sg.BF16, sg.F16, 4)])
-def test_gemv_dtype_mix(ctx, orc, wd, xd, B):
-    say(f"gemv dtypes w={wd} x={xd} B={B}")
-    run_gemv(ctx, orc, 517, 264, B, wd, xd, 12, seed=10 + B)
-
-
-@pytest.mark.parametrize("M,B", [(512, 1), (512, 8), (513, 1), (513, 8), (511, 3)])
-def test_gemv_page_table_staging_boundary(ctx, orc, M, B):
-    """W of 256 pages (its table staged once per workgroup) and of 257 pages
-    (staged per tile), on both the vector and the MFMA path."""
-    say(f"gemv bf16 {M}x1024 B={B}, 4 KiB pages")
-    run_gemv(ctx, orc, M, 1024, B, sg.BF16, sg.BF16, 12, seed=M + B)
-
-
-@pytest.mark.parametrize("M,K,B,dt", [(300, 11008, 8, sg.BF16), (37, 3000, 3, sg.F16),
-                                      (64, 1024, 4, sg.BF16), (17, 8, 8, sg.F16)])
-def test_gemv_mfma_k_chunks(ctx, orc, M, K, B, dt):
-    """The MFMA path takes rows in chunks of 2 KiB, two chunks (one per
-    register set) per loop trip:
-    an odd chunk count (11, 3, 1), a ragged last chunk and a row far shorter
-    than a chunk."""
-    say(f"gemv mfma {M}x{K} B={B} dtype {dt}, 4 KiB pages")
-    run_gemv(ctx, orc, M, K, B, dt, dt, 12, seed=M + K + B)
-
-
-@pytest.mark.parametrize("M,K,B,cus,dt", [(203, 3000, 8, 10, sg.BF16), (4096, 11008, 4, 192, sg.BF16),
-                                         (37, 11008, 3, [1, 2], sg.BF16), (203, 3000, 5, 10, sg.F16)])
+@pytest.mark.parametrize("M,K,B,cus,dt", gc.HALF_TILES)
 def test_gemv_mfma_half_tiles(ctx, orc, M, K, B, cus, dt):
     """The MFMA path takes 8-row tiles (upper half of the A operand zero)
     when they leave the busiest CU fewer rows than 16-row tiles: a ragged
     last tile, the 4096 x 11008 layer on 192 CUs, two CUs.  A mask of one CU
     per 16-row tile (16-row tiles there) gives the same bits."""
-    say(f"gemv mfma {M}x{K} B={B} dtype {dt} on {cus if isinstance(cus, list) else cus} CUs (8-row tiles)")
-    cu_set = cus if isinstance(cus, list) else range(cus)
-    y8 = run_gemv(ctx, orc, M, K, B, dt, dt, 16, seed=M + B, cus=cu_set)
+    say(f"gemv mfma {M}x{K} B={B} dtype {dt} on {cus} CUs (8-row tiles)")
+    y8 = run_gemv(ctx, orc, M, K, B, dt, dt, 16, seed=M + B, cus=cus)
     t16 = -(-M // 16)
     assert t16 <= ctx.num_cus
     y16 = run_gemv(ctx, orc, M, K, B, dt, dt, 16, seed=M + B, cus=range(t16), check=False)
     assert (y8.view(np.uint32) == y16.view(np.uint32)).all()
-
-
-@pytest.mark.parametrize("M,K,cus", [(37, 11008, None), (4097, 11008, None), (2000, 9000, 64),
-                                      (3, 8200, [7])])
-def test_gemv_long_rows_batch1(ctx, orc, M, K, cus):
-    """Batch 1 with rows above 8 KiB: two-row tiles when each allowed CU has
-    few tiles, four-row tiles otherwise (the mask decides too)."""
-    say(f"gemv bf16 {M}x{K} B=1 on {'all' if cus is None else cus if isinstance(cus, list) else cus} CUs")
-    cu_set = None if cus is None else (cus if isinstance(cus, list) else range(cus))
-    run_gemv(ctx, orc, M, K, 1, sg.BF16, sg.BF16, 16, seed=M + K, cus=cu_set)
-
-
-@pytest.mark.parametrize("shift,B", [(10, 1), (10, 8), (11, 2), (11, 5)])
-def test_gemv_sector_pages(ctx, orc, shift, B):
-    """W in 1 KiB and 2 KiB pages (the paper's sector granularities)."""
-    say(f"gemv bf16 300x1024 B={B}, {1 << (shift - 10)} KiB pages")
-    run_gemv(ctx, orc, 300, 1024, B, sg.BF16, sg.BF16, shift, seed=shift + B)
-
-
-@pytest.mark.parametrize("M,K,B", [(1, 11008, 1), (1, 11008, 8), (1, 8, 1), (1, 8, 4), (2, 4096, 3)])
-def test_gemv_single_rows(ctx, orc, M, K, B):
-    """One or two output rows: a single tile with most of its rows outside M
-    (vector path, and MFMA from batch 3)."""
-    say(f"gemv bf16 {M}x{K} B={B}")
-    run_gemv(ctx, orc, M, K, B, sg.BF16, sg.BF16, 16, seed=M * 7 + K + B)
 
 
 def test_zero_length_triad_and_relayout_touch_nothing(ctx):
@@ -609,10 +668,49 @@ def test_zero_length_triad_and_relayout_touch_nothing(ctx):
     assert (to_host(dst) == 5).all()
 
 
-@pytest.mark.parametrize("M,K,B", [(4096, 11008, 1), (11008, 4096, 8)])
-def test_gemv_config3_full_size(ctx, orc, M, K, B):
-    say(f"gemv bf16 {M}x{K} B={B}, 2 MiB pages, colours 0..47 of 64")
-    run_gemv(ctx, orc, M, K, B, sg.BF16, sg.BF16, 21, seed=M + B)
+C3_CACHE = {}
+
+
+@pytest.fixture(scope="module")
+def c3_weights(orc):
+    """The two C3 layers (bf16, N(0, 0.02)) in 2 MiB pages on colours 0..47
+    of 64, uploaded once; freed at the end of the module."""
+    def get(M, K):
+        if (M, K) not in C3_CACHE:
+            C3_CACHE.clear()
+            torch.cuda.empty_cache()
+            C3_CACHE[(M, K)] = upload_w(orc, M, K, sg.BF16, 21, range(48), seed=M, masks_seed=1,
+                                        n_masks=6)
+        return C3_CACHE[(M, K)]
+    yield get
+    C3_CACHE.clear()
+
+
+@pytest.mark.parametrize("M,K", gc.C3_LAYERS)
+@pytest.mark.parametrize("B", gc.C3_BATCHES)
+def test_gemv_config3_sweep(ctx, orc, c3_weights, M, K, B):
+    """The full C3 sweep: both layers at their real size (bf16, 2 MiB pages
+    on colours 0..47) at every batch on the first 64/128/192/256 CUs -- every
+    kernel variant the benchmark times for this configuration (vector path
+    with 2-, 4- and 8-row tiles, MFMA with 8- and 16-row tiles).  Each
+    result is within the oracle bound and bitwise equal across the masks."""
+    pool, pt, d_pool, d_pt, pool_pages = c3_weights(M, K)
+    xb = x_bits(sg.BF16, B * K, M + B + 2)
+    d_x = to_dev(xb)
+    ref, absdot = orc.gemv(pool, pt, sg.BF16, M, K, xb, sg.BF16, B, 21)
+    ys = []
+    for n in gc.C3_CUS:
+        if n > ctx.num_cus:
+            continue
+        plan = sg.gemv_plan(n, sg.BF16, M, K, sg.BF16, B)
+        say(f"gemv C3 {M}x{K} B={B} on {n} CUs: {plan['path']} rows {plan['rows']} "
+            f"loads {plan['loads']}")
+        y = launch_gemv(ctx, d_pool, d_pt, pool_pages, M, K, B, sg.BF16, sg.BF16, d_x, 21,
+                        range(n))
+        gemv_check(ctx, y, ref, absdot, M, K, B, sg.BF16, sg.BF16, range(n), tag="c3")
+        ys.append(y)
+    for y in ys[1:]:
+        assert (y.view(np.uint32) == ys[0].view(np.uint32)).all()
 
 
 def test_gemv_bitwise_identical_across_cu_masks(ctx, orc):
@@ -802,6 +900,87 @@ def test_two_streams_disjoint_masks_run_concurrently(ctx, orc):
     y_ref, absdot = orc.gemv(wb, np.arange(wpages, dtype=np.uint32), orc.BF16, M, K, xb, orc.BF16,
                              1, shift)
     gemv_ok(to_host(d_y).reshape(1, M), y_ref, absdot)
+
+
+def test_corun_config4_disjoint_colours_and_cus(ctx, orc):
+    """The co-located pair at its real size, from one pool under one hash
+    (6 masks on address bits 21..40): the LS GEMV (bf16 4096 x 11008, batch
+    1) on colours 0..47 in 2 MiB pages and CUs 0..191, concurrent with the BE
+    triad on three 2 GiB fp32 arrays on colours 48..63 in 64 KiB pages and
+    CUs 192..255.  The two page sets share no 2 MiB region of the pool; every
+    GEMV output is within the oracle bound and 2^18 sampled triad elements
+    equal the oracle's fmaf."""
+    n_cus = ctx.num_cus
+    ls_cus, be_cus = range(n_cus * 3 // 4), range(n_cus * 3 // 4, n_cus)
+    masks = synth.xor_masks(6, seed=1, min_bit=21)
+    M, K, wshift, shift = 4096, 11008, 21, 16
+    elems = 1 << 29
+    pages = elems * 4 >> shift
+    region = 1 << (wshift - shift)                 # 64 KiB pages per 2 MiB region
+    w_pages = -(-(M * K * 2) >> wshift)
+    pool_regions = int((3 * pages / region) * 4 * 1.1) + 4 * w_pages + 64
+    raw, base, off = aligned_pool(pool_regions, wshift)
+    say(f"corun C4: one pool of {pool_regions} x 2 MiB, masks {[hex(m) for m in masks]}")
+    # LS table (2 MiB pages) and BE table (64 KiB pages) from the same pool
+    d_wpt = torch.empty(w_pages, dtype=torch.int32, device=DEV)
+    sg.colour_alloc_pagetable(ctx, masks, base, wshift, pool_regions, range(48), w_pages, d_wpt)
+    d_bpt = torch.empty(3 * pages, dtype=torch.int32, device=DEV)
+    sg.colour_alloc_pagetable(ctx, masks, base, shift, pool_regions * region, range(48, 64),
+                              3 * pages, d_bpt)
+    wpt = to_host(d_wpt).view(np.uint32)
+    bpt = to_host(d_bpt).view(np.uint32)
+    ref_wpt, _ = orc.pagetable(masks, base, wshift, pool_regions, synth.colour_set_bits(range(48)),
+                               w_pages)
+    assert (wpt == ref_wpt).all()
+    assert not set(wpt.tolist()) & set((bpt // region).tolist())
+    # LS weights and BE inputs placed through the tables
+    wb = w_bits(sg.BF16, M * K, 41)
+    xb = x_bits(sg.BF16, K, 42)
+    d_w = to_dev(wb)
+    w_ident = torch.arange(w_pages, dtype=torch.int32, device=DEV)
+    W = sg.paged(base, d_wpt, pool_regions)
+    sg.bimodal_relayout(ctx, W, sg.paged(d_w, w_ident, w_pages), M * K * 2, wshift)
+    b = synth.uniform_f32(elems, seed=43)
+    c = synth.uniform_f32(elems, seed=44)
+    ident = torch.arange(pages, dtype=torch.int32, device=DEV)
+    T = [sg.paged(base, d_bpt[i * pages:(i + 1) * pages], pool_regions * region) for i in range(3)]
+    for i, h in ((1, b), (2, c)):
+        d_h = to_dev(h)
+        sg.bimodal_relayout(ctx, T[i], sg.paged(d_h, ident, pages), elems * 4, shift)
+        del d_h
+    d_x = to_dev(xb)
+    d_y = torch.full((M,), float("nan"), dtype=torch.float32, device=DEV)
+    torch.cuda.synchronize()
+    s_ls, s_be = torch.cuda.Stream(), torch.cuda.Stream()
+    sg.set_cu_mask(ctx, s_ls, ls_cus)
+    sg.set_cu_mask(ctx, s_be, be_cus)
+    try:
+        say("  BE triad 3 x 2 GiB on 64 CUs with 40 LS GEMVs on 192 CUs")
+        sg.colored_stream(ctx, T[0], T[1], T[2], 3.0, elems, shift, s_be)
+        for _ in range(40):
+            sg.colored_gemv(ctx, W, sg.BF16, M, K, d_x, sg.BF16, 1, d_y, wshift, s_ls)
+        torch.cuda.synchronize()
+    finally:
+        sg.set_cu_mask(ctx, s_ls, None)
+        sg.set_cu_mask(ctx, s_be, None)
+    y_ref, absdot = orc.gemv(wb, np.arange(w_pages, dtype=np.uint32), orc.BF16, M, K, xb,
+                             orc.BF16, 1, wshift)
+    gemv_check(ctx, to_host(d_y).reshape(1, M), y_ref, absdot, M, K, 1, sg.BF16, sg.BF16,
+               ls_cus, tag="c4")
+    rng = np.random.default_rng(45)
+    idx = np.sort(rng.choice(elems, size=1 << 18, replace=False)).astype(np.int64)
+    epp = (1 << shift) // 4
+    pa = bpt[:pages].astype(np.int64)
+    where = off // 4 + pa[idx // epp] * epp + idx % epp
+    got = to_host(raw.view(torch.float32)[torch.from_numpy(where).to(DEV)])
+    ref = np.empty(idx.size, np.float32)
+    ident_h = np.arange(-(-idx.size // epp), dtype=np.uint32)
+    bs = np.zeros(ident_h.size * epp, np.float32); bs[:idx.size] = b[idx]
+    cs = np.zeros(ident_h.size * epp, np.float32); cs[:idx.size] = c[idx]
+    full = np.zeros(ident_h.size * epp, np.float32)
+    orc.triad(full, ident_h, bs, ident_h, cs, ident_h, 3.0, idx.size, shift)
+    ref[:] = full[:idx.size]
+    assert (got.view(np.uint32) == ref.view(np.uint32)).all()
 
 
 def test_zz_no_device_flags_raised():

@@ -461,7 +461,10 @@ def test_lut_from_xor_hash_agrees_with_the_xor_path(orc):
 def test_pagetable_lut_needs_every_partition_of_the_page(orc):
     """Masks below the page bits make partitions of one page differ; a page
     then qualifies only if all of them are in the set, so the table form
-    takes a subset of the pages the base-address rule would take."""
+    takes a subset of the pages the base-address rule takes.  The XOR path
+    applies the same whole-page rule by enumerating in-page mask bits, so
+    the two forms give the same table whenever no mask bit lies below the
+    partition size."""
     s, origin = 10, 0
     entries = 1 << 12
     masks = [m & ~((1 << 10) - 1) for m in synth.xor_masks(4, seed=6, min_bit=10)]
@@ -470,8 +473,62 @@ def test_pagetable_lut_needs_every_partition_of_the_page(orc):
     shift = 12
     pages = (entries << s) >> shift
     got_pt, gf = orc.pagetable_lut(lut, origin, s, origin, shift, pages, S, pages)
-    base_pt, bf = orc.pagetable(masks, origin, shift, pages, S, pages)
-    assert set(got_pt.tolist()) <= set(base_pt.tolist()) and gf < bf
+    base = [i for i in range(pages) if _page_colour_py(masks, origin + (i << shift)) < 10]
+    assert set(got_pt.tolist()) < set(base)
     for p in got_pt:
         cols = [orc.colour((int(p) << shift) + (j << s), masks) for j in range(4)]
         assert all(c < 10 for c in cols)
+    xor_pt, xf = orc.pagetable(masks, origin, shift, pages, S, pages)
+    assert xf == gf and (xor_pt == got_pt).all()
+
+
+# --------------------------------------------- whole pages (paper section 6) ---
+
+def _np_colours(addrs, masks):
+    """Colours of many addresses by numpy bit counting (independent of the C
+    oracle): bit k = parity of the bits of addr & M_k."""
+    a = np.asarray(addrs, dtype=np.uint64)
+    out = np.zeros(a.shape, dtype=np.int64)
+    for k, m in enumerate(masks):
+        v = a & np.uint64(m)
+        par = np.zeros(a.shape, dtype=np.uint64)
+        for b in range(48):
+            par ^= (v >> np.uint64(b)) & np.uint64(1)
+        out |= par.astype(np.int64) << k
+    return out
+
+
+@pytest.mark.parametrize("shift,lo,seed", [(10, 8, 3), (11, 9, 4), (12, 10, 5)])
+def test_pagetable_whole_page_rule_brute_force(orc, shift, lo, seed):
+    """Masks that reach below the page size: a page qualifies exactly when
+    the colour of every one of its bytes is in the set (brute force over all
+    bytes of every page)."""
+    masks = synth.xor_masks(3, seed=seed, min_bit=lo, hi_bit=lo + 12)
+    origin = 7 << 30
+    pool = 96
+    P = 1 << shift
+    addrs = origin + np.arange(pool * P, dtype=np.uint64)
+    cols = _np_colours(addrs, masks).reshape(pool, P)
+    for S in ([0, 1, 2, 3], [0, 2, 4, 6], [1, 3, 5, 7], [0, 1, 4, 5, 6, 7], list(range(8)), [5]):
+        member = np.isin(cols, S).all(axis=1)
+        expect = np.nonzero(member)[0]
+        pt, found = orc.pagetable(masks, origin, shift, pool, synth.colour_set_bits(S), pool)
+        assert found == expect.size and pt.tolist() == expect.tolist(), S
+
+
+def test_pagetable_whole_page_closed_forms(orc):
+    """M0 = bit 9 splits every 1 KiB page into colours {c, c ^ 1}; M1 = bit
+    16 gives colour bit 1 = bit 6 of the page index."""
+    masks = [1 << 9, 1 << 16]
+    pt, found = orc.pagetable(masks, 0, 10, 256, synth.colour_set_bits([2, 3]), 256)
+    assert pt.tolist() == [i for i in range(256) if (i >> 6) & 1]
+    _, found = orc.pagetable(masks, 0, 10, 256, synth.colour_set_bits([0, 2]), 256)
+    assert found == 0
+    _, found = orc.pagetable(masks, 0, 10, 256, synth.colour_set_bits([0, 1, 2]), 256)
+    assert found == 128
+    # one mask inside the page: no proper subset of the colours holds a page
+    for S in ([0], [1]):
+        _, found = orc.pagetable([1 << 12], 0, 16, 64, synth.colour_set_bits(S), 64)
+        assert found == 0
+    pt, found = orc.pagetable([1 << 12], 0, 16, 64, synth.colour_set_bits([0, 1]), 64)
+    assert found == 64 and pt.tolist() == list(range(64))
