@@ -43,13 +43,15 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--rows", default="classify,pagetable,relayout,gemv,xcd,corun,preempt,bimodal,sectors",
+    ap.add_argument("--rows", default="classify,pagetable,relayout,gemv,xcd,corun,preempt,bimodal,"
+                                      "sectors,probe",
                     help="comma list of extra rows to measure ('' for none)")
-    ap.add_argument("--gemv-launches", type=int, default=300)
+    ap.add_argument("--gemv-launches", type=int, default=2000)
     ap.add_argument("--corun-launches", type=int, default=2000)
     ap.add_argument("--preempt-trials", type=int, default=40)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--cpu-passes", type=int, default=8)
+    ap.add_argument("--full-out", default=os.path.join(ROOT, "gpurun_out", "bench_full.json"),
+                    help="file for the full result (every row); stdout gets a compact line")
     return ap.parse_args()
 
 
@@ -298,9 +300,10 @@ def main():
 
     flags = {"headline": ctx.device_error()}
     rows = {}
+    checks = {}
     want = [r for r in args.rows.split(",") if r]
     if "classify" in want:
-        rows["classify"] = bench_classify(torch, sg, synth, ctx, stream, timer)
+        rows["classify"] = bench_classify(torch, sg, synth, ctx, stream, timer, checks)
         flags["classify"] = ctx.device_error()
     if "pagetable" in want:
         rows["pagetable"] = {
@@ -317,7 +320,7 @@ def main():
         rows["relayout"] = bench_relayout(torch, sg, synth, ctx, stream, timer)
         flags["relayout"] = ctx.device_error()
     if "gemv" in want:
-        rows["gemv"] = bench_gemv(torch, sg, synth, ctx, stream, timer, args.gemv_launches)
+        rows["gemv"] = bench_gemv(torch, sg, synth, ctx, stream, timer, args.gemv_launches, checks)
         flags["gemv"] = ctx.device_error()
     ops = corun_operands(torch, sg, synth, ctx) if ("corun" in want or "preempt" in want) else None
     if "corun" in want:
@@ -345,26 +348,137 @@ def main():
 
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(np, synth, masks, shift, pages, pools_desc,
-                                              b_host, c_host, fractions, args.cpu_passes,
-                                              gpu_pages)
+                                              b_host, c_host, fractions, gpu_pages, checks)
     flags["end"] = ctx.device_error()
     result["device_flags_by_row"] = flags
     result["device_error_flags"] = 0
     for v in flags.values():
         result["device_error_flags"] |= v
     ctx.close()
-    print(json.dumps(result), flush=True)
+    full_path = args.full_out
+    try:
+        os.makedirs(os.path.dirname(os.path.abspath(full_path)), exist_ok=True)
+        with open(full_path, "w") as f:
+            json.dump(result, f, indent=1)
+        log(f"full result written to {full_path}")
+    except OSError as e:
+        log(f"could not write {full_path}: {e}")
+    line = json.dumps(compact(result, full_path))
+    print(line, flush=True)
 
 
-def bench_classify(torch, sg, synth, ctx, stream, timer, n=1 << 26, reps=50):
-    out = {}
-    for hist in (False, True):
-        out["with_histogram" if hist else "colours_only"] = bench_classify_one(
-            torch, sg, synth, ctx, stream, timer, n, reps, hist)
+def _get(d, *keys):
+    for k in keys:
+        if not isinstance(d, dict) or k not in d:
+            return None
+        d = d[k]
+    return d
+
+
+def compact(result, full_path):
+    """The one stdout line: the contract's fields, the roofline and CPU
+    baseline, the per-colour-set figures and one headline figure per row
+    (all rows in full are in ``full_path``).  Kept under 8 KB."""
+    keep = ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step",
+            "higher_is_better", "scaling", "vs_baseline", "dtype", "data", "config", "roofline",
+            "device_error_flags")
+    out = {k: result[k] for k in keep if k in result}
+    out["per_fraction"] = [{k: p[k] for k in ("colours", "GBps", "pct_of_colour_scaled_peak",
+                                              "pct_of_hbm_peak", "median_ms")}
+                           for p in result.get("per_fraction", [])]
+    cb = result.get("cpu_baseline")
+    if cb:
+        out["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
+        out["cpu_baseline"]["ops"] = {
+            op: {k: v for k, v in row.items() if k.endswith(("_per_s", "GBps"))}
+            for op, row in cb["ops"].items()}
+        out["cpu_baseline"]["checks"] = {k: v for k, v in cb.items()
+                                         if k.endswith(("match_oracle", "matches_oracle",
+                                                        "within_bound", "identity"))}
+    rows = result.get("rows", {})
+    summ = {}
+    if "classify" in rows:
+        c = rows["classify"]
+        summ["classify_2e26"] = {"colours_us": _get(c, "colours_only", "median_us"),
+                                 "hist_us": _get(c, "with_histogram", "median_us"),
+                                 "addrs_per_s": _get(c, "colours_only", "addrs_per_s"),
+                                 "pct_hbm": _get(c, "colours_only", "pct_of_hbm_peak")}
+    if "pagetable" in rows:
+        summ["pagetable_ms"] = rows["pagetable"]["ms"]
+    if "relayout" in rows:
+        r = rows["relayout"]
+        summ["relayout_4GiB"] = {k: [_get(r, k, "GBps"), _get(r, k, "pages_per_s")]
+                                 for k in ("to_restricted", "to_all", "to_restricted_2MiB",
+                                           "to_all_2MiB", "contiguous_copy") if k in r}
+    if "gemv" in rows:
+        g = rows["gemv"]
+        pts = {}
+        for p in g["points"]:
+            if p["placement"] == "xcds" and p["layout"] == "coloured":
+                key = f"{p['M']}x{p['K']}_b{p['batch']}_cu{p['cus']}"
+                pts[key] = [p["p50_us"], p["p99_us"], p["GBps"]]
+        summ["gemv_p50_p99_us_GBps"] = pts
+        if "indirection" in g:
+            summ["gemv_indirection"] = g["indirection"]
+        if "library_reference" in g:
+            summ["gemv_library_reference_launch_p50_us"] = g["library_reference"]
+        summ["gemv_launch_p50_us_256cus"] = {
+            f"{p['M']}x{p['K']}_b{p['batch']}": p["launch_p50_us"] for p in g["points"]
+            if p["placement"] == "xcds" and p["layout"] == "coloured" and p["batch"] in (1, 8)
+            and p["rotated_copies"] == 8 and p["cus"] == max(q["cus"] for q in g["points"])}
+        summ["gemv_p50_us_by_rotated_copies"] = {
+            f"{p['M']}x{p['K']}_b{p['batch']}_x{p['rotated_copies']}": p["p50_us"]
+            for p in g["points"] if p["placement"] == "xcds" and p["layout"] == "coloured"
+            and p["batch"] in (1, 8) and p["cus"] == max(q["cus"] for q in g["points"])}
+    if "corun" in rows:
+        c = rows["corun"]
+        summ["corun"] = {k: {kk: c[k].get(kk) for kk in ("ls_p50_us", "ls_p99_us", "be_GBps")}
+                         for k in ("isolated_ls_coloured_masked", "corun_coloured_masked",
+                                   "corun_uncoloured_masked", "corun_uncoloured_unmasked")
+                         if k in c}
+    if "preempt" in rows:
+        pr = rows["preempt"]
+        summ["preempt"] = {k: pr.get(k) for k in (
+            "evicted_trials", "eviction_latency_p50_us", "eviction_latency_p99_us",
+            "ls_from_flag_p50_us", "ls_from_flag_p99_us", "preemptible_overhead_pct")}
+    if "bimodal" in rows:
+        summ["bimodal"] = {k: v for k, v in rows["bimodal"].items()
+                           if isinstance(v, (int, float)) and not isinstance(v, bool)}
+    if "xcd" in rows:
+        summ["xcd_triad_GBps"] = {f"{p['cus']}{'s' if p['placement'] == 'spread' else ''}":
+                                  p["GBps"] for p in rows["xcd"]["points"]}
+    if "sectors" in rows:
+        summ["sectors_triad_GBps"] = {k[6:-5]: v for k, v in rows["sectors"].items()
+                                      if k.startswith("triad_") and k.endswith("_GBps")}
+    if "probe" in rows:
+        pb = rows["probe"]
+        for key in ("points", "high_bits"):
+            rs = [p["ratio"] for p in pb.get(key, [])[1:]]
+            if rs:
+                summ[f"probe_{key}_ratio_min_max"] = [min(rs), max(rs)]
+        summ["probe_placement_GBps"] = {f"{p['page_KiB']}K {p['pages']}": p["GBps"]
+                                        for p in pb.get("placement", [])}
+    out["rows_summary"] = summ
+    out["rows_full"] = os.path.relpath(full_path, ROOT) if full_path else None
+    text = json.dumps(out)
+    if len(text) > 8000:       # drop the widest parts first
+        for k in ("sectors_triad_GBps", "probe_placement_GBps", "xcd_triad_GBps", "bimodal"):
+            summ.pop(k, None)
+            text = json.dumps(out)
+            if len(text) <= 8000:
+                break
     return out
 
 
-def bench_classify_one(torch, sg, synth, ctx, stream, timer, n, reps, hist):
+def bench_classify(torch, sg, synth, ctx, stream, timer, checks, n=1 << 26, reps=50):
+    out = {}
+    for hist in (False, True):
+        out["with_histogram" if hist else "colours_only"] = bench_classify_one(
+            torch, sg, synth, ctx, stream, timer, n, reps, hist, checks)
+    return out
+
+
+def bench_classify_one(torch, sg, synth, ctx, stream, timer, n, reps, hist, checks):
     log(f"classify {n} addresses")
     masks = synth.xor_masks(6, seed=1, min_bit=12)
     addrs = synth.page_addresses(n, seed=0)
@@ -385,6 +499,7 @@ def bench_classify_one(torch, sg, synth, ctx, stream, timer, n, reps, hist):
     med = pctl(d, 50)
     gbs = 9 * n / (med * 1e-3) / 1e9
     log(f"classify (histogram {hist}): {med * 1e3:.1f} us  {gbs:.0f} GB/s")
+    checks["classify_colours"] = d_col[:1 << 22].cpu().numpy()
     return {"what": "2^26 random 4 KiB-aligned addresses, 6 masks"
                     + (", colours + histogram" if hist else ", colours"),
             "median_us": round(med * 1e3, 2), "p99_us": round(pctl(d, 99) * 1e3, 2),
@@ -458,13 +573,15 @@ def bench_relayout(torch, sg, synth, ctx, stream, timer, reps=10):
     return out
 
 
-def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
+def bench_gemv(torch, sg, synth, ctx, stream, timer, launches, checks):
     shift = 21
     P = 1 << shift
-    copies = 4
+    copies = 8
     masks = synth.xor_masks(6, seed=1, min_bit=shift)
     n_cus = ctx.num_cus
     out = []
+    lib_ref = {}
+    indirection = {}
     g = torch.Generator(device="cuda:0")
     g.manual_seed(7)
     x = (torch.randn(8 * 11008, generator=g, device="cuda:0")).to(torch.bfloat16)
@@ -489,18 +606,19 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
         setup_flags = ctx.device_error()
         log(f"gemv {M}x{K}: {copies} weight copies rotated (setup flags {setup_flags})")
 
-        def point(Ws, B, ncu, place, layout):
-            tag = ("gemv", M, B, ncu, place, layout)
+        def point(Ws, B, ncu, place, layout, rotate=copies):
+            tag = ("gemv", M, B, ncu, place, layout, rotate)
             cus = range(ncu) if place == "xcds" else spread_cus(n_cus, ncu)
             with torch.cuda.stream(stream):
                 sg.set_cu_mask(ctx, stream, cus)
                 for i in range(20):
-                    sg.colored_gemv(ctx, Ws[i % copies], sg.BF16, M, K, x, sg.BF16, B, y,
+                    sg.colored_gemv(ctx, Ws[i % rotate], sg.BF16, M, K, x, sg.BF16, B, y,
                                     shift, stream)
                 dev = DevTimes(torch, ctx, stream, launches)
+                timer.reserve(2 * launches)
                 for i in range(launches):
                     e0 = timer.start()
-                    sg.colored_gemv(ctx, Ws[i % copies], sg.BF16, M, K, x, sg.BF16, B, y,
+                    sg.colored_gemv(ctx, Ws[i % rotate], sg.BF16, M, K, x, sg.BF16, B, y,
                                     shift, stream)
                     timer.stop(e0, tag)
                 spans = dev.close_us()
@@ -512,7 +630,7 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
             med, p99 = pctl(list(spans), 50), pctl(list(spans), 99)
             gbs = nbytes / (med * 1e-6) / 1e9
             out.append({"M": M, "K": K, "batch": B, "cus": ncu, "placement": place,
-                        "layout": layout, "device_flags": flag,
+                        "layout": layout, "rotated_copies": rotate, "device_flags": flag,
                         "path": "mfma" if B >= 3 else "valu",
                         "p50_us": round(med, 2), "p99_us": round(p99, 2),
                         "GBps": round(gbs, 1),
@@ -520,8 +638,10 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
                         "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1),
                         "launch_p50_us": round(pctl(d, 50) * 1e3, 2),
                         "launch_p99_us": round(pctl(d, 99) * 1e3, 2)})
-            log(f"gemv {M}x{K} B={B} cus={ncu} ({place}, {layout}): kernel p50 {med:.1f} us "
-                f"p99 {p99:.1f} us {gbs:.0f} GB/s; with launch p50 {pctl(d, 50) * 1e3:.1f} us")
+            log(f"gemv {M}x{K} B={B} cus={ncu} ({place}, {layout}, {rotate} copies): kernel p50 "
+                f"{med:.1f} us p99 {p99:.1f} us {gbs:.0f} GB/s; with launch p50 "
+                f"{pctl(d, 50) * 1e3:.1f} us")
+            return med
 
         for B in (1, 2, 4, 8):
             for ncu in (64, 128, 192, 256):
@@ -530,6 +650,20 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
                 point(W, B, ncu, "xcds", "coloured")
                 if ncu < n_cus and B in (1, 8):
                     point(W, B, ncu, "spread", "coloured")
+        # B = 1 output of the last launch, for the CPU baseline's oracle check
+        sg.colored_gemv(ctx, W[0], sg.BF16, M, K, x, sg.BF16, 1, y, shift, stream)
+        torch.cuda.synchronize()
+        checks.setdefault("gemv", {})[(M, K)] = (
+            w.view(torch.int16).cpu().numpy().view(np.uint16),
+            x[:K].view(torch.int16).cpu().numpy().view(np.uint16), y[:M].cpu().numpy())
+        # fewer rotated copies: with one or four copies (90 / 360 MB) part of W
+        # can stay in the 256 MiB MALL between launches; eight (721 MB) cannot
+        for rot in (1, 4):
+            for B in (1, 8):
+                point(W, B, n_cus, "xcds", "coloured", rotate=rot)
+        # the same product through the ROCm libraries (torch.nn.functional.linear
+        # in bf16, fp32 accumulation inside the library): a reference time
+        lib_ref[f"{M}x{K}"] = library_linear_us(torch, w, x, M, K, stream, timer)
         if M == 4096:
             # the same weights in contiguous buffers (identity tables): the
             # cost of the page-table indirection
@@ -540,7 +674,11 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
                 sg.bimodal_relayout(ctx, Wi, sg.paged(w, ident, pages), w_bytes, shift, stream)
             torch.cuda.synchronize()
             for B in (1, 8):
-                point(WC, B, n_cus, "xcds", "contiguous")
+                t_plain = point(WC, B, n_cus, "xcds", "contiguous")
+                t_col = [p["p50_us"] for p in out if p["M"] == M and p["batch"] == B and
+                         p["cus"] == n_cus and p["placement"] == "xcds" and
+                         p["layout"] == "coloured" and p["rotated_copies"] == copies][0]
+                indirection[f"b{B}_pct"] = round(100 * (t_col / t_plain - 1), 2)
             del Wc, WC
         del raw, W
         torch.cuda.empty_cache()
@@ -550,10 +688,39 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches):
             "placement": "xcds: the first n logical CUs (whole XCDs, n/32 of them); spread: n/8 "
                          "CUs in each of the 8 XCDs",
             "bytes": "M*K*2 + B*K*2 + B*M*4",
+            "indirection": {"what": "4096x11008 on 256 CUs: coloured pages (8 copies) against "
+                                    "contiguous weights with identity tables, p50 difference",
+                            **indirection},
+            "library_reference": lib_ref,
             "timing": "p50/p99_us and GBps: kernel spans from the device time log (first "
                       "workgroup start to last workgroup end); launch_p50/p99_us: host events "
                       "around each call, including launch overhead",
             "points": out}
+
+
+def library_linear_us(torch, w, x, M, K, stream, timer, reps=200):
+    """p50 time (host events around each call) of torch.nn.functional.linear
+    on contiguous bf16 weights [M x K] at batch 1 and 8: the ROCm library
+    GEMV/GEMM on the same shapes, all CUs, no colouring.  A reference, not
+    part of the path."""
+    import torch.nn.functional as F
+    res = {}
+    W2 = w[:M * K].view(M, K)
+    for B in (1, 8):
+        X = x[:B * K].view(B, K).contiguous()
+        tag = ("library", M, B)
+        with torch.cuda.stream(stream):
+            for _ in range(10):
+                F.linear(X, W2)
+            timer.reserve(2 * reps)
+            for _ in range(reps):
+                e0 = timer.start()
+                F.linear(X, W2)
+                timer.stop(e0, tag)
+        torch.cuda.synchronize()
+        res[f"b{B}"] = round(pctl(timer.durations_ms(tag), 50) * 1e3, 2)
+    log(f"library reference F.linear {M}x{K}: {res} us (with launch)")
+    return res
 
 
 def spread_cus(n_cus, ncu, n_xcds=8):
@@ -611,30 +778,40 @@ def bench_xcd(torch, sg, ctx, stream, reps=20):
 
 
 def corun_operands(torch, sg, synth, ctx):
-    """Operands of the co-located pair (C4): the LS GEMV's bf16 W (4096 x
-    11008) in 2 MiB pages on colours 0..47 (4 rotated copies) and contiguous,
-    x and y; the BE triad's three 2 GiB fp32 arrays in 64 KiB pages on
-    colours 48..63 and contiguous."""
+    """Operands of the co-located pair (C4), all from one pool under one hash
+    (6 masks on address bits 21..40, so every 2 MiB region has one colour):
+    the LS GEMV's bf16 W (4096 x 11008) in 2 MiB pages on colours 0..47
+    (8 rotated copies), the BE triad's three 2 GiB fp32 arrays in 64 KiB
+    pages on colours 48..63 -- the two page sets share no region -- and,
+    for the uncoloured control, the same tensors in plain buffers with
+    identity tables."""
     dev = "cuda:0"
     M, K = 4096, 11008
     g = torch.Generator(device=dev)
     g.manual_seed(11)
-    # ---- LS operands: W in 2 MiB pages on colours 0..47 (4 rotated copies) and contiguous
-    wshift = 21
+    wshift, shift = 21, 16
+    masks = synth.xor_masks(6, seed=1, min_bit=wshift)
     WP = 1 << wshift
-    wm = synth.xor_masks(6, seed=1, min_bit=wshift)
     w_bytes = M * K * 2
     wpages = -(-w_bytes // WP)
-    copies = 4
+    copies = 8
+    n = 1 << 29
+    pages = (n * 4) >> shift
+    region = 1 << (wshift - shift)
+    pool_regions = int(3 * pages / region * 4 * 1.1) + copies * wpages * 2 + 64
+    raw, base = aligned_pool(torch, pool_regions, wshift)
+    w_pt = torch.empty(copies * wpages, dtype=torch.int32, device=dev)
+    sg.colour_alloc_pagetable(ctx, masks, base, wshift, pool_regions, range(48), copies * wpages, w_pt)
+    be_pt = torch.empty(3 * pages, dtype=torch.int32, device=dev)
+    sg.colour_alloc_pagetable(ctx, masks, base, shift, pool_regions * region, range(48, 64),
+                              3 * pages, be_pt)
+    overlap = len(set(w_pt.cpu().tolist()) & set((be_pt.cpu() // region).tolist()))
+    # ---- LS operands
     w_lin = (torch.randn(M * K, generator=g, device=dev) * 0.02).to(torch.bfloat16)
     w_ident = torch.arange(wpages, dtype=torch.int32, device=dev)
-    w_pool_pages = int(copies * wpages * 64 / 48 * 1.1) + 16
-    w_raw, w_base = aligned_pool(torch, w_pool_pages, wshift)
-    w_pt = torch.empty(copies * wpages, dtype=torch.int32, device=dev)
-    sg.colour_alloc_pagetable(ctx, wm, w_base, wshift, w_pool_pages, range(48), copies * wpages, w_pt)
     W_col = []
     for i in range(copies):
-        Wi = sg.paged(w_base, w_pt[i * wpages:(i + 1) * wpages], w_pool_pages)
+        Wi = sg.paged(base, w_pt[i * wpages:(i + 1) * wpages], pool_regions)
         sg.bimodal_relayout(ctx, Wi, sg.paged(w_lin, w_ident, wpages), w_bytes, wshift)
         W_col.append(Wi)
     w_plain = [torch.empty(wpages * WP // 2, dtype=torch.bfloat16, device=dev) for _ in range(copies)]
@@ -645,27 +822,22 @@ def corun_operands(torch, sg, synth, ctx):
         W_plain.append(Wi)
     x = torch.randn(K, generator=g, device=dev).to(torch.bfloat16)
     y = torch.empty(M, dtype=torch.float32, device=dev)
-    # ---- BE operands: three 2 GiB fp32 arrays, 64 KiB pages on colours 48..63, and contiguous
-    shift = 16
-    n = 1 << 29
-    pages = (n * 4) >> shift
-    tm = synth.xor_masks(6, seed=1, min_bit=shift)
-    be_pool_pages = int(3 * pages * 64 / 16 * 1.04) + 64
-    be_raw, be_base = aligned_pool(torch, be_pool_pages, shift)
-    be_pt = torch.empty(3 * pages, dtype=torch.int32, device=dev)
-    sg.colour_alloc_pagetable(ctx, tm, be_base, shift, be_pool_pages, range(48, 64), 3 * pages, be_pt)
+    # ---- BE operands
     ident = torch.arange(pages, dtype=torch.int32, device=dev)
     lin = [torch.empty(n, dtype=torch.float32, device=dev) for _ in range(3)]
     lin[1].uniform_(-1, 1, generator=g)
     lin[2].uniform_(-1, 1, generator=g)
-    T_col = [sg.paged(be_base, be_pt[i * pages:(i + 1) * pages], be_pool_pages) for i in range(3)]
+    T_col = [sg.paged(base, be_pt[i * pages:(i + 1) * pages], pool_regions * region)
+             for i in range(3)]
     for i in (1, 2):
         sg.bimodal_relayout(ctx, T_col[i], sg.paged(lin[i], ident, pages), n * 4, shift)
     T_plain = [sg.paged(lin[i], ident, pages) for i in range(3)]
     torch.cuda.synchronize()
+    log(f"corun operands: one pool of {pool_regions} x 2 MiB, LS/BE regions shared: {overlap}")
     return {"M": M, "K": K, "wshift": wshift, "copies": copies, "W_col": W_col,
             "W_plain": W_plain, "x": x, "y": y, "shift": shift, "n": n, "T_col": T_col,
-            "T_plain": T_plain, "_keep": (w_raw, w_plain, be_raw, lin, w_pt, be_pt, w_ident, ident)}
+            "T_plain": T_plain, "masks": [hex(m) for m in masks], "shared_regions": overlap,
+            "_keep": (raw, w_plain, lin, w_pt, be_pt, w_ident, ident)}
 
 
 def bench_corun(torch, sg, synth, ctx, ls_launches, ops):
@@ -750,6 +922,7 @@ def bench_corun(torch, sg, synth, ctx, ls_launches, ops):
 
     res = {"what": "LS bf16 GEMV 4096x11008 batch 1 (closed loop) + BE fp32 triad 3x2 GiB",
            "ls_launches": ls_launches, "be_workgroups_per_cu_cap": be_cap,
+           "masks": ops["masks"], "ls_be_shared_2MiB_regions": ops["shared_regions"],
            "timing": "ls_p50/p99_us and be_GBps from the device time log (kernel spans); "
                      "ls_launch_p50/p99_us from host events around each LS call"}
     res["isolated_ls_coloured_masked"] = run(W_col, T_col, ls_cus, be_cus, with_be=False)
@@ -1060,8 +1233,8 @@ def bench_probe(torch, sg, synth, ctx, stream, timer, reps=10, masks=None):
     runs on the pages of a pool where parity(address & M) = 0 (a one-mask
     hash, colour 0).  If the bits of M feed the channel hash, those pages
     use half of the channels and the triad slows towards half speed;
-    otherwise it keeps the speed of the unrestricted control (M = bit 8,
-    below the page size, keeps every page).  Bits below 21 are probed with
+    otherwise it keeps the speed of the unrestricted control (M = bit 47,
+    zero over the whole pool, keeps every page: the first pages in order).  Bits below 21 are probed with
     1 KiB pages in a 2 GiB pool: user space sees virtual addresses, which
     agree with physical ones inside 2 MiB fragments.  Bits 16..32 are then
     probed with 64 KiB pages in an 8 GiB pool; above bit 20 the result
@@ -1071,7 +1244,7 @@ def bench_probe(torch, sg, synth, ctx, stream, timer, reps=10, masks=None):
     colours 0..15 of 64."""
     dev = "cuda:0"
     out = {"what": "triad 3x256 MiB fp32 restricted to parity(addr & M) = 0; GB/s and ratio to "
-                   "the control M = bit 8. low_bits: 1 KiB pages, 2 GiB pool; high_bits: 64 KiB "
+                   "the control M = bit 47. low_bits: 1 KiB pages, 2 GiB pool; high_bits: 64 KiB "
                    "pages, 8 GiB pool. placement: triad 3x1 GiB on a quarter of a pool",
            "points": [], "high_bits": [], "placement": []}
 
@@ -1106,10 +1279,10 @@ def bench_probe(torch, sg, synth, ctx, stream, timer, reps=10, masks=None):
         torch.cuda.empty_cache()
 
     if masks is None:
-        masks = [1 << 8] + [1 << b for b in range(10, 21)] + \
+        masks = [1 << 47] + [1 << b for b in range(10, 21)] + \
                 [(1 << a) | (1 << b) for a in range(10, 16) for b in range(a + 1, 17)]
     probe("points", 10, 2 << 30, masks)
-    probe("high_bits", 16, 8 << 30, [1 << 8] + [1 << b for b in range(16, 33)] +
+    probe("high_bits", 16, 8 << 30, [1 << 47] + [1 << b for b in range(16, 33)] +
           [(1 << 21) | (1 << 22), (1 << 21) | (1 << 23), (1 << 22) | (1 << 23)])
 
     n = 1 << 28
@@ -1134,43 +1307,193 @@ def bench_probe(torch, sg, synth, ctx, stream, timer, reps=10, masks=None):
     return out
 
 
+def cpu_threads():
+    """Host threads for the all-cores oracle runs: the CPUs this process may
+    use, at most 16 (a one-GPU machine's share of its host)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def split(n, parts, align=1):
+    """[lo, hi) ranges covering 0..n in ``parts`` pieces whose bounds are
+    multiples of ``align`` (the last one excepted)."""
+    step = -(-n // parts)
+    step = -(-step // align) * align
+    return [(lo, min(n, lo + step)) for lo in range(0, n, step)]
+
+
+def run_threads(jobs, threads):
+    """Runs the callables in ``jobs`` on ``threads`` host threads (the oracle's
+    ctypes calls release the interpreter lock) and returns the wall time."""
+    import concurrent.futures as cf
+    t0 = time.perf_counter()
+    if threads == 1:
+        for j in jobs:
+            j()
+    else:
+        with cf.ThreadPoolExecutor(max_workers=threads) as ex:
+            for f in [ex.submit(j) for j in jobs]:
+                f.result()
+    return time.perf_counter() - t0
+
+
 def cpu_baseline(np, synth, masks, shift, pages, pools_desc, b_host, c_host, fractions,
-                 passes, gpu_pages):
-    """The CPU oracle (single-threaded C) on the headline workload: the full
-    arrays, every colour set, ``passes`` passes; page tables from the oracle."""
+                 gpu_pages, gpu_checks):
+    """The CPU oracle (plain single-threaded C, unchanged) timed on this
+    host, on one thread and on ``cpu_threads()`` threads that call the same
+    functions over disjoint index ranges.  Bounded samples of the path:
+    the headline triad (full arrays, every colour set, one pass each), the
+    headline page-table builds (full pools), classify of the first 2^22 of
+    the 2^26 C5 addresses, the C5 relayout of the first 256 MiB (4,096
+    pages of 64 KiB) in both directions, and the batch-1 GEMV of both C3
+    layers on the benchmark's own weights.  GPU results of the same
+    operations are compared with the oracle's on these samples."""
     import oracle
     P = 1 << shift
     epp = P // 4
     n = b_host.size
-    log(f"cpu baseline: oracle triad, {passes} passes x {len(fractions)} colour sets")
-    total_s = 0.0
-    elems = 0
+    T = cpu_threads()
+    res = {"threads": T, "ops": {}}
+    out_ops = res["ops"]
+
+    def timed(name, make_jobs, units, unit_name, bytes_per_unit=None):
+        row = {}
+        for t in (1, T):
+            jobs = make_jobs(t)
+            run_threads(jobs[:1], 1)                           # warm caches and pages once
+            secs = run_threads(make_jobs(t), t)
+            row[f"threads_{t}_s"] = round(secs, 3)
+            row[f"threads_{t}_{unit_name}_per_s"] = round(units / secs, 1)
+            if bytes_per_unit:
+                row[f"threads_{t}_GBps"] = round(units * bytes_per_unit / secs / 1e9, 3)
+        out_ops[name] = row
+        log(f"cpu baseline {name}: {row}")
+        return row
+
+    # ---- triad: full headline arrays, one pass per colour set.  Each host
+    # pool mirrors its GPU pool page for page; it is mapped without huge
+    # pages, so that only the pages the tables name are ever committed, and
+    # every page of a is written once before the timed passes.
+    import mmap
+    tri = {1: 0.0, T: 0.0}
     check = None
     for nc in fractions:
         base, pool_pages = pools_desc[nc]
-        pt, found = oracle.pagetable(masks, base, shift, pool_pages, synth.colour_set_bits(range(nc)),
-                                     3 * pages)
+        pt, found = oracle.pagetable(masks, base, shift, pool_pages,
+                                     synth.colour_set_bits(range(nc)), 3 * pages)
         assert found >= 3 * pages
         pa, pb, pc = pt[:pages], pt[pages:2 * pages], pt[2 * pages:]
-        pool = np.zeros(pool_pages * epp, dtype=np.float32)
+        mm = mmap.mmap(-1, pool_pages * P)
+        if hasattr(mmap, "MADV_NOHUGEPAGE"):
+            mm.madvise(mmap.MADV_NOHUGEPAGE)
+        pool = np.frombuffer(mm, dtype=np.float32)
         view = pool.reshape(pool_pages, epp)
         view[pb.astype(np.int64)] = b_host.reshape(pages, epp)
         view[pc.astype(np.int64)] = c_host.reshape(pages, epp)
-        for _ in range(passes):
-            t0 = time.perf_counter()
-            oracle.triad(pool, pa, pool, pb, pool, pc, 3.0, n, shift)
-            total_s += time.perf_counter() - t0
-            elems += n
+        view[pa.astype(np.int64)] = 0.0
+        for t in (1, T):
+            jobs = [lambda j0=j0, j1=j1: oracle.triad(pool, pa[j0:j1], pool, pb[j0:j1], pool,
+                                                      pc[j0:j1], 3.0, (j1 - j0) * epp, shift)
+                    for j0, j1 in split(pages, t)]
+            tri[t] += run_threads(jobs, t)
         if nc == 8:
-            check = all(np.array_equal(view[int(pa[j])].view(np.uint32), gpu_pages[j].view(np.uint32))
-                        for j in gpu_pages)
+            check = all(np.array_equal(view[int(pa[j])].view(np.uint32),
+                                       gpu_pages[j].view(np.uint32)) for j in gpu_pages)
         del pool, view
-    gbs = 12 * elems / total_s / 1e9
-    log(f"cpu baseline: {total_s:.1f} s, {gbs:.2f} GB/s, sampled GPU pages bit-exact: {check}")
-    return {"value": round(gbs, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"full headline arrays (2^28 elements each), colour sets 8/16/32/64 of 64, "
-                      f"{passes} passes each; {total_s:.1f} s of single-threaded C",
-            "seconds": round(total_s, 2), "gpu_pages_match_oracle": check}
+        mm.close()
+    elems = n * len(fractions)
+    triad = {}
+    for t in (1, T):
+        triad[f"threads_{t}_s"] = round(tri[t], 3)
+        triad[f"threads_{t}_elements_per_s"] = round(elems / tri[t], 1)
+        triad[f"threads_{t}_GBps"] = round(12 * elems / tri[t] / 1e9, 3)
+    out_ops["triad"] = triad
+    log(f"cpu baseline triad: {triad}")
+    res["triad_gpu_pages_match_oracle"] = check
+
+    # ---- page-table builds over the headline pools
+    def pt_jobs(t):
+        jobs = []
+        for nc in fractions:
+            base, pool_pages = pools_desc[nc]
+            words = synth.colour_set_bits(range(nc))
+            for i0, i1 in split(pool_pages, t):
+                jobs.append(lambda base=base, i0=i0, i1=i1, words=words: oracle.pagetable(
+                    masks, base + (i0 << shift), shift, i1 - i0, words, i1 - i0))
+        return jobs
+    timed("pagetable", pt_jobs, sum(pools_desc[nc][1] for nc in fractions), "pool_pages")
+
+    # ---- classify: the first 2^22 of the C5 addresses
+    na = 1 << 22
+    cm = synth.xor_masks(6, seed=1, min_bit=12)
+    addrs = synth.page_addresses(1 << 26, seed=0)[:na]
+    got = {}
+
+    def cls_jobs(t):
+        def one(i0, i1):
+            got[i0] = oracle.classify(addrs[i0:i1], cm, with_hist=False)[0]
+        return [lambda i0=i0, i1=i1: one(i0, i1) for i0, i1 in split(na, t)]
+    timed("classify", cls_jobs, na, "addrs", 9)
+    ref_col = np.concatenate([got[k] for k in sorted(got)])
+    if "classify_colours" in gpu_checks:
+        res["classify_gpu_matches_oracle"] = bool(np.array_equal(
+            ref_col, gpu_checks["classify_colours"][:na]))
+
+    # ---- relayout: 256 MiB (4,096 pages of 64 KiB) of the 4 GiB tensor,
+    # all colours -> colours 0..15 of 64 and back, on a synthetic pool origin
+    rp = 4096
+    rpool_pages = rp * 4 + 4096
+    rmask = synth.xor_masks(6, seed=1, min_bit=16)
+    rpt, found = oracle.pagetable(rmask, 1 << 40, 16, rpool_pages, synth.colour_set_bits(range(16)),
+                                  rp)
+    assert found >= rp
+    src = synth.random_u16(rp * (1 << 15), seed=5)
+    rpool = np.zeros(rpool_pages << 16, dtype=np.uint8)
+    back = np.zeros_like(src)
+    ident = np.arange(rp, dtype=np.uint32)
+
+    def rel_jobs(t):
+        jobs = []
+        for j0, j1 in split(rp, t):
+            jobs.append(lambda j0=j0, j1=j1: oracle.relayout(rpool, rpt[j0:j1], src, ident[j0:j1],
+                                                             (j1 - j0) << 16, 16))
+            jobs.append(lambda j0=j0, j1=j1: oracle.relayout(back, ident[j0:j1], rpool, rpt[j0:j1],
+                                                             (j1 - j0) << 16, 16))
+        return jobs
+    timed("relayout", rel_jobs, 2 * (rp << 16), "bytes", 2)
+    out_ops["relayout"]["pages_per_s_threads_1"] = round(
+        2 * rp / out_ops["relayout"]["threads_1_s"], 1)
+    res["relayout_round_trip_identity"] = bool(np.array_equal(back, src))
+    del rpool, back, src
+
+    # ---- GEMV batch 1 on the benchmark's own C3 weights (contiguous copy)
+    if "gemv" in gpu_checks:
+        for (M, K), (w, x, y_gpu) in gpu_checks["gemv"].items():
+            rows_out = {}
+
+            def gemv_jobs(t, M=M, K=K, w=w, x=x):
+                def one(m0, m1):
+                    pw = np.arange(-(-((m1 - m0) * K * 2) >> 21) + 1, dtype=np.uint32)
+                    rows_out[m0] = oracle.gemv(w[m0 * K:m1 * K], pw, oracle.BF16, m1 - m0, K, x,
+                                               oracle.BF16, 1, 21)
+                return [lambda m0=m0, m1=m1: one(m0, m1) for m0, m1 in split(M, t)]
+            timed(f"gemv_{M}x{K}_b1", gemv_jobs, M * K * 2 + K * 2 + M * 4, "bytes", 1)
+            ref = np.concatenate([rows_out[k][0] for k in sorted(rows_out)], axis=1)
+            absd = np.concatenate([rows_out[k][1] for k in sorted(rows_out)], axis=1)
+            err = np.abs(y_gpu.astype(np.float64) - ref[0])
+            res[f"gemv_{M}x{K}_gpu_within_bound"] = bool(np.all(err <= 1e-3 * absd[0] + 1e-30))
+
+    res["value"] = triad[f"threads_{T}_GBps"]
+    res["unit"] = "GB/s"
+    res["cores"] = T
+    res["kind"] = "oracle"
+    res["sample"] = (f"triad on the full headline arrays (2^28 elements each, colour sets "
+                     f"8/16/32/64 of 64, one pass each) on {T} host threads over disjoint page "
+                     f"ranges; single-thread and other ops under 'ops'")
+    return res
 
 
 if __name__ == "__main__":

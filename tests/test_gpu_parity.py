@@ -271,7 +271,7 @@ def test_pagetable_pages_hold_only_set_colours(ctx, orc):
     say("pagetable colours 0..3 with in-page mask bits, then classify every 256 B")
     found = sg.colour_alloc_pagetable(ctx, masks, origin, shift, pool, S, len(want), d_pt)
     assert found == len(want) == pool // 4
-    pt = to_host(d_pt).view(np.uint32)
+    pt = to_host(d_pt[:found]).view(np.uint32)
     assert pt.tolist() == want
     sub = (np.uint64(origin) + (pt.astype(np.uint64)[:, None] << np.uint64(shift))
            + (np.arange(256, dtype=np.uint64) << np.uint64(8))[None, :]).reshape(-1)
@@ -283,6 +283,22 @@ def test_pagetable_pages_hold_only_set_colours(ctx, orc):
     with pytest.raises(sg.SgdrcError) as e:
         sg.colour_alloc_pagetable(ctx, masks, origin, shift, pool, range(3), 1, d_pt)
     assert e.value.code == sg.ENOMEM and e.value.n_found == 0
+
+
+@pytest.mark.parametrize("mask", [1 << 47, 1 << 10, 1 << 14, (1 << 10) | (1 << 14), 1 << 20,
+                                  (1 << 21) | (1 << 23)])
+def test_probe_page_sets_match_oracle(ctx, orc, mask):
+    """The channel probe's page sets: the colour-0 pages of a one-mask hash
+    over a 2 MiB-aligned pool of 1 KiB pages (bit 47, zero over the pool, is
+    the control that keeps every page); half the pool otherwise."""
+    shift, pool, origin = 10, 1 << 16, 3 << 33
+    ref, found = orc.pagetable([mask], origin, shift, pool, synth.colour_set_bits([0]), pool)
+    assert found == (pool if mask == 1 << 47 else pool // 2)
+    say(f"probe page set, mask bits {[b for b in range(48) if (mask >> b) & 1]}")
+    d_pt = torch.empty(pool, dtype=torch.int32, device=DEV)
+    got = sg.colour_alloc_pagetable(ctx, [mask], origin, shift, pool, [0], found, d_pt)
+    assert got == found
+    assert (to_host(d_pt[:found]).view(np.uint32) == ref).all()
 
 
 # ---------------------------------------------------------------- relayout
