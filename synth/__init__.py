@@ -17,8 +17,12 @@ kernels, paper section 7.2 and section 9.1.1):
   drawn from ``default_rng(mask_seed)``; ``min_bit`` is the largest page
   shift of the configuration, so that no mask bit falls inside a page and
   every page has one colour (the paper colours whole sectors); the whole set
-  of K masks is redrawn from the same stream until the masks are linearly
-  independent over GF(2), so that all 2**K colours exist;
+  of K masks is redrawn from the same stream until the masks, and also the
+  masks cut down to their K + 2 lowest bits b..b+K+1, are linearly
+  independent over GF(2): then all 2**K colours exist and every aligned run
+  of 2**(K+2) pages holds each colour equally often (consecutive pages
+  interleave over the colours, as hardware channel hashes interleave
+  consecutive blocks over channels), so small pools reach every colour;
 * fp32 data: N(0,1), or U[-1,1) built as ``2*u - 1`` from numpy's 24-bit
   float32 uniforms (every value is a multiple of 2**-23);
 * bf16 data: float32 N(0, sigma) rounded to nearest-even to bf16 bits;
@@ -52,7 +56,9 @@ def xor_masks(n_masks: int, seed: int = 1, min_bit: int = 12,
 
     Returns a list of python ints.  Bits below ``min_bit`` (the page shift)
     stay clear, so a page of 2**min_bit bytes hashes to one colour.  Redraws
-    the whole set from one stream until the masks have GF(2) rank K.
+    the whole set from one stream until the masks have GF(2) rank K, and so
+    have the masks cut down to their K + 2 lowest bits (when the bit range
+    holds that many).
     """
     if not 1 <= n_masks <= 8:
         raise ValueError("1 <= n_masks <= 8")
@@ -61,9 +67,10 @@ def xor_masks(n_masks: int, seed: int = 1, min_bit: int = 12,
         raise ValueError("not enough mask bits above min_bit for full rank")
     rng = np.random.default_rng(seed)
     width = hi_bit - lo + 1
+    window = ((1 << min(n_masks + 2, width)) - 1) << lo
     while True:
         masks = [int(rng.integers(0, 2 ** width)) << lo for _ in range(n_masks)]
-        if gf2_rank(masks) == n_masks:
+        if gf2_rank(masks) == n_masks and gf2_rank([m & window for m in masks]) == n_masks:
             return masks
 
 

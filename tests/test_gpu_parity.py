@@ -306,7 +306,7 @@ def test_probe_page_sets_match_oracle(ctx, orc, mask):
 def make_tables(orc, shift, n_pages, S, seed, K=6):
     """Oracle page table of n_pages pages of colours S, and a pool size with room."""
     S = list(S)
-    pool_pages = int(n_pages * (1 << K) / len(S) * 1.5) + 64
+    pool_pages = max(int(n_pages * (1 << K) / len(S) * 1.5) + 64, 1 << (K + 3))
     masks = synth.xor_masks(K, seed=seed, min_bit=shift)
     pt, found = orc.pagetable(masks, 0, shift, pool_pages, synth.colour_set_bits(S), n_pages)
     assert found >= n_pages
