@@ -193,6 +193,27 @@ int set_cu_mask(sgdrc_ctx *ctx, void *stream, const sgdrc_cu_mask *mask);
  * queue left (64 per context, shared with the streams). */
 int sgdrc_set_eviction_flag(sgdrc_ctx *ctx, void *stream, const uint32_t *d_flag);
 
+/* Testing aid for preemptible launches: later preemptible launches on
+ * ``stream`` and their resumptions behave as if the eviction flag were read
+ * as raised at the start of, and after the claim of, any tile whose index
+ * is ``tile`` or more (one integer compare per tile, no waiting): the
+ * workgroup that starts such a tile finishes it and leaves, and one that
+ * has just claimed such a tile hands it back.  This gives tests a mid-run
+ * eviction at a chosen point, independent of timing.  tile == 0 switches
+ * it off (the default).  Host-only. */
+int sgdrc_set_eviction_hook(sgdrc_ctx *ctx, void *stream, uint32_t tile);
+
+/* Forgets everything the context keeps for ``stream`` -- CU mask,
+ * workgroup cap, time log, eviction flag and hook, the record of its last
+ * preemptible launch -- and returns its work queues to the context, after
+ * waiting for the stream.  A suspended launch of the stream that was never
+ * resumed is discarded (raising SGDRC_DEVERR_SUSPENDED_DROPPED).  A later
+ * use of the same handle starts afresh with all CUs allowed.  Call it
+ * before a stream is destroyed or its handle may be handed out again (a
+ * stream pool such as PyTorch's reuses handles); a context holds at most
+ * 64 work queues at once.  No-op for a stream never used. */
+int sgdrc_stream_release(sgdrc_ctx *ctx, void *stream);
+
 /* Enqueues on ``stream`` the continuation of the stream's last preemptible
  * launch, under the stream's current CU mask and eviction flag, with the
  * same arguments (the caller keeps their buffers alive).  If that launch

@@ -103,6 +103,8 @@ def lib() -> ctypes.CDLL:
             "sgdrc_resume": ([vp, vp], i32),
             "sgdrc_signal_flag": ([vp, vp, vp, u32, vp], i32),
             "sgdrc_suspended": ([vp, vp, P(u64)], i32),
+            "sgdrc_set_eviction_hook": ([vp, vp, u32], i32),
+            "sgdrc_stream_release": ([vp, vp], i32),
             "sgdrc_tidal_masks": ([u32, P(u32), u32, u32, u32, P(CuMask), P(CuMask)], i32),
             "sgdrc_bm_create": ([vp, P(vp)], i32),
             "sgdrc_bm_destroy": ([vp], i32),
@@ -268,6 +270,17 @@ def set_eviction_flag(ctx, stream, flag) -> None:
     preemptible by the device word ``flag`` (an int32 CUDA tensor of at
     least one element, or a raw address); None switches it off."""
     _check(lib().sgdrc_set_eviction_flag(_h(ctx), _stream(stream), _addr(flag)))
+
+
+def set_eviction_hook(ctx, stream, tile: int) -> None:
+    """Testing aid: later preemptible launches on ``stream`` act as if the
+    eviction flag rose at tile index ``tile`` (0 switches it off)."""
+    _check(lib().sgdrc_set_eviction_hook(_h(ctx), _stream(stream), int(tile)))
+
+
+def stream_release(ctx, stream) -> None:
+    """Forget the context's state for ``stream`` (mask, cap, flags, queues)."""
+    _check(lib().sgdrc_stream_release(_h(ctx), _stream(stream)))
 
 
 def resume(ctx, stream=None) -> None:

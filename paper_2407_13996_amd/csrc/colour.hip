@@ -506,36 +506,45 @@ static int check_table(const sgdrc_colour_table *t)
     return SGDRC_OK;
 }
 
-// The ordered compaction shared by both page tests: scratch, counting pass,
-// scan, emitting pass (``launch``), then the count back to the host.
+// Scratch of one build: the scan's total (256 bytes, aligned), then the
+// per-workgroup offsets (uint64) and counts (uint32).
+size_t pt_scratch_bytes(uint64_t pool_pages)
+{
+    const uint64_t nblocks = (pool_pages + kPtBlockPages - 1) / kPtBlockPages;
+    return 256 + nblocks * sizeof(uint64_t) + nblocks * sizeof(uint32_t);
+}
+
+// Enqueues the ordered compaction shared by both page tests (counting pass,
+// scan, emitting pass: ``launch``) on ``s`` with the scratch at ``base``; the
+// count of qualifying pages goes to *d_total.
+template <class Launch>
+static int enqueue_pagetable(uint64_t pool_pages, const sgdrc_colour_set *set, void *base,
+                             uint64_t *d_total, hipStream_t s, Launch launch)
+{
+    const uint64_t nblocks = (pool_pages + kPtBlockPages - 1) / kPtBlockPages;
+    uint8_t *b = static_cast<uint8_t *>(base);
+    uint64_t *d_offsets = reinterpret_cast<uint64_t *>(b + 256);
+    uint32_t *d_counts = reinterpret_cast<uint32_t *>(b + 256 + nblocks * sizeof(uint64_t));
+    SetArgs sa;
+    for (int i = 0; i < 4; ++i) {
+        sa.w[2 * i] = (uint32_t)set->bits[i];
+        sa.w[2 * i + 1] = (uint32_t)(set->bits[i] >> 32);
+    }
+    return launch(sa, nblocks, d_counts, d_offsets, d_total, s);
+}
+
+// The synchronous build: the context's scratch (allocated at init for the
+// largest pool), then the count back to the host.
 template <class Launch>
 static int build_pagetable(Ctx *c, uint64_t pool_pages, const sgdrc_colour_set *set,
                            uint64_t n_needed, uint64_t *n_found, void *stream, Launch launch)
 {
     std::lock_guard<std::mutex> lock(g_pt_mu);
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    const uint64_t nblocks = (pool_pages + kPtBlockPages - 1) / kPtBlockPages;
-    const size_t need = 256 + nblocks * sizeof(uint64_t) + nblocks * sizeof(uint32_t);
-    if (c->scratch_bytes < need) {
-        SGDRC_HIP(hipDeviceSynchronize());
-        if (c->d_scratch)
-            SGDRC_HIP(hipFree(c->d_scratch));
-        c->d_scratch = nullptr;
-        c->scratch_bytes = 0;
-        size_t bytes = need < (1u << 20) ? (1u << 20) : need;
-        SGDRC_HIP(hipMalloc(&c->d_scratch, bytes));
-        c->scratch_bytes = bytes;
-    }
-    uint8_t *base = static_cast<uint8_t *>(c->d_scratch);
-    uint64_t *d_total = reinterpret_cast<uint64_t *>(base);
-    uint64_t *d_offsets = reinterpret_cast<uint64_t *>(base + 256);
-    uint32_t *d_counts = reinterpret_cast<uint32_t *>(base + 256 + nblocks * sizeof(uint64_t));
-    SetArgs sa;
-    for (int i = 0; i < 4; ++i) {
-        sa.w[2 * i] = (uint32_t)set->bits[i];
-        sa.w[2 * i + 1] = (uint32_t)(set->bits[i] >> 32);
-    }
-    int rc = launch(sa, nblocks, d_counts, d_offsets, d_total, s);
+    if (c->scratch_bytes < pt_scratch_bytes(pool_pages))
+        return set_error(SGDRC_EINVAL, "pool larger than the context's page-table scratch");
+    uint64_t *d_total = static_cast<uint64_t *>(c->d_scratch);
+    int rc = enqueue_pagetable(pool_pages, set, c->d_scratch, d_total, s, launch);
     if (rc)
         return rc;
     SGDRC_HIP(hipMemcpyAsync(c->h_pinned, d_total, sizeof(uint64_t), hipMemcpyDeviceToHost, s));

@@ -54,16 +54,27 @@ int popcount_mask(const sgdrc_cu_mask &m)
     return n;
 }
 
+int take_slot(Ctx *c)
+{
+    if (!c->free_slots.empty()) {
+        const int s = c->free_slots.back();
+        c->free_slots.pop_back();
+        return s;
+    }
+    return c->next_slot < kMaxStreams ? c->next_slot++ : -1;
+}
+
 int stream_state(Ctx *c, void *stream, StreamState **out)
 {
     std::lock_guard<std::mutex> lock(c->mu);
     auto it = c->streams.find(stream);
     if (it == c->streams.end()) {
-        if (c->next_slot >= kMaxStreams)
-            return set_error(SGDRC_EINVAL, "more than %d streams used with one context",
-                             kMaxStreams);
+        const int slot = take_slot(c);
+        if (slot < 0)
+            return set_error(SGDRC_EINVAL, "more than %d work queues in use with one context "
+                             "(sgdrc_stream_release gives a stream's back)", kMaxStreams);
         StreamState st;
-        st.slot = c->next_slot++;
+        st.slot = slot;
         st.mask = c->all_cus;
         it = c->streams.emplace(stream, st).first;
     }
@@ -104,6 +115,7 @@ int make_gate(Ctx *c, void *stream, uint64_t n_tiles, int group_cus, Gate *g, La
         g->evict = st->evict ? st->evict
                              : reinterpret_cast<const uint32_t *>(
                                    reinterpret_cast<const char *>(g->q) + offsetof(QueueSlot, zero));
+    g->evict_at = preemptible ? st->evict_at : 0u;
     g->err = c->d_err;
     g->log_cu = c->log_cu;
     g->log_tile = c->log_tile;
@@ -412,6 +424,10 @@ int sgdrc_init(int device, sgdrc_ctx **out)
     TRY(hipMalloc(&c->d_err, sizeof(uint32_t)));
     TRY(hipMemset(c->d_err, 0, sizeof(uint32_t)));
     TRY(hipHostMalloc(&c->h_pinned, 8 * sizeof(uint64_t), hipHostMallocDefault));
+    // the page-table build's scratch for the largest pool (2^32 pages): a
+    // build never allocates, so it never waits for the whole device
+    c->scratch_bytes = pt_scratch_bytes(1ull << 32);
+    TRY(hipMalloc(&c->d_scratch, c->scratch_bytes));
 #undef TRY
     rc = probe_topology(c, prop.multiProcessorCount);
     if (rc) {
@@ -597,13 +613,65 @@ int sgdrc_set_eviction_flag(sgdrc_ctx *ctx, void *stream, const uint32_t *d_flag
         return rc;
     std::lock_guard<std::mutex> lock(c->mu);
     if (d_flag && st->slot_ev < 0) {
-        if (c->next_slot >= kMaxStreams)
-            return set_error(SGDRC_EINVAL, "more than %d work queues used with one context",
-                             kMaxStreams);
-        st->slot_ev = c->next_slot++;
+        const int slot = take_slot(c);
+        if (slot < 0)
+            return set_error(SGDRC_EINVAL, "more than %d work queues in use with one context "
+                             "(sgdrc_stream_release gives a stream's back)", kMaxStreams);
+        st->slot_ev = slot;
     }
     st->ev_on = d_flag != nullptr;
     st->evict = d_flag;
+    return SGDRC_OK;
+}
+
+int sgdrc_set_eviction_hook(sgdrc_ctx *ctx, void *stream, uint32_t tile)
+{
+    clear_error();
+    Ctx *c = nullptr;
+    int rc = check_ctx(ctx, &c);
+    if (rc)
+        return rc;
+    StreamState *st = nullptr;
+    rc = stream_state(c, stream, &st);
+    if (rc)
+        return rc;
+    std::lock_guard<std::mutex> lock(c->mu);
+    st->evict_at = tile;
+    return SGDRC_OK;
+}
+
+int sgdrc_stream_release(sgdrc_ctx *ctx, void *stream)
+{
+    clear_error();
+    Ctx *c = nullptr;
+    int rc = check_ctx(ctx, &c);
+    if (rc)
+        return rc;
+    int slot = -1, slot_ev = -1;
+    {
+        std::lock_guard<std::mutex> lock(c->mu);
+        auto it = c->streams.find(stream);
+        if (it == c->streams.end())
+            return SGDRC_OK;
+        slot = it->second.slot;
+        slot_ev = it->second.slot_ev;
+    }
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    SGDRC_HIP(hipStreamSynchronize(s));
+    if (slot_ev >= 0) {
+        // a suspended launch that was never resumed is dropped, so that the
+        // slot is idle for its next owner
+        hipLaunchKernelGGL(k_slot_discard, dim3(1), dim3(64), 0, s, c->d_queues + slot_ev,
+                           c->d_err);
+        SGDRC_HIP(hipGetLastError());
+        SGDRC_HIP(hipStreamSynchronize(s));
+    }
+    std::lock_guard<std::mutex> lock(c->mu);
+    c->streams.erase(stream);
+    if (slot >= 0)
+        c->free_slots.push_back(slot);
+    if (slot_ev >= 0)
+        c->free_slots.push_back(slot_ev);
     return SGDRC_OK;
 }
 
@@ -640,6 +708,7 @@ int sgdrc_resume(sgdrc_ctx *ctx, void *stream)
                             : reinterpret_cast<const uint32_t *>(
                                   reinterpret_cast<const char *>(g.q) + offsetof(QueueSlot, zero));
         g.resume = 1;
+        g.evict_at = st->evict_at;
         g.log_cu = c->log_cu;
         g.log_tile = c->log_tile;
         g.log_cap = c->log_cap;

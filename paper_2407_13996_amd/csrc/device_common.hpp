@@ -90,7 +90,16 @@ struct Gate {
     uint32_t xcc_allowed;        // bit x: XCC_ID x has allowed CUs
     const uint32_t *evict;       // preemptible launches: eviction flag (non-zero = stop)
     uint32_t resume;             // preemptible launches: 1 = continue a suspended launch
+    uint32_t evict_at;           // preemptible launches, testing aid: the flag counts as
+                                 // raised for tiles at or beyond this index (0 = off)
 };
+
+// The testing aid of preemptible launches: whether tile ``tile`` is to be
+// treated as if the eviction flag had risen before it (a plain compare).
+__device__ __forceinline__ uint32_t evict_hook(const Gate &g, uint32_t tile)
+{
+    return (g.evict_at != 0u && tile >= g.evict_at) ? 1u : 0u;
+}
 
 __device__ __forceinline__ uint32_t hw_key()
 {
@@ -339,6 +348,7 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
                         if (i < lim) {
                             tile = __hip_atomic_load(&g.q->hb[i % kHandBackCap], __ATOMIC_RELAXED,
                                                      __HIP_MEMORY_SCOPE_AGENT);
+                            fl |= evict_hook(g, tile);
                             if (tile >= n_tiles) {
                                 // never expected: skip the entry, keep draining
                                 err |= kDevErrHandBack;
@@ -384,7 +394,8 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
                 // and this tile is the workgroup's last
                 uint32_t fl = 0u;
                 if (EV && threadIdx.x == 0)
-                    fl = __hip_atomic_load(g.evict, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    fl = __hip_atomic_load(g.evict, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) |
+                         evict_hook(g, lo + k);
                 if (CL == Claim::Ahead && threadIdx.x == 0)
                     next = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 auto claim = [&]() {
@@ -407,7 +418,7 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
                     // start); late: the flag rose after that, so the ticket
                     // just claimed is handed back instead of worked on
                     const bool halt = EV && fl != 0u;
-                    const bool late = EV && !halt && fl2 != 0u;
+                    const bool late = EV && !halt && (fl2 | evict_hook(g, lo + next)) != 0u;
                     if (late && next < hi - lo)
                         hand_back(g.q, lo + next);
                     s_ticket = (halt || late) ? kLutNone : next;

@@ -10,6 +10,7 @@
 #include <mutex>
 #include <string>
 #include <unordered_map>
+#include <vector>
 
 #include "device_common.hpp"
 #include "sgdrc.h"
@@ -48,6 +49,7 @@ struct StreamState {
     Gate ev_gate{};             // tile ranges and queue-group layout of that launch
     uint64_t ev_tiles = 0;
     int ev_per_cu = 1;
+    uint32_t evict_at = 0;      // testing aid: the flag counts as raised from this tile (0 = off)
 };
 
 // What a gated launch needs besides the Gate itself.
@@ -71,7 +73,7 @@ struct Ctx {
     uint64_t *d_hist_acc = nullptr;      // kMaxStreams x kHistBins
     uint32_t *d_err = nullptr;           // one word
 
-    void *d_scratch = nullptr;           // page-table build scratch
+    void *d_scratch = nullptr;           // page-table build scratch, sized for the largest pool
     size_t scratch_bytes = 0;
     uint64_t *h_pinned = nullptr;        // 8 words of pinned host memory
 
@@ -82,7 +84,16 @@ struct Ctx {
     std::mutex mu;
     std::unordered_map<void *, StreamState> streams;
     int next_slot = 0;
+    std::vector<int> free_slots;         // queue slots given back by sgdrc_stream_release
 };
+
+// A free queue slot (one released by a stream, else a new one), or -1 when
+// all kMaxStreams are taken.  Caller holds c->mu.
+int take_slot(Ctx *c);
+
+// Page-table build scratch for a pool of ``pool_pages`` pages (colour.hip).
+size_t pt_scratch_bytes(uint64_t pool_pages);
+
 
 // ------------------------------------------------------------ error text
 

@@ -145,15 +145,56 @@ def _delay(stream, us):
             x.normal_()
 
 
-def test_triad_evicted_mid_run_every_tile_once(ctx, orc):
-    """The flag is raised from another stream while the triad runs; after
-    resumptions on a smaller mask, every tile was processed once."""
+def finish(ctx, st, rounds=4):
+    """Resume ``st`` until its preemptible launch has no tiles left."""
+    r = 0
+    while sg.suspended(ctx, st) and r < rounds:
+        sg.resume(ctx, st)
+        r += 1
+    assert sg.suspended(ctx, st) == 0
+
+
+@pytest.mark.parametrize("at", [64, 1000, 3000])
+def test_triad_evicted_mid_run_every_tile_once(ctx, orc, at):
+    """Evicted mid-run at a chosen tile (the eviction hook makes the flag
+    count as raised from tile ``at`` on: workgroups past it stop, tickets
+    claimed past it are handed back), then resumed on a quarter of the CUs:
+    every tile processed once, the result exact."""
     n_cu = ctx.num_cus
     tr = Triad(orc, 16, 64 * 1024 * 1024 + 3, seed=50)    # 256 MiB arrays, 4097 tiles
+    st = torch.cuda.Stream()
+    flag = torch.zeros(1, dtype=torch.int32, device=DEV)
+    logs = Logs(ctx, tr.tiles)
+    try:
+        sg.set_eviction_flag(ctx, st, flag)
+        sg.set_eviction_hook(ctx, st, at)
+        tr.launch(ctx, st)
+        left = sg.suspended(ctx, st)
+        say(f"evicted from tile {at}: {left} of {tr.tiles} tiles left")
+        assert 0 < left < tr.tiles - at + 1
+        sg.set_eviction_hook(ctx, st, 0)
+        sg.set_cu_mask(ctx, st, range(n_cu // 4))
+        finish(ctx, st)
+        cl, tl = logs.snapshot()
+    finally:
+        logs.close()
+        sg.set_eviction_hook(ctx, st, 0)
+        sg.set_cu_mask(ctx, st, None)
+        sg.set_eviction_flag(ctx, st, None)
+    tr.check()
+    assert (tl == 1).all(), np.unique(tl, return_counts=True)
+    assert cl.sum() == tr.tiles
+
+
+def test_triad_evicted_by_another_stream(ctx, orc):
+    """The flag raised by a kernel on another stream while the triad runs
+    (wherever the timing puts it): after resumptions on a smaller mask,
+    every tile was processed once and the result is exact."""
+    n_cu = ctx.num_cus
+    tr = Triad(orc, 16, 64 * 1024 * 1024 + 3, seed=52)
     st, st2 = torch.cuda.Stream(), torch.cuda.Stream()
     flag = torch.zeros(1, dtype=torch.int32, device=DEV)
-    mid = 0
-    for delay_us in (5, 20, 40, 80, 160):
+    for delay_us in (5, 40, 160):
         tr.reset()
         flag.zero_()
         torch.cuda.synchronize()
@@ -167,15 +208,10 @@ def test_triad_evicted_mid_run_every_tile_once(ctx, orc):
             left = sg.suspended(ctx, st)
             torch.cuda.synchronize()
             say(f"flag after ~{delay_us} us: {left} of {tr.tiles} tiles left")
-            mid += 0 < left < tr.tiles
             flag.zero_()
             torch.cuda.synchronize()
             sg.set_cu_mask(ctx, st, range(n_cu // 4))
-            rounds = 0
-            while sg.suspended(ctx, st) and rounds < 4:
-                sg.resume(ctx, st)
-                rounds += 1
-            assert sg.suspended(ctx, st) == 0
+            finish(ctx, st)
             cl, tl = logs.snapshot()
         finally:
             logs.close()
@@ -184,63 +220,40 @@ def test_triad_evicted_mid_run_every_tile_once(ctx, orc):
         tr.check()
         assert (tl == 1).all(), np.unique(tl, return_counts=True)
         assert cl.sum() == tr.tiles
-    if mid == 0:
-        # every result above was checked; only the timing did not cooperate
-        pytest.skip("the flag never landed while the launch ran (stream timing of this run)")
 
 
 def test_triad_resumption_evicted_mid_run_again(ctx, orc):
-    """Evicted mid-run, resumed on 16 CUs and evicted mid-run again (tiles
-    handed back by the first eviction are worked through first, and may be
-    handed back again), then finished on all CUs: every tile once."""
-    n_cu = ctx.num_cus
+    """Evicted at tile 1000, resumed on 16 CUs and evicted again at tile
+    2500 (the tiles handed back by the first eviction are worked through
+    first), then finished on all CUs: every tile once."""
     tr = Triad(orc, 16, 64 * 1024 * 1024 + 3, seed=55)    # 256 MiB arrays, 4097 tiles
-    st, st2 = torch.cuda.Stream(), torch.cuda.Stream()
+    st = torch.cuda.Stream()
     flag = torch.zeros(1, dtype=torch.int32, device=DEV)
-    twice = 0
-    for d1, d2 in ((20, 100), (40, 300), (80, 600)):
-        tr.reset()
-        flag.zero_()
-        torch.cuda.synchronize()
-        logs = Logs(ctx, tr.tiles)
-        try:
-            sg.set_eviction_flag(ctx, st, flag)
-            tr.launch(ctx, st)
-            _delay(st2, d1)
-            with torch.cuda.stream(st2):
-                flag.fill_(1)
-            left1 = sg.suspended(ctx, st)
-            torch.cuda.synchronize()
-            flag.zero_()
-            torch.cuda.synchronize()
-            sg.set_cu_mask(ctx, st, range(16))
-            sg.resume(ctx, st)
-            _delay(st2, d2)
-            with torch.cuda.stream(st2):
-                flag.fill_(1)
-            left2 = sg.suspended(ctx, st)
-            torch.cuda.synchronize()
-            say(f"evicted after ~{d1} us: {left1} left; resumed on 16 CUs, evicted after ~{d2} us: "
-                f"{left2} left of {tr.tiles}")
-            twice += 0 < left2 < left1
-            flag.zero_()
-            torch.cuda.synchronize()
-            sg.set_cu_mask(ctx, st, None)
-            rounds = 0
-            while sg.suspended(ctx, st) and rounds < 4:
-                sg.resume(ctx, st)
-                rounds += 1
-            assert sg.suspended(ctx, st) == 0
-            cl, tl = logs.snapshot()
-        finally:
-            logs.close()
-            sg.set_cu_mask(ctx, st, None)
-            sg.set_eviction_flag(ctx, st, None)
-        tr.check()
-        assert (tl == 1).all(), np.unique(tl, return_counts=True)
-        assert cl.sum() == tr.tiles
-    if twice == 0:
-        pytest.skip("no resumption was evicted mid-run (stream timing of this run)")
+    logs = Logs(ctx, tr.tiles)
+    try:
+        sg.set_eviction_flag(ctx, st, flag)
+        sg.set_eviction_hook(ctx, st, 1000)
+        tr.launch(ctx, st)
+        left1 = sg.suspended(ctx, st)
+        sg.set_eviction_hook(ctx, st, 2500)
+        sg.set_cu_mask(ctx, st, range(16))
+        sg.resume(ctx, st)
+        left2 = sg.suspended(ctx, st)
+        say(f"evicted at tile 1000: {left1} left; resumed on 16 CUs, evicted at 2500: "
+            f"{left2} left of {tr.tiles}")
+        assert 0 < left2 < left1 < tr.tiles
+        sg.set_eviction_hook(ctx, st, 0)
+        sg.set_cu_mask(ctx, st, None)
+        finish(ctx, st)
+        cl, tl = logs.snapshot()
+    finally:
+        logs.close()
+        sg.set_eviction_hook(ctx, st, 0)
+        sg.set_cu_mask(ctx, st, None)
+        sg.set_eviction_flag(ctx, st, None)
+    tr.check()
+    assert (tl == 1).all(), np.unique(tl, return_counts=True)
+    assert cl.sum() == tr.tiles
 
 
 def test_resume_after_completion_does_nothing(ctx, orc):
@@ -336,10 +349,11 @@ def test_relayout_evicted_then_resumed(ctx, orc, shift, n_bytes):
     assert (to_host(d_dst).view(np.uint8) == ref).all()
 
 
-def test_relayout_evicted_mid_run_every_tile_once(ctx, orc):
-    """A 128 MiB relayout on 16 CUs, evicted from another stream while it
-    runs (tiles claimed just before the flag rose are handed back), then
-    finished on all CUs: byte-exact, every 64 KiB tile once."""
+@pytest.mark.parametrize("at", [100, 1000])
+def test_relayout_evicted_mid_run_every_tile_once(ctx, orc, at):
+    """A 128 MiB relayout on 16 CUs evicted mid-run at tile ``at`` (tickets
+    claimed past it are handed back), then finished on all CUs: byte-exact,
+    every 64 KiB tile once."""
     shift, n_bytes = 16, 128 * 1024 * 1024 + 9
     P = 1 << shift
     n_pages = -(-n_bytes // P)
@@ -354,46 +368,71 @@ def test_relayout_evicted_mid_run_every_tile_once(ctx, orc):
     d_dst = torch.zeros(pool * P // 2, dtype=torch.int16, device=DEV)
     ref = np.zeros(pool * P, dtype=np.uint8)
     orc.relayout(ref, pt_d, src.view(np.uint8), pt_s, n_bytes, shift)
-    st, st2 = torch.cuda.Stream(), torch.cuda.Stream()
+    st = torch.cuda.Stream()
     flag = torch.zeros(1, dtype=torch.int32, device=DEV)
     dpt_s, dpt_d = to_dev(pt_s), to_dev(pt_d)
-    mid = 0
-    for delay_us in (0, 30, 100, 250, 500):
-        d_dst.zero_()
-        flag.zero_()
-        torch.cuda.synchronize()
-        logs = Logs(ctx, tiles)
-        try:
-            sg.set_eviction_flag(ctx, st, flag)
-            sg.set_cu_mask(ctx, st, range(16))
-            sg.bimodal_relayout(ctx, sg.paged(d_dst, dpt_d, pool), sg.paged(d_src, dpt_s, pool),
-                                n_bytes, shift, st)
-            _delay(st2, delay_us)
-            with torch.cuda.stream(st2):
-                flag.fill_(1)
-            left = sg.suspended(ctx, st)
-            torch.cuda.synchronize()
-            say(f"relayout flag after ~{delay_us} us: {left} of {tiles} tiles left")
-            mid += 0 < left < tiles
-            flag.zero_()
-            torch.cuda.synchronize()
-            sg.set_cu_mask(ctx, st, None)
-            rounds = 0
-            while sg.suspended(ctx, st) and rounds < 4:
-                sg.resume(ctx, st)
-                rounds += 1
-            assert sg.suspended(ctx, st) == 0
-            cl, tl = logs.snapshot()
-        finally:
-            logs.close()
-            sg.set_cu_mask(ctx, st, None)
-            sg.set_eviction_flag(ctx, st, None)
-        assert (to_host(d_dst).view(np.uint8) == ref).all()
-        assert (tl == 1).all(), np.unique(tl, return_counts=True)
-        assert cl.sum() == tiles
-    if mid == 0:
-        # every result above was checked; only the timing did not cooperate
-        pytest.skip("the flag never landed while the launch ran (stream timing of this run)")
+    logs = Logs(ctx, tiles)
+    try:
+        sg.set_eviction_flag(ctx, st, flag)
+        sg.set_eviction_hook(ctx, st, at)
+        sg.set_cu_mask(ctx, st, range(16))
+        sg.bimodal_relayout(ctx, sg.paged(d_dst, dpt_d, pool), sg.paged(d_src, dpt_s, pool),
+                            n_bytes, shift, st)
+        left = sg.suspended(ctx, st)
+        say(f"relayout evicted from tile {at}: {left} of {tiles} tiles left")
+        assert 0 < left < tiles - at + 1
+        sg.set_eviction_hook(ctx, st, 0)
+        sg.set_cu_mask(ctx, st, None)
+        finish(ctx, st)
+        cl, tl = logs.snapshot()
+    finally:
+        logs.close()
+        sg.set_eviction_hook(ctx, st, 0)
+        sg.set_cu_mask(ctx, st, None)
+        sg.set_eviction_flag(ctx, st, None)
+    assert (to_host(d_dst).view(np.uint8) == ref).all()
+    assert (tl == 1).all(), np.unique(tl, return_counts=True)
+    assert cl.sum() == tiles
+
+
+def test_stream_release_forgets_state_and_returns_queues(ctx, orc):
+    """sgdrc_stream_release: 100 preemptible streams in turn (two work
+    queues each, 200 in all against 64 per context) each run a triad and
+    are released; a released stream handle starts again on all CUs; a
+    suspended launch is dropped on release."""
+    n_cu = ctx.num_cus
+    tr = Triad(orc, 16, 40 * 16384, seed=110)
+    flag = torch.zeros(1, dtype=torch.int32, device=DEV)
+    for i in range(100):
+        s = torch.cuda.Stream()
+        sg.set_eviction_flag(ctx, s, flag)
+        sg.set_cu_mask(ctx, s, [i % n_cu])
+        tr.launch(ctx, s)
+        assert sg.suspended(ctx, s) == 0
+        sg.stream_release(ctx, s)
+    tr.check()
+    st = torch.cuda.Stream()
+    sg.set_cu_mask(ctx, st, range(8))
+    sg.stream_release(ctx, st)
+    logs = Logs(ctx, tr.tiles)
+    try:
+        tr.reset()
+        tr.launch(ctx, st)                      # same handle: all CUs again
+        cl, tl = logs.snapshot()
+    finally:
+        logs.close()
+    tr.check()
+    assert (tl == 1).all() and len(set(np.nonzero(cl)[0].tolist()) - set(range(8))) > 0
+    # a suspended launch is discarded by the release
+    flag.fill_(1)
+    torch.cuda.synchronize()
+    sg.set_eviction_flag(ctx, st, flag)
+    tr.launch(ctx, st)
+    assert sg.suspended(ctx, st) == tr.tiles
+    sg.stream_release(ctx, st)
+    assert ctx.device_error() == sg.DEVERR_SUSPENDED_DROPPED
+    flag.zero_()
+    sg.stream_release(ctx, torch.cuda.Stream())  # never used: nothing to do
 
 
 def test_tidal_handover_ls_gemv_and_evicted_triad(ctx, orc):
