@@ -574,6 +574,7 @@ def bench_relayout(torch, sg, synth, ctx, stream, timer, reps=10):
 
 
 def bench_gemv(torch, sg, synth, ctx, stream, timer, launches, checks):
+    import numpy as np
     shift = 21
     P = 1 << shift
     copies = 8
