@@ -283,6 +283,27 @@ int colour_alloc_pagetable(sgdrc_ctx *ctx, const sgdrc_hash *hash, uint64_t addr
                            const sgdrc_colour_set *set, uint64_t n_needed, uint32_t *d_pt,
                            uint64_t *n_found, void *stream);
 
+/* colour_alloc_pagetable for callers that cannot allocate: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.  It
+ * allocates nothing and never waits for the device: the same table as
+ * colour_alloc_pagetable goes to d_pt, but the call is asynchronous on
+ * ``stream``, the count of qualifying pages in the pool goes to *d_n_found
+ * (device memory, one uint64, 8-byte aligned) instead of a host variable,
+ * and a shortfall is no error: the caller compares *d_n_found with
+ * n_needed (d_pt then holds all the qualifying pages).  Its scratch is a
+ * fixed 192.25 KiB block of the library's own device memory, one per
+ * device and held until the process ends, which limits pool_pages to 2^26.
+ * Every call on a device shares that block: calls that overlap on one GPU
+ * (on different streams or host threads) race, and the caller must order
+ * them.  Every scratch word a call reads is first written by the same
+ * call, so nothing needs clearing between calls.  EINVAL: as
+ * colour_alloc_pagetable, pool_pages above 2^26, d_n_found NULL or
+ * misaligned. */
+int colour_alloc_pagetable_noalloc(sgdrc_ctx *ctx, const sgdrc_hash *hash, uint64_t addr_origin,
+                                   uint32_t page_shift, uint64_t pool_pages,
+                                   const sgdrc_colour_set *set, uint64_t n_needed, uint32_t *d_pt,
+                                   uint64_t *d_n_found, void *stream);
+
 /* A colour table (paper section 5.3: for hashes that are not XOR-linear, a
  * table made offline holds the channel of every 1 KiB partition): lut[i]
  * (device memory) is the colour of the bytes [origin + i 2^shift,

@@ -105,6 +105,8 @@ def lib() -> ctypes.CDLL:
             "sgdrc_suspended": ([vp, vp, P(u64)], i32),
             "sgdrc_set_eviction_hook": ([vp, vp, u32], i32),
             "sgdrc_stream_release": ([vp, vp], i32),
+            "colour_alloc_pagetable_noalloc": ([vp, P(Hash), u64, u32, u64, P(ColourSet), u64, vp,
+                                                vp, vp], i32),
             "sgdrc_tidal_masks": ([u32, P(u32), u32, u32, u32, P(CuMask), P(CuMask)], i32),
             "sgdrc_bm_create": ([vp, P(vp)], i32),
             "sgdrc_bm_destroy": ([vp], i32),
@@ -333,6 +335,20 @@ def colour_alloc_pagetable(ctx, masks, addr_origin: int, page_shift: int, pool_p
                                       _addr(pt), ctypes.byref(found), _stream(stream))
     _check(rc, found.value)
     return found.value
+
+
+def colour_alloc_pagetable_noalloc(ctx, masks, addr_origin: int, page_shift: int,
+                                   pool_pages: int, colours, n_needed: int, pt, n_found,
+                                   stream=None) -> None:
+    """Asynchronous, allocation-free page-table build: the table goes to
+    ``pt`` and the count of qualifying pages to ``n_found`` (a device int64
+    tensor of one element); no shortfall error."""
+    _check(lib().colour_alloc_pagetable_noalloc(_h(ctx), ctypes.byref(make_hash(masks)),
+                                                int(addr_origin), int(page_shift),
+                                                int(pool_pages),
+                                                ctypes.byref(make_set(words_of(colours))),
+                                                int(n_needed), _addr(pt), _addr(n_found),
+                                                _stream(stream)))
 
 
 def colour_table(lut, origin: int, shift: int) -> ColourTable:

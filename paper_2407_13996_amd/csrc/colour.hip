@@ -514,6 +514,28 @@ size_t pt_scratch_bytes(uint64_t pool_pages)
     return 256 + nblocks * sizeof(uint64_t) + nblocks * sizeof(uint32_t);
 }
 
+// The no-allocation build's scratch: a fixed block of the library's own
+// device memory (one per device, held until the process ends) for pools of
+// up to kNoAllocMaxPages pages.  Host code never passes the array's name to
+// a kernel (in host code it is only a stand-in): it uses the device address
+// that noalloc_scratch_init looks up once per context, with the context's
+// device current.
+constexpr uint64_t kNoAllocMaxPages = 1ull << 26;
+constexpr size_t kNoAllocScratch = 256 + (kNoAllocMaxPages / kPtBlockPages) * 12u;  // 192.25 KiB
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratch];
+
+int noalloc_scratch_init(Ctx *c)
+{
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess)
+        return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p)
+        return set_error(SGDRC_EHIP, "no device address for the page-table scratch");
+    c->d_static_scratch = p;
+    return SGDRC_OK;
+}
+
 // Enqueues the ordered compaction shared by both page tests (counting pass,
 // scan, emitting pass: ``launch``) on ``s`` with the scratch at ``base``; the
 // count of qualifying pages goes to *d_total.
@@ -623,6 +645,44 @@ int colour_alloc_pagetable(sgdrc_ctx *ctx, const sgdrc_hash *hash, uint64_t addr
                                                 d_pt, nblocks, d_counts, d_offsets, d_total, s);
                                return rc;
                            });
+}
+
+int colour_alloc_pagetable_noalloc(sgdrc_ctx *ctx, const sgdrc_hash *hash, uint64_t addr_origin,
+                                   uint32_t page_shift, uint64_t pool_pages,
+                                   const sgdrc_colour_set *set, uint64_t n_needed, uint32_t *d_pt,
+                                   uint64_t *d_n_found, void *stream)
+{
+    clear_error();
+    int rc = check_hash(hash);
+    if (rc)
+        return rc;
+    if ((rc = check_pool_args(addr_origin, page_shift, pool_pages, set, n_needed, d_pt,
+                              d_n_found)))
+        return rc;
+    if (reinterpret_cast<uintptr_t>(d_n_found) & 7u)
+        return set_error(SGDRC_EINVAL, "d_n_found not 8-byte aligned");
+    if (pool_pages > kNoAllocMaxPages)
+        return set_error(SGDRC_EINVAL, "pool_pages %llu above the %llu pages the fixed scratch "
+                         "serves", (unsigned long long)pool_pages,
+                         (unsigned long long)kNoAllocMaxPages);
+    if ((rc = check_set(set, 1u << hash->n_masks)))
+        return rc;
+    Ctx *c = nullptr;
+    if ((rc = check_ctx(ctx, &c)))
+        return rc;
+    const HashArgs h = hash_args(hash);
+    const sgdrc_colour_set whole = page_colour_set(hash, page_shift, *set);
+    return enqueue_pagetable(pool_pages, &whole, c->d_static_scratch, d_n_found,
+                             reinterpret_cast<hipStream_t>(stream),
+                             [&](const SetArgs &sa, uint64_t nblocks, uint32_t *d_counts,
+                                 uint64_t *d_offsets, uint64_t *d_total, hipStream_t s) {
+                                 int rc = SGDRC_OK;
+                                 SGDRC_DISPATCH_K(hash->n_masks, launch_pagetable_xor, c, h,
+                                                  addr_origin, page_shift, pool_pages, sa,
+                                                  n_needed, d_pt, nblocks, d_counts, d_offsets,
+                                                  d_total, s);
+                                 return rc;
+                             });
 }
 
 int colour_classify_table(sgdrc_ctx *ctx, const sgdrc_colour_table *table,

@@ -429,6 +429,11 @@ int sgdrc_init(int device, sgdrc_ctx **out)
     c->scratch_bytes = pt_scratch_bytes(1ull << 32);
     TRY(hipMalloc(&c->d_scratch, c->scratch_bytes));
 #undef TRY
+    rc = noalloc_scratch_init(c);
+    if (rc) {
+        free_ctx(c);
+        return rc;
+    }
     rc = probe_topology(c, prop.multiProcessorCount);
     if (rc) {
         free_ctx(c);

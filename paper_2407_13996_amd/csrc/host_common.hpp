@@ -75,6 +75,8 @@ struct Ctx {
 
     void *d_scratch = nullptr;           // page-table build scratch, sized for the largest pool
     size_t scratch_bytes = 0;
+    void *d_static_scratch = nullptr;    // the device address of the no-allocation build's
+                                         // scratch (a static device array of colour.hip)
     uint64_t *h_pinned = nullptr;        // 8 words of pinned host memory
 
     uint32_t *log_cu = nullptr;
@@ -94,6 +96,10 @@ int take_slot(Ctx *c);
 // Page-table build scratch for a pool of ``pool_pages`` pages (colour.hip).
 size_t pt_scratch_bytes(uint64_t pool_pages);
 
+// Looks up the device address of the no-allocation page-table build's
+// static scratch on the current device and records it in ``c`` (colour.hip;
+// called by sgdrc_init with the context's device current).
+int noalloc_scratch_init(Ctx *c);
 
 // ------------------------------------------------------------ error text
 
