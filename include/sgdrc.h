@@ -134,6 +134,14 @@ int sgdrc_set_worklog(sgdrc_ctx *ctx, uint32_t *d_cu_tiles, uint32_t *d_tile_vis
  * context (0 if none); lets a caller size and read the work log. */
 int sgdrc_last_tiles(sgdrc_ctx *ctx, void *stream, uint64_t *tiles);
 
+/* How the last launch enqueued on ``stream`` distributed its tiles:
+ * SGDRC_SCHED_QUEUE (atomic ticket queues per group of CUs, with stealing)
+ * or SGDRC_SCHED_STATIC (colored_gemv under a mask made of whole XCDs: each
+ * workgroup derives its tiles from its XCD and index, no atomics).  For
+ * tests and tools. */
+enum { SGDRC_SCHED_QUEUE = 0, SGDRC_SCHED_STATIC = 1 };
+int sgdrc_last_schedule(sgdrc_ctx *ctx, void *stream, uint32_t *schedule);
+
 /* Optional per-launch device time log, for measuring kernel latency without
  * host launch overhead.  Launch i on ``stream`` (counted from this call) of
  * colour_classify, bimodal_relayout, colored_stream or colored_gemv writes
@@ -165,7 +173,11 @@ int sgdrc_set_stream_occupancy(sgdrc_ctx *ctx, void *stream, uint32_t max_wgs_pe
  * set used by every later launch on ``stream``: each workgroup reads its
  * CU identity from the hardware registers and exits unless that CU is in
  * the set; the remaining workgroups take tiles from an atomic queue until it
- * is empty.  mask == NULL restores all CUs.  Host-only, takes effect at the
+ * is empty.  A colored_gemv under a mask made of whole XCDs (the usual
+ * case: all CUs, or n x 32 CUs) needs no queue: the hardware hands
+ * workgroup i of a grid to the XCD of workgroup i mod (XCD count), which
+ * sgdrc_init checks, so a workgroup on an allowed XCD derives its tiles from
+ * its XCD and index alone (SGDRC_SCHED_STATIC).  mask == NULL restores all CUs.  Host-only, takes effect at the
  * next launch, never recreates the stream.  EINVAL: empty mask or a bit at
  * or above sgdrc_num_cus(). */
 int set_cu_mask(sgdrc_ctx *ctx, void *stream, const sgdrc_cu_mask *mask);

@@ -95,6 +95,7 @@ def lib() -> ctypes.CDLL:
             "sgdrc_device_error": ([vp, P(u32)], i32),
             "sgdrc_set_worklog": ([vp, vp, vp, u64], i32),
             "sgdrc_last_tiles": ([vp, vp, P(u64)], i32),
+            "sgdrc_last_schedule": ([vp, vp, P(u32)], i32),
             "sgdrc_set_timelog": ([vp, vp, vp, u32], i32),
             "sgdrc_wallclock_khz": ([vp, P(u32)], i32),
             "set_cu_mask": ([vp, vp, P(CuMask)], i32),
@@ -230,6 +231,12 @@ class Context:
         t = ctypes.c_uint64()
         _check(lib().sgdrc_last_tiles(self.handle, _stream(stream), ctypes.byref(t)))
         return t.value
+
+    def last_schedule(self, stream=None) -> str:
+        """'static' or 'queue': how the last launch on ``stream`` took its tiles."""
+        v = ctypes.c_uint32()
+        _check(lib().sgdrc_last_schedule(self.handle, _stream(stream), ctypes.byref(v)))
+        return "static" if v.value == 1 else "queue"
 
     def set_timelog(self, stream=None, slots=None) -> None:
         """Log {start, end} device-clock ticks of each later launch on

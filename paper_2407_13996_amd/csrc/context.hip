@@ -97,7 +97,7 @@ static uint32_t xcc_allowed(const Ctx *c, const sgdrc_cu_mask &m)
 }
 
 int make_gate(Ctx *c, void *stream, uint64_t n_tiles, int group_cus, Gate *g, LaunchInfo *li,
-              bool preemptible)
+              bool preemptible, bool allow_static)
 {
     StreamState *st = nullptr;
     int rc = stream_state(c, stream, &st);
@@ -165,6 +165,33 @@ int make_gate(Ctx *c, void *stream, uint64_t n_tiles, int group_cus, Gate *g, La
     g->n_groups = (uint32_t)n_groups;
     g->grp_shift = shift;
     g->xcc_allowed = xcc_allowed(c, st->mask);
+    // static schedule: every XCD either wholly allowed or wholly not
+    g->statics = 0u;
+    std::memset(g->xcd_rank, 0xFF, sizeof g->xcd_rank);
+    g->n_allowed_xcd = 0u;
+    g->n_xcd = (uint32_t)c->n_xcds;
+    if (allow_static && !preemptible && c->static_ok) {
+        bool whole = true;
+        uint8_t rank[kMaxXcds];
+        std::memset(rank, 0xFF, sizeof rank);
+        uint32_t a = 0;
+        for (int x = 0; x < c->n_xcds && whole; ++x) {
+            int on = 0;
+            const int first = c->xcd_first_cu[x], count = c->xcd_first_cu[x + 1] - first;
+            for (int cu = first; cu < first + count; ++cu)
+                on += (int)((st->mask.bits[cu >> 6] >> (cu & 63)) & 1ull);
+            if (on == count)
+                rank[(c->keys[first] >> 8) & 0xFu] = (uint8_t)a++;
+            else if (on != 0)
+                whole = false;
+        }
+        if (whole && a > 0) {
+            g->statics = 1u;
+            std::memcpy(g->xcd_rank, rank, sizeof rank);
+            g->n_allowed_xcd = a;
+        }
+    }
+    st->last_schedule = g->statics;
     st->last_tiles = n_tiles;
     li->allowed = (int)total;
     li->wg_cap = st->wg_cap;
@@ -217,6 +244,32 @@ __global__ __launch_bounds__(64) void k_signal_flag(uint32_t *flag, uint32_t val
     if (stamp)
         __hip_atomic_store(stamp, __builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// One wavefront: the end stamp of a statically scheduled launch is the
+// largest of its partial end stamps, which are cleared for the next launch.
+__global__ __launch_bounds__(64) void k_tlog_reduce(QueueSlot *q, uint64_t *tlog)
+{
+    uint64_t *p = &q->tpart[threadIdx.x * (kCounterStride / 2)];
+    uint64_t v = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(p, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        const uint64_t o = __shfl_xor(v, off, 64);
+        v = o > v ? o : v;
+    }
+    if (threadIdx.x == 0)
+        __hip_atomic_store(&tlog[1], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+int finish_static_tlog(const Gate &g, hipStream_t s)
+{
+    if (!g.statics || !g.tlog)
+        return SGDRC_OK;
+    static_assert(kTimePartials == 64, "one lane per partial");
+    hipLaunchKernelGGL(k_tlog_reduce, dim3(1), dim3(64), 0, s, g.q, g.tlog);
+    SGDRC_HIP(hipGetLastError());
+    return SGDRC_OK;
 }
 
 int stream_allowed_cus(Ctx *c, void *stream)
@@ -304,9 +357,27 @@ __global__ void k_cu_probe(uint32_t *keys, uint32_t n, uint32_t spins)
         keys[blockIdx.x] = key;
 }
 
+// Whether workgroup i of the probe grid ran on the XCD of workgroup
+// i mod n_xcds, with the first n_xcds workgroups on n_xcds different XCDs
+// (the partition the static schedule relies on).
+static bool xcd_partition_holds(const std::vector<uint32_t> &raw, int n_xcds)
+{
+    if (n_xcds < 1 || raw.size() < (size_t)n_xcds || raw.size() % (size_t)n_xcds)
+        return false;
+    uint32_t seen = 0;
+    for (int r = 0; r < n_xcds; ++r)
+        seen |= 1u << ((raw[r] >> 8) & 0xFu);
+    if (__builtin_popcount(seen) != n_xcds)
+        return false;
+    for (size_t i = 0; i < raw.size(); ++i)
+        if (((raw[i] ^ raw[i % n_xcds]) >> 8) & 0xFu)
+            return false;
+    return true;
+}
+
 static int probe_topology(Ctx *c, int expected)
 {
-    std::vector<uint32_t> uniq;
+    std::vector<uint32_t> uniq, raw;
     for (int attempt = 0; attempt < 3; ++attempt) {
         const uint32_t n = (uint32_t)expected * (48u << attempt);
         uint32_t *d_keys = nullptr;
@@ -321,6 +392,7 @@ static int probe_topology(Ctx *c, int expected)
         (void)hipFree(d_keys);
         if (e != hipSuccess)
             return hip_fail(e, "CU probe");
+        raw = keys;
         std::sort(keys.begin(), keys.end());
         keys.erase(std::unique(keys.begin(), keys.end()), keys.end());
         uniq = keys;
@@ -353,6 +425,7 @@ static int probe_topology(Ctx *c, int expected)
     c->n_xcds = n_xcds;
     for (int x = n_xcds; x <= kMaxXcds; ++x)
         c->xcd_first_cu[x] = expected;
+    c->static_ok = xcd_partition_holds(raw, n_xcds);
     c->num_cus = expected;
     std::memset(&c->all_cus, 0, sizeof c->all_cus);
     for (int i = 0; i < expected; ++i)
@@ -523,6 +596,21 @@ int sgdrc_last_tiles(sgdrc_ctx *ctx, void *stream, uint64_t *tiles)
     std::lock_guard<std::mutex> lock(c->mu);
     auto it = c->streams.find(stream);
     *tiles = it == c->streams.end() ? 0 : it->second.last_tiles;
+    return SGDRC_OK;
+}
+
+int sgdrc_last_schedule(sgdrc_ctx *ctx, void *stream, uint32_t *schedule)
+{
+    clear_error();
+    if (!schedule)
+        return set_error(SGDRC_EINVAL, "schedule is NULL");
+    Ctx *c = nullptr;
+    int rc = check_ctx(ctx, &c);
+    if (rc)
+        return rc;
+    std::lock_guard<std::mutex> lock(c->mu);
+    auto it = c->streams.find(stream);
+    *schedule = it == c->streams.end() ? 0u : it->second.last_schedule;
     return SGDRC_OK;
 }
 

@@ -37,6 +37,9 @@ constexpr int kCounterStride = 32;  // 32-bit words between counters (128 bytes)
 // launch: at most one per workgroup per launch, so at most twice the grid
 // of one launch is ever live in the ring.
 constexpr uint32_t kHandBackCap = 2048;
+// Partial end stamps of a statically scheduled launch's time log: 64
+// addresses, so that no more than a grid / 64 workgroups meet on one.
+constexpr int kTimePartials = 64;
 
 // Work distribution state of one stream.  The CUs of each XCD are cut into
 // runs of 2^grp_shift CUs ("queue groups"; a launch picks the run length:
@@ -71,6 +74,9 @@ struct QueueSlot {
     uint32_t hb_take[kCounterStride];
     uint32_t hb_limit[kCounterStride];
     uint32_t hb[kHandBackCap];
+    // statically scheduled launches with a time log: the latest end stamp
+    // of the workgroups whose index is i mod kTimePartials, one per 128 bytes
+    uint64_t tpart[kTimePartials * kCounterStride / 2];
 };
 
 // Per-launch gate arguments (passed by value in the kernel arguments).
@@ -92,6 +98,13 @@ struct Gate {
     uint32_t resume;             // preemptible launches: 1 = continue a suspended launch
     uint32_t evict_at;           // preemptible launches, testing aid: the flag counts as
                                  // raised for tiles at or beyond this index (0 = off)
+    // Static schedule (statics = 1; masks made of whole XCDs, see
+    // static_tile_loop): the rank of each XCC_ID among the allowed XCDs
+    // (0xFF = not allowed), their number, and the device's XCD count.
+    uint32_t statics;
+    uint8_t xcd_rank[kMaxXcds];
+    uint32_t n_allowed_xcd;
+    uint32_t n_xcd;
 };
 
 // The testing aid of preemptible launches: whether tile ``tile`` is to be
@@ -589,6 +602,65 @@ __device__ __forceinline__ void gated_tile_loop(const Gate &g, uint32_t n_tiles,
     }
     if (err != 0u)
         raise_flag(g.err, err);
+}
+
+// Static schedule for launches whose CU mask is a union of whole XCDs (the
+// host sets g.statics).  The hardware hands the workgroups of a grid to the
+// XCDs by index modulo the XCD count (checked at context creation), so a
+// workgroup knows its XCD from XCC_ID and its rank among the workgroups of
+// that XCD from blockIdx alone: no table lookup, no ticket, no arrival
+// counter.  With A allowed XCDs and W workgroups per XCD, the workgroup of
+// rank r on the allowed XCD of rank a is worker v = r A + a of W A, and
+// takes tiles v, v + W A, ... -- consecutive tiles on different XCDs, as a
+// plain grid would place them.  Workgroups on other XCDs leave at once.
+// With a time log, workgroup 0 stamps the start and every workgroup, once
+// its stores are done, raises partial end stamp blockIdx mod kTimePartials
+// to its end time; the host reduces the partials with k_tlog_reduce after
+// the launch.  ``prologue`` and ``body`` as in gated_tile_loop (``claim`` has
+// no effect).
+template <typename Prologue, typename Body>
+__device__ __forceinline__ void static_tile_loop(const Gate &g, uint32_t n_tiles, Prologue prologue,
+                                                 Body body)
+{
+    uint32_t xcc;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+    const uint32_t a = g.xcd_rank[xcc & 0xFu];
+    // the work log names the logical CU: one table read, only when logging
+    const uint32_t cu = g.log_cu ? (my_cu_entry(g) & 0xFFFFu) : (uint32_t)kMaxCus;
+    prologue();
+    if (g.tlog && blockIdx.x == 0 && threadIdx.x == 0)
+        __hip_atomic_store(&g.tlog[0], __builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    uint32_t err = 0u;
+    if (a != 0xFFu) {
+        const uint32_t workers = (gridDim.x / g.n_xcd) * g.n_allowed_xcd;
+        for (uint32_t t = (blockIdx.x / g.n_xcd) * g.n_allowed_xcd + a; t < n_tiles; t += workers) {
+            log_tile(g, cu, t);
+            body(t, cu, err, NoOp());
+        }
+    }
+    if (g.tlog) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (threadIdx.x == 0)
+            __hip_atomic_fetch_max(&g.q->tpart[(blockIdx.x % kTimePartials) * (kCounterStride / 2)],
+                                   (uint64_t)__builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (err != 0u)
+        raise_flag(g.err, err);
+}
+
+// The gate's two schedules behind one call: static for masks of whole XCDs
+// (g.statics, a uniform branch), the ticket queues otherwise.
+template <Claim CL, typename Prologue, typename Body>
+__device__ __forceinline__ void tile_loop(const Gate &g, uint32_t n_tiles, Prologue prologue, Body body)
+{
+    if (g.statics)
+        static_tile_loop(g, n_tiles, prologue, body);
+    else
+        gated_tile_loop<CL>(g, n_tiles, prologue, body, NoOp(), NoOp());
 }
 
 // Wavefront-granular form of gated_tile_loop, for bodies whose work is

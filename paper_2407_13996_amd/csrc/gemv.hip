@@ -248,7 +248,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
         }
         __syncthreads();
     };
-    gated_tile_loop<Claim::Ahead>(g, n_tiles, prologue, body, NoOp(), NoOp());
+    tile_loop<Claim::Ahead>(g, n_tiles, prologue, body);
     if (pro_err)
         raise_flag(g.err, pro_err);
 }
@@ -426,7 +426,7 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(4)
         }
         __syncthreads();
     };
-    gated_tile_loop<Claim::Ahead>(g, n_tiles, prologue, body, NoOp(), NoOp());
+    tile_loop<Claim::Ahead>(g, n_tiles, prologue, body);
     if (pro_err)
         raise_flag(g.err, pro_err);
 }
@@ -639,17 +639,17 @@ int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, 
         return set_error(SGDRC_EINVAL, "no kernel for the plan (library fault)");
     Gate g;
     LaunchInfo li;
-    rc = make_gate(c, stream, plan.tiles, kGemvGroupCus, &g, &li);
+    rc = make_gate(c, stream, plan.tiles, kGemvGroupCus, &g, &li, false, true);
     if (rc)
         return rc;
     const int threads = plan.path == SGDRC_GEMV_MFMA ? kMfmaThreads : kGemvThreads;
     const uint32_t grid = gated_grid(c, kernel_occupancy(k, threads), plan.tiles, li);
-    hipLaunchKernelGGL(k, dim3(grid), dim3(threads), 0, reinterpret_cast<hipStream_t>(stream),
-                       static_cast<const uint8_t *>(w->pool), w->pt, w->pool_pages, M, K,
-                       static_cast<const uint8_t *>(d_x), batch, d_y, page_shift,
-                       (uint32_t)plan.tiles, g);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    hipLaunchKernelGGL(k, dim3(grid), dim3(threads), 0, s, static_cast<const uint8_t *>(w->pool),
+                       w->pt, w->pool_pages, M, K, static_cast<const uint8_t *>(d_x), batch, d_y,
+                       page_shift, (uint32_t)plan.tiles, g);
     SGDRC_HIP(hipGetLastError());
-    return SGDRC_OK;
+    return finish_static_tlog(g, s);
 }
 
 }  // extern "C"

@@ -50,6 +50,7 @@ struct StreamState {
     uint64_t ev_tiles = 0;
     int ev_per_cu = 1;
     uint32_t evict_at = 0;      // testing aid: the flag counts as raised from this tile (0 = off)
+    uint32_t last_schedule = 0; // schedule of the last launch: 0 ticket queues, 1 static
 };
 
 // What a gated launch needs besides the Gate itself.
@@ -67,6 +68,9 @@ struct Ctx {
     sgdrc_cu_mask all_cus{};
     int n_xcds = 0;
     int xcd_first_cu[kMaxXcds + 1] = {};  // logical CUs of XCD x: [first[x], first[x+1])
+    // the dispatcher hands workgroup i of a grid to the XCD of workgroup
+    // i mod n_xcds (checked by the topology probe); enables the static schedule
+    bool static_ok = false;
 
     uint32_t *d_lut = nullptr;           // kLutSize entries: logical CU | group << 16
     QueueSlot *d_queues = nullptr;       // kMaxStreams
@@ -126,7 +130,12 @@ int stream_state(Ctx *c, void *stream, StreamState **out);
 // stream's preemptible queue slot and eviction flag (the stream must have
 // eviction on).
 int make_gate(Ctx *c, void *stream, uint64_t n_tiles, int group_cus, Gate *g, LaunchInfo *li,
-              bool preemptible = false);
+              bool preemptible = false, bool allow_static = false);
+
+// After a launch with gate ``g`` on ``s``: if it ran the static schedule
+// with a time log, enqueues the reduction of its partial end stamps into
+// the log slot (k_tlog_reduce).
+int finish_static_tlog(const Gate &g, hipStream_t s);
 
 // CUs that the stream's mask allows (all CUs for a stream not seen yet).
 int stream_allowed_cus(Ctx *c, void *stream);

@@ -743,6 +743,80 @@ def test_gemv_bitwise_identical_across_cu_masks(ctx, orc):
             assert (y.view(np.uint32) == same[0].view(np.uint32)).all()
 
 
+@pytest.mark.parametrize("M,K,B", [(4096, 11008, 1), (11008, 4096, 8), (777, 2048, 2), (5, 64, 1)])
+def test_gemv_static_schedule_visits_each_tile_once(ctx, orc, M, K, B):
+    """Masks of whole XCDs (all CUs, the first 32/96/192 CUs, XCDs 1 and 6)
+    take the static schedule, any other mask the ticket queues: every tile is
+    taken exactly once, only by allowed CUs, and the output bits are the same
+    under every mask."""
+    n = ctx.num_cus
+    x_count = n // 32
+    shift = 21 if M * K * 2 >= (1 << 24) else 12
+    pool, pt, d_pool, d_pt, pool_pages = upload_w(orc, M, K, sg.BF16, shift, range(48), M + K,
+                                                  1, 6)
+    xb = x_bits(sg.BF16, B * K, M + 3)
+    d_x = to_dev(xb)
+    ref, absdot = orc.gemv(pool, pt, sg.BF16, M, K, xb, sg.BF16, B, shift)
+    stream = torch.cuda.current_stream()
+    masks = [(None, "static"), (range(32), "static"), (range(96), "static"),
+             (list(range(32, 64)) + list(range(192, 224)), "static"),
+             (range(100), "queue"), (synth.random_cu_subset(n, 37, seed=8), "queue")]
+    ys = []
+    for cus, want in masks:
+        cl_ = torch.zeros(n, dtype=torch.int32, device=DEV)
+        tiles_cap = M + 64
+        tl_ = torch.zeros(tiles_cap, dtype=torch.int32, device=DEV)
+        ctx.set_worklog(cl_, tl_)
+        try:
+            y = launch_gemv(ctx, d_pool, d_pt, pool_pages, M, K, B, sg.BF16, sg.BF16, d_x, shift, cus)
+            tiles = ctx.last_tiles(stream)
+            sched = ctx.last_schedule(stream)
+        finally:
+            ctx.set_worklog(None, None)
+        say(f"gemv {M}x{K} B={B} mask {'all' if cus is None else len(list(cus))}: {sched}, "
+            f"{tiles} tiles")
+        assert x_count != 8 or sched == want
+        cl, tl = to_host(cl_), to_host(tl_)
+        assert (tl[:tiles] == 1).all() and (tl[tiles:] == 0).all()
+        allowed = set(range(n)) if cus is None else set(cus)
+        assert set(np.nonzero(cl)[0].tolist()) <= allowed and cl.sum() == tiles
+        gemv_check(ctx, y, ref, absdot, M, K, B, sg.BF16, sg.BF16, cus, tag="sched")
+        ys.append(y)
+    for y in ys[1:]:
+        assert (y.view(np.uint32) == ys[0].view(np.uint32)).all()
+
+
+def test_gemv_timelog_static_schedule(ctx, orc):
+    """The time log of statically scheduled GEMVs: the end stamp is the
+    largest of the workgroups' partial stamps (reduced after each launch and
+    cleared), so every span is positive and within the host-event time."""
+    M, K = 4096, 11008
+    pool, pt, d_pool, d_pt, pool_pages = upload_w(orc, M, K, sg.BF16, 21, range(48), 1, 1, 6)
+    d_x = to_dev(x_bits(sg.BF16, K, 2))
+    d_y = torch.empty(M, dtype=torch.float32, device=DEV)
+    stream = torch.cuda.current_stream()
+    slots = torch.zeros(2 * 4, dtype=torch.int64, device=DEV)
+    khz = ctx.wallclock_khz
+    ctx.set_timelog(stream, slots)
+    spans = []
+    try:
+        for i in range(8):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            sg.colored_gemv(ctx, sg.paged(d_pool, d_pt, pool_pages), sg.BF16, M, K, d_x, sg.BF16,
+                            1, d_y, 21, stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            assert ctx.last_schedule(stream) == "static"
+            t = to_host(slots).astype(np.int64).reshape(4, 2)[i % 4]
+            span = (int(t[1]) - int(t[0])) / khz
+            spans.append(span)
+            assert 0 < span <= e0.elapsed_time(e1) + 0.01, (span, e0.elapsed_time(e1))
+    finally:
+        ctx.set_timelog(stream, None)
+    say(f"  static GEMV spans (us): {[round(x * 1e3, 1) for x in spans]}")
+
+
 # ------------------------------------------------------------- time log
 
 def test_timelog_brackets_each_launch(ctx):
