@@ -27,7 +27,7 @@ typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kGemvThreads = 256;
 constexpr int kGemvWaves = kGemvThreads / 64;
-constexpr int kGemvRowsMax = 8;  // rows per tile, vector-ALU path (at most)
+constexpr int kGemvRowsMax = 4;  // rows per tile, vector-ALU path (at most)
 constexpr int kMfmaRows = 16;    // rows per tile, MFMA path
 // MFMA path: 8 waves split K, so that a 16-row tile keeps twice the loads of
 // a 4-wave workgroup in flight (measured best of 4, 8 and 16 waves for both
@@ -438,16 +438,17 @@ static int dtype_size(int dt) { return dt == SGDRC_F32 ? 4 : 2; }
 
 // The launch plan of colored_gemv: which kernel, tile height and loads in
 // flight, decided from the shape and the number of CUs the mask allows.
-// Rows per tile and slices in flight for the vector-ALU path, by batch and
-// row length (measured on MI355X over the 4096x11008 and 11008x4096 bf16
-// layers): the choice keeps every lane busy in as few rounds as possible
-// and the tile count no larger than the workgroups the occupancy allows.
-// Batch 1 with long rows: when each allowed CU has few tiles (``few``) the
-// kernel is bound by the latency of a tile, and two-row tiles that load a
-// whole row of up to 24 KiB in one round (six 16-byte loads per lane)
-// finish sooner (one-tile launches 4.9 against 6.7 us, 4096 x 11008 on 192
-// CUs 23.4 against 24.2 us); with many tiles per CU, four-row tiles with
-// two rounds amortise the per-tile costs better (64 CUs: 45.2 against 47.1).
+// Vector-ALU path, measured on MI355X over the 4096x11008 and 11008x4096
+// bf16 layers under the static schedule (masks of 64..256 CUs, eight
+// rotated weight copies): four-row tiles, the whole row in flight per lane
+// where it fits (two 16-byte loads per lane and row for rows of 8 KiB,
+// three for longer ones), except batch 1 with long rows when each allowed CU
+// has few tiles (``few``): the kernel is then bound by the latency of one
+// tile, and two-row tiles that load a 22 KB row in one round (six loads per
+// lane) finish sooner (4096 x 11008 on 256 CUs 15.1 against 15.2 us, on 192
+// CUs 17.9 against 18.9 us); with many tiles per CU, four-row tiles win (64
+// CUs 38.4 against 42.2 us).  The row shape never changes a result: every
+// lane sums its own 16-byte slices in the same order whatever the tile.
 //
 // MFMA tile height by the rows of the busiest CU: 8-row tiles when they cut
 // its rows by a fifth or more (fewer tiles than CUs, or a last round that
@@ -476,26 +477,18 @@ static sgdrc_gemv_plan make_plan(uint32_t allowed, int w_dtype, uint32_t M, uint
         const uint64_t chunks = (kv + kMfmaChunkSlices - 1u) / kMfmaChunkSlices;
         p.sum_depth = (uint32_t)(chunks * (uint64_t)kMfmaStepsPerWave + 32u + (kMfmaWaves - 1));
     } else {
-        // rows of more than 512 slices of 16 bytes take two rounds of loads
+        // rows of more than 512 slices of 16 bytes take more than two
+        // loads per lane
         const bool long_rows = row_bytes > 512u * 16u;
         // at most six four-row tiles per allowed CU
         const bool few = (M + 3u) / 4u <= 6u * a;
         p.path = SGDRC_GEMV_VALU;
         p.batch_cols = batch <= 1 ? 1u : batch <= 2 ? 2u : batch <= 4 ? 4u : 8u;
-        if (batch <= 1) {
-            if (long_rows) {
-                p.rows = few ? 2u : 4u;
-                p.loads = few ? 6u : 4u;
-            } else {
-                p.rows = 8u;
-                p.loads = 2u;
-            }
-        } else if (batch <= 2) {
-            p.rows = 8u;
-            p.loads = long_rows ? 3u : 2u;
-        } else {
-            p.rows = 4u;
-            p.loads = 2u;
+        p.rows = 4u;
+        p.loads = long_rows && batch <= 2 ? 3u : 2u;
+        if (batch <= 1 && long_rows && few) {
+            p.rows = 2u;
+            p.loads = 6u;
         }
         // per output: each lane's FMA chain over its slices, the butterfly
         // over 64 lanes, then the 4 waves' partials
@@ -514,10 +507,10 @@ static GemvKernel valu_kernel(const sgdrc_gemv_plan &p)
     if (p.batch_cols == NB && p.rows == R && p.loads == U)                \
         return k_gemv_valu<WT, XT, NB, R, U>;
     SGDRC_VALU(1, 2, 6)
-    SGDRC_VALU(1, 4, 4)
-    SGDRC_VALU(1, 8, 2)
-    SGDRC_VALU(2, 8, 3)
-    SGDRC_VALU(2, 8, 2)
+    SGDRC_VALU(1, 4, 3)
+    SGDRC_VALU(1, 4, 2)
+    SGDRC_VALU(2, 4, 3)
+    SGDRC_VALU(2, 4, 2)
     SGDRC_VALU(4, 4, 2)
     SGDRC_VALU(8, 4, 2)
 #undef SGDRC_VALU
