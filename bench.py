@@ -401,6 +401,8 @@ def compact(result, full_path):
         c = rows["classify"]
         summ["classify_2e26"] = {"colours_us": _get(c, "colours_only", "median_us"),
                                  "hist_us": _get(c, "with_histogram", "median_us"),
+                                 "colours_span_us": _get(c, "colours_only", "kernel_span_p50_us"),
+                                 "hist_span_us": _get(c, "with_histogram", "kernel_span_p50_us"),
                                  "addrs_per_s": _get(c, "colours_only", "addrs_per_s"),
                                  "pct_hbm": _get(c, "colours_only", "pct_of_hbm_peak")}
     if "pagetable" in rows:
@@ -491,6 +493,11 @@ def bench_classify_one(torch, sg, synth, ctx, stream, timer, n, reps, hist, chec
     with torch.cuda.stream(stream):
         for _ in range(5):
             sg.colour_classify(ctx, masks, d_addrs, d_col, d_hist, stream)
+        dev = DevTimes(torch, ctx, stream, reps)
+        for _ in range(reps):
+            sg.colour_classify(ctx, masks, d_addrs, d_col, d_hist, stream)
+        spans = dev.close_us()
+        timer.reserve(2 * reps)
         for _ in range(reps):
             e0 = timer.start()
             sg.colour_classify(ctx, masks, d_addrs, d_col, d_hist, stream)
@@ -498,12 +505,18 @@ def bench_classify_one(torch, sg, synth, ctx, stream, timer, n, reps, hist, chec
         torch.cuda.synchronize()
     d = timer.durations_ms(tag)
     med = pctl(d, 50)
+    span = pctl(list(spans), 50)
     gbs = 9 * n / (med * 1e-3) / 1e9
-    log(f"classify (histogram {hist}): {med * 1e3:.1f} us  {gbs:.0f} GB/s")
+    log(f"classify (histogram {hist}): {med * 1e3:.1f} us with launch, kernel span {span:.1f} us, "
+        f"{gbs:.0f} GB/s")
     checks["classify_colours"] = d_col[:1 << 22].cpu().numpy()
     return {"what": "2^26 random 4 KiB-aligned addresses, 6 masks"
                     + (", colours + histogram" if hist else ", colours"),
             "median_us": round(med * 1e3, 2), "p99_us": round(pctl(d, 99) * 1e3, 2),
+            "kernel_span_p50_us": round(span, 2), "kernel_span_p99_us": round(pctl(list(spans), 99), 2),
+            "timing": "median_us/p99_us: host events around each call (launch overhead, and the "
+                      "finishing kernel of a statically scheduled launch, included); kernel_span: "
+                      "device time log of the main kernel",
             "addrs_per_s": round(n / (med * 1e-3), 0), "GBps": round(gbs, 1),
             "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1), "bytes_per_addr": 9}
 

@@ -4,9 +4,9 @@
 // classify kernel hands out tiles to single wavefronts.  A wavefront
 // streams its tile's 8-byte addresses through buffer loads, each
 // instruction reading 1 KiB of consecutive addresses and each lane keeping
-// 16 such loads (32 addresses) in flight, colours them by table lookups
+// 8 such loads (16 addresses) in flight, colours them by table lookups
 // (the hash is linear over GF(2)), and writes one colour byte per address:
-// it passes its tile's 2048 colour bytes through its own 2 KiB of LDS so
+// it passes its tile's 1024 colour bytes through its own 1 KiB of LDS so
 // that each lane stores 16 consecutive colours per 16-byte store.  Tiles
 // cover the largest multiple of 16 addresses, through buffer ranges that end
 // there (so the tile body has no branch around its memory accesses); the
@@ -78,21 +78,40 @@ __device__ __forceinline__ uint32_t table_colour(const TableArgs &t, uint64_t a)
 }
 
 constexpr int kClsThreads = 256;
-constexpr int kClsLoads = 16;                            // 16-byte loads per lane per tile
-constexpr uint32_t kClsWaveTile = 64u * 2u * kClsLoads;  // 2048 addresses per wavefront
+constexpr int kClsLoads = 8;                             // 16-byte loads per lane per tile
+constexpr uint32_t kClsWaveTile = 64u * 2u * kClsLoads;  // 1024 addresses per wavefront
 constexpr uint32_t kClsWaves = kClsThreads / 64;
-// Each wavefront takes its own tiles of kClsWaveTile addresses (32,768
-// tickets for 2^26 addresses), so the work queues serve runs of 8 CUs: one
-// device-wide counter serialises its atomics at about 12 ns each.
+// Each wavefront takes its own tiles of kClsWaveTile addresses; under a mask
+// of whole XCDs by the static schedule, otherwise through work queues of 8
+// CUs (one device-wide counter serialises its atomics at about 12 ns each).
 constexpr int kClsGroupCus = 8;
-// Workgroups per CU: one, with or without the histogram (two or more, or
-// 32 or 8 loads per lane, measured slower on MI355X).
-constexpr int kClsWgsPerCu = 1;
-constexpr int kClsHistWgsPerCu = 1;
+// Two workgroups per CU with eight loads per lane: 2^26 addresses in
+// 95-96 us (static) or 100 us (queues) on MI355X, against 105-125 us for one
+// workgroup with 16 or 32 loads, or three with 8.
+constexpr int kClsWgsPerCu = 2;
+constexpr int kClsHistWgsPerCu = 2;
 
 // Histogram bins are replicated 16 times in LDS (copy = lane % 16) so that
 // the LDS atomics of one wavefront rarely meet on one address.
 constexpr int kHistCopies = 16;
+
+// hist_out[b] = the sum of bin b over the kHistAccCopies accumulator copies,
+// which are cleared for the next launch (every thread of one workgroup).
+template <uint32_t kBins>
+__device__ __forceinline__ void publish_histogram(uint64_t *hist_acc, uint64_t *hist_out)
+{
+    for (uint32_t b = threadIdx.x; b < kBins; b += blockDim.x) {
+        uint64_t v = 0;
+#pragma unroll
+        for (int r = 0; r < kHistAccCopies; ++r) {
+            v += __hip_atomic_load(&hist_acc[r * kHistBins + b], __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&hist_acc[r * kHistBins + b], (uint64_t)0, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
+        hist_out[b] = v;
+    }
+}
 
 // TAB: colours come from a colour table in device memory (one gathered
 // byte per address) instead of the XOR hash; K is then 8 (256 bins).
@@ -161,6 +180,9 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
     };
     auto flush = [&]() {
         if (HIST) {
+            uint32_t xcc;
+            asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+            uint64_t *acc = hist_acc + (xcc % (uint32_t)kHistAccCopies) * kHistBins;
             __syncthreads();
             for (uint32_t b = threadIdx.x; b < kBins; b += kClsThreads) {
                 uint32_t v = 0;
@@ -170,7 +192,7 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
                     s_hist[b * kHistCopies + r] = 0;
                 }
                 if (v)
-                    __hip_atomic_fetch_add(&hist_acc[b], (uint64_t)v, __ATOMIC_RELAXED,
+                    __hip_atomic_fetch_add(&acc[b], (uint64_t)v, __ATOMIC_RELAXED,
                                            __HIP_MEMORY_SCOPE_AGENT);
             }
         }
@@ -191,13 +213,7 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
         if (HIST) {
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
-            for (uint32_t b = threadIdx.x; b < kBins; b += kClsThreads) {
-                const uint64_t v = __hip_atomic_load(&hist_acc[b], __ATOMIC_RELAXED,
-                                                     __HIP_MEMORY_SCOPE_AGENT);
-                hist_out[b] = v;
-                __hip_atomic_store(&hist_acc[b], (uint64_t)0, __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
-            }
+            publish_histogram<kBins>(hist_acc, hist_out);
         }
     };
     // the byte tables, visible to the whole workgroup after the loop's
@@ -213,7 +229,35 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
             s_lut[t][e] = (uint8_t)colour_of<K>((uint32_t)a, (uint32_t)(a >> 32), h);
         }
     };
-    gated_wave_loop(g, n_tiles, prologue, body, flush, epilogue);
+    if (g.statics)
+        static_wave_loop(g, n_tiles, prologue, body, flush);
+    else
+        gated_wave_loop(g, n_tiles, prologue, body, flush, epilogue);
+}
+
+// After a statically scheduled classify (one workgroup, stream-ordered
+// after it): colour the last n mod 16 addresses and publish the histogram
+// the workgroups accumulated in hist_acc, clearing it for the next launch.
+template <int K, bool HIST, bool TAB>
+__global__ __launch_bounds__(kClsThreads) void k_classify_finish(const uint64_t *__restrict__ addrs,
+                                                                 uint64_t n, uint8_t *__restrict__ colours,
+                                                                 HashArgs h, TableArgs tab,
+                                                                 uint64_t *hist_acc, uint64_t *hist_out)
+{
+    constexpr uint32_t kBins = 1u << K;
+    const uint64_t i = (n & ~15ull) + threadIdx.x;
+    if (i < n) {
+        const uint64_t a = addrs[i];
+        const uint32_t c = TAB ? table_colour(tab, a) : colour_of<K>((uint32_t)a, (uint32_t)(a >> 32), h);
+        colours[i] = (uint8_t)c;
+        if (HIST)
+            __hip_atomic_fetch_add(&hist_acc[c], (uint64_t)1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (HIST) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        publish_histogram<kBins>(hist_acc, hist_out);
+    }
 }
 
 constexpr int kPtThreads = 256;
@@ -353,10 +397,10 @@ static int launch_classify(Ctx *c, const HashArgs &h, const TableArgs &tab,
     const uint64_t wg_tiles = (n_tiles + kClsWaves - 1) / kClsWaves;
     Gate g;
     LaunchInfo li;
-    int rc = make_gate(c, stream, n_tiles, kClsGroupCus, &g, &li);
+    int rc = make_gate(c, stream, n_tiles, kClsGroupCus, &g, &li, false, true);
     if (rc)
         return rc;
-    uint64_t *acc = c->d_hist_acc + (size_t)(g.q - c->d_queues) * kHistBins;
+    uint64_t *acc = c->d_hist_acc + (size_t)(g.q - c->d_queues) * kHistAccCopies * kHistBins;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (d_hist) {
         static const int occ = occupancy(k_classify<K, true, TAB>, kClsThreads);
@@ -370,7 +414,18 @@ static int launch_classify(Ctx *c, const HashArgs &h, const TableArgs &tab,
                            d_addrs, n, d_colours, h, tab, acc, d_hist, (uint32_t)n_tiles, g);
     }
     SGDRC_HIP(hipGetLastError());
-    return SGDRC_OK;
+    if (g.statics) {
+        // the statically scheduled grid has no last workgroup: the tail and
+        // the histogram's publication follow in a kernel of their own
+        if (d_hist)
+            hipLaunchKernelGGL((k_classify_finish<K, true, TAB>), dim3(1), dim3(kClsThreads), 0, s,
+                               d_addrs, n, d_colours, h, tab, acc, d_hist);
+        else if (n & 15u)
+            hipLaunchKernelGGL((k_classify_finish<K, false, TAB>), dim3(1), dim3(kClsThreads), 0, s,
+                               d_addrs, n, d_colours, h, tab, acc, d_hist);
+        SGDRC_HIP(hipGetLastError());
+    }
+    return finish_static_tlog(g, s);
 }
 
 template <int K>

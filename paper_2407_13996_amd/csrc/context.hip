@@ -492,8 +492,10 @@ int sgdrc_init(int device, sgdrc_ctx **out)
     TRY(hipMalloc(&c->d_lut, kLutSize * sizeof(uint32_t)));
     TRY(hipMalloc(&c->d_queues, kMaxStreams * sizeof(QueueSlot)));
     TRY(hipMemset(c->d_queues, 0, kMaxStreams * sizeof(QueueSlot)));
-    TRY(hipMalloc(&c->d_hist_acc, (size_t)kMaxStreams * kHistBins * sizeof(uint64_t)));
-    TRY(hipMemset(c->d_hist_acc, 0, (size_t)kMaxStreams * kHistBins * sizeof(uint64_t)));
+    TRY(hipMalloc(&c->d_hist_acc,
+                  (size_t)kMaxStreams * kHistAccCopies * kHistBins * sizeof(uint64_t)));
+    TRY(hipMemset(c->d_hist_acc, 0,
+                  (size_t)kMaxStreams * kHistAccCopies * kHistBins * sizeof(uint64_t)));
     TRY(hipMalloc(&c->d_err, sizeof(uint32_t)));
     TRY(hipMemset(c->d_err, 0, sizeof(uint32_t)));
     TRY(hipHostMalloc(&c->h_pinned, 8 * sizeof(uint64_t), hipHostMallocDefault));

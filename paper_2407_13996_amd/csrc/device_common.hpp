@@ -808,6 +808,49 @@ __device__ __forceinline__ void gated_wave_loop(const Gate &g, uint32_t n_tiles,
         raise_flag(g.err, err);
 }
 
+// Static form of gated_wave_loop, for masks made of whole XCDs (g.statics,
+// as static_tile_loop): the workers are the wavefronts, numbered so that the
+// waves of one workgroup take consecutive tiles, and wave v of the W
+// workers takes tiles v, v + W, ...  ``flush`` runs once the workgroup's
+// waves are done; there is no last workgroup, so no epilogue: the host
+// enqueues whatever must follow the whole grid as a kernel of its own.
+template <typename Prologue, typename Body, typename Flush>
+__device__ __forceinline__ void static_wave_loop(const Gate &g, uint32_t n_tiles, Prologue prologue,
+                                                 Body body, Flush flush)
+{
+    uint32_t xcc;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+    const uint32_t a = g.xcd_rank[xcc & 0xFu];
+    const uint32_t cu = g.log_cu ? (my_cu_entry(g) & 0xFFFFu) : (uint32_t)kMaxCus;
+    prologue();
+    if (g.tlog && blockIdx.x == 0 && threadIdx.x == 0)
+        __hip_atomic_store(&g.tlog[0], __builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    uint32_t err = 0u;
+    if (a != 0xFFu) {
+        const uint32_t waves = blockDim.x >> 6;
+        const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        const uint32_t workers = (gridDim.x / g.n_xcd) * g.n_allowed_xcd * waves;
+        for (uint32_t t = ((blockIdx.x / g.n_xcd) * g.n_allowed_xcd + a) * waves + wave; t < n_tiles;
+             t += workers) {
+            log_tile_wave(g, cu, t);
+            body(t, cu, err, NoOp());
+        }
+        flush();
+    }
+    if (g.tlog) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (threadIdx.x == 0)
+            __hip_atomic_fetch_max(&g.q->tpart[(blockIdx.x % kTimePartials) * (kCounterStride / 2)],
+                                   (uint64_t)__builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (err != 0u)
+        raise_flag(g.err, err);
+}
+
 // Page-table lookup with the range check every kernel applies: an entry
 // outside the pool yields kBadPage and sets kDevErrPtRange in ``err``.
 __device__ __forceinline__ uint32_t checked_page(const uint32_t *pt, uint64_t j,

@@ -20,6 +20,10 @@ namespace sgdrc {
 constexpr uint32_t kCtxMagic = 0x53474452u;  // "SGDR"
 constexpr int kMaxStreams = 64;
 constexpr int kHistBins = 256;
+// Copies of each stream's histogram accumulators in device memory: a
+// workgroup adds its counts to the copy of its XCD, so that the workgroups'
+// device-scope atomics spread over eight addresses per bin.
+constexpr int kHistAccCopies = 8;
 // CUs served by one work queue.  Long streaming kernels use one queue for
 // the whole device (0): tiles are then taken in address order by all CUs
 // together, which measured faster on MI355X than splitting the address range
@@ -74,7 +78,7 @@ struct Ctx {
 
     uint32_t *d_lut = nullptr;           // kLutSize entries: logical CU | group << 16
     QueueSlot *d_queues = nullptr;       // kMaxStreams
-    uint64_t *d_hist_acc = nullptr;      // kMaxStreams x kHistBins
+    uint64_t *d_hist_acc = nullptr;      // kMaxStreams x kHistAccCopies x kHistBins
     uint32_t *d_err = nullptr;           // one word
 
     void *d_scratch = nullptr;           // page-table build scratch, sized for the largest pool

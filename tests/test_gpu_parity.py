@@ -895,7 +895,7 @@ def test_cu_mask_confines_work_and_visits_each_tile_once(ctx, orc):
 
 
 def test_classify_wavefront_tiles_under_cu_masks(ctx, orc):
-    """Classify hands its tiles (2048 addresses) to single wavefronts: under
+    """Classify hands its tiles (1024 addresses) to single wavefronts: under
     every mask each tile is taken once, only allowed CUs work, and colours
     and histogram equal the oracle's."""
     n_cu = ctx.num_cus
@@ -905,7 +905,7 @@ def test_classify_wavefront_tiles_under_cu_masks(ctx, orc):
     ref, ref_hist = orc.classify(addrs, masks)
     d_addrs = to_dev(addrs)
     stream = torch.cuda.current_stream()
-    tiles_expected = (n & ~15) // 2048 + (1 if (n & ~15) % 2048 else 0)
+    tiles_expected = (n & ~15) // 1024 + (1 if (n & ~15) % 1024 else 0)
     for cus in [list(range(64)), synth.random_cu_subset(n_cu, 20, seed=8), [5], [n_cu - 1],
                 list(range(n_cu))]:
         say(f"classify under a mask of {len(cus)} CUs")
