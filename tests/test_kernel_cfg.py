@@ -13,25 +13,13 @@ shows by closing it with a scalar branch (on SCC or VCC, never on EXEC).
 This test compiles every source to gfx950 assembly and checks, for every
 barrier at loop depth 2 or more, the back-edges of the inner loops around it.
 """
-import os
 import re
-import subprocess
 
 import pytest
 
-ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-CSRC = os.path.join(ROOT, "paper_2407_13996_amd", "csrc")
+from kernel_asm import device_asm
+
 SOURCES = ["stream.hip", "gemv.hip", "colour.hip", "context.hip"]
-
-
-def device_asm(src: str, tmp_path) -> str:
-    """gfx950 assembly of one source, compiled with the library's own flags."""
-    from paper_2407_13996_amd import build as B
-    out = tmp_path / (os.path.splitext(src)[0] + ".s")
-    flags = [f for f in B.CFLAGS if f not in ("-fPIC", "-Wall")]
-    cmd = [B.HIPCC, *flags, "--cuda-device-only", "-S", os.path.join(CSRC, src), "-o", str(out)]
-    subprocess.run(cmd, check=True, capture_output=True)
-    return out.read_text()
 
 
 def barrier_depths(asm: str):
@@ -88,8 +76,8 @@ def divergent_barrier_loops(asm: str):
 
 
 @pytest.mark.parametrize("src", SOURCES)
-def test_no_barrier_in_divergent_loop(src, tmp_path):
-    asm = device_asm(src, tmp_path)
+def test_no_barrier_in_divergent_loop(src):
+    asm = device_asm(src)
     found = list(barrier_depths(asm))
     if src != "context.hip":
         assert found, "expected barriers in the persistent kernels"
