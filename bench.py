@@ -50,8 +50,9 @@ def parse():
     ap.add_argument("--corun-launches", type=int, default=2000)
     ap.add_argument("--preempt-trials", type=int, default=40)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--full-out", default=os.path.join(ROOT, "gpurun_out", "bench_full.json"),
-                    help="file for the full result (every row); stdout gets a compact line")
+    ap.add_argument("--full-out", default="",
+                    help="file for the full result (every row); without it the full result goes "
+                         "to stderr as one JSON line; stdout gets a compact line")
     return ap.parse_args()
 
 
@@ -355,15 +356,19 @@ def main():
     for v in flags.values():
         result["device_error_flags"] |= v
     ctx.close()
-    full_path = args.full_out
-    try:
-        os.makedirs(os.path.dirname(os.path.abspath(full_path)), exist_ok=True)
-        with open(full_path, "w") as f:
-            json.dump(result, f, indent=1)
-        log(f"full result written to {full_path}")
-    except OSError as e:
-        log(f"could not write {full_path}: {e}")
-    line = json.dumps(compact(result, full_path))
+    full_path = args.full_out or "stderr"
+    if args.full_out:
+        try:
+            os.makedirs(os.path.dirname(os.path.abspath(full_path)), exist_ok=True)
+            with open(full_path, "w") as f:
+                json.dump(result, f, indent=1)
+            log(f"full result written to {full_path}")
+        except OSError as e:
+            log(f"could not write {full_path}: {e}")
+            args.full_out = ""
+    if not args.full_out:
+        log("full result: " + json.dumps(result))
+    line = json.dumps(compact(result, full_path if args.full_out else "stderr"))
     print(line, flush=True)
 
 
@@ -462,7 +467,7 @@ def compact(result, full_path):
         summ["probe_placement_GBps"] = {f"{p['page_KiB']}K {p['pages']}": p["GBps"]
                                         for p in pb.get("placement", [])}
     out["rows_summary"] = summ
-    out["rows_full"] = os.path.relpath(full_path, ROOT) if full_path else None
+    out["rows_full"] = os.path.relpath(full_path, ROOT) if full_path != "stderr" else "stderr"
     text = json.dumps(out)
     if len(text) > 8000:       # drop the widest parts first
         for k in ("sectors_triad_GBps", "probe_placement_GBps", "xcd_triad_GBps", "bimodal"):

@@ -20,3 +20,20 @@ def orc():
     import oracle
     oracle.lib()
     return oracle
+
+
+def pytest_terminal_summary(terminalreporter):
+    """Report the GEMV parity tests' observed error against the bound of the
+    kernel's summation tree (largest |y - ref| / sum|W x| per case)."""
+    log = None
+    for name, mod in list(sys.modules.items()):
+        if name.rsplit(".", 1)[-1] == "test_gpu_parity":
+            log = getattr(mod, "ERR_LOG", None)
+    if not log:
+        return
+    tr = terminalreporter
+    worst = max(r / (2 * d * 2.0 ** -24) for r, d in log.values())
+    tr.write_line(f"GEMV error: {len(log)} checks; largest observed error / bound = {worst:.3f}")
+    for (M, K, B, wd, xd, n, tag), (r, d) in sorted(log.items(), key=lambda kv: str(kv[0])):
+        tr.write_line(f"  {M}x{K} B={B} w={wd} x={xd} cus={n} {tag}: max|err|/sum|Wx| = {r:.3g}, "
+                      f"bound {2 * d * 2.0 ** -24:.3g} (depth {d})")
