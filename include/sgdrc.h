@@ -19,8 +19,17 @@
  *    The caller owns every buffer it passes and keeps it alive until the
  *    enqueued work is done.  The library owns only its context workspace.
  *  - ``stream`` is a hipStream_t handle (NULL = the legacy default stream).
- *    Every operation is asynchronous on that stream except
- *    colour_alloc_pagetable, which returns after its work has finished.
+ *    Every operation is asynchronous on that stream except those documented
+ *    as waiting: colour_alloc_pagetable and colour_alloc_pagetable_table
+ *    (they return the count to the host), sgdrc_suspended,
+ *    sgdrc_stream_release, sgdrc_device_error, sgdrc_init and
+ *    sgdrc_destroy.
+ *  - colour_classify, colour_classify_table, colour_alloc_pagetable_noalloc,
+ *    bimodal_relayout, bimodal_relayout_batch, colored_stream and
+ *    colored_gemv enqueue kernels only (no memset, copy or host wait), and
+ *    every per-launch value travels in the kernel arguments, so they may be
+ *    captured into a HIP graph and replayed, except on a stream with an
+ *    eviction flag (preemptible launches are resumed from the host).
  *  - Page tables are arrays of uint32 pool-page indices.  Logical byte b of
  *    a paged tensor lives at pool + pt[b >> page_shift] * 2^page_shift +
  *    (b & (2^page_shift - 1)).  Kernels check every page-table entry
@@ -31,10 +40,13 @@
  *    threads; operations on one stream are ordered, operations on different
  *    streams may run concurrently (each stream gets its own work queue).
  *  - CU masks (set_cu_mask) confine every tile of work to the allowed CUs.
- *    The grid's last workgroup, which may sit on any CU, also handles a
- *    launch's remainder below the 16-byte access granularity (the last
+ *    A launch's remainder below the 16-byte access granularity (the last
  *    n mod 16 bytes of a relayout or triad, the last n mod 16 addresses of
- *    a classify) and any tiles left if no workgroup reached an allowed CU.
+ *    a classify) and, on the ticket queues, any tiles left if no workgroup
+ *    reached an allowed CU are handled by the grid's last workgroup, which
+ *    may sit on any CU; under the static schedule (see set_cu_mask) a
+ *    classify's remainder and histogram total are produced by a
+ *    one-workgroup kernel enqueued right after the grid, also on any CU.
  */
 #ifndef SGDRC_H
 #define SGDRC_H
@@ -136,9 +148,10 @@ int sgdrc_last_tiles(sgdrc_ctx *ctx, void *stream, uint64_t *tiles);
 
 /* How the last launch enqueued on ``stream`` distributed its tiles:
  * SGDRC_SCHED_QUEUE (atomic ticket queues per group of CUs, with stealing)
- * or SGDRC_SCHED_STATIC (colored_gemv under a mask made of whole XCDs: each
- * workgroup derives its tiles from its XCD and index, no atomics).  For
- * tests and tools. */
+ * or SGDRC_SCHED_STATIC (colored_gemv, colour_classify and
+ * colour_classify_table under a mask made of whole XCDs: each workgroup
+ * derives its tiles from its XCD and index, no atomics).  For tests and
+ * tools. */
 enum { SGDRC_SCHED_QUEUE = 0, SGDRC_SCHED_STATIC = 1 };
 int sgdrc_last_schedule(sgdrc_ctx *ctx, void *stream, uint32_t *schedule);
 
@@ -147,7 +160,9 @@ int sgdrc_last_schedule(sgdrc_ctx *ctx, void *stream, uint32_t *schedule);
  * colour_classify, bimodal_relayout, colored_stream or colored_gemv writes
  * two uint64 ticks of the device wall clock to d_slots[2*(i % n_slots)]:
  * the time workgroup 0 (the first one dispatched) started and the time the
- * last workgroup finished.  d_slots: device memory, 2 * n_slots entries,
+ * last workgroup finished.  (Under the static schedule every workgroup
+ * records its end in one of 64 partial stamps and a one-wavefront kernel
+ * enqueued after the grid writes their maximum.)  d_slots: device memory, 2 * n_slots entries,
  * 8-byte aligned, owned by the caller.  d_slots == NULL switches the log
  * off.  Host-only.  EINVAL: n_slots == 0 with d_slots != NULL, misaligned
  * slots. */
@@ -173,8 +188,9 @@ int sgdrc_set_stream_occupancy(sgdrc_ctx *ctx, void *stream, uint32_t max_wgs_pe
  * set used by every later launch on ``stream``: each workgroup reads its
  * CU identity from the hardware registers and exits unless that CU is in
  * the set; the remaining workgroups take tiles from an atomic queue until it
- * is empty.  A colored_gemv under a mask made of whole XCDs (the usual
- * case: all CUs, or n x 32 CUs) needs no queue: the hardware hands
+ * is empty.  A colored_gemv or colour_classify under a mask made of whole
+ * XCDs (the usual case: all CUs, or n x 32 CUs) needs no queue: the
+ * hardware hands
  * workgroup i of a grid to the XCD of workgroup i mod (XCD count), which
  * sgdrc_init checks, so a workgroup on an allowed XCD derives its tiles from
  * its XCD and index alone (SGDRC_SCHED_STATIC).  mask == NULL restores all CUs.  Host-only, takes effect at the
@@ -403,7 +419,7 @@ int colored_stream(sgdrc_ctx *ctx, const sgdrc_paged *a, const sgdrc_paged *b,
  * only on (M, K, batch, dtypes), never on the CU mask, so results are
  * bitwise reproducible.  EINVAL: batch outside 1..8, M or K zero, K *
  * esize(w_dtype) not a multiple of 16, x of 4 GiB or more, a tile's rows
- * (8, or 16 on MFMA) spanning more pages than one tile may stage, unknown
+ * (4, or 16 on MFMA) spanning more pages than one tile stages (256), unknown
  * dtype, NULL pointers, unaligned pointers. */
 int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, uint32_t K,
                  const void *d_x, int x_dtype, uint32_t batch, float *d_y,
