@@ -34,7 +34,10 @@ CONFIG1 = [(1024, 1024, 1, F32, F32, 16, None)]
 # MFMA 8-row tiles: (M, K, batch, allowed CUs, dtype); each also runs with
 # one CU per 16-row tile
 HALF_TILES = [(203, 3000, 8, 10, BF16), (4096, 11008, 4, 192, BF16), (37, 11008, 3, [1, 2], BF16),
-              (203, 3000, 5, 10, F16)]
+              (203, 3000, 5, 10, F16),
+              # 2, 4 and 8 chunks per row, several 8-row tiles per workgroup
+              (1040, 4096, 8, 64, BF16), (1040, 4096, 4, 64, BF16), (520, 2048, 8, 32, BF16),
+              (1040, 8192, 8, 64, BF16), (1040, 4096, 8, 64, F16)]
 MASKS_777 = [(777, 2048, B, BF16, BF16, 16, cus) for B in (1, 8) for cus in (None, 64, 128, 37)]
 C4_LS = [(4096, 11008, 1, BF16, BF16, 21, 192)]
 

@@ -895,9 +895,10 @@ def test_cu_mask_confines_work_and_visits_each_tile_once(ctx, orc):
 
 
 def test_classify_wavefront_tiles_under_cu_masks(ctx, orc):
-    """Classify hands its tiles (1024 addresses) to single wavefronts: under
-    every mask each tile is taken once, only allowed CUs work, and colours
-    and histogram equal the oracle's."""
+    """Classify hands its tiles (1024 addresses) to single wavefronts, by the
+    static schedule under masks of whole XCDs (adjacent or not) and through
+    the ticket queues otherwise: under every mask each tile is taken once,
+    only allowed CUs work, and colours and histogram equal the oracle's."""
     n_cu = ctx.num_cus
     n = (1 << 20) + 37
     masks = synth.xor_masks(6, seed=5, min_bit=12)
@@ -906,8 +907,10 @@ def test_classify_wavefront_tiles_under_cu_masks(ctx, orc):
     d_addrs = to_dev(addrs)
     stream = torch.cuda.current_stream()
     tiles_expected = (n & ~15) // 1024 + (1 if (n & ~15) % 1024 else 0)
-    for cus in [list(range(64)), synth.random_cu_subset(n_cu, 20, seed=8), [5], [n_cu - 1],
-                list(range(n_cu))]:
+    whole_xcds = n_cu == 256   # masks of whole XCDs take the static schedule
+    for cus, want in [(list(range(64)), "static"), (synth.random_cu_subset(n_cu, 20, seed=8), "queue"),
+                      ([5], "queue"), ([n_cu - 1], "queue"), (list(range(n_cu)), "static"),
+                      (list(range(32, 64)) + list(range(192, 224)), "static")]:
         say(f"classify under a mask of {len(cus)} CUs")
         d_col = torch.full((n + 16,), 0xEE, dtype=torch.uint8, device=DEV)
         d_hist = torch.zeros(64, dtype=torch.int64, device=DEV)
@@ -917,10 +920,12 @@ def test_classify_wavefront_tiles_under_cu_masks(ctx, orc):
         sg.set_cu_mask(ctx, stream, cus)
         sg.colour_classify(ctx, masks, d_addrs, d_col, d_hist, stream)
         tiles = ctx.last_tiles(stream)
+        sched = ctx.last_schedule(stream)
         ctx.set_worklog(None, None)
         sg.set_cu_mask(ctx, stream, None)
         cl, tl = to_host(cu_log), to_host(tile_log)
         assert tiles == tiles_expected
+        assert not whole_xcds or sched == want, (len(cus), sched)
         assert (tl[:tiles] == 1).all() and (tl[tiles:] == 0).all()
         assert set(np.nonzero(cl)[0].tolist()) <= set(cus)
         assert cl.sum() == tiles
