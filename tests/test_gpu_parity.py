@@ -952,6 +952,32 @@ def test_out_of_range_page_entry_is_flagged_not_accessed(ctx):
     assert ctx.device_error() == 0
 
 
+@pytest.mark.parametrize("shift,B", [(21, 1), (21, 8), (12, 1), (12, 8)])
+def test_gemv_out_of_range_page_entry_is_flagged_not_accessed(ctx, orc, shift, B):
+    """A W page-table entry beyond the pool: the GEMV reads none of that
+    page (its bytes count as zero), raises the range flag, and every output
+    equals the oracle's on a copy of W with that page zeroed.  With 2 MiB
+    pages every tile lies inside one page (on the MFMA path: a buffer
+    resource per row, of length zero for the bad page); with 4 KiB pages a
+    tile spans many (a table read per load).  Batch 1 takes the vector
+    path, batch 8 the MFMA path."""
+    M, K, wd = 1024, 4096, sg.BF16
+    say(f"gemv bad page entry: {1 << (shift - 10)} KiB pages, B={B}")
+    pool, pt, d_pool, d_pt, pool_pages = upload_w(orc, M, K, wd, shift, range(48), M + B, 1, 6)
+    n_pages = -(-M * K * 2 // (1 << shift))
+    k = n_pages // 2
+    bad = d_pt.clone()
+    bad[k] = pool_pages + 100
+    xb = x_bits(wd, B * K, 11)
+    assert ctx.device_error() == 0
+    y = launch_gemv(ctx, d_pool, bad, pool_pages, M, K, B, wd, wd, to_dev(xb), shift, None)
+    assert ctx.device_error() == sg.DEVERR_PT_RANGE
+    zeroed = pool.copy()
+    zeroed.reshape(pool_pages, 1 << shift)[int(pt[k])] = 0
+    ref, absdot = orc.gemv(zeroed, pt, wd, M, K, xb, wd, B, shift)
+    gemv_check(ctx, y, ref, absdot, M, K, B, wd, wd, None, tag="bad page")
+
+
 def test_two_streams_disjoint_masks_run_concurrently(ctx, orc):
     """A GEMV stream on CUs 0..3/4 and a triad stream on the rest, launched
     back to back so that they overlap; both results match the oracle and no
