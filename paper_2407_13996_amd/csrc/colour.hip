@@ -176,7 +176,7 @@ __global__ __launch_bounds__(kClsThreads) void k_classify(const uint64_t *__rest
         const Rsrc rc = make_rsrc(colours + base, valid);
 #pragma unroll
         for (int q = 0; q < kClsLoads / 8; ++q)
-            buf_store_nt(rc, q * 1024u + lane * 16u, out[q]);
+            buf_store_sc1(rc, q * 1024u + lane * 16u, out[q]);
     };
     auto flush = [&]() {
         if (HIST) {

@@ -875,6 +875,12 @@ constexpr int kAuxNt = 2;  // cache policy: non-temporal
 // than left dirty in it); measured 1.5-2.5 percent faster than non-temporal
 // alone for the triad and the relayout on MI355X, SC1 alone no faster.
 constexpr int kAuxStore = 16 | kAuxNt;
+// Classify's colour stores: SC1 without the non-temporal bit.  Its stores
+// are one byte per eight bytes read, and with NT they cost 5-6 percent of
+// the kernel (2^26 addresses on MI355X: 102.3 against 96.7 us, with
+// histogram 105 against 99; SC0+SC1 the same as SC1, cached stores or NT
+// alone 98.7-98.8 us).
+constexpr int kAuxStoreSc1 = 16;
 
 __device__ __forceinline__ Rsrc make_rsrc(const void *base, uint32_t bytes)
 {
@@ -890,6 +896,11 @@ __device__ __forceinline__ u32x4 buf_load_nt(Rsrc r, uint32_t off)
 __device__ __forceinline__ void buf_store_nt(Rsrc r, uint32_t off, u32x4 v)
 {
     __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, v), r, off, 0, kAuxStore);
+}
+
+__device__ __forceinline__ void buf_store_sc1(Rsrc r, uint32_t off, u32x4 v)
+{
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, v), r, off, 0, kAuxStoreSc1);
 }
 
 __device__ __forceinline__ u32x4 load_nt(const void *p)
