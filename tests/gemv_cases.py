@@ -30,6 +30,12 @@ SECTORS = [(300, 1024, B, BF16, BF16, shift, None) for shift, B in
            [(10, 1), (10, 8), (11, 2), (11, 5)]]
 SINGLE_ROWS = [(M, K, B, BF16, BF16, 16, None) for M, K, B in
                [(1, 11008, 1), (1, 11008, 8), (1, 8, 1), (1, 8, 4), (2, 4096, 3)]]
+# 2 MiB pages with tiles on both sides of a page end and a ragged last
+# tile: 1100 x 2000 bf16 spans three pages; with all CUs the MFMA path takes
+# 8-row tiles (tile 65 straddles the first page end), on 40 CUs 16-row
+# tiles (tile 32 straddles it)
+PAGE_EDGES = [(1100, 2000, B, BF16, BF16, 21, None) for B in (1, 4, 8)] + \
+    [(1100, 2000, 8, BF16, BF16, 21, 40)]
 CONFIG1 = [(1024, 1024, 1, F32, F32, 16, None)]
 # MFMA 8-row tiles: (M, K, batch, allowed CUs, dtype); each also runs with
 # one CU per 16-row tile
@@ -45,6 +51,7 @@ C4_LS = [(4096, 11008, 1, BF16, BF16, 21, 192)]
 def gpu_cases():
     """Every (shape, mask size) a GPU test launches the GEMV with."""
     cases = RAGGED + DTYPE_MIX + STAGING + MFMA_CHUNKS + LONG_ROWS + SECTORS + SINGLE_ROWS
+    cases += PAGE_EDGES
     cases += CONFIG1 + C4_LS + MASKS_777
     for M, K, B, cus, dt in HALF_TILES:
         n = cus if isinstance(cus, int) else len(cus)

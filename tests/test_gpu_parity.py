@@ -644,13 +644,16 @@ def test_gemv_config1_fp32_1024(ctx, orc):
 
 
 @pytest.mark.parametrize("case", gc.RAGGED + gc.DTYPE_MIX + gc.STAGING + gc.MFMA_CHUNKS
-                         + gc.LONG_ROWS + gc.SECTORS + gc.SINGLE_ROWS, ids=_case_id)
+                         + gc.LONG_ROWS + gc.SECTORS + gc.SINGLE_ROWS + gc.PAGE_EDGES,
+                         ids=_case_id)
 def test_gemv_matches_oracle(ctx, orc, case):
     """Ragged shapes (1003 x 1000, batches 1..8), mixed dtypes, W tables of
     256 pages (staged once per workgroup) and 257 (staged per tile), MFMA
     chunk counts (odd, ragged last chunk, rows far shorter than a chunk),
-    long rows at batch 1 on few and many CUs, 1-2 KiB sector pages, and
-    single-row matrices (most of the tile outside M)."""
+    long rows at batch 1 on few and many CUs, 1-2 KiB sector pages,
+    single-row matrices (most of the tile outside M), and 2 MiB pages with
+    tiles inside one page (per-row buffer resources on the MFMA path) beside
+    tiles that straddle a page end (a table read per load)."""
     M, K, B, wd, xd, shift, cus = case
     say(f"gemv {_case_id(case)}")
     run_gemv(ctx, orc, M, K, B, wd, xd, shift, seed=M + K + B + shift, cus=cus)
