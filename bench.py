@@ -434,6 +434,11 @@ def compact(result, full_path):
             f"{p['M']}x{p['K']}_b{p['batch']}": p["launch_p50_us"] for p in g["points"]
             if p["placement"] == "xcds" and p["layout"] == "coloured" and p["batch"] in (1, 8)
             and p["rotated_copies"] == 8 and p["cus"] == max(q["cus"] for q in g["points"])}
+        if g.get("graph_ls"):
+            gl = g["graph_ls"]
+            summ["gemv_ls_launch_p50_p99_us_direct_graph"] = [
+                gl["direct_launch_p50_us"], gl["direct_launch_p99_us"], gl["graph_launch_p50_us"],
+                gl["graph_launch_p99_us"], gl["graph_matches_direct"]]
         summ["gemv_p50_us_by_rotated_copies"] = {
             f"{p['M']}x{p['K']}_b{p['batch']}_x{p['rotated_copies']}": p["p50_us"]
             for p in g["points"] if p["placement"] == "xcds" and p["layout"] == "coloured"
@@ -602,6 +607,7 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches, checks):
     out = []
     lib_ref = {}
     indirection = {}
+    graph_ls = {}
     g = torch.Generator(device="cuda:0")
     g.manual_seed(7)
     x = (torch.randn(8 * 11008, generator=g, device="cuda:0")).to(torch.bfloat16)
@@ -669,6 +675,63 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches, checks):
                 f"{pctl(d, 50) * 1e3:.1f} us")
             return med
 
+        def graph_point(B, ncu):
+            """Launch-inclusive latency of the LS call (host events around
+            each call) launched directly and as a replay of a HIP graph that
+            captured it (one graph per weight copy, captured on ``stream``
+            under the same CU mask), in interleaved blocks of launches; and
+            whether a replay writes the same bits as the direct call."""
+            tag_d, tag_g = ("gemv-direct", M, B, ncu), ("gemv-graph", M, B, ncu)
+            with torch.cuda.stream(stream):
+                sg.set_cu_mask(ctx, stream, range(ncu))
+                for i in range(20):
+                    sg.colored_gemv(ctx, W[i % copies], sg.BF16, M, K, x, sg.BF16, B, y,
+                                    shift, stream)
+                torch.cuda.synchronize()
+                graphs = []
+                for i in range(copies):
+                    gr = torch.cuda.CUDAGraph()
+                    with torch.cuda.graph(gr, stream=stream):
+                        sg.colored_gemv(ctx, W[i], sg.BF16, M, K, x, sg.BF16, B, y, shift,
+                                        stream)
+                    graphs.append(gr)
+                for i in range(20):
+                    graphs[i % copies].replay()
+                timer.reserve(4 * launches)
+                block = 100
+                for b0 in range(0, launches, block):
+                    for i in range(b0, min(b0 + block, launches)):
+                        e0 = timer.start()
+                        sg.colored_gemv(ctx, W[i % copies], sg.BF16, M, K, x, sg.BF16, B, y,
+                                        shift, stream)
+                        timer.stop(e0, tag_d)
+                    for i in range(b0, min(b0 + block, launches)):
+                        e0 = timer.start()
+                        graphs[i % copies].replay()
+                        timer.stop(e0, tag_g)
+                torch.cuda.synchronize()
+                sg.colored_gemv(ctx, W[1], sg.BF16, M, K, x, sg.BF16, B, y, shift, stream)
+                torch.cuda.synchronize()
+                direct = y[:B * M].clone()
+                y.fill_(-1.0)
+                graphs[1].replay()
+                torch.cuda.synchronize()
+                same = bool(torch.equal(direct.view(torch.int32), y[:B * M].view(torch.int32)))
+                sg.set_cu_mask(ctx, stream, None)
+                torch.cuda.synchronize()
+            del graphs
+            dd, dg = timer.durations_ms(tag_d), timer.durations_ms(tag_g)
+            r = {"M": M, "K": K, "batch": B, "cus": ncu, "launches": launches,
+                 "direct_launch_p50_us": round(pctl(dd, 50) * 1e3, 2),
+                 "direct_launch_p99_us": round(pctl(dd, 99) * 1e3, 2),
+                 "graph_launch_p50_us": round(pctl(dg, 50) * 1e3, 2),
+                 "graph_launch_p99_us": round(pctl(dg, 99) * 1e3, 2),
+                 "graph_matches_direct": same, "device_flags": ctx.device_error()}
+            log(f"gemv {M}x{K} B={B} cus={ncu}: launch p50/p99 direct {r['direct_launch_p50_us']}"
+                f" / {r['direct_launch_p99_us']} us, graph replay {r['graph_launch_p50_us']} / "
+                f"{r['graph_launch_p99_us']} us (same bits: {same})")
+            return r
+
         for B in (1, 2, 4, 8):
             for ncu in (64, 128, 192, 256):
                 if ncu > n_cus:
@@ -706,6 +769,9 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches, checks):
                          p["layout"] == "coloured" and p["rotated_copies"] == copies][0]
                 indirection[f"b{B}_pct"] = round(100 * (t_col / t_plain - 1), 2)
             del Wc, WC
+            # the LS layer of the co-located pair (batch 1 on 192 CUs) as a
+            # HIP graph replay
+            graph_ls = graph_point(1, n_cus * 3 // 4)
         del raw, W
         torch.cuda.empty_cache()
     return {"what": "bf16 W on 48/64 colours in 2 MiB pages, bf16 x, fp32 y; "
@@ -718,6 +784,7 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches, checks):
                                     "contiguous weights with identity tables, p50 difference",
                             **indirection},
             "library_reference": lib_ref,
+            "graph_ls": graph_ls,
             "timing": "p50/p99_us and GBps: kernel spans from the device time log (first "
                       "workgroup start to last workgroup end); launch_p50/p99_us: host events "
                       "around each call in a separate loop without the log, including launch "
