@@ -303,9 +303,21 @@ def main():
     rows = {}
     checks = {}
     want = [r for r in args.rows.split(",") if r]
+
+    def row(name, fn):
+        """Runs one row; a row that raises is recorded as such (with the
+        error) and the others still run, so the headline line is printed."""
+        try:
+            rows[name] = fn()
+        except Exception as e:  # noqa: BLE001 - any failure of an auxiliary row
+            import traceback
+            traceback.print_exc(file=sys.stderr)
+            rows[name] = {"error": f"{type(e).__name__}: {e}"}
+            torch.cuda.synchronize()
+        flags[name] = ctx.device_error()
+
     if "classify" in want:
-        rows["classify"] = bench_classify(torch, sg, synth, ctx, stream, timer, checks)
-        flags["classify"] = ctx.device_error()
+        row("classify", lambda: bench_classify(torch, sg, synth, ctx, stream, timer, checks))
     if "pagetable" in want:
         rows["pagetable"] = {
             "what": "colour_alloc_pagetable over the headline pool (synchronous call)",
@@ -318,32 +330,25 @@ def main():
     del arrays, tables, t8, b_lin, c_lin
     torch.cuda.empty_cache()
     if "relayout" in want:
-        rows["relayout"] = bench_relayout(torch, sg, synth, ctx, stream, timer)
-        flags["relayout"] = ctx.device_error()
+        row("relayout", lambda: bench_relayout(torch, sg, synth, ctx, stream, timer))
     if "gemv" in want:
-        rows["gemv"] = bench_gemv(torch, sg, synth, ctx, stream, timer, args.gemv_launches, checks)
-        flags["gemv"] = ctx.device_error()
+        row("gemv", lambda: bench_gemv(torch, sg, synth, ctx, stream, timer, args.gemv_launches,
+                                       checks))
     ops = corun_operands(torch, sg, synth, ctx) if ("corun" in want or "preempt" in want) else None
     if "corun" in want:
-        rows["corun"] = bench_corun(torch, sg, synth, ctx, args.corun_launches, ops)
-        flags["corun"] = ctx.device_error()
+        row("corun", lambda: bench_corun(torch, sg, synth, ctx, args.corun_launches, ops))
     if "preempt" in want:
-        rows["preempt"] = bench_preempt(torch, sg, synth, ctx, ops, args.preempt_trials)
-        flags["preempt"] = ctx.device_error()
+        row("preempt", lambda: bench_preempt(torch, sg, synth, ctx, ops, args.preempt_trials))
     del ops
     torch.cuda.empty_cache()
     if "bimodal" in want:
-        rows["bimodal"] = bench_bimodal(torch, sg, synth, ctx, stream)
-        flags["bimodal"] = ctx.device_error()
+        row("bimodal", lambda: bench_bimodal(torch, sg, synth, ctx, stream))
     if "sectors" in want:
-        rows["sectors"] = bench_sectors(torch, sg, synth, ctx, stream, timer)
-        flags["sectors"] = ctx.device_error()
+        row("sectors", lambda: bench_sectors(torch, sg, synth, ctx, stream, timer))
     if "xcd" in want:
-        rows["xcd"] = bench_xcd(torch, sg, ctx, stream)
-        flags["xcd"] = ctx.device_error()
+        row("xcd", lambda: bench_xcd(torch, sg, ctx, stream))
     if "probe" in want:
-        rows["probe"] = bench_probe(torch, sg, synth, ctx, stream, timer)
-        flags["probe"] = ctx.device_error()
+        row("probe", lambda: bench_probe(torch, sg, synth, ctx, stream, timer))
     if rows:
         result["rows"] = rows
 
@@ -400,7 +405,10 @@ def compact(result, full_path):
         out["cpu_baseline"]["checks"] = {k: v for k, v in cb.items()
                                          if k.endswith(("match_oracle", "matches_oracle",
                                                         "within_bound", "identity"))}
-    rows = result.get("rows", {})
+    rows = {k: v for k, v in result.get("rows", {}).items() if "error" not in v}
+    errors = {k: v["error"] for k, v in result.get("rows", {}).items() if "error" in v}
+    if errors:
+        out["row_errors"] = errors
     summ = {}
     if "classify" in rows:
         c = rows["classify"]
@@ -434,7 +442,7 @@ def compact(result, full_path):
             f"{p['M']}x{p['K']}_b{p['batch']}": p["launch_p50_us"] for p in g["points"]
             if p["placement"] == "xcds" and p["layout"] == "coloured" and p["batch"] in (1, 8)
             and p["rotated_copies"] == 8 and p["cus"] == max(q["cus"] for q in g["points"])}
-        if g.get("graph_ls"):
+        if g.get("graph_ls") and "error" not in g["graph_ls"]:
             gl = g["graph_ls"]
             summ["gemv_ls_launch_p50_p99_us_direct_graph"] = [
                 gl["direct_launch_p50_us"], gl["direct_launch_p99_us"], gl["graph_launch_p50_us"],
@@ -770,8 +778,14 @@ def bench_gemv(torch, sg, synth, ctx, stream, timer, launches, checks):
                 indirection[f"b{B}_pct"] = round(100 * (t_col / t_plain - 1), 2)
             del Wc, WC
             # the LS layer of the co-located pair (batch 1 on 192 CUs) as a
-            # HIP graph replay
-            graph_ls = graph_point(1, n_cus * 3 // 4)
+            # HIP graph replay (recorded as an error, not fatal, if capture
+            # fails on this stack)
+            try:
+                graph_ls = graph_point(1, n_cus * 3 // 4)
+            except Exception as e:  # noqa: BLE001
+                torch.cuda.synchronize()
+                sg.set_cu_mask(ctx, stream, None)
+                graph_ls = {"error": f"{type(e).__name__}: {e}"}
         del raw, W
         torch.cuda.empty_cache()
     return {"what": "bf16 W on 48/64 colours in 2 MiB pages, bf16 x, fp32 y; "
