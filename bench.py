@@ -1417,7 +1417,8 @@ def bench_probe(torch, sg, synth, ctx, stream, timer, reps=10, masks=None):
 
 def cpu_threads():
     """Host threads for the all-cores oracle runs: the CPUs this process may
-    use, at most 16 (a one-GPU machine's share of its host)."""
+    use, at most 16 (one GPU's share of the host cores of an eight-GPU
+    node)."""
     try:
         n = len(os.sched_getaffinity(0))
     except AttributeError:
