@@ -1,0 +1,164 @@
+"""Seeded random parity sweep.  Shapes, lengths, page sizes, colour sets,
+CU masks and (for the GEMV) batch and dtypes are drawn from fixed seeds;
+every case runs one entry point and compares it with the oracle: bit-exact
+for classify, histogram, triad and relayout, the summation-tree bound for
+the GEMV.  Masks are all CUs, whole XCDs (the static schedule) or a random
+subset (the ticket queues)."""
+import sys
+
+import numpy as np
+import pytest
+
+import synth
+import paper_2407_13996_amd as sg
+import test_gpu_parity as tp
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+DEV = "cuda:0"
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    c = sg.Context(0)
+    yield c
+    assert c.device_error() == 0
+    c.close()
+
+
+def draw_mask(rng, num_cus):
+    """None, whole XCDs or a random subset, one third each."""
+    kind = int(rng.integers(0, 3))
+    if kind == 0:
+        return None
+    if kind == 1:
+        return range(32 * int(rng.integers(1, num_cus // 32 + 1)))
+    return synth.random_cu_subset(num_cus, int(rng.integers(1, num_cus)), seed=int(rng.integers(1 << 30)))
+
+
+class Masked:
+    """Applies a CU mask to the current stream for the duration."""
+
+    def __init__(self, ctx, cus):
+        self.ctx, self.cus = ctx, cus
+
+    def __enter__(self):
+        if self.cus is not None:
+            sg.set_cu_mask(self.ctx, None, self.cus)
+
+    def __exit__(self, *exc):
+        if self.cus is not None:
+            sg.set_cu_mask(self.ctx, None, None)
+
+
+def mask_name(cus):
+    return "all" if cus is None else f"{len(list(cus))} CUs"
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_classify(ctx, orc, seed):
+    rng = np.random.default_rng(1000 + seed)
+    n = int(rng.integers(0, 300_000))
+    K = int(rng.integers(1, 9))
+    hist = bool(rng.integers(0, 2))
+    cus = draw_mask(rng, ctx.num_cus)
+    say(f"random classify seed={seed}: n={n} K={K} hist={hist} mask {mask_name(cus)}")
+    masks = synth.xor_masks(K, seed=seed + 1, min_bit=12)
+    addrs = synth.page_addresses(max(n, 1), seed=seed)[:n]
+    d_addrs = tp.to_dev(addrs) if n else torch.empty(0, dtype=torch.int64, device=DEV)
+    d_col = torch.full((max(n, 16) + 16,), 0xEE, dtype=torch.uint8, device=DEV)
+    d_hist = torch.full((1 << K,), 12345, dtype=torch.int64, device=DEV) if hist else None
+    with Masked(ctx, cus):
+        sg.colour_classify(ctx, masks, d_addrs, d_col, d_hist)
+    got = tp.to_host(d_col)
+    ref, ref_hist = orc.classify(addrs, masks)
+    assert (got[:n] == ref).all()
+    assert (got[n:] == 0xEE).all()
+    if hist:
+        assert (tp.to_host(d_hist).astype(np.uint64) == ref_hist).all()
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_triad(ctx, orc, seed):
+    rng = np.random.default_rng(2000 + seed)
+    shift = int(rng.integers(10, 22))
+    P = 1 << shift
+    n = int(rng.integers(0, min(600_000, 40 * P // 4) + 1))
+    s = float(np.float32(rng.uniform(-4, 4)))
+    cus = draw_mask(rng, ctx.num_cus)
+    sets = [range(c0, c0 + w) for c0, w in
+            ((int(rng.integers(0, 48)), int(rng.integers(1, 17))) for _ in range(3))]
+    say(f"random triad seed={seed}: shift={shift} n={n} s={s} sets "
+        f"{[(r.start, r.stop) for r in sets]} mask {mask_name(cus)}")
+    n_pages = max(1, -(-n * 4 // P))
+    tabs = [tp.make_tables(orc, shift, n_pages, S, 30 + seed + i) for i, S in enumerate(sets)]
+    pools = max(t[1] for t in tabs)
+    pts = [t[0] for t in tabs]
+    epp = P // 4
+    a0 = synth.uniform_f32(pools * epp, seed=seed + 1)
+    b = synth.uniform_f32(pools * epp, seed=seed + 2)
+    c = synth.uniform_f32(pools * epp, seed=seed + 3)
+    d_a, d_b, d_c = tp.to_dev(a0), tp.to_dev(b), tp.to_dev(c)
+    with Masked(ctx, cus):
+        sg.colored_stream(ctx, sg.paged(d_a, tp.to_dev(pts[0]), pools),
+                          sg.paged(d_b, tp.to_dev(pts[1]), pools),
+                          sg.paged(d_c, tp.to_dev(pts[2]), pools), s, n, shift)
+    ref = a0.copy()
+    orc.triad(ref, pts[0], b, pts[1], c, pts[2], s, n, shift)
+    assert (tp.to_host(d_a).view(np.uint32) == ref.view(np.uint32)).all()
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_relayout(ctx, orc, seed):
+    rng = np.random.default_rng(3000 + seed)
+    shift = int(rng.integers(10, 22))
+    P = 1 << shift
+    n_bytes = int(rng.integers(0, min(3_000_000, 40 * P) + 1))
+    cus = draw_mask(rng, ctx.num_cus)
+    say(f"random relayout seed={seed}: shift={shift} n_bytes={n_bytes} mask {mask_name(cus)}")
+    n_pages = max(1, -(-n_bytes // P))
+    pt_s, src_pages = tp.make_tables(orc, shift, n_pages, range(int(rng.integers(0, 32)), 48), 50 + seed)
+    pt_d, dst_pages = tp.make_tables(orc, shift, n_pages, range(int(rng.integers(1, 64))), 90 + seed)
+    src = synth.random_bytes(src_pages * P, seed=seed + 5)
+    dst0 = synth.random_bytes(dst_pages * P, seed=seed + 6)
+    d_src, d_dst = tp.to_dev(src), tp.to_dev(dst0)
+    with Masked(ctx, cus):
+        sg.bimodal_relayout(ctx, sg.paged(d_dst, tp.to_dev(pt_d), dst_pages),
+                            sg.paged(d_src, tp.to_dev(pt_s), src_pages), n_bytes, shift)
+    ref = dst0.copy()
+    orc.relayout(ref, pt_d, src, pt_s, n_bytes, shift)
+    assert (tp.to_host(d_dst) == ref).all()
+
+
+DTYPES = [(sg.BF16, sg.BF16), (sg.F16, sg.F16), (sg.F32, sg.F32), (sg.BF16, sg.F32),
+          (sg.F32, sg.BF16), (sg.F16, sg.F32), (sg.F32, sg.F16), (sg.BF16, sg.F16)]
+SIZE = {sg.F32: 4, sg.BF16: 2, sg.F16: 2}
+
+
+@pytest.mark.parametrize("seed", range(48))
+def test_random_gemv(ctx, orc, seed):
+    rng = np.random.default_rng(4000 + seed)
+    wd, xd = DTYPES[int(rng.integers(0, len(DTYPES)))] if seed % 3 else DTYPES[seed % 2]
+    B = int(rng.integers(1, 9))
+    M = int(rng.integers(1, 1500))
+    step = 16 // SIZE[wd]                   # rows are whole 16-byte slices
+    K = step * int(rng.integers(1, 6000 // step + 1))
+    row = K * SIZE[wd]
+    # a tile's rows (16 at most) must span at most 254 pages
+    lo = max(10, int(np.ceil(np.log2(max(1, 16 * row / 250)))))
+    shift = int(rng.integers(lo, 22))
+    cus = draw_mask(rng, ctx.num_cus)
+    S = range(int(rng.integers(0, 16)), int(rng.integers(17, 65)))
+    say(f"random gemv seed={seed}: {M}x{K} B={B} w={wd} x={xd} shift={shift} colours "
+        f"{S.start}..{S.stop - 1} mask {mask_name(cus)}")
+    pool, pt, d_pool, d_pt, pool_pages = tp.upload_w(orc, M, K, wd, shift, S, seed, seed + 1, 6)
+    xb = tp.x_bits(xd, B * K, seed + 2)
+    y = tp.launch_gemv(ctx, d_pool, d_pt, pool_pages, M, K, B, wd, xd, tp.to_dev(xb), shift,
+                       tp.cu_list(cus))
+    ref, absdot = orc.gemv(pool, pt, wd, M, K, xb, xd, B, shift)
+    tp.gemv_check(ctx, y, ref, absdot, M, K, B, wd, xd, tp.cu_list(cus), tag=f"random {seed}")
