@@ -162,3 +162,44 @@ def test_random_gemv(ctx, orc, seed):
                        tp.cu_list(cus))
     ref, absdot = orc.gemv(pool, pt, wd, M, K, xb, xd, B, shift)
     tp.gemv_check(ctx, y, ref, absdot, M, K, B, wd, xd, tp.cu_list(cus), tag=f"random {seed}")
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_pagetable(ctx, orc, seed):
+    """Random hashes (mask bits up to three positions inside the page, so a
+    page may carry several colours), pool sizes, origins, colour sets and
+    table lengths, through the synchronous and the allocation-free builds;
+    a shortfall must report the oracle's count."""
+    rng = np.random.default_rng(5000 + seed)
+    shift = int(rng.integers(10, 22))
+    K = int(rng.integers(1, 9))
+    lo = int(rng.integers(max(8, shift - 3), shift + 5))
+    masks = synth.xor_masks(K, seed=seed + 7, min_bit=lo)
+    pool = int(rng.integers(1, 200_001))
+    origin = int(rng.integers(0, 1 << (40 - shift))) << shift
+    S = sorted(int(c) for c in rng.choice(1 << K, size=int(rng.integers(1, (1 << K) + 1)),
+                                        replace=False))
+    n = int(rng.integers(1, pool + 1))
+    cus = draw_mask(rng, ctx.num_cus)
+    say(f"random pagetable seed={seed}: shift={shift} K={K} mask bits from {lo} pool={pool} "
+        f"|S|={len(S)} n={n} mask {mask_name(cus)}")
+    ref, ref_found = orc.pagetable(masks, origin, shift, pool, synth.colour_set_bits(S), n)
+    d_pt = torch.full((n + 8,), -1, dtype=torch.int32, device=DEV)
+    with Masked(ctx, cus):
+        if ref_found >= n:
+            assert sg.colour_alloc_pagetable(ctx, masks, origin, shift, pool, S, n, d_pt) == ref_found
+        else:
+            with pytest.raises(sg.SgdrcError) as e:
+                sg.colour_alloc_pagetable(ctx, masks, origin, shift, pool, S, n, d_pt)
+            assert e.value.code == sg.ENOMEM and e.value.n_found == ref_found
+    k = min(n, ref_found)
+    got = tp.to_host(d_pt).view(np.uint32)
+    assert (got[:k] == ref[:k]).all()
+    assert (got[n:] == 0xFFFFFFFF).all()
+    # the allocation-free build writes the same table and the full count
+    d_pt2 = torch.full((n + 8,), -1, dtype=torch.int32, device=DEV)
+    d_found = torch.full((1,), -1, dtype=torch.int64, device=DEV)
+    with Masked(ctx, cus):
+        sg.colour_alloc_pagetable_noalloc(ctx, masks, origin, shift, pool, S, n, d_pt2, d_found)
+    assert int(tp.to_host(d_found)[0]) == ref_found
+    assert (tp.to_host(d_pt2).view(np.uint32)[:k] == ref[:k]).all()
