@@ -203,3 +203,92 @@ def test_random_pagetable(ctx, orc, seed):
         sg.colour_alloc_pagetable_noalloc(ctx, masks, origin, shift, pool, S, n, d_pt2, d_found)
     assert int(tp.to_host(d_found)[0]) == ref_found
     assert (tp.to_host(d_pt2).view(np.uint32)[:k] == ref[:k]).all()
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_colour_table(ctx, orc, seed):
+    """Colour tables (paper section 5.3) of random size, partition size,
+    origin and holes: classify (with or without the 256-bin histogram,
+    addresses inside, below and past the table) and the page-table build
+    (pages of 1 KiB to 64 KiB, pools reaching past either end of the table)
+    against the oracle."""
+    rng = np.random.default_rng(6000 + seed)
+    lut_shift = int(rng.integers(10, 14))
+    entries = int(rng.integers(1, 1 << 17))
+    origin = int(rng.integers(1, 1 << 20)) << 20
+    lut = tp.random_table(entries, seed=seed, colours=int(rng.integers(1, 257)) if seed % 2 else 64,
+                          holes=float(rng.uniform(0, 0.05)))
+    t = sg.colour_table(tp.to_dev(lut), origin, lut_shift)
+    cus = draw_mask(rng, ctx.num_cus)
+    n = int(rng.integers(0, 200_000))
+    hist = bool(rng.integers(0, 2))
+    span = entries << lut_shift
+    addrs = (origin + rng.integers(-(1 << 16), span + (1 << 16), size=max(n, 1))).astype(np.uint64)[:n]
+    say(f"random colour table seed={seed}: {entries} partitions of 2^{lut_shift}, n={n} "
+        f"hist={hist} mask {mask_name(cus)}")
+    d_addrs = tp.to_dev(addrs) if n else torch.empty(0, dtype=torch.int64, device=DEV)
+    d_col = torch.full((max(n, 16) + 16,), 0xEE, dtype=torch.uint8, device=DEV)
+    d_hist = torch.full((256,), 777, dtype=torch.int64, device=DEV) if hist else None
+    with Masked(ctx, cus):
+        sg.colour_classify_table(ctx, t, d_addrs, d_col, d_hist)
+    ref, ref_hist = orc.classify_lut(addrs, lut, origin, lut_shift)
+    got = tp.to_host(d_col)
+    assert (got[:n] == ref).all() and (got[n:] == 0xEE).all()
+    if hist:
+        assert (tp.to_host(d_hist).astype(np.uint64) == ref_hist).all()
+    # page tables through the same table
+    page_shift = int(rng.integers(10, 17))
+    addr_origin = (origin - (int(rng.integers(0, 64)) << page_shift))
+    pool = max(1, (span + int(rng.integers(0, 1 << 17))) >> page_shift)
+    # colours 0..254 (255 marks a partition with no colour)
+    S = sorted(int(c) for c in rng.choice(255, size=int(rng.integers(1, 256)), replace=False))
+    ref_pt, ref_found = orc.pagetable_lut(lut, origin, lut_shift, addr_origin, page_shift, pool,
+                                          synth.colour_set_bits(S), pool)
+    n_need = int(rng.integers(1, pool + 1))
+    say(f"  table page tables: pages 2^{page_shift}, pool {pool}, |S|={len(S)}, need {n_need}, "
+        f"oracle finds {ref_found}")
+    d_pt = torch.full((n_need + 8,), -1, dtype=torch.int32, device=DEV)
+    with Masked(ctx, cus):
+        if ref_found >= n_need:
+            assert sg.colour_alloc_pagetable_table(ctx, t, addr_origin, page_shift, pool, S, n_need,
+                                                   d_pt) == ref_found
+        else:
+            with pytest.raises(sg.SgdrcError) as e:
+                sg.colour_alloc_pagetable_table(ctx, t, addr_origin, page_shift, pool, S, n_need,
+                                                d_pt)
+            assert e.value.code == sg.ENOMEM and e.value.n_found == ref_found
+    k = min(n_need, ref_found)
+    got = tp.to_host(d_pt).view(np.uint32)
+    assert (got[:k] == ref_pt[:k]).all() and (got[n_need:] == 0xFFFFFFFF).all()
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_relayout_batch(ctx, orc, seed):
+    """Batches of 1 to 40 relayout items of random page sizes (1 to 64 KiB)
+    and lengths (empty ones included) under random CU masks."""
+    rng = np.random.default_rng(7000 + seed)
+    n_items = int(rng.integers(1, 41))
+    cus = draw_mask(rng, ctx.num_cus)
+    say(f"random relayout batch seed={seed}: {n_items} items, mask {mask_name(cus)}")
+    items, refs, devs, keep = [], [], [], []
+    for i in range(n_items):
+        shift = int(rng.integers(10, 17))   # 2 MiB pages: in the single relayout sweep
+        P = 1 << shift
+        n_bytes = 0 if rng.random() < 0.1 else int(rng.integers(1, min(400_000, 8 * P) + 1))
+        n_pages = max(1, -(-n_bytes // P))
+        pt_s, src_pages = tp.make_tables(orc, shift, n_pages, range(16), 300 + 40 * seed + i)
+        pt_d, dst_pages = tp.make_tables(orc, shift, n_pages, range(32, 48), 700 + 40 * seed + i)
+        src = synth.random_bytes(src_pages * P, seed=1000 * seed + i)
+        dst0 = synth.random_bytes(dst_pages * P, seed=1000 * seed + 500 + i)
+        d_src, d_dst, d_ps, d_pd = tp.to_dev(src), tp.to_dev(dst0), tp.to_dev(pt_s), tp.to_dev(pt_d)
+        keep += [d_src, d_ps, d_pd]
+        items.append((sg.paged(d_dst, d_pd, dst_pages), sg.paged(d_src, d_ps, src_pages), n_bytes,
+                      shift))
+        ref = dst0.copy()
+        orc.relayout(ref, pt_d, src, pt_s, n_bytes, shift)
+        refs.append(ref)
+        devs.append(d_dst)
+    with Masked(ctx, cus):
+        sg.bimodal_relayout_batch(ctx, items)
+    for i, (d, ref) in enumerate(zip(devs, refs)):
+        assert (tp.to_host(d) == ref).all(), i
