@@ -292,3 +292,48 @@ def test_random_relayout_batch(ctx, orc, seed):
         sg.bimodal_relayout_batch(ctx, items)
     for i, (d, ref) in enumerate(zip(devs, refs)):
         assert (tp.to_host(d) == ref).all(), i
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_preemption(ctx, orc, seed):
+    """A preemptible triad evicted at a random tile (the eviction hook), its
+    resumption evicted again at a later random tile or not, then finished,
+    each launch under a random CU mask: every tile worked exactly once and
+    the result equals the oracle's."""
+    import test_gpu_preempt as tpp
+    rng = np.random.default_rng(8000 + seed)
+    n = int(rng.integers(1, 16 * 1024 * 1024))
+    tr = tpp.Triad(orc, 16, n, seed=90 + seed)
+    h1 = int(rng.integers(1, tr.tiles + 2))
+    h2 = int(rng.integers(h1 + 1, tr.tiles + 3)) if rng.random() < 0.6 else 0
+    masks = [draw_mask(rng, ctx.num_cus) for _ in range(3)]
+    say(f"random preemption seed={seed}: n={n} ({tr.tiles} tiles), evicted at {h1}, then "
+        f"{h2 or 'not'}; masks {[mask_name(m) for m in masks]}")
+    st = torch.cuda.Stream()
+    flag = torch.zeros(1, dtype=torch.int32, device=DEV)
+    logs = tpp.Logs(ctx, tr.tiles)
+    try:
+        sg.set_eviction_flag(ctx, st, flag)
+        sg.set_cu_mask(ctx, st, masks[0])
+        sg.set_eviction_hook(ctx, st, h1)
+        tr.launch(ctx, st)
+        left1 = sg.suspended(ctx, st)
+        if h2:
+            sg.set_cu_mask(ctx, st, masks[1])
+            sg.set_eviction_hook(ctx, st, h2)
+            sg.resume(ctx, st)
+        left2 = sg.suspended(ctx, st)
+        say(f"  left after the first launch {left1}, after the second {left2}")
+        sg.set_eviction_hook(ctx, st, 0)
+        sg.set_cu_mask(ctx, st, masks[2])
+        tpp.finish(ctx, st)
+        cl, tl = logs.snapshot()
+    finally:
+        logs.close()
+        sg.set_eviction_hook(ctx, st, 0)
+        sg.set_cu_mask(ctx, st, None)
+        sg.set_eviction_flag(ctx, st, None)
+        sg.stream_release(ctx, st)
+    tr.check()
+    assert (tl == 1).all(), np.unique(tl, return_counts=True)
+    assert cl.sum() == tr.tiles
