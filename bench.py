@@ -886,7 +886,7 @@ def bench_xcd(torch, sg, ctx, stream, reps=20):
 
 
 def corun_operands(torch, sg, synth, ctx):
-    """Operands of the co-located pair (C4), all from one pool under one hash
+    """Operands of the co-located pair (LS GEMV and BE triad), all from one pool under one hash
     (6 masks on address bits 21..40, so every 2 MiB region has one colour):
     the LS GEMV's bf16 W (4096 x 11008) in 2 MiB pages on colours 0..47
     (8 rotated copies), the BE triad's three 2 GiB fp32 arrays in 64 KiB
@@ -1046,7 +1046,7 @@ def bench_corun(torch, sg, synth, ctx, ls_launches, ops):
 
 
 def bench_preempt(torch, sg, synth, ctx, ops, trials):
-    """Tidal handover (paper section 7.1) at the C4 sizes.  The BE triad
+    """Tidal handover (paper section 7.1) at the co-located pair's sizes.  The BE triad
     (3 x 2 GiB, colours 48..63) starts on all CUs as a preemptible launch.
     After a random delay the LS side raises the eviction flag in its own
     stream order (a device store stamped with the device clock), takes the
@@ -1156,7 +1156,7 @@ def bench_preempt(torch, sg, synth, ctx, ops, trials):
 
 
 def bench_bimodal(torch, sg, synth, ctx, stream, reps=20, launches=100):
-    """Bimodal LS tensors (paper section 7.2) at the C3 shapes: both bf16
+    """Bimodal LS tensors (paper section 7.2) at the LS layer shapes: both bf16
     matrices (4096x11008, 11008x4096; 2 MiB pages) registered as
     latency-sensitive tensors with an all-channel form and a form on colours
     0..47.  Reported: the time of a state change (the runtime relays both
@@ -1201,7 +1201,7 @@ def bench_bimodal(torch, sg, synth, ctx, stream, reps=20, launches=100):
             e1.record(stream)
             torch.cuda.synchronize()
             trans[st].append(e0.elapsed_time(e1))
-    out = {"what": "two bf16 C3 matrices as LS tensors: all-channel form vs colours 0..47 "
+    out = {"what": "two bf16 LS matrices (4096x11008, 11008x4096) as LS tensors: all-channel form vs colours 0..47 "
                    "(2 MiB pages)", "bytes_moved_per_change": total}
     for st, name in ((sg.BM_COLOCATED, "to_colocated"), (sg.BM_MONOPOLY, "to_monopoly")):
         ms = float(np.median(trans[st]))
@@ -1231,7 +1231,7 @@ def bench_bimodal(torch, sg, synth, ctx, stream, reps=20, launches=100):
 
 def bench_sectors(torch, sg, synth, ctx, stream, timer, reps=20):
     """Colouring granularity (paper section 6: 1-2 KiB sectors; section 5.3:
-    a colour table for hashes that are not XOR-linear).  The C2 triad (three
+    a colour table for hashes that are not XOR-linear).  The streaming triad (three
     1 GiB fp32 arrays, colours 0..15 of 64) with 1, 2, 4 and 64 KiB pages:
     the cost of finer page-table indirection.  Then classify and the page-
     table build through a random colour table of 2^26 1 KiB partitions
@@ -1456,8 +1456,8 @@ def cpu_baseline(np, synth, masks, shift, pages, pools_desc, b_host, c_host, fra
     functions over disjoint index ranges.  Bounded samples of the path:
     the headline triad (full arrays, every colour set, one pass each), the
     headline page-table builds (full pools), classify of the first 2^22 of
-    the 2^26 C5 addresses, the C5 relayout of the first 256 MiB (4,096
-    pages of 64 KiB) in both directions, and the batch-1 GEMV of both C3
+    the 2^26 classify addresses, the 4 GiB relayout's first 256 MiB (4,096
+    pages of 64 KiB) in both directions, and the batch-1 GEMV of both LS
     layers on the benchmark's own weights.  GPU results of the same
     operations are compared with the oracle's on these samples."""
     import oracle
@@ -1535,7 +1535,7 @@ def cpu_baseline(np, synth, masks, shift, pages, pools_desc, b_host, c_host, fra
         return jobs
     timed("pagetable", pt_jobs, sum(pools_desc[nc][1] for nc in fractions), "pool_pages")
 
-    # ---- classify: the first 2^22 of the C5 addresses
+    # ---- classify: the first 2^22 of the 2^26 classify addresses
     na = 1 << 22
     cm = synth.xor_masks(6, seed=1, min_bit=12)
     addrs = synth.page_addresses(1 << 26, seed=0)[:na]
@@ -1578,7 +1578,7 @@ def cpu_baseline(np, synth, masks, shift, pages, pools_desc, b_host, c_host, fra
     res["relayout_round_trip_identity"] = bool(np.array_equal(back, src))
     del rpool, back, src
 
-    # ---- GEMV batch 1 on the benchmark's own C3 weights (contiguous copy)
+    # ---- GEMV batch 1 on the benchmark's own LS-layer weights (contiguous copy)
     if "gemv" in gpu_checks:
         for (M, K), (w, x, y_gpu) in gpu_checks["gemv"].items():
             rows_out = {}

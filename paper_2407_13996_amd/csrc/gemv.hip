@@ -365,8 +365,8 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(4)
         // The rows of 16-row block b = m0 / 16 walk their chunks starting at
         // chunk b mod n_chunks (then wrapping), so that the workgroups
         // streaming at one moment read different offsets of their rows
-        // instead of all the same one.  On MI355X (both 2 MiB-paged C3
-        // layers, batch 4 and 8, same session): 2.3-4.2 percent faster on
+        // instead of all the same one.  On MI355X (the bf16 4096 x 11008
+        // and 11008 x 4096 layers in 2 MiB pages, batch 4 and 8, same session): 2.3-4.2 percent faster on
         // 256 CUs, up to 6.9 percent on 192, up to 1.6 percent slower at
         // batch 8 on 64 CUs, where each CU streams several tiles and the
         // wrap splits each row in two runs; walking odd blocks backwards

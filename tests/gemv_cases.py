@@ -9,13 +9,13 @@ launches is also launched by some GPU test).  A case is
 BF16, F32, F16 = 1, 0, 2
 NUM_CUS = 256          # MI355X
 
-# the memory-bound layers of the LS configuration (bf16, 2 MiB pages)
-C3_LAYERS = [(4096, 11008), (11008, 4096)]
-C3_BATCHES = [1, 2, 4, 8]
-C3_CUS = [64, 128, 192, 256]
+# the memory-bound layers of the latency-sensitive workload (bf16, 2 MiB pages)
+LS_LAYERS = [(4096, 11008), (11008, 4096)]
+LS_BATCHES = [1, 2, 4, 8]
+LS_CUS = [64, 128, 192, 256]
 
-# every GPU GEMV case besides the C3 sweep (which covers C3_LAYERS x
-# C3_BATCHES x C3_CUS in full)
+# every GPU GEMV case besides the sweep of the LS layers (which covers
+# LS_LAYERS x LS_BATCHES x LS_CUS in full)
 RAGGED = [(1003, 1000, B, BF16, BF16, 12, None) for B in (1, 2, 3, 4, 5, 8)]
 DTYPE_MIX = [(517, 264, B, wd, xd, 12, None) for wd, xd, B in
              [(F32, BF16, 2), (BF16, F32, 8), (F16, F16, 6), (F16, F32, 1), (F32, F16, 7),
@@ -36,7 +36,7 @@ SINGLE_ROWS = [(M, K, B, BF16, BF16, 16, None) for M, K, B in
 # tiles (tile 32 straddles it)
 PAGE_EDGES = [(1100, 2000, B, BF16, BF16, 21, None) for B in (1, 4, 8)] + \
     [(1100, 2000, 8, BF16, BF16, 21, 40)]
-CONFIG1 = [(1024, 1024, 1, F32, F32, 16, None)]
+FP32_1024 = [(1024, 1024, 1, F32, F32, 16, None)]
 # MFMA 8-row tiles: (M, K, batch, allowed CUs, dtype); each also runs with
 # one CU per 16-row tile
 HALF_TILES = [(203, 3000, 8, 10, BF16), (4096, 11008, 4, 192, BF16), (37, 11008, 3, [1, 2], BF16),
@@ -45,27 +45,27 @@ HALF_TILES = [(203, 3000, 8, 10, BF16), (4096, 11008, 4, 192, BF16), (37, 11008,
               (1040, 4096, 8, 64, BF16), (1040, 4096, 4, 64, BF16), (520, 2048, 8, 32, BF16),
               (1040, 8192, 8, 64, BF16), (1040, 4096, 8, 64, F16)]
 MASKS_777 = [(777, 2048, B, BF16, BF16, 16, cus) for B in (1, 8) for cus in (None, 64, 128, 37)]
-C4_LS = [(4096, 11008, 1, BF16, BF16, 21, 192)]
+CORUN_LS = [(4096, 11008, 1, BF16, BF16, 21, 192)]
 
 
 def gpu_cases():
     """Every (shape, mask size) a GPU test launches the GEMV with."""
     cases = RAGGED + DTYPE_MIX + STAGING + MFMA_CHUNKS + LONG_ROWS + SECTORS + SINGLE_ROWS
     cases += PAGE_EDGES
-    cases += CONFIG1 + C4_LS + MASKS_777
+    cases += FP32_1024 + CORUN_LS + MASKS_777
     for M, K, B, cus, dt in HALF_TILES:
         n = cus if isinstance(cus, int) else len(cus)
         cases += [(M, K, B, dt, dt, 16, n), (M, K, B, dt, dt, 16, -(-M // 16))]
-    cases += [(M, K, B, BF16, BF16, 21, cus) for M, K in C3_LAYERS for B in C3_BATCHES
-              for cus in C3_CUS]
+    cases += [(M, K, B, BF16, BF16, 21, cus) for M, K in LS_LAYERS for B in LS_BATCHES
+              for cus in LS_CUS]
     return cases
 
 
 def bench_cases():
     """Every (shape, mask size) the benchmark times."""
-    cases = [(1024, 1024, 1, F32, F32, 16, None)]                   # C1
-    cases += [(M, K, B, BF16, BF16, 21, cus) for M, K in C3_LAYERS  # C3, whole and spread XCDs
-              for B in C3_BATCHES for cus in C3_CUS]
-    cases += C4_LS                                                   # C4 LS layer
-    cases += [(M, K, 1, BF16, BF16, 21, None) for M, K in C3_LAYERS]  # bimodal LS tensors
+    cases = [(1024, 1024, 1, F32, F32, 16, None)]                   # 1024 x 1024 fp32, 64 KiB pages
+    cases += [(M, K, B, BF16, BF16, 21, cus) for M, K in LS_LAYERS  # LS layers, whole and spread XCDs
+              for B in LS_BATCHES for cus in LS_CUS]
+    cases += CORUN_LS                                                   # LS layer of the co-located pair
+    cases += [(M, K, 1, BF16, BF16, 21, None) for M, K in LS_LAYERS]  # bimodal LS tensors
     return cases

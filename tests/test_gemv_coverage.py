@@ -28,7 +28,7 @@ def test_every_benchmarked_gemv_variant_is_gpu_tested():
 
 
 def test_plan_matches_the_c3_sweep_expectations():
-    """The two C3 layers at batch 1 and 8 on 256 CUs: the vector path with
+    """The two LS layers (4096x11008, 11008x4096) at batch 1 and 8 on 256 CUs: the vector path with
     two-row tiles for 4096 x 11008 batch 1 (six loads per lane: one round
     over a 22 KB row), MFMA from batch 3 on, and a summation depth far below
     the 1e-3 criterion's K."""

@@ -182,7 +182,7 @@ def test_pagetable_table_matches_oracle(ctx, orc, lut_shift, page_shift, S):
 # --------------------------------------------------------------- page table
 
 @pytest.mark.parametrize("shift,pool,K,S,n,origin", [
-    (16, 1024, 4, range(4), 64, 1 << 40),          # config 1: 4 MiB in 64 KiB pages, colours 0..3 of 16
+    (16, 1024, 4, range(4), 64, 1 << 40),          # 4 MiB in 64 KiB pages, colours 0..3 of 16
     (12, 200003, 6, range(16), 40000, 0),
     (21, 5000, 6, range(48), 3000, 1 << 33),
     (16, 393216, 6, range(8), 3 * 16384, 1 << 36),  # three 1 GiB arrays at 8 of 64 colours
@@ -444,7 +444,7 @@ def aligned_pool(n_pages, shift):
     return raw, raw.data_ptr() + off, off
 
 
-def test_classify_full_size_config5(ctx, orc):
+def test_classify_2e26_addresses_full_size(ctx, orc):
     """2^26 random 4 KiB-aligned addresses, 6 masks: every colour and the
     histogram equal the oracle's."""
     n = 1 << 26
@@ -461,8 +461,8 @@ def test_classify_full_size_config5(ctx, orc):
 
 
 @pytest.mark.parametrize("elems,colours,cus", [
-    (1 << 28, range(8), None),               # C2 at the smallest colour set, all CUs
-    (1 << 29, range(48, 64), range(192, 256)),  # C4's BE stream: 2 GiB arrays, 64 CUs
+    (1 << 28, range(8), None),               # three 1 GiB arrays at 8 of 64 colours, all CUs
+    (1 << 29, range(48, 64), range(192, 256)),  # the co-located pair's BE stream: 2 GiB arrays, 64 CUs
 ])
 def test_triad_full_size_sampled(ctx, orc, elems, colours, cus):
     """Full-size triad through GPU-built page tables (compared with the
@@ -512,7 +512,7 @@ def test_triad_full_size_sampled(ctx, orc, elems, colours, cus):
     assert (got.view(np.uint32) == ref[:k].view(np.uint32)).all()
 
 
-def test_relayout_full_size_config5(ctx, orc):
+def test_relayout_4gib_fp16_full_size(ctx, orc):
     """4 GiB fp16 tensor (65,536 pages of 64 KiB) from the all-colour page set
     to 16 of 64 colours and back: every restricted page holds its source page
     at the oracle table's position, and the round trip is the identity."""
@@ -638,7 +638,7 @@ def _case_id(c):
     return f"{M}x{K}-B{B}-w{wd}x{xd}-p{1 << (shift - 10)}K-cus{cus}"
 
 
-def test_gemv_config1_fp32_1024(ctx, orc):
+def test_gemv_fp32_1024x1024(ctx, orc):
     say("gemv 1024x1024 fp32 B=1, 64 KiB pages, colours 0..3 of 16")
     run_gemv(ctx, orc, 1024, 1024, 1, sg.F32, sg.F32, 16, S=range(4), n_masks=4)
 
@@ -687,42 +687,42 @@ def test_zero_length_triad_and_relayout_touch_nothing(ctx):
     assert (to_host(dst) == 5).all()
 
 
-C3_CACHE = {}
+LS_CACHE = {}
 
 
 @pytest.fixture(scope="module")
-def c3_weights(orc):
-    """The two C3 layers (bf16, N(0, 0.02)) in 2 MiB pages on colours 0..47
+def ls_weights(orc):
+    """The two LS layers, 4096x11008 and 11008x4096 (bf16, N(0, 0.02)) in 2 MiB pages on colours 0..47
     of 64, uploaded once; freed at the end of the module."""
     def get(M, K):
-        if (M, K) not in C3_CACHE:
-            C3_CACHE.clear()
+        if (M, K) not in LS_CACHE:
+            LS_CACHE.clear()
             torch.cuda.empty_cache()
-            C3_CACHE[(M, K)] = upload_w(orc, M, K, sg.BF16, 21, range(48), seed=M, masks_seed=1,
+            LS_CACHE[(M, K)] = upload_w(orc, M, K, sg.BF16, 21, range(48), seed=M, masks_seed=1,
                                         n_masks=6)
-        return C3_CACHE[(M, K)]
+        return LS_CACHE[(M, K)]
     yield get
-    C3_CACHE.clear()
+    LS_CACHE.clear()
 
 
-@pytest.mark.parametrize("M,K", gc.C3_LAYERS)
-@pytest.mark.parametrize("B", gc.C3_BATCHES)
-def test_gemv_config3_sweep(ctx, orc, c3_weights, M, K, B):
-    """The full C3 sweep: both layers at their real size (bf16, 2 MiB pages
+@pytest.mark.parametrize("M,K", gc.LS_LAYERS)
+@pytest.mark.parametrize("B", gc.LS_BATCHES)
+def test_gemv_ls_layers_sweep(ctx, orc, ls_weights, M, K, B):
+    """The full sweep of the LS layers: both at their real size (bf16, 2 MiB pages
     on colours 0..47) at every batch on the first 64/128/192/256 CUs -- every
     kernel variant the benchmark times for this configuration (vector path
     with 2-, 4- and 8-row tiles, MFMA with 8- and 16-row tiles).  Each
     result is within the oracle bound and bitwise equal across the masks."""
-    pool, pt, d_pool, d_pt, pool_pages = c3_weights(M, K)
+    pool, pt, d_pool, d_pt, pool_pages = ls_weights(M, K)
     xb = x_bits(sg.BF16, B * K, M + B + 2)
     d_x = to_dev(xb)
     ref, absdot = orc.gemv(pool, pt, sg.BF16, M, K, xb, sg.BF16, B, 21)
     ys = []
-    for n in gc.C3_CUS:
+    for n in gc.LS_CUS:
         if n > ctx.num_cus:
             continue
         plan = sg.gemv_plan(n, sg.BF16, M, K, sg.BF16, B)
-        say(f"gemv C3 {M}x{K} B={B} on {n} CUs: {plan['path']} rows {plan['rows']} "
+        say(f"gemv LS layer {M}x{K} B={B} on {n} CUs: {plan['path']} rows {plan['rows']} "
             f"loads {plan['loads']}")
         y = launch_gemv(ctx, d_pool, d_pt, pool_pages, M, K, B, sg.BF16, sg.BF16, d_x, 21,
                         range(n))
@@ -1026,7 +1026,7 @@ def test_two_streams_disjoint_masks_run_concurrently(ctx, orc):
     gemv_ok(to_host(d_y).reshape(1, M), y_ref, absdot)
 
 
-def test_corun_config4_disjoint_colours_and_cus(ctx, orc):
+def test_corun_disjoint_colours_and_cus(ctx, orc):
     """The co-located pair at its real size, from one pool under one hash
     (6 masks on address bits 21..40): the LS GEMV (bf16 4096 x 11008, batch
     1) on colours 0..47 in 2 MiB pages and CUs 0..191, concurrent with the BE
@@ -1044,7 +1044,7 @@ def test_corun_config4_disjoint_colours_and_cus(ctx, orc):
     w_pages = -(-(M * K * 2) >> wshift)
     pool_regions = int((3 * pages / region) * 4 * 1.1) + 4 * w_pages + 64
     raw, base, off = aligned_pool(pool_regions, wshift)
-    say(f"corun C4: one pool of {pool_regions} x 2 MiB, masks {[hex(m) for m in masks]}")
+    say(f"corun: one pool of {pool_regions} x 2 MiB, masks {[hex(m) for m in masks]}")
     # LS table (2 MiB pages) and BE table (64 KiB pages) from the same pool
     d_wpt = torch.empty(w_pages, dtype=torch.int32, device=DEV)
     sg.colour_alloc_pagetable(ctx, masks, base, wshift, pool_regions, range(48), w_pages, d_wpt)

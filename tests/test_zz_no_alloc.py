@@ -46,7 +46,7 @@ def both(ctx, masks, origin, shift, pool, S, n):
 
 def test_noalloc_pagetable_matches_the_allocating_build(ctx):
     masks = synth.xor_masks(6, seed=1, min_bit=16)
-    # the C2 pool at 8 of 64 colours, then a smaller pool and table
+    # the streaming triad's pool at 8 of 64 colours (three 1 GiB arrays), then a smaller pool and table
     for origin, shift, pool, S, n in [(1 << 36, 16, 393216, range(8), 3 * 16384),
                                       (1 << 40, 16, 50000, range(16, 40), 3000)]:
         say(f"noalloc page table: pool {pool} pages of {1 << (shift - 10)} KiB, |S| {len(S)}, n {n}")
