@@ -38,6 +38,18 @@ def test_library_exports_every_declared_symbol(L):
     assert not missing, missing
 
 
+def test_library_exports_nothing_else():
+    """The dynamic symbol table's functions are exactly the header's (the
+    link's version script keeps the C++ internals local)."""
+    import shutil
+    import subprocess
+    nm = shutil.which("nm") or shutil.which("llvm-nm") or "/opt/rocm/llvm/bin/llvm-nm"
+    out = subprocess.run([nm, "-D", "--defined-only", sg.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = sorted(line.split()[-1] for line in out.splitlines() if " T " in line)
+    assert exported == declared_functions()
+
+
 NULL = None
 
 
