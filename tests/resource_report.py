@@ -21,7 +21,8 @@ PAIRS = [
     ("GEMV batch 1, 2 rows x 6 slices", "sgdrc::k_gemv_valu<1, 1, 1, 2, 6>", "gemv.hip", "plain_gemv<2, 6>"),
     ("GEMV batch 1, 4 rows x 3 slices", "sgdrc::k_gemv_valu<1, 1, 1, 4, 3>", "gemv.hip", "plain_gemv<4, 3>"),
     ("GEMV batch 1, 4 rows x 2 slices", "sgdrc::k_gemv_valu<1, 1, 1, 4, 2>", "gemv.hip", "plain_gemv<4, 2>"),
-    ("GEMV batch 3-8, MFMA 16-row tiles", "sgdrc::k_gemm_mfma<1, 16>", "gemv.hip", None),
+    ("GEMV batch 5-8, MFMA 16-row tiles", "sgdrc::k_gemm_mfma<1, 16, 8>", "gemv.hip", None),
+    ("GEMV batch 3-4, MFMA 16-row tiles", "sgdrc::k_gemm_mfma<1, 16, 4>", "gemv.hip", None),
     ("classify, 8 loads per lane", "sgdrc::k_classify<6, false, false>", "colour.hip", "plain_classify<8>"),
     ("classify + histogram", "sgdrc::k_classify<6, true, false>", "colour.hip", "plain_classify<8>"),
 ]
