@@ -43,7 +43,9 @@ HALF_TILES = [(203, 3000, 8, 10, BF16), (4096, 11008, 4, 192, BF16), (37, 11008,
               (203, 3000, 5, 10, F16),
               # 2, 4 and 8 chunks per row, several 8-row tiles per workgroup
               (1040, 4096, 8, 64, BF16), (1040, 4096, 4, 64, BF16), (520, 2048, 8, 32, BF16),
-              (1040, 8192, 8, 64, BF16), (1040, 4096, 8, 64, F16)]
+              (1040, 8192, 8, 64, BF16), (1040, 4096, 8, 64, F16),
+              # four staged x rows (batch 3-4) in f16
+              (1040, 4096, 4, 64, F16), (203, 3000, 3, 10, F16)]
 MASKS_777 = [(777, 2048, B, BF16, BF16, 16, cus) for B in (1, 8) for cus in (None, 64, 128, 37)]
 CORUN_LS = [(4096, 11008, 1, BF16, BF16, 21, 192)]
 

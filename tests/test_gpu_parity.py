@@ -673,6 +673,29 @@ def test_gemv_mfma_half_tiles(ctx, orc, M, K, B, cus, dt):
     assert (y8.view(np.uint32) == y16.view(np.uint32)).all()
 
 
+@pytest.mark.parametrize("dt", [sg.BF16, sg.F16], ids=["bf16", "f16"])
+def test_gemv_mfma_x_rows_same_bits(ctx, orc, dt):
+    """The MFMA path stages four rows of x at batch 3-4 and eight at batch
+    5-8.  A batch column's sums do not depend on the other columns, so the
+    first rows of batch-5 and batch-8 launches equal batch-3 and batch-4
+    launches over the same rows of x bit for bit; each launch also matches
+    the oracle (1003 x 1000: a ragged last tile and a ragged last chunk)."""
+    M, K, shift = 1003, 1000, 16
+    say(f"gemv mfma {M}x{K} dtype {dt}: batches 3, 4, 5, 8 over shared rows of x")
+    pool, pt, d_pool, d_pt, pool_pages = upload_w(orc, M, K, dt, shift, range(48), 7, 1, 6)
+    xb = x_bits(dt, 8 * K, 9)
+    ys = {}
+    for B in (3, 4, 5, 8):
+        p = sg.gemv_plan(ctx.num_cus, dt, M, K, dt, B)
+        assert p["path"] == "mfma" and p["batch_cols"] == (4 if B <= 4 else 8), p
+        x = np.ascontiguousarray(xb[:B * K])
+        ys[B] = launch_gemv(ctx, d_pool, d_pt, pool_pages, M, K, B, dt, dt, to_dev(x), shift, None)
+        ref, absdot = orc.gemv(pool, pt, dt, M, K, x, dt, B, shift)
+        gemv_check(ctx, ys[B], ref, absdot, M, K, B, dt, dt, None, tag=f"batch {B}")
+    for lo, hi in ((3, 5), (4, 8), (3, 8)):
+        assert (ys[lo].view(np.uint32) == ys[hi][:lo].view(np.uint32)).all(), (lo, hi)
+
+
 def test_zero_length_triad_and_relayout_touch_nothing(ctx):
     shift, P = 16, 65536
     pt = torch.zeros(1, dtype=torch.int32, device=DEV)
