@@ -430,8 +430,10 @@ int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, 
  * path (vector ALUs or MFMA), rows of W per tile, loads in flight (vector
  * path: 16-byte loads per lane and row; MFMA: register sets of 2 KiB row
  * chunks), the batch columns the kernel is compiled for, the tile count,
- * and sum_depth: the most roundings any product W[m][k] x[b][k] meets on its
- * way into y (the fp32 additions and FMAs of the kernel's fixed summation
+ * x_once (vector path: 1 when each workgroup loads x once and keeps it in
+ * registers, for rows that one round of loads covers; it changes no
+ * result), and sum_depth: the most roundings any product W[m][k] x[b][k]
+ * meets on its way into y (the fp32 additions and FMAs of the kernel's fixed summation
  * tree, each MFMA counted as up to 32 additions), so that
  * |y - exact| <= sum_depth * 2^-24 * sum_k |W[m][k] x[b][k]| to first order
  * (products of bf16 or f16 operands are exact in fp32).  Lets tests and
@@ -445,7 +447,7 @@ typedef struct {
     uint32_t batch_cols;
     uint64_t tiles;
     uint32_t sum_depth;
-    uint32_t reserved;
+    uint32_t x_once;
 } sgdrc_gemv_plan;
 
 int colored_gemv_plan(uint32_t allowed_cus, int w_dtype, uint32_t M, uint32_t K, int x_dtype,

@@ -62,7 +62,7 @@ class Paged(ctypes.Structure):
 class GemvPlan(ctypes.Structure):
     _fields_ = [("path", ctypes.c_uint32), ("rows", ctypes.c_uint32), ("loads", ctypes.c_uint32),
                 ("batch_cols", ctypes.c_uint32), ("tiles", ctypes.c_uint64),
-                ("sum_depth", ctypes.c_uint32), ("reserved", ctypes.c_uint32)]
+                ("sum_depth", ctypes.c_uint32), ("x_once", ctypes.c_uint32)]
 
 
 GEMV_VALU, GEMV_MFMA = 0, 1
@@ -420,7 +420,8 @@ def gemv_plan(allowed_cus: int, w_dtype: int, M: int, K: int, x_dtype: int, batc
     _check(lib().colored_gemv_plan(int(allowed_cus), int(w_dtype), int(M), int(K), int(x_dtype),
                                  int(batch), ctypes.byref(p)))
     return {"path": "mfma" if p.path == GEMV_MFMA else "valu", "rows": p.rows, "loads": p.loads,
-            "batch_cols": p.batch_cols, "tiles": p.tiles, "sum_depth": p.sum_depth}
+            "batch_cols": p.batch_cols, "tiles": p.tiles, "sum_depth": p.sum_depth,
+            "x_once": bool(p.x_once)}
 
 
 class Bimodal:

@@ -125,8 +125,10 @@ __device__ __forceinline__ TilePages tile_pages(bool whole, const uint32_t *pt, 
     return stage_pages(pt, pool_pages, byte_lo, byte_hi, shift, s_pt, err);
 }
 
-// R rows per tile; U 16-byte slices per lane and row in flight.
-template <int WT, int XT, int NB, int R, int U>
+// R rows per tile; U 16-byte slices per lane and row in flight; XO: x is
+// loaded once per workgroup (the host sets it only for rows that one round
+// of loads covers).
+template <int WT, int XT, int NB, int R, int U, bool XO>
 __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
     const uint8_t *__restrict__ w_pool, const uint32_t *__restrict__ pt, uint64_t pool_pages,
     uint32_t M, uint32_t K, const uint8_t *__restrict__ x, uint32_t nb, float *__restrict__ y,
@@ -144,7 +146,45 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
     const uint64_t w_pages = ((uint64_t)M * row_bytes + pmask) >> shift;
     const bool whole = w_pages <= (uint64_t)kPtCap;
     uint32_t pro_err = 0u;
-    auto prologue = [&]() { stage_whole_table(pt, pool_pages, w_pages, s_pt, pro_err); };
+    // x of slice kv for every batch row (zeros out of range)
+    auto load_x = [&](uint32_t kv, uint32_t (&xs)[NB][XW]) __attribute__((always_inline)) {
+        const bool ok = kv < KV;
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+#pragma unroll
+            for (int i = 0; i < XW; ++i)
+                xs[b][i] = 0u;
+            if (ok && (uint32_t)b < nb) {
+                const uint8_t *xp = x + ((uint64_t)b * K + (uint64_t)kv * EPV) * XSZ;
+                if (XW == 2) {
+                    u32x2 v = *reinterpret_cast<const u32x2 *>(xp);
+                    xs[b][0] = v.x;
+                    xs[b][1] = v.y;
+                } else {
+#pragma unroll
+                    for (int q = 0; q < XW / 4; ++q) {
+                        u32x4 v = *reinterpret_cast<const u32x4 *>(xp + 16 * q);
+                        xs[b][4 * q + 0] = v.x;
+                        xs[b][4 * q + 1] = v.y;
+                        xs[b][4 * q + 2] = v.z;
+                        xs[b][4 * q + 3] = v.w;
+                    }
+                }
+            }
+        }
+    };
+    // XO (a row that one round of loads covers): every tile uses the same
+    // x slices per lane, loaded once per workgroup and kept in registers.
+    constexpr bool x_once = XO;
+    uint32_t xk[U][NB][XW];
+    auto prologue = [&]() {
+        stage_whole_table(pt, pool_pages, w_pages, s_pt, pro_err);
+        if (x_once) {
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                load_x((uint32_t)(u * kGemvWaves) * 64u + wave * 64u + lane, xk[u]);
+        }
+    };
 
     auto body = [&](uint32_t t, uint32_t, uint32_t &err, auto &&) {
         const uint32_t m0 = t * R;
@@ -160,7 +200,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
 
         for (uint32_t j = 0; (j * kGemvWaves + wave) * 64u < KV; j += U) {
             u32x4 wv[U][R];
-            uint32_t xv[U][NB][XW];
+            uint32_t xl[U][NB][XW];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const uint32_t kv = ((j + u) * kGemvWaves + wave) * 64u + lane;
@@ -175,30 +215,10 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_valu(
                             wv[u][r] = load_nt(w_pool + ((uint64_t)p << shift) + (off & pmask));
                     }
                 }
-#pragma unroll
-                for (int b = 0; b < NB; ++b) {
-#pragma unroll
-                    for (int i = 0; i < XW; ++i)
-                        xv[u][b][i] = 0u;
-                    if (ok && (uint32_t)b < nb) {
-                        const uint8_t *xp = x + ((uint64_t)b * K + (uint64_t)kv * EPV) * XSZ;
-                        if (XW == 2) {
-                            u32x2 v = *reinterpret_cast<const u32x2 *>(xp);
-                            xv[u][b][0] = v.x;
-                            xv[u][b][1] = v.y;
-                        } else {
-#pragma unroll
-                            for (int q = 0; q < XW / 4; ++q) {
-                                u32x4 v = *reinterpret_cast<const u32x4 *>(xp + 16 * q);
-                                xv[u][b][4 * q + 0] = v.x;
-                                xv[u][b][4 * q + 1] = v.y;
-                                xv[u][b][4 * q + 2] = v.z;
-                                xv[u][b][4 * q + 3] = v.w;
-                            }
-                        }
-                    }
-                }
+                if (!x_once)
+                    load_x(kv, xl[u]);
             }
+            const uint32_t (&xv)[U][NB][XW] = x_once ? xk : xl;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 float xf[NB][EPV];
@@ -578,6 +598,18 @@ static sgdrc_gemv_plan make_plan(uint32_t allowed, int w_dtype, uint32_t M, uint
             p.rows = 2u;
             p.loads = 6u;
         }
+        // x once per workgroup when one round of loads covers a row (every
+        // tile then reads the same x slices per lane) and x is at least half
+        // the bytes a tile reads, batch 1-2 (wider batches would hold too
+        // many registers).  Same bits either way.  Measured on MI355X (bf16,
+        // 2 MiB pages, eight rotated weight copies, two same-box A/B runs):
+        // 4096 x 11008 batch 1 3.1-3.5 percent faster on 256 CUs and
+        // 3.6-7.3 percent on 192, 11008 x 4096 batch 2 5.5-9.3 percent
+        // faster on 64..256 CUs;
+        // with x a quarter of a tile's bytes (four-row tiles, batch 1) it
+        // was up to 2.8 percent slower, so those keep per-tile x loads.
+        const uint64_t round_slices = (uint64_t)p.loads * (uint64_t)kGemvThreads;
+        p.x_once = kv <= round_slices && p.batch_cols <= 2u && 2u * p.batch_cols >= p.rows ? 1u : 0u;
         // per output: each lane's FMA chain over its slices, the butterfly
         // over 64 lanes, then the 4 waves' partials
         const uint64_t epv = 16u / (uint64_t)dtype_size(w_dtype);
@@ -591,16 +623,19 @@ static sgdrc_gemv_plan make_plan(uint32_t allowed, int w_dtype, uint32_t M, uint
 template <int WT, int XT>
 static GemvKernel valu_kernel(const sgdrc_gemv_plan &p)
 {
-#define SGDRC_VALU(NB, R, U)                                              \
-    if (p.batch_cols == NB && p.rows == R && p.loads == U)                \
-        return k_gemv_valu<WT, XT, NB, R, U>;
-    SGDRC_VALU(1, 2, 6)
-    SGDRC_VALU(1, 4, 3)
-    SGDRC_VALU(1, 4, 2)
-    SGDRC_VALU(2, 4, 3)
-    SGDRC_VALU(2, 4, 2)
-    SGDRC_VALU(4, 4, 2)
-    SGDRC_VALU(8, 4, 2)
+#define SGDRC_VALU(NB, R, U, XO)                                                      \
+    if (p.batch_cols == NB && p.rows == R && p.loads == U && p.x_once == (XO ? 1u : 0u)) \
+        return k_gemv_valu<WT, XT, NB, R, U, XO>;
+    SGDRC_VALU(1, 2, 6, false)
+    SGDRC_VALU(1, 2, 6, true)
+    SGDRC_VALU(1, 4, 3, false)
+    SGDRC_VALU(1, 4, 2, false)
+    SGDRC_VALU(2, 4, 3, false)
+    SGDRC_VALU(2, 4, 3, true)
+    SGDRC_VALU(2, 4, 2, false)
+    SGDRC_VALU(2, 4, 2, true)
+    SGDRC_VALU(4, 4, 2, false)
+    SGDRC_VALU(8, 4, 2, false)
 #undef SGDRC_VALU
     return nullptr;
 }

@@ -18,9 +18,11 @@ PAIRS = [
     ("triad, 16 slices per lane and array", "sgdrc::k_triad<16, false>", "stream.hip", "plain_triad<16>"),
     ("triad, preemptible", "sgdrc::k_triad<16, true>", "stream.hip", "plain_triad<16>"),
     ("relayout (copy), 16 slices per lane", "sgdrc::k_relayout<16, false>", "stream.hip", "plain_copy<16>"),
-    ("GEMV batch 1, 2 rows x 6 slices", "sgdrc::k_gemv_valu<1, 1, 1, 2, 6>", "gemv.hip", "plain_gemv<2, 6>"),
-    ("GEMV batch 1, 4 rows x 3 slices", "sgdrc::k_gemv_valu<1, 1, 1, 4, 3>", "gemv.hip", "plain_gemv<4, 3>"),
-    ("GEMV batch 1, 4 rows x 2 slices", "sgdrc::k_gemv_valu<1, 1, 1, 4, 2>", "gemv.hip", "plain_gemv<4, 2>"),
+    ("GEMV batch 1, 2 rows x 6 slices", "sgdrc::k_gemv_valu<1, 1, 1, 2, 6, false>", "gemv.hip", "plain_gemv<2, 6>"),
+    ("GEMV batch 1, 2 rows x 6 slices, x once per workgroup", "sgdrc::k_gemv_valu<1, 1, 1, 2, 6, true>", "gemv.hip",
+     "plain_gemv<2, 6>"),
+    ("GEMV batch 1, 4 rows x 3 slices", "sgdrc::k_gemv_valu<1, 1, 1, 4, 3, false>", "gemv.hip", "plain_gemv<4, 3>"),
+    ("GEMV batch 1, 4 rows x 2 slices", "sgdrc::k_gemv_valu<1, 1, 1, 4, 2, false>", "gemv.hip", "plain_gemv<4, 2>"),
     ("GEMV batch 5-8, MFMA 16-row tiles", "sgdrc::k_gemm_mfma<1, 16, 8>", "gemv.hip", None),
     ("GEMV batch 3-4, MFMA 16-row tiles", "sgdrc::k_gemm_mfma<1, 16, 4>", "gemv.hip", None),
     ("classify, 8 loads per lane", "sgdrc::k_classify<6, false, false>", "colour.hip", "plain_classify<8>"),

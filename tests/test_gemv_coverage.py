@@ -14,7 +14,7 @@ def _variant(case):
     p = sg.gemv_plan(gc.NUM_CUS if cus is None else cus, wd, M, K, xd, B)
     esize = 4 if wd == gc.F32 else 2
     whole = -(-(M * K * esize) // (1 << shift)) <= 256   # table staged once per workgroup
-    return (p["path"], p["rows"], p["loads"], p["batch_cols"], wd, xd, whole)
+    return (p["path"], p["rows"], p["loads"], p["batch_cols"], p["x_once"], wd, xd, whole)
 
 
 def test_every_benchmarked_gemv_variant_is_gpu_tested():
