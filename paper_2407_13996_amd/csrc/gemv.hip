@@ -608,8 +608,11 @@ static sgdrc_gemv_plan make_plan(uint32_t allowed, int w_dtype, uint32_t M, uint
         // faster on 64..256 CUs;
         // with x a quarter of a tile's bytes (four-row tiles, batch 1) it
         // was up to 2.8 percent slower, so those keep per-tile x loads.
+        // (W and x of one type, as measured; a wider x would hold twice the
+        // registers)
         const uint64_t round_slices = (uint64_t)p.loads * (uint64_t)kGemvThreads;
-        p.x_once = kv <= round_slices && p.batch_cols <= 2u && 2u * p.batch_cols >= p.rows ? 1u : 0u;
+        p.x_once = w_dtype == x_dtype && kv <= round_slices && p.batch_cols <= 2u &&
+                   2u * p.batch_cols >= p.rows ? 1u : 0u;
         // per output: each lane's FMA chain over its slices, the butterfly
         // over 64 lanes, then the 4 waves' partials
         const uint64_t epv = 16u / (uint64_t)dtype_size(w_dtype);
@@ -627,15 +630,17 @@ static GemvKernel valu_kernel(const sgdrc_gemv_plan &p)
     if (p.batch_cols == NB && p.rows == R && p.loads == U && p.x_once == (XO ? 1u : 0u)) \
         return k_gemv_valu<WT, XT, NB, R, U, XO>;
     SGDRC_VALU(1, 2, 6, false)
-    SGDRC_VALU(1, 2, 6, true)
     SGDRC_VALU(1, 4, 3, false)
     SGDRC_VALU(1, 4, 2, false)
     SGDRC_VALU(2, 4, 3, false)
-    SGDRC_VALU(2, 4, 3, true)
     SGDRC_VALU(2, 4, 2, false)
-    SGDRC_VALU(2, 4, 2, true)
     SGDRC_VALU(4, 4, 2, false)
     SGDRC_VALU(8, 4, 2, false)
+    if constexpr (WT == XT) {  // x once per workgroup: one type only
+        SGDRC_VALU(1, 2, 6, true)
+        SGDRC_VALU(2, 4, 3, true)
+        SGDRC_VALU(2, 4, 2, true)
+    }
 #undef SGDRC_VALU
     return nullptr;
 }

@@ -673,6 +673,25 @@ def test_gemv_mfma_half_tiles(ctx, orc, M, K, B, cus, dt):
     assert (y8.view(np.uint32) == y16.view(np.uint32)).all()
 
 
+@pytest.mark.parametrize("case", gc.X_ONCE, ids=_case_id)
+def test_gemv_x_once_matches_oracle_and_per_tile_x(ctx, orc, case):
+    """Vector path with x loaded once per workgroup (rows that one round of
+    loads covers, x half a tile's bytes; f16 and bf16, a K tail inside the
+    round, 4 KiB pages) against the oracle.  At batch 1 a mask of few CUs
+    gives four-row tiles with x loaded per tile: the same bits."""
+    M, K, B, wd, xd, shift, cus = case
+    p = sg.gemv_plan(cus or ctx.num_cus, wd, M, K, xd, B)
+    assert p["x_once"], p
+    say(f"gemv x once {_case_id(case)}")
+    y = run_gemv(ctx, orc, M, K, B, wd, xd, shift, seed=M + K + B, cus=cus)
+    if B == 1:
+        few = 4
+        q = sg.gemv_plan(few, wd, M, K, xd, B)
+        assert not q["x_once"] and q["rows"] == 4, q
+        y2 = run_gemv(ctx, orc, M, K, B, wd, xd, shift, seed=M + K + B, cus=few, check=False)
+        assert (y.view(np.uint32) == y2.view(np.uint32)).all()
+
+
 @pytest.mark.parametrize("dt", [sg.BF16, sg.F16], ids=["bf16", "f16"])
 def test_gemv_mfma_x_rows_same_bits(ctx, orc, dt):
     """The MFMA path stages four rows of x at batch 3-4 and eight at batch
