@@ -554,9 +554,16 @@ static int dtype_size(int dt) { return dt == SGDRC_F32 ? 4 : 2; }
 // has few tiles (``few``): the kernel is then bound by the latency of one
 // tile, and two-row tiles that load a 22 KB row in one round (six loads per
 // lane) finish sooner (4096 x 11008 on 256 CUs 15.1 against 15.2 us, on 192
-// CUs 17.9 against 18.9 us); with many tiles per CU, four-row tiles win (64
-// CUs 38.4 against 42.2 us).  The row shape never changes a result: every
-// lane sums its own 16-byte slices in the same order whatever the tile.
+// CUs 17.9 against 18.9 us); with many tiles per CU, four-row tiles won (64
+// CUs 38.4 against 42.2 us) until x was loaded once per workgroup (below):
+// with that, two-row tiles over one round of loads win on every mask for
+// rows of W and x of one type (4096 x 11008 on 64 and 128 CUs 1.6-5.7
+// percent faster, whole or spread XCDs), so they are taken whenever six
+// loads cover the row.  For 8 KiB rows (11008 x 4096) two-row tiles with x
+// once were up to 6.5 percent faster on whole XCDs but up to 7.7 percent
+// slower on spread CUs, and stay four-row.  The row shape never changes a
+// result: every lane sums its own 16-byte slices in the same order whatever
+// the tile.
 //
 // MFMA tile height by the rows of the busiest CU: 8-row tiles when they cut
 // its rows by a fifth or more (fewer tiles than CUs, or a last round that
@@ -594,7 +601,8 @@ static sgdrc_gemv_plan make_plan(uint32_t allowed, int w_dtype, uint32_t M, uint
         p.batch_cols = batch <= 1 ? 1u : batch <= 2 ? 2u : batch <= 4 ? 4u : 8u;
         p.rows = 4u;
         p.loads = long_rows && batch <= 2 ? 3u : 2u;
-        if (batch <= 1 && long_rows && few) {
+        const bool one_round6 = w_dtype == x_dtype && kv <= 6u * (uint64_t)kGemvThreads;
+        if (batch <= 1 && long_rows && (few || one_round6)) {
             p.rows = 2u;
             p.loads = 6u;
         }

@@ -677,19 +677,28 @@ def test_gemv_mfma_half_tiles(ctx, orc, M, K, B, cus, dt):
 def test_gemv_x_once_matches_oracle_and_per_tile_x(ctx, orc, case):
     """Vector path with x loaded once per workgroup (rows that one round of
     loads covers, x half a tile's bytes; f16 and bf16, a K tail inside the
-    round, 4 KiB pages) against the oracle.  At batch 1 a mask of few CUs
-    gives four-row tiles with x loaded per tile: the same bits."""
+    round, 4 KiB pages) against the oracle.  The same x values passed as
+    fp32 take the same tile shape with x loaded per tile (W and x differ in
+    type), and their products are exact, so the bits must match."""
     M, K, B, wd, xd, shift, cus = case
     p = sg.gemv_plan(cus or ctx.num_cus, wd, M, K, xd, B)
     assert p["x_once"], p
     say(f"gemv x once {_case_id(case)}")
-    y = run_gemv(ctx, orc, M, K, B, wd, xd, shift, seed=M + K + B, cus=cus)
-    if B == 1:
-        few = 4
-        q = sg.gemv_plan(few, wd, M, K, xd, B)
-        assert not q["x_once"] and q["rows"] == 4, q
-        y2 = run_gemv(ctx, orc, M, K, B, wd, xd, shift, seed=M + K + B, cus=few, check=False)
-        assert (y.view(np.uint32) == y2.view(np.uint32)).all()
+    seed = M + K + B
+    pool, pt, d_pool, d_pt, pool_pages = upload_w(orc, M, K, wd, shift, range(48), seed, 1, 6)
+    xb = x_bits(xd, B * K, seed + 2)
+    y = launch_gemv(ctx, d_pool, d_pt, pool_pages, M, K, B, wd, xd, to_dev(xb), shift, cu_list(cus))
+    ref, absdot = orc.gemv(pool, pt, wd, M, K, xb, xd, B, shift)
+    gemv_check(ctx, y, ref, absdot, M, K, B, wd, xd, cu_list(cus))
+    if xd == sg.BF16:
+        xf = (xb.astype(np.uint32) << 16).view(np.float32)
+    else:
+        xf = xb.view(np.float16).astype(np.float32)
+    q = sg.gemv_plan(cus or ctx.num_cus, wd, M, K, sg.F32, B)
+    assert not q["x_once"] and (q["rows"], q["loads"]) == (p["rows"], p["loads"]), (p, q)
+    y2 = launch_gemv(ctx, d_pool, d_pt, pool_pages, M, K, B, wd, sg.F32, to_dev(xf.view(np.uint32)),
+                     shift, cu_list(cus))
+    assert (y.view(np.uint32) == y2.view(np.uint32)).all()
 
 
 @pytest.mark.parametrize("dt", [sg.BF16, sg.F16], ids=["bf16", "f16"])
