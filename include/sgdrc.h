@@ -430,8 +430,9 @@ int colored_gemv(sgdrc_ctx *ctx, const sgdrc_paged *w, int w_dtype, uint32_t M, 
  * path (vector ALUs or MFMA), rows of W per tile, loads in flight (vector
  * path: 16-byte loads per lane and row; MFMA: register sets of 2 KiB row
  * chunks), the batch columns the kernel is compiled for, the tile count,
- * x_once (vector path: 1 when each workgroup loads x once and keeps it in
- * registers, for rows that one round of loads covers; it changes no
+ * x_once (1 when each workgroup loads x once: on the vector path into
+ * registers, for rows that one round of loads covers; on the MFMA path the
+ * whole K into LDS, at batch 3-4 with rows of at most 8 KiB; it changes no
  * result), and sum_depth: the most roundings any product W[m][k] x[b][k]
  * meets on its way into y (the fp32 additions and FMAs of the kernel's fixed summation
  * tree, each MFMA counted as up to 32 additions), so that

@@ -47,6 +47,11 @@ HALF_TILES = [(203, 3000, 8, 10, BF16), (4096, 11008, 4, 192, BF16), (37, 11008,
               # four staged x rows (batch 3-4) in f16
               (1040, 4096, 4, 64, F16), (203, 3000, 3, 10, F16)]
 MASKS_777 = [(777, 2048, B, BF16, BF16, 16, cus) for B in (1, 8) for cus in (None, 64, 128, 37)]
+# MFMA batch 3-4 with x for the whole K in LDS: a ragged last chunk in 2 MiB
+# pages, a full 8 KiB row in 4 KiB pages on the ticket queues, three chunks
+# (a pad chunk) in f16
+X_STAGED = [(1100, 4000, 4, BF16, BF16, 21, None), (700, 4096, 3, F16, F16, 12, 37),
+            (333, 3000, 4, F16, F16, 16, 64)]
 # x loaded once per workgroup (rows one round of loads covers, x half a
 # tile's bytes): f16 beside the bf16 LS layers, and a K tail inside the round
 X_ONCE = [(200, 8192, 1, F16, F16, 16, 64), (300, 4096, 2, F16, F16, 16, None),
@@ -58,7 +63,7 @@ def gpu_cases():
     """Every (shape, mask size) a GPU test launches the GEMV with."""
     cases = RAGGED + DTYPE_MIX + STAGING + MFMA_CHUNKS + LONG_ROWS + SECTORS + SINGLE_ROWS
     cases += PAGE_EDGES
-    cases += FP32_1024 + CORUN_LS + MASKS_777 + X_ONCE
+    cases += FP32_1024 + CORUN_LS + MASKS_777 + X_ONCE + X_STAGED
     for M, K, B, cus, dt in HALF_TILES:
         n = cus if isinstance(cus, int) else len(cus)
         cases += [(M, K, B, dt, dt, 16, n), (M, K, B, dt, dt, 16, -(-M // 16))]

@@ -23,8 +23,10 @@ PAIRS = [
      "plain_gemv<2, 6>"),
     ("GEMV batch 1, 4 rows x 3 slices", "sgdrc::k_gemv_valu<1, 1, 1, 4, 3, false>", "gemv.hip", "plain_gemv<4, 3>"),
     ("GEMV batch 1, 4 rows x 2 slices", "sgdrc::k_gemv_valu<1, 1, 1, 4, 2, false>", "gemv.hip", "plain_gemv<4, 2>"),
-    ("GEMV batch 5-8, MFMA 16-row tiles", "sgdrc::k_gemm_mfma<1, 16, 8>", "gemv.hip", None),
-    ("GEMV batch 3-4, MFMA 16-row tiles", "sgdrc::k_gemm_mfma<1, 16, 4>", "gemv.hip", None),
+    ("GEMV batch 5-8, MFMA 16-row tiles", "sgdrc::k_gemm_mfma<1, 16, 8, false>", "gemv.hip", None),
+    ("GEMV batch 3-4, MFMA 16-row tiles", "sgdrc::k_gemm_mfma<1, 16, 4, false>", "gemv.hip", None),
+    ("GEMV batch 3-4, MFMA 16-row tiles, x for the whole K in LDS", "sgdrc::k_gemm_mfma<1, 16, 4, true>", "gemv.hip",
+     None),
     ("classify, 8 loads per lane", "sgdrc::k_classify<6, false, false>", "colour.hip", "plain_classify<8>"),
     ("classify + histogram", "sgdrc::k_classify<6, true, false>", "colour.hip", "plain_classify<8>"),
 ]

@@ -644,7 +644,7 @@ def test_gemv_fp32_1024x1024(ctx, orc):
 
 
 @pytest.mark.parametrize("case", gc.RAGGED + gc.DTYPE_MIX + gc.STAGING + gc.MFMA_CHUNKS
-                         + gc.LONG_ROWS + gc.SECTORS + gc.SINGLE_ROWS + gc.PAGE_EDGES,
+                         + gc.LONG_ROWS + gc.SECTORS + gc.SINGLE_ROWS + gc.PAGE_EDGES + gc.X_STAGED,
                          ids=_case_id)
 def test_gemv_matches_oracle(ctx, orc, case):
     """Ragged shapes (1003 x 1000, batches 1..8), mixed dtypes, W tables of
@@ -704,10 +704,12 @@ def test_gemv_x_once_matches_oracle_and_per_tile_x(ctx, orc, case):
 @pytest.mark.parametrize("dt", [sg.BF16, sg.F16], ids=["bf16", "f16"])
 def test_gemv_mfma_x_rows_same_bits(ctx, orc, dt):
     """The MFMA path stages four rows of x at batch 3-4 and eight at batch
-    5-8.  A batch column's sums do not depend on the other columns, so the
-    first rows of batch-5 and batch-8 launches equal batch-3 and batch-4
-    launches over the same rows of x bit for bit; each launch also matches
-    the oracle (1003 x 1000: a ragged last tile and a ragged last chunk)."""
+    5-8 (here at batch 3-4 for the whole K at once, skipping the pad chunk,
+    at batch 5-8 chunk by chunk).  A batch column's sums do not depend on
+    the other columns, so the first rows of batch-5 and batch-8 launches
+    equal batch-3 and batch-4 launches over the same rows of x bit for bit;
+    each launch also matches the oracle (1003 x 1000: a ragged last tile
+    and a ragged last chunk)."""
     M, K, shift = 1003, 1000, 16
     say(f"gemv mfma {M}x{K} dtype {dt}: batches 3, 4, 5, 8 over shared rows of x")
     pool, pt, d_pool, d_pt, pool_pages = upload_w(orc, M, K, dt, shift, range(48), 7, 1, 6)
@@ -716,6 +718,7 @@ def test_gemv_mfma_x_rows_same_bits(ctx, orc, dt):
     for B in (3, 4, 5, 8):
         p = sg.gemv_plan(ctx.num_cus, dt, M, K, dt, B)
         assert p["path"] == "mfma" and p["batch_cols"] == (4 if B <= 4 else 8), p
+        assert p["x_once"] == (B <= 4), p   # whole-K x in LDS at batch 3-4 (rows of 2000 bytes)
         x = np.ascontiguousarray(xb[:B * K])
         ys[B] = launch_gemv(ctx, d_pool, d_pt, pool_pages, M, K, B, dt, dt, to_dev(x), shift, None)
         ref, absdot = orc.gemv(pool, pt, dt, M, K, x, dt, B, shift)
