@@ -50,3 +50,22 @@ def test_plan_rejects_bad_arguments():
         sg.gemv_plan(64, gc.BF16, 16, 12, gc.BF16, 1)     # K * 2 not a multiple of 16
     with pytest.raises(sg.SgdrcError):
         sg.gemv_plan(64, gc.BF16, 16, 16, gc.BF16, 9)
+
+
+def test_plan_x_once_rules():
+    """Which launches load x once per workgroup: vector path when one round
+    of loads covers a row and x is half a tile's bytes (W and x of one
+    type); MFMA path at batch 3-4 with rows of at most 8 KiB."""
+    for cus in (64, 128, 192, 256):
+        p = sg.gemv_plan(cus, gc.BF16, 4096, 11008, gc.BF16, 1)
+        assert (p["path"], p["rows"], p["loads"], p["x_once"]) == ("valu", 2, 6, True), (cus, p)
+        assert not sg.gemv_plan(cus, gc.BF16, 4096, 11008, gc.F32, 1)["x_once"]
+        assert not sg.gemv_plan(cus, gc.BF16, 11008, 4096, gc.BF16, 1)["x_once"]   # x a quarter
+        assert sg.gemv_plan(cus, gc.BF16, 11008, 4096, gc.BF16, 2)["x_once"]
+        assert not sg.gemv_plan(cus, gc.BF16, 4096, 11008, gc.BF16, 2)["x_once"]   # two rounds
+        q = sg.gemv_plan(cus, gc.BF16, 11008, 4096, gc.BF16, 4)
+        assert q["path"] == "mfma" and q["batch_cols"] == 4 and q["x_once"], (cus, q)
+        assert not sg.gemv_plan(cus, gc.BF16, 4096, 11008, gc.BF16, 4)["x_once"]   # 22 KB rows
+        assert not sg.gemv_plan(cus, gc.BF16, 11008, 4096, gc.BF16, 8)["x_once"]   # eight x rows
+    # rows longer than six loads per lane cover keep per-tile x
+    assert not sg.gemv_plan(256, gc.BF16, 512, 16384, gc.BF16, 1)["x_once"]
